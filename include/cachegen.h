@@ -1,0 +1,167 @@
+/*
+ * cachegen.h — C ABI of the CacheGen KV-cache codec for AMD Instinct MI355X (gfx950).
+ *
+ * The codec (CacheGen, SIGCOMM '24, Sec. 5.2 "KV cache encoding") turns an fp16 KV cache into
+ * compact bitstreams in four steps, and decodes them back:
+ *   1. token groups of G consecutive tokens; the first token of a group is the anchor and is
+ *      quantized on its own at 8 bits, the others are coded as a delta against that anchor
+ *      (Sec. 5.2 "Change-based encoding"; 8-bit anchors: Sec. 5.2 "Layer-wise quantization");
+ *   2. vectorwise quantization whose delta bin width grows with layer depth
+ *      (Sec. 5.2 "Layer-wise quantization"; default bins 0.5 / 1 / 1.5: App. C.2), with an
+ *      encoding level chosen per context chunk (Sec. 5.3 "Workflow");
+ *   3. one symbol distribution per (layer, K/V, channel) for deltas and one for anchors,
+ *      counted over the context (Sec. 5.2 "Arithmetic coding"; Sec. 6 "Speed optimization");
+ *   4. arithmetic coding of the symbols into bitstreams, and GPU arithmetic decoding back to
+ *      fp16 KV (Sec. 5.2 "Arithmetic coding"; Sec. 6 "Speed optimization").
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  B = n_ctx contexts, L = n_layers, T = n_tokens, C = n_channels per K and per V.
+ *  KV layout (fp16 bit patterns, uint16_t): kv[b][l][kv][t][ch], kv = 0 for K and 1 for V,
+ *  channel fastest. Element count n_elem = B*L*2*T*C (64-bit).
+ *  Chunks: tokens are split into NC = ceil(T/chunk_len) chunks; the last may be partial.
+ *  Token groups restart at every chunk start (chunks decode independently, Sec. 5.3).
+ *  One arithmetic-coder stream per (b, c, l, kv, ch) with stream index
+ *      s = (((b*NC + c)*L + l)*2 + kv)*C + ch        (S = B*NC*L*2*C streams)
+ *  so every chunk's streams are contiguous in the payload.
+ *  Symbols: a quantized value q in [-127, 127] is symbol q + 127 in [0, 254] (255 symbols).
+ *  Scale (per stream): m = max |x| over the chunk's tokens; s = (m == 0) ? 1 : m / 127 (fp32).
+ *  Anchor (token j of a chunk with j % G == 0): q = rint(clamp(x / s, -127, 127)); a = q * s.
+ *  Delta (other tokens): w = (layer_bin[l] * level_mult[level]) * s; d = x - a;
+ *                        q = rint(clamp(d / w, -127, 127)).
+ *  Reconstruction: anchor fp16(a); delta fp16(a + q * w). All fp32 arithmetic is IEEE
+ *  binary32, round-to-nearest-even, no fused multiply-add; fp16 conversion rounds to nearest even.
+ *
+ *  CDF tables: uint16_t cum[256] per distribution with cum[0] = 0, cum[i+1] = cum[i] + freq[i]
+ *  for i in [0, 253], every freq >= 1, total 65536. Entry 255 is padding (written 0); the
+ *  top of the last interval, 65536, is implicit.
+ *    cdf_anchor[l][kv][ch][256]                       (level independent)
+ *    cdf_delta [level][l][kv][ch][256]                (one table set per encoding level)
+ *
+ *  Bitstreams: integer arithmetic coder with 32-bit code registers (Witten, Neal and Cleary,
+ *  CACM 30(6), 1987), bitwise renormalisation, 2-bit termination. Bits are written MSB-first
+ *  into uint32_t words; each stream is zero-padded to a whole word. offsets[0] = 0 and
+ *  offsets[s+1] = offsets[s] + (words of stream s), uint64_t, so stream s occupies
+ *  words[offsets[s] .. offsets[s+1]).
+ *
+ *  Memory: every array argument is a DEVICE pointer owned by the caller, except cg_params and
+ *  the arrays it points to, which are HOST memory read during the call only. The library
+ *  keeps no state between calls and never allocates device memory; scratch comes from the
+ *  caller's workspace argument. Calls are asynchronous on the given HIP stream unless a
+ *  description says otherwise; a non-zero return means nothing was launched, except
+ *  CG_ERR_HIP, which reports a failed launch.
+ */
+#ifndef CACHEGEN_H
+#define CACHEGEN_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Return codes. */
+enum {
+  CG_OK = 0,
+  CG_ERR_ARG = -1,        /* null pointer, level out of range, chunk range out of range   */
+  CG_ERR_SHAPE = -2,      /* a dimension <= 0, group_size < 1, chunk_len < 1, n_levels not
+                             in [1, 8], or a size whose index space overflows 64 bits       */
+  CG_ERR_CAPACITY = -3,   /* words_cap or workspace_bytes below what the call needs        */
+  CG_ERR_NONFINITE = -4,  /* the KV input holds NaN or +-Inf (checked on the host side of
+                             the call; see cg_fit_cdf / cg_encode)                          */
+  CG_ERR_HIP = -5,        /* a HIP runtime call or kernel launch failed                     */
+  CG_ERR_PARAM = -6       /* a layer_bin or level_mult entry is not finite and > 0          */
+};
+
+typedef struct cg_params {
+  int32_t n_ctx;          /* B */
+  int32_t n_layers;       /* L */
+  int32_t n_tokens;       /* T */
+  int32_t n_channels;     /* C = kv_heads * head_dim, the same for K and V */
+  int32_t group_size;     /* G, tokens per group, 10 in the paper (Sec. 5.2) */
+  int32_t chunk_len;      /* tokens per chunk, 1.5K in the paper (Sec. 5.3); 1536 here */
+  int32_t n_levels;       /* number of encoding levels, 1..8 */
+  const float* layer_bin; /* [L] base delta bin width per layer in units of the scale s
+                             (three layer groups 0.5 / 1 / 1.5 by default, App. C.2)    */
+  const float* level_mult;/* [n_levels] multiplier of the bin width per encoding level */
+} cg_params;
+
+/* Number of chunks NC and of streams S for these parameters; 0 if the shape is invalid. */
+int64_t cg_num_chunks(const cg_params* p);
+int64_t cg_num_streams(const cg_params* p);
+
+/* Upper bound on the total number of payload words cg_encode can produce: each symbol costs at
+ * most 18 renormalisation shifts and the termination 2 bits, so stream s needs at most
+ * ceil((18 * n_s + 2) / 32) words where n_s is its token count. 0 if the shape is invalid. */
+uint64_t cg_encode_bound_words(const cg_params* p);
+
+/* Device scratch that cg_encode needs (bytes): a worst-case slot per stream plus per-stream
+ * lengths and the scan's partial sums. 0 if the shape is invalid. */
+uint64_t cg_encode_workspace_bytes(const cg_params* p);
+
+/* Fit the symbol distributions at encoding level `level` (Sec. 5.2 "Arithmetic coding":
+ * one distribution per layer-channel for deltas and one for anchors; Sec. 6: counted over the
+ * symbols of the context being coded).
+ *   kv_f16          [B][L][2][T][C] fp16, device.
+ *   level           0 <= level < n_levels: deltas of EVERY chunk are quantized with
+ *                   level_mult[level] for this fit.
+ *   cdf_anchor      out [L][2][C][256], device; may be NULL to skip the anchor tables.
+ *   cdf_delta_level out [L][2][C][256], device: the delta tables of this level, i.e. the
+ *                   slice cdf_delta[level] of the layout above.
+ * Counts c_i (i in [0, 254]) are taken over all B*NC chunks; with N = sum c_i,
+ * freq_i = 1 + floor(c_i * 65281 / N), and the remainder 65536 - sum freq_i is added to the
+ * symbol with the largest count (lowest index on ties); N = 0 gives the uniform table.
+ * Returns CG_OK, or an error before anything is launched. Does not scan for non-finite input
+ * (cg_check_finite does). */
+int cg_fit_cdf(const cg_params* p, const uint16_t* kv_f16, int32_t level,
+               uint16_t* cdf_anchor, uint16_t* cdf_delta_level, hipStream_t stream);
+
+/* Encode the whole KV cache (Sec. 5.2: delta, layer-wise quantization, arithmetic coding;
+ * Sec. 5.3: each chunk at its own level).
+ *   kv_f16       [B][L][2][T][C] fp16, device.
+ *   chunk_level  [B][NC] uint8, device: level of every (context, chunk); all equal for a
+ *                single-level encode.
+ *   cdf_anchor   [L][2][C][256], cdf_delta [n_levels][L][2][C][256], device (from cg_fit_cdf).
+ *   words        out, device, capacity words_cap >= cg_encode_bound_words(p).
+ *   offsets      out [S + 1] uint64, device; offsets[S] is the payload length in words.
+ *   scales       out [S] fp32, device: the per-stream scale s.
+ *   workspace    device scratch of workspace_bytes >= cg_encode_workspace_bytes(p).
+ * chunk_level values must be < n_levels (an out-of-range level is clamped to n_levels - 1 on
+ * the device). Asynchronous. */
+int cg_encode(const cg_params* p, const uint16_t* kv_f16, const uint8_t* chunk_level,
+              const uint16_t* cdf_anchor, const uint16_t* cdf_delta,
+              uint32_t* words, uint64_t words_cap, uint64_t* offsets, float* scales,
+              void* workspace, uint64_t workspace_bytes, hipStream_t stream);
+
+/* Decode chunks [chunk_begin, chunk_end) of every context back to fp16 KV (Sec. 5.2; the
+ * GPU decoder of Sec. 6; chunk ranges allow decoding a chunk as soon as it arrives, Sec. 6).
+ *   words, offsets [S + 1], scales [S], chunk_level [B][NC], cdf_anchor, cdf_delta: device,
+ *                as produced by cg_encode / cg_fit_cdf.
+ *   kv_out_f16   out [B][L][2][T][C] fp16, device; only the token rows of the requested
+ *                chunks are written.
+ * Bits past the end of a stream read as zero and every loop is bounded by the stream's token
+ * count, so a corrupt payload yields wrong values but never an out-of-range access, provided
+ * offsets is non-decreasing and offsets[S] does not exceed the words buffer. Asynchronous. */
+int cg_decode(const cg_params* p, const uint32_t* words, const uint64_t* offsets,
+              const float* scales, const uint8_t* chunk_level,
+              const uint16_t* cdf_anchor, const uint16_t* cdf_delta,
+              int32_t chunk_begin, int32_t chunk_end, uint16_t* kv_out_f16,
+              hipStream_t stream);
+
+/* Scan kv_f16 [n_elem] for NaN / Inf (fp16 exponent field all ones), using flag_dev, one
+ * caller-owned device uint32_t, as scratch. Synchronises `stream`. Returns CG_OK,
+ * CG_ERR_NONFINITE, or an error code. The quantizer is defined for finite input only;
+ * callers that cannot vouch for their input run this first. */
+int cg_check_finite(const cg_params* p, const uint16_t* kv_f16, uint32_t* flag_dev,
+                    hipStream_t stream);
+
+/* Static description of a return code; never NULL. */
+const char* cg_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CACHEGEN_H */

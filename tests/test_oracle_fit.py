@@ -1,0 +1,72 @@
+"""Pins of the oracle's distribution fit (CacheGen Sec. 5.2 "Arithmetic coding"; Sec. 6)."""
+import numpy as np
+import pytest
+
+import oracle
+from conftest import golden_rows
+from paper_2310_07240_amd import workloads as W
+
+
+@pytest.mark.parametrize("row", golden_rows("fit_closed_form.txt"), ids=lambda r: r[0])
+def test_closed_form(row):
+    name, counts, expected = row
+    c = np.zeros(255, np.int64)
+    if counts != "-":
+        for kv in counts.split(","):
+            i, v = kv.split(":")
+            c[int(i)] = int(v)
+    t = oracle.normalize(c)
+    assert t[0] == 0 and t[255] == 0
+    for kv in expected.split(","):
+        i, v = kv.split(":")
+        assert int(t[int(i)]) == int(v), (i, t[int(i)], v)
+    c32 = oracle.cum32(t).astype(np.int64)
+    assert np.all(np.diff(c32) >= 1) and c32[255] == 65536
+
+
+def test_invariants_random_counts():
+    rng = np.random.default_rng(1)
+    for _ in range(200):
+        c = rng.integers(0, 10**int(rng.integers(1, 9)), size=255) * (rng.random(255) < rng.random())
+        t = oracle.cum32(oracle.normalize(c)).astype(np.int64)
+        f = np.diff(t)
+        assert t[0] == 0 and t[255] == 65536 and f.min() >= 1
+        N = c.sum()
+        if N == 0:
+            continue
+        base = 1 + (c * 65281) // N
+        top = int(np.argmax(c))                                     # first maximum
+        exp = base.copy(); exp[top] += 65536 - base.sum()
+        assert np.array_equal(f, exp)
+
+
+def test_fit_counts_every_chunk_and_context():
+    """The fitted table equals the normalisation of the symbol histogram over all chunks and
+    contexts of the stream's (layer, K/V, channel)."""
+    w = W.small(n_ctx=2, n_layers=2, n_tokens=70, n_channels=5, chunk_len=32)
+    kv = W.generate(w)
+    shape = oracle.shape_from(w)
+    ca, cd = oracle.fit_cdf(kv, shape, 1, threads=3)
+    cl = np.ones((w.n_ctx, w.n_chunks), np.uint8)
+    for l in range(2):
+        for k in range(2):
+            for ch in range(5):
+                hist_a = np.zeros(255, np.int64); hist_d = np.zeros(255, np.int64)
+                for b in range(2):
+                    for c in range(w.n_chunks):
+                        s = (((b * w.n_chunks + c) * 2 + l) * 2 + k) * 5 + ch
+                        sc, sym, _ = oracle.stream_symbols(kv, shape, cl, s)
+                        anchor = np.arange(sym.size) % w.group_size == 0
+                        hist_a += np.bincount(sym[anchor], minlength=255)
+                        hist_d += np.bincount(sym[~anchor], minlength=255)
+                assert np.array_equal(ca[l, k, ch], oracle.normalize(hist_a))
+                assert np.array_equal(cd[l, k, ch], oracle.normalize(hist_d))
+
+
+def test_fit_is_thread_count_independent():
+    w = W.small(n_layers=3, n_tokens=64, n_channels=9)
+    kv = W.generate(w)
+    shape = oracle.shape_from(w)
+    a1, d1 = oracle.fit_cdf(kv, shape, 0, threads=1)
+    a2, d2 = oracle.fit_cdf(kv, shape, 0, threads=5)
+    assert np.array_equal(a1, a2) and np.array_equal(d1, d2)
