@@ -1,0 +1,252 @@
+"""Python binding of the codec's C ABI (include/cachegen.h).
+
+Argument marshalling only: every step of the codec runs in the HIP kernels of
+``libcachegen.so``. torch supplies device buffers and the HIP stream handle. There is no CPU
+fallback: if the library is missing or no GPU is present, the calls raise.
+
+Names follow the C ABI: ``cg_fit_cdf``, ``cg_encode``, ``cg_decode`` (plus the size queries);
+``Codec`` bundles the parameters and allocates outputs for the common whole-cache calls.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libcachegen.so")
+
+CG_OK = 0
+ERRORS = {-1: "CG_ERR_ARG", -2: "CG_ERR_SHAPE", -3: "CG_ERR_CAPACITY", -4: "CG_ERR_NONFINITE",
+          -5: "CG_ERR_HIP", -6: "CG_ERR_PARAM"}
+
+EXPORTS = ("cg_num_chunks", "cg_num_streams", "cg_encode_bound_words",
+           "cg_encode_workspace_bytes", "cg_fit_cdf", "cg_encode", "cg_decode",
+           "cg_check_finite", "cg_strerror")
+
+
+class CodecError(RuntimeError):
+    def __init__(self, code: int, what: str):
+        self.code = code
+        super().__init__(f"{what}: {ERRORS.get(code, code)} ({strerror(code)})")
+
+
+class _CParams(ctypes.Structure):
+    _fields_ = [("n_ctx", ctypes.c_int32), ("n_layers", ctypes.c_int32),
+                ("n_tokens", ctypes.c_int32), ("n_channels", ctypes.c_int32),
+                ("group_size", ctypes.c_int32), ("chunk_len", ctypes.c_int32),
+                ("n_levels", ctypes.c_int32),
+                ("layer_bin", ctypes.POINTER(ctypes.c_float)),
+                ("level_mult", ctypes.POINTER(ctypes.c_float))]
+
+
+_LIB = None
+_P = ctypes.c_void_p
+
+
+def lib():
+    """Load libcachegen.so (raises if it has not been built)."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2310_07240_amd.build` (no CPU fallback exists)")
+        L = ctypes.CDLL(LIB_PATH)
+        PP = ctypes.POINTER(_CParams)
+        L.cg_num_chunks.argtypes = [PP]; L.cg_num_chunks.restype = ctypes.c_int64
+        L.cg_num_streams.argtypes = [PP]; L.cg_num_streams.restype = ctypes.c_int64
+        L.cg_encode_bound_words.argtypes = [PP]; L.cg_encode_bound_words.restype = ctypes.c_uint64
+        L.cg_encode_workspace_bytes.argtypes = [PP]
+        L.cg_encode_workspace_bytes.restype = ctypes.c_uint64
+        L.cg_fit_cdf.argtypes = [PP, _P, ctypes.c_int32, _P, _P, _P]
+        L.cg_fit_cdf.restype = ctypes.c_int
+        L.cg_encode.argtypes = [PP, _P, _P, _P, _P, _P, ctypes.c_uint64, _P, _P, _P,
+                                ctypes.c_uint64, _P]
+        L.cg_encode.restype = ctypes.c_int
+        L.cg_decode.argtypes = [PP, _P, _P, _P, _P, _P, _P, ctypes.c_int32, ctypes.c_int32, _P, _P]
+        L.cg_decode.restype = ctypes.c_int
+        L.cg_check_finite.argtypes = [PP, _P, _P, _P]
+        L.cg_check_finite.restype = ctypes.c_int
+        L.cg_strerror.argtypes = [ctypes.c_int]
+        L.cg_strerror.restype = ctypes.c_char_p
+        _LIB = L
+    return _LIB
+
+
+def strerror(code: int) -> str:
+    return lib().cg_strerror(int(code)).decode()
+
+
+@dataclass
+class CodecParams:
+    """cg_params: shape of the KV cache and the quantizer's tables (host memory)."""
+    n_ctx: int
+    n_layers: int
+    n_tokens: int
+    n_channels: int
+    layer_bin: tuple
+    level_mult: tuple
+    group_size: int = 10
+    chunk_len: int = 1536
+
+    @classmethod
+    def of(cls, obj) -> "CodecParams":
+        return cls(obj.n_ctx, obj.n_layers, obj.n_tokens, obj.n_channels, tuple(obj.layer_bin),
+                   tuple(obj.level_mult), obj.group_size, obj.chunk_len)
+
+    @property
+    def n_levels(self) -> int:
+        return len(self.level_mult)
+
+    @property
+    def kv_shape(self):
+        return (self.n_ctx, self.n_layers, 2, self.n_tokens, self.n_channels)
+
+    def c(self):
+        """The C struct plus the arrays it points into (keep both alive for the call)."""
+        lb = np.ascontiguousarray(self.layer_bin, np.float32)
+        lm = np.ascontiguousarray(self.level_mult, np.float32)
+        s = _CParams(self.n_ctx, self.n_layers, self.n_tokens, self.n_channels, self.group_size,
+                     self.chunk_len, len(lm), lb.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
+                     lm.ctypes.data_as(ctypes.POINTER(ctypes.c_float)))
+        return s, (lb, lm)
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _check(rc: int, what: str):
+    if rc != CG_OK:
+        raise CodecError(rc, what)
+
+
+# --------------------------------------------------------------------------------------------
+# size queries (host only)
+# --------------------------------------------------------------------------------------------
+def cg_num_chunks(p: CodecParams) -> int:
+    s, keep = p.c()
+    return int(lib().cg_num_chunks(ctypes.byref(s)))
+
+
+def cg_num_streams(p: CodecParams) -> int:
+    s, keep = p.c()
+    return int(lib().cg_num_streams(ctypes.byref(s)))
+
+
+def cg_encode_bound_words(p: CodecParams) -> int:
+    s, keep = p.c()
+    return int(lib().cg_encode_bound_words(ctypes.byref(s)))
+
+
+def cg_encode_workspace_bytes(p: CodecParams) -> int:
+    s, keep = p.c()
+    return int(lib().cg_encode_workspace_bytes(ctypes.byref(s)))
+
+
+# --------------------------------------------------------------------------------------------
+# the three codec calls
+# --------------------------------------------------------------------------------------------
+def cg_fit_cdf(p: CodecParams, kv, level: int, cdf_anchor, cdf_delta_level, stream=None):
+    s, keep = p.c()
+    _check(lib().cg_fit_cdf(ctypes.byref(s), _ptr(kv), int(level), _ptr(cdf_anchor),
+                            _ptr(cdf_delta_level), _stream(stream)), "cg_fit_cdf")
+
+
+def cg_encode(p: CodecParams, kv, chunk_level, cdf_anchor, cdf_delta, words, offsets, scales,
+              workspace, stream=None):
+    s, keep = p.c()
+    _check(lib().cg_encode(ctypes.byref(s), _ptr(kv), _ptr(chunk_level), _ptr(cdf_anchor),
+                           _ptr(cdf_delta), _ptr(words), words.numel(), _ptr(offsets),
+                           _ptr(scales), _ptr(workspace), workspace.numel() * workspace.element_size(),
+                           _stream(stream)), "cg_encode")
+
+
+def cg_decode(p: CodecParams, words, offsets, scales, chunk_level, cdf_anchor, cdf_delta,
+              chunk_begin: int, chunk_end: int, kv_out, stream=None):
+    s, keep = p.c()
+    _check(lib().cg_decode(ctypes.byref(s), _ptr(words), _ptr(offsets), _ptr(scales),
+                           _ptr(chunk_level), _ptr(cdf_anchor), _ptr(cdf_delta), int(chunk_begin),
+                           int(chunk_end), _ptr(kv_out), _stream(stream)), "cg_decode")
+
+
+def cg_check_finite(p: CodecParams, kv, flag, stream=None) -> bool:
+    s, keep = p.c()
+    rc = lib().cg_check_finite(ctypes.byref(s), _ptr(kv), _ptr(flag), _stream(stream))
+    if rc == -4:
+        return False
+    _check(rc, "cg_check_finite")
+    return True
+
+
+# --------------------------------------------------------------------------------------------
+# convenience: allocate outputs with torch and call the above
+# --------------------------------------------------------------------------------------------
+class Codec:
+    """Whole-cache codec on one GPU. Buffers are torch tensors on `device`."""
+
+    def __init__(self, params: CodecParams, device="cuda"):
+        import torch
+        self.torch = torch
+        self.p = params
+        self.device = torch.device(device)
+        self.n_chunks = cg_num_chunks(params)
+        self.n_streams = cg_num_streams(params)
+        if self.n_streams == 0:
+            raise CodecError(-2, "Codec")
+        self.bound_words = cg_encode_bound_words(params)
+        self.ws_bytes = cg_encode_workspace_bytes(params)
+        self._ws = None
+        self._words = None
+
+    def _empty(self, shape, dtype):
+        return self.torch.empty(shape, dtype=dtype, device=self.device)
+
+    def fit(self, kv, stream=None):
+        """Anchor tables [L,2,C,256] and delta tables of every level [NLV,L,2,C,256]."""
+        t = self.torch
+        L, C = self.p.n_layers, self.p.n_channels
+        ca = self._empty((L, 2, C, 256), t.int16)
+        cd = self._empty((self.p.n_levels, L, 2, C, 256), t.int16)
+        for lv in range(self.p.n_levels):
+            cg_fit_cdf(self.p, kv, lv, ca if lv == 0 else None, cd[lv], stream)
+        return ca, cd
+
+    def workspace(self):
+        if self._ws is None:
+            self._ws = self._empty((self.ws_bytes,), self.torch.uint8)
+        return self._ws
+
+    def encode(self, kv, chunk_level, cdf_anchor, cdf_delta, stream=None, words=None):
+        """Returns (words [bound], offsets [S+1], scales [S]); offsets[S] is the payload length."""
+        t = self.torch
+        if words is None:
+            if self._words is None:
+                self._words = self._empty((self.bound_words,), t.int32)
+            words = self._words
+        offsets = self._empty((self.n_streams + 1,), t.int64)
+        scales = self._empty((self.n_streams,), t.float32)
+        cg_encode(self.p, kv, chunk_level, cdf_anchor, cdf_delta, words, offsets, scales,
+                  self.workspace(), stream)
+        return words, offsets, scales
+
+    def decode(self, words, offsets, scales, chunk_level, cdf_anchor, cdf_delta,
+               chunk_begin=0, chunk_end=None, out=None, stream=None):
+        if chunk_end is None:
+            chunk_end = self.n_chunks
+        if out is None:
+            out = self.torch.zeros(self.p.kv_shape, dtype=self.torch.int16, device=self.device)
+        cg_decode(self.p, words, offsets, scales, chunk_level, cdf_anchor, cdf_delta,
+                  chunk_begin, chunk_end, out, stream)
+        return out

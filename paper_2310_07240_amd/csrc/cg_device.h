@@ -1,0 +1,100 @@
+// cg_device.h — device-side definitions shared by the codec's HIP kernels (gfx950).
+//
+// Kernel-side view of the codec parameters and the small helpers every kernel uses: fp16
+// conversion, the quantizer (CacheGen Sec. 5.2, "Change-based encoding" and "Layer-wise
+// quantization"), wave-level reductions, and the launchers the C ABI calls.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#define CG_MAX_LAYERS 512
+#define CG_MAX_LEVELS 8
+#define CG_NSYM 255
+#define CG_TOTAL 65536u
+
+// Parameters as the kernels see them. Passed by value (kernel argument segment, < 4 KiB).
+struct KParams {
+  int32_t B, L, T, C;      // contexts, layers, tokens, channels per K and per V
+  int32_t G, CL, NC, NLV;  // group size, chunk length, chunks, levels
+  int32_t nblk;            // 64-channel blocks per (b, c, l, kv) = ceil(C / 64)
+  int32_t pad_;
+  int64_t S;               // streams
+  float layer_bin[CG_MAX_LAYERS];
+  float level_mult[CG_MAX_LEVELS];
+};
+
+__device__ __forceinline__ float cg_h2f(uint16_t h) {
+  return (float)__builtin_bit_cast(_Float16, h);               // exact widening
+}
+
+__device__ __forceinline__ uint16_t cg_f2h(float f) {
+  return __builtin_bit_cast(uint16_t, (_Float16)f);            // round to nearest even
+}
+
+// Quantize v by step `step` to an integer in [-127, 127]: rint(clamp(v / step)). The division
+// is the correctly rounded IEEE one (the library is built without fast-math), rint rounds half
+// to even.
+__device__ __forceinline__ int cg_quant(float v, float step) {
+  float r = v / step;
+  r = fminf(fmaxf(r, -127.0f), 127.0f);
+  return (int)__builtin_rintf(r);
+}
+
+// Stream index of (b, c, l, kv, ch): chunk-major so each chunk's streams are contiguous.
+__device__ __forceinline__ int64_t cg_stream(const KParams& P, int64_t bclk, int ch) {
+  return bclk * P.C + ch;
+}
+
+// Element offset of token t, channel ch in the [B][L][2][T][C] tensor for row group (b, l, kv).
+__device__ __forceinline__ int64_t cg_elem(const KParams& P, int b, int l, int k, int64_t t,
+                                           int ch) {
+  return ((((int64_t)b * P.L + l) * 2 + k) * P.T + t) * P.C + ch;
+}
+
+template <typename T>
+__device__ __forceinline__ T cg_wave_sum(T v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// Inclusive prefix sum across the 64 lanes of a wave.
+__device__ __forceinline__ uint32_t cg_wave_incl_scan(uint32_t v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    uint32_t n = __shfl_up(v, o, 64);
+    if (lane >= o) v += n;
+  }
+  return v;
+}
+
+__device__ __forceinline__ uint64_t cg_wave_incl_scan64(uint64_t v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    uint64_t n = __shfl_up(v, o, 64);
+    if (lane >= o) v += n;
+  }
+  return v;
+}
+
+// Launchers (return hipError_t of the launch).
+hipError_t cg_launch_fit(const KParams& P, const uint16_t* kv, int level, uint16_t* cdf_anchor,
+                         uint16_t* cdf_delta_level, hipStream_t st);
+hipError_t cg_launch_encode(const KParams& P, const uint16_t* kv, const uint8_t* chunk_level,
+                            const uint16_t* cdf_anchor, const uint16_t* cdf_delta,
+                            uint32_t* words, uint64_t* offsets, float* scales, void* ws,
+                            uint32_t slot_words, hipStream_t st);
+hipError_t cg_launch_decode(const KParams& P, const uint32_t* words, const uint64_t* offsets,
+                            const float* scales, const uint8_t* chunk_level,
+                            const uint16_t* cdf_anchor, const uint16_t* cdf_delta, int c_begin,
+                            int c_end, uint16_t* out, hipStream_t st);
+hipError_t cg_launch_check_finite(const uint16_t* kv, int64_t n, uint32_t* flag, hipStream_t st);
+
+// Workspace layout of cg_encode (byte offsets, 256-aligned).
+struct EncWorkspace {
+  uint64_t slots_off, lens_off, partial_off, total;
+};
+EncWorkspace cg_encode_ws_layout(int64_t S, uint32_t slot_words);

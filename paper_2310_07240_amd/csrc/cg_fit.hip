@@ -1,0 +1,146 @@
+// cg_fit.hip — symbol-distribution fit (CacheGen Sec. 5.2 "Arithmetic coding": one
+// distribution per channel-layer for deltas and one for anchors; Sec. 6: frequencies counted
+// over the context's quantized symbols).
+//
+// One workgroup per (layer, K/V, 64-channel block). Its 8 waves walk every (context, chunk)
+// pair of that block; a lane owns one channel and runs the quantizer over the chunk's tokens
+// (one pass for the absmax scale, one to quantize), counting symbols into LDS histograms.
+// Rows are read 64 channels (128 B) at a time, so every load is one coalesced line. After a
+// barrier each wave normalises histograms to 16-bit cumulative tables: per-lane partial sums,
+// a wave reduction for the total, the argmax and the frequency sum, and a wave prefix scan.
+#include "cg_device.h"
+
+namespace {
+
+constexpr int kFitWaves = 8;
+constexpr int kFitThreads = kFitWaves * 64;
+constexpr int kHist = 256;  // 255 symbols, padded
+
+// Normalise one histogram [255] into cum[256] (entry 255 = 0) with one wave.
+__device__ void normalize_wave(const uint32_t* cnt, uint16_t* out) {
+  const int lane = threadIdx.x & 63;
+  uint32_t c[4];
+  uint64_t local = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    int i = lane * 4 + j;
+    c[j] = i < CG_NSYM ? cnt[i] : 0u;
+    local += c[j];
+  }
+  uint64_t N = cg_wave_sum<uint64_t>(local);
+  if (N == 0) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) c[j] = (lane * 4 + j) < CG_NSYM ? 1u : 0u;
+    N = CG_NSYM;
+  }
+  // argmax with the lowest index on ties
+  uint32_t best = 0;
+  int besti = 0x7fffffff;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int i = lane * 4 + j;
+    if (i < CG_NSYM && (besti == 0x7fffffff || c[j] > best)) { best = c[j]; besti = i; }
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    uint32_t ob = __shfl_xor(best, o, 64);
+    int oi = __shfl_xor(besti, o, 64);
+    if (ob > best || (ob == best && oi < besti)) { best = ob; besti = oi; }
+  }
+  uint32_t f[4];
+  uint32_t fl = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    int i = lane * 4 + j;
+    f[j] = i < CG_NSYM ? 1u + (uint32_t)(((uint64_t)c[j] * (CG_TOTAL - CG_NSYM)) / N) : 0u;
+    fl += f[j];
+  }
+  uint32_t sumf = cg_wave_sum<uint32_t>(fl);
+  uint32_t rem = CG_TOTAL - sumf;
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    if (lane * 4 + j == besti) { f[j] += rem; fl += rem; }
+  uint32_t incl = cg_wave_incl_scan(fl);
+  uint32_t run = incl - fl;  // exclusive prefix of this lane's first symbol
+  uint16_t o[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    int i = lane * 4 + j;
+    o[j] = i < CG_NSYM ? (uint16_t)run : (uint16_t)0;
+    run += f[j];
+  }
+  // 4 consecutive u16 per lane: one 8-byte store, the wave writes the 512-byte table at once
+  uint64_t packed = (uint64_t)o[0] | ((uint64_t)o[1] << 16) | ((uint64_t)o[2] << 32) |
+                    ((uint64_t)o[3] << 48);
+  reinterpret_cast<uint64_t*>(out)[lane] = packed;
+}
+
+__global__ __launch_bounds__(kFitThreads) void fit_kernel(KParams P, const uint16_t* __restrict__ kv,
+                                                         int level, uint16_t* __restrict__ cdf_anchor,
+                                                         uint16_t* __restrict__ cdf_delta) {
+  extern __shared__ uint32_t cnt[];  // [2 kinds][64 channels][256]
+  const int cb = blockIdx.x % P.nblk;
+  const int lk = blockIdx.x / P.nblk;
+  const int l = lk >> 1, k = lk & 1;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+
+  for (int i = threadIdx.x; i < 2 * 64 * kHist; i += kFitThreads) cnt[i] = 0;
+  __syncthreads();
+
+  const int ch = cb * 64 + lane;
+  const bool act = ch < P.C;
+  const float wfac = P.layer_bin[l] * P.level_mult[level];
+  uint32_t* ha = cnt + lane * kHist;
+  uint32_t* hd = cnt + (64 + lane) * kHist;
+  const int pairs = P.B * P.NC;
+  for (int pr = wave; pr < pairs; pr += kFitWaves) {
+    const int b = pr / P.NC, c = pr % P.NC;
+    const int t0 = c * P.CL;
+    const int n = min(P.CL, P.T - t0);
+    if (!act) continue;
+    const uint16_t* x = kv + cg_elem(P, b, l, k, t0, ch);
+    float m = 0.0f;
+    for (int j = 0; j < n; ++j) m = fmaxf(m, fabsf(cg_h2f(x[(int64_t)j * P.C])));
+    const float s = (m == 0.0f) ? 1.0f : m / 127.0f;
+    const float w = wfac * s;
+    float a = 0.0f;
+    int g = 0;
+    for (int j = 0; j < n; ++j) {
+      const float v = cg_h2f(x[(int64_t)j * P.C]);
+      if (g == 0) {
+        const int q = cg_quant(v, s);
+        a = (float)q * s;
+        atomicAdd(&ha[q + 127], 1u);
+      } else {
+        const int q = cg_quant(v - a, w);
+        atomicAdd(&hd[q + 127], 1u);
+      }
+      g = (g + 1 == P.G) ? 0 : g + 1;
+    }
+  }
+  __syncthreads();
+
+  for (int tb = wave; tb < 128; tb += kFitWaves) {
+    const int kind = tb >> 6, cl = tb & 63;
+    const int chx = cb * 64 + cl;
+    if (chx >= P.C) continue;
+    if (kind == 0 && cdf_anchor == nullptr) continue;
+    uint16_t* dst = (kind == 0 ? cdf_anchor : cdf_delta) +
+                    ((int64_t)(l * 2 + k) * P.C + chx) * 256;
+    normalize_wave(cnt + tb * kHist, dst);
+  }
+}
+
+}  // namespace
+
+hipError_t cg_launch_fit(const KParams& P, const uint16_t* kv, int level, uint16_t* cdf_anchor,
+                         uint16_t* cdf_delta_level, hipStream_t st) {
+  const size_t lds = 2 * 64 * kHist * sizeof(uint32_t);
+  hipError_t e = hipFuncSetAttribute((const void*)fit_kernel,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  const int64_t grid = (int64_t)P.L * 2 * P.nblk;
+  hipLaunchKernelGGL(fit_kernel, dim3((unsigned)grid), dim3(kFitThreads), lds, st, P, kv, level,
+                     cdf_anchor, cdf_delta_level);
+  return hipGetLastError();
+}

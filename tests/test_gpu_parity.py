@@ -1,0 +1,77 @@
+"""GPU parity: the HIP codec against the CPU oracle, bit for bit (tables, scales, offsets,
+payload words, decoded fp16), on small seeded workloads that span several 64-channel blocks,
+ragged chunks and groups, and the codec's degenerate inputs. Every test calls the C ABI."""
+import numpy as np
+import pytest
+
+from paper_2310_07240_amd import workloads as W
+from gpu_helpers import compare_full, run_gpu, run_oracle, say, assert_same, torch_cuda
+
+pytestmark = pytest.mark.gpu
+
+SMALL = [
+    W.small(),                                                     # C=70: a ragged channel block
+    W.small(name="c130_ctx2_heavy", n_ctx=2, n_tokens=61, chunk_len=20, n_channels=130,
+            heavy_ctx=(1,)),
+    W.small(name="g1_all_anchors", group_size=1, n_tokens=40, chunk_len=16),
+    W.small(name="one_chunk", n_tokens=37, chunk_len=1536, level_mult=(1.0,), random_levels=False),
+    W.small(name="l1_c1_t1", n_layers=1, n_channels=1, n_tokens=1, chunk_len=7),
+    W.small(name="l1_c64_t23", n_layers=1, n_channels=64, n_tokens=23, chunk_len=7),
+    W.small(name="g7_levels3", group_size=7, n_tokens=200, chunk_len=64, n_channels=96,
+            level_mult=(1.0, 2.0, 4.0)),
+    W.small(name="long_chunk_1536", n_layers=2, n_tokens=1600, chunk_len=1536, n_channels=65,
+            level_mult=(1.0, 8.0)),
+]
+
+
+@pytest.mark.parametrize("w", SMALL, ids=lambda w: w.name)
+def test_small_workloads_bit_exact(w):
+    kv = W.generate(w)
+    o = run_oracle(w, kv)
+    g = run_gpu(w, kv, decode_oracle_payload=(o["words"], o["offsets"], o["scales"], o["ca"], o["cd"]))
+    compare_full(w, g, o)
+    assert_same("decode of oracle payload", g["out_from_oracle_payload"], o["out"])
+
+
+@pytest.mark.parametrize("kind", ["zeros", "constant", "subnormal", "ties", "clamp", "signs"])
+def test_edge_inputs_bit_exact(kind):
+    w = W.small(name=f"edge_{kind}", n_tokens=64, chunk_len=25, n_channels=80)
+    kv = W.edge_case_kv(w, kind)
+    o = run_oracle(w, kv)
+    g = run_gpu(w, kv)
+    compare_full(w, g, o)
+
+
+def test_tiny_config_bit_exact():
+    w = W.TINY
+    kv = W.generate(w)
+    o = run_oracle(w, kv)
+    g = run_gpu(w, kv, decode_oracle_payload=(o["words"], o["offsets"], o["scales"], o["ca"], o["cd"]))
+    compare_full(w, g, o)
+    assert_same("decode of oracle payload", g["out_from_oracle_payload"], o["out"])
+
+
+def test_chunk_range_decode_and_determinism():
+    torch = torch_cuda()
+    from paper_2310_07240_amd.cachegen import Codec, CodecParams
+    w = W.small(name="ranges", n_ctx=2, n_tokens=130, chunk_len=40, n_channels=100)
+    kv_np = W.generate(w)
+    codec = Codec(CodecParams.of(w))
+    kv = torch.from_numpy(kv_np.view(np.int16)).cuda()
+    cl = torch.from_numpy(w.chunk_levels()).cuda()
+    ca, cd = codec.fit(kv)
+    words, offsets, scales = codec.encode(kv, cl, ca, cd)
+    full = codec.decode(words, offsets, scales, cl, ca, cd).cpu().numpy()
+    again = codec.decode(words, offsets, scales, cl, ca, cd).cpu().numpy()
+    assert_same("decode twice", full, again)
+    w2, o2, s2 = codec.encode(kv, cl, ca, cd, words=torch.empty_like(words))
+    n = int(offsets[-1])
+    assert_same("encode twice", w2[:n].cpu().numpy(), words[:n].cpu().numpy())
+    for c0, c1 in [(0, 1), (1, 3), (3, 4), (2, 2)]:
+        say(f"ranges: decode chunks [{c0}, {c1})")
+        part = codec.decode(words, offsets, scales, cl, ca, cd, c0, c1).cpu().numpy()
+        t0, t1 = c0 * w.chunk_len, min(c1 * w.chunk_len, w.n_tokens)
+        assert_same(f"chunks {c0}:{c1}", part[..., t0:t1, :], full[..., t0:t1, :])
+        mask = np.ones(w.n_tokens, bool)
+        mask[t0:t1] = False
+        assert np.all(part[..., mask, :] == 0)
