@@ -23,6 +23,7 @@ import zlib
 from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass, field
 import os
+import threading
 
 import numpy as np
 
@@ -142,31 +143,71 @@ def _outlier_channels(w: Workload, l: int, k: int) -> np.ndarray:
     return rng.choice(w.n_channels, size=n, replace=False)
 
 
-def slab(w: Workload, b: int, l: int, k: int, n_tokens: int | None = None) -> np.ndarray:
-    """fp16 values [T, C] of context b, layer l, K/V k (first n_tokens rows if given)."""
-    T = w.n_tokens if n_tokens is None else n_tokens
-    C = w.n_channels
+_TLS = threading.local()
+
+
+def _scratch(T: int, C: int) -> tuple[np.ndarray, np.ndarray]:
+    """Two reusable float64 [T, C] buffers per thread (first-touch page faults are costly)."""
+    key = (T, C)
+    if getattr(_TLS, "key", None) != key:
+        _TLS.key = key
+        _TLS.a = np.empty((T, C), np.float64)
+        _TLS.b = np.empty((T, C), np.float64)
+    return _TLS.a, _TLS.b
+
+
+def _student_t3(rng, shape, out=None, tmp=None):
+    """Student-t with 3 degrees of freedom as z / sqrt(chi2_3 / 3) from four normals."""
+    if out is None:
+        out = np.empty(shape, np.float64)
+    if tmp is None:
+        tmp = np.empty(shape, np.float64)
+    rng.standard_normal(out=tmp)
+    np.square(tmp, out=tmp)
+    acc = tmp.copy() if tmp.size < 4096 else tmp          # chi2 accumulator
+    for _ in range(2):
+        rng.standard_normal(out=out)
+        np.square(out, out=out)
+        acc += out
+    acc /= 3.0
+    np.sqrt(acc, out=acc)
+    rng.standard_normal(out=out)
+    out /= acc
+    return out
+
+
+def slab_into(w: Workload, b: int, l: int, k: int, out: np.ndarray) -> np.ndarray:
+    """Fill out (fp16 view, [T', C] with T' <= T) with context b, layer l, K/V k."""
+    T, C = out.shape
     rng = np.random.default_rng([w.seed, b, l, k])
     scale = np.exp(rng.uniform(math.log(0.1), math.log(4.0), size=C))
     oc = _outlier_channels(w, l, k)
     scale[oc] *= 20.0
-    x = np.empty((T, C), np.float64)
+    x, z = _scratch(T, C)
+    x[0] = 0.0
     if b in w.heavy_ctx:
-        beta = rng.standard_t(3, size=C)
-        z = rng.standard_t(3, size=(T - 1, C)) / math.sqrt(3.0)
-        x[0] = 0.0
-        np.cumsum(0.5 * z, axis=0, out=x[1:])
+        beta = _student_t3(rng, (C,))
+        _student_t3(rng, (T - 1, C), out=z[: T - 1], tmp=x[1:])
+        z[: T - 1] *= 0.5 / math.sqrt(3.0)
+        np.cumsum(z[: T - 1], axis=0, out=x[1:])
         x += beta
         x *= scale
     else:
         base = rng.standard_normal(C)
-        steps = rng.standard_normal((T - 1, C))
-        steps *= 0.05 * scale
-        x[0] = 0.0
-        np.cumsum(steps, axis=0, out=x[1:])
+        rng.standard_normal(out=z[: T - 1])
+        z[: T - 1] *= 0.05 * scale
+        np.cumsum(z[: T - 1], axis=0, out=x[1:])
         x += scale * base
     np.clip(x, -FP16_MAX, FP16_MAX, out=x)
-    return x.astype(np.float16)
+    np.copyto(out, x, casting="unsafe")          # float64 -> float16, round to nearest even
+    return out
+
+
+def slab(w: Workload, b: int, l: int, k: int, n_tokens: int | None = None) -> np.ndarray:
+    """fp16 values [T, C] of context b, layer l, K/V k (first n_tokens rows if given)."""
+    out = np.empty((w.n_tokens, w.n_channels), np.float16)
+    slab_into(w, b, l, k, out)
+    return out if n_tokens is None else out[:n_tokens].copy()
 
 
 def generate(w: Workload, out: np.ndarray | None = None, threads: int | None = None) -> np.ndarray:
@@ -178,7 +219,7 @@ def generate(w: Workload, out: np.ndarray | None = None, threads: int | None = N
 
     def run(j):
         b, l, k = j
-        o[b, l, k] = slab(w, b, l, k)
+        slab_into(w, b, l, k, o[b, l, k])
 
     threads = threads or min(16, max(1, len(os.sched_getaffinity(0))))
     if threads == 1 or len(jobs) == 1:
