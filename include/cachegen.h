@@ -65,12 +65,13 @@ extern "C" {
 /* Return codes. */
 enum {
   CG_OK = 0,
-  CG_ERR_ARG = -1,        /* null pointer, level out of range, chunk range out of range   */
+  CG_ERR_ARG = -1,        /* null or misaligned pointer (tables need 16-byte alignment,
+                             offsets 8, words and scales 4, the workspace 256), level or
+                             chunk range out of range                                       */
   CG_ERR_SHAPE = -2,      /* a dimension <= 0, group_size < 1, chunk_len < 1, n_levels not
                              in [1, 8], or a size whose index space overflows 64 bits       */
   CG_ERR_CAPACITY = -3,   /* words_cap or workspace_bytes below what the call needs        */
-  CG_ERR_NONFINITE = -4,  /* the KV input holds NaN or +-Inf (checked on the host side of
-                             the call; see cg_fit_cdf / cg_encode)                          */
+  CG_ERR_NONFINITE = -4,  /* the KV input holds NaN or +-Inf (reported by cg_check_finite) */
   CG_ERR_HIP = -5,        /* a HIP runtime call or kernel launch failed                     */
   CG_ERR_PARAM = -6       /* a layer_bin or level_mult entry is not finite and > 0          */
 };

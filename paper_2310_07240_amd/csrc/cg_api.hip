@@ -130,7 +130,7 @@ int cg_decode(const cg_params* p, const uint32_t* words, const uint64_t* offsets
   if (!words || !offsets || !scales || !chunk_level || !cdf_anchor || !cdf_delta || !kv_out_f16)
     return CG_ERR_ARG;
   if (chunk_begin < 0 || chunk_end > K.NC || chunk_begin > chunk_end) return CG_ERR_ARG;
-  if (!aligned(cdf_anchor, 8) || !aligned(cdf_delta, 8) || !aligned(offsets, 8) ||
+  if (!aligned(cdf_anchor, 16) || !aligned(cdf_delta, 16) || !aligned(offsets, 8) ||
       !aligned(words, 4) || !aligned(kv_out_f16, 2))
     return CG_ERR_ARG;
   if (chunk_begin == chunk_end) return CG_OK;
