@@ -76,6 +76,10 @@ enum {
   CG_ERR_PARAM = -6       /* a layer_bin or level_mult entry is not finite and > 0          */
 };
 
+/* cg_decode may read (but never uses) up to this many words past offsets[S]: a words buffer
+ * handed to cg_decode must be readable that far. A buffer sized by cg_encode_bound_words is. */
+#define CG_TAIL_WORDS 8
+
 typedef struct cg_params {
   int32_t n_ctx;          /* B */
   int32_t n_layers;       /* L */
@@ -93,9 +97,10 @@ typedef struct cg_params {
 int64_t cg_num_chunks(const cg_params* p);
 int64_t cg_num_streams(const cg_params* p);
 
-/* Upper bound on the total number of payload words cg_encode can produce: each symbol costs at
- * most 18 renormalisation shifts and the termination 2 bits, so stream s needs at most
- * ceil((18 * n_s + 2) / 32) words where n_s is its token count. 0 if the shape is invalid. */
+/* Capacity (in words) that cg_encode requires for its payload buffer: the sum over streams of
+ * ceil((18 * n_s + 2) / 32), n_s being the stream's token count (each symbol costs at most 18
+ * renormalisation shifts and the termination 2 bits), plus CG_TAIL_WORDS. 0 if the shape is
+ * invalid. */
 uint64_t cg_encode_bound_words(const cg_params* p);
 
 /* Device scratch that cg_encode needs (bytes): a worst-case slot per stream plus per-stream
@@ -142,9 +147,12 @@ int cg_encode(const cg_params* p, const uint16_t* kv_f16, const uint8_t* chunk_l
  *                as produced by cg_encode / cg_fit_cdf.
  *   kv_out_f16   out [B][L][2][T][C] fp16, device; only the token rows of the requested
  *                chunks are written.
- * Bits past the end of a stream read as zero and every loop is bounded by the stream's token
- * count, so a corrupt payload yields wrong values but never an out-of-range access, provided
- * offsets is non-decreasing and offsets[S] does not exceed the words buffer. Asynchronous. */
+ * The words buffer must be readable up to offsets[S] + CG_TAIL_WORDS. Bits after a stream's
+ * codeword never change its decoded symbols (whatever follows, the code value stays inside the
+ * coder's final interval), so the decoder may read into the next stream or the tail. Every
+ * loop is bounded by the stream's token count: a corrupt payload yields wrong values but never
+ * an out-of-range access, provided offsets is non-decreasing and offsets[S] + CG_TAIL_WORDS
+ * words are readable. Asynchronous. */
 int cg_decode(const cg_params* p, const uint32_t* words, const uint64_t* offsets,
               const float* scales, const uint8_t* chunk_level,
               const uint16_t* cdf_anchor, const uint16_t* cdf_delta,

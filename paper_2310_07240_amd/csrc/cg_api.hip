@@ -74,7 +74,7 @@ uint64_t cg_encode_bound_words(const cg_params* p) {
     const int64_t n = (c + 1) * (int64_t)K.CL <= K.T ? K.CL : K.T - (int64_t)c * K.CL;
     total += (uint64_t)per_chunk * ((18ull * (uint64_t)n + 2ull + 31ull) / 32ull);
   }
-  return total;
+  return total + CG_TAIL_WORDS;
 }
 
 uint64_t cg_encode_workspace_bytes(const cg_params* p) {

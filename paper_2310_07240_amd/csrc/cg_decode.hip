@@ -7,9 +7,10 @@
 //   up to 16 such waves that share (layer, K/V, channel block) and therefore share their
 //   distribution tables, which are staged in LDS once per workgroup:
 //     * delta tables (9 of 10 symbols): the whole 16-bit cumulative table, 256 entries, at a
-//       516-byte stride so the 64 lanes' tables start in different banks; entry 255 holds a
-//       0xFFFF sentinel. Search: a fixed 8-step binary search (every lane takes the same steps,
-//       no divergence), each probe an LDS read with an immediate offset.
+//       520-byte stride (8-byte aligned; neighbouring lanes start in different banks), entries
+//       255..259 holding 0xFFFF sentinels. Search: a 4-ary search over four levels (three
+//       probes per level, the same steps in every lane, no divergence), the last level a single
+//       aligned 8-byte read of four neighbouring entries.
 //     * anchor tables (1 of 10 symbols; broad distributions): only 16 fences cum[16 f] per
 //       table stay in LDS (36-byte stride). A 4-step fence search picks the block of 16
 //       symbols, one 32-byte global load brings that block (L2-resident), and a 4-step binary
@@ -28,51 +29,32 @@
 //   3. renormalisation in one step: n1 = clz(low ^ high) shared leading bits, then n3
 //      "middle half" steps (run of low = 1 / high = 0 from bit 30 down); D and rm1 both shift
 //      left by n = n1 + n3 taking in n stream bits (D) or ones (rm1).
-// The payload is read through a 64-bit bit buffer with two words prefetched ahead, so the
-// global load latency is covered by the symbols decoded in between.
+// The payload is read through a 64-bit bit buffer fed from words requested one epoch (four
+// tokens) ahead (see the reader state in the kernel). The words buffer must be readable
+// CG_TAIL_WORDS words past offsets[S].
+#include "../../include/cachegen.h"
 #include "cg_device.h"
 
 namespace {
 
 constexpr int kMaxWaves = 16;
-constexpr int kTabStride = 258;    // u16 per delta table in LDS (256 + 2 pad -> 516 bytes)
+constexpr int kTabStride = 260;    // u16 per delta table in LDS (256 + 4 pad -> 520 bytes)
 constexpr int kFenceStride = 18;   // u16 per anchor fence row (16 + 2 pad -> 36 bytes)
+constexpr int kEpoch = 4;          // tokens between bitstream requests
+constexpr int kRows = 8;           // decoded token rows staged in LDS per wave before a store
 
-struct BitIn {
-  uint64_t buf;         // unread bits, left-aligned
-  uint32_t avail;       // valid bits in buf, >= 32 between symbols
-  uint32_t w1, w2;      // the next two payload words (already requested)
-  const uint32_t* p;    // next word to request
-  const uint32_t* end;  // one past the stream's last word
+__device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
-  __device__ __forceinline__ uint32_t fetch() {
-    uint32_t w = 0;
-    if (p < end) w = *p;
-    ++p;
-    return w;
-  }
-  // Take n bits, 0 <= n <= 31.
-  __device__ __forceinline__ uint32_t take(uint32_t n) {
-    const uint32_t bits = n ? (uint32_t)(buf >> (64 - n)) : 0u;
-    buf <<= n;
-    avail -= n;
-    if (avail < 32) {
-      buf |= (uint64_t)w1 << (32 - avail);
-      avail += 32;
-      w1 = w2;
-      w2 = fetch();
-    }
-    return bits;
-  }
-};
-
-// Cumulative frequency of symbol i (0..255) in an LDS delta table / a global anchor table.
-__device__ __forceinline__ uint32_t cum_lds(const uint16_t* t, int i) {
-  return i >= CG_NSYM ? CG_TOTAL : (uint32_t)t[i];
+// x * c + c2 >> 16 as one 32x32+64 multiply-add. The addend passes through an empty asm so the
+// compiler cannot fold x*c + c into a 64-bit (x + 1) * c.
+__device__ __forceinline__ uint32_t scaled_off(uint32_t x, uint32_t c) {
+  uint32_t c2 = c;
+  asm volatile("" : "+v"(c2));
+  return (uint32_t)(((uint64_t)x * c + c2) >> 16);
 }
-__device__ __forceinline__ uint32_t cum_glb(const uint16_t* t, int i) {
-  return i >= CG_NSYM ? CG_TOTAL : (uint32_t)t[i];
-}
+
+// Make the compiler wait here for a register produced by a load (once, outside the loop).
+__device__ __forceinline__ void settle(uint32_t v) { asm volatile("" ::"v"(v)); }
 
 __global__ __launch_bounds__(1024) void decode_kernel(
     KParams P, const uint32_t* __restrict__ words, const uint64_t* __restrict__ offsets,
@@ -85,7 +67,8 @@ __global__ __launch_bounds__(1024) void decode_kernel(
   __shared__ int s_level_of_set[CG_MAX_LEVELS];
   __shared__ int s_nsets;
   uint16_t* fences = smem;                       // [64][kFenceStride]
-  uint16_t* tabs = smem + 64 * kFenceStride;     // [nsets][64][kTabStride]
+  uint16_t* obuf_all = smem + 64 * kFenceStride; // [nw][kRows][64] decoded rows per wave
+  uint16_t* tabs = obuf_all + nw * kRows * 64;   // [nsets][64][kTabStride]
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int nwaves = blockDim.x >> 6;
@@ -98,11 +81,11 @@ __global__ __launch_bounds__(1024) void decode_kernel(
   rest /= P.nblk;
   const int k = rest & 1, l = rest >> 1;
 
-  const int pair = grp * nw + wave;
+  const int pair = uni(grp * nw + wave);
   const bool active = pair < n_pairs;
-  const int b = active ? pair / ncr : 0;
-  const int c = active ? c_begin + pair % ncr : 0;
-  const int lv = active ? min((int)chunk_level[(int64_t)b * P.NC + c], P.NLV - 1) : 0;
+  const int b = uni(active ? pair / ncr : 0);
+  const int c = uni(active ? c_begin + pair % ncr : 0);
+  const int lv = uni(active ? min((int)chunk_level[(int64_t)b * P.NC + c], P.NLV - 1) : 0);
 
   if (threadIdx.x == 0) s_mask = 0u;
   __syncthreads();
@@ -130,6 +113,7 @@ __global__ __launch_bounds__(1024) void decode_kernel(
     if (lane == 63) v1 = (v1 & 0xFFFFu) | 0xFFFF0000u;  // entry 255: sentinel above any target
     dst[lane] = v0;
     dst[lane + 64] = v1;
+    if (lane < 2) dst[128 + lane] = 0xFFFFFFFFu;        // entries 256..259: sentinels
   }
   // ---- anchor fences cum[16 f] ----
   for (int idx = threadIdx.x; idx < 64 * 16; idx += blockDim.x) {
@@ -139,132 +123,223 @@ __global__ __launch_bounds__(1024) void decode_kernel(
   }
   __syncthreads();
 
+  if (!active) return;
   const int ch = cb * 64 + lane;
-  if (!active || ch >= P.C) return;
+  const bool valid = ch < P.C;     // lanes past the last channel only help write rows
+  const int chv = valid ? ch : cb * 64;
 
   const int64_t bclk = (((int64_t)b * P.NC + c) * P.L + l) * 2 + k;
-  const int64_t sidx = cg_stream(P, bclk, ch);
-  const int t0 = c * P.CL;
-  const int n = min(P.CL, P.T - t0);
+  const int64_t sidx = cg_stream(P, bclk, chv);
+  const int tok0 = c * P.CL;
+  const int n = uni(min(P.CL, P.T - tok0));
   const float s = scales[sidx];
   const float bw = P.layer_bin[l] * P.level_mult[lv];
   const float w = bw * s;
   const uint16_t* dtab = tabs + (s_set_of_level[lv] * 64 + lane) * kTabStride;
   const uint16_t* ftab = fences + lane * kFenceStride;
-  const uint16_t* gA = cdfA + ((int64_t)(l * 2 + k) * P.C + ch) * 256;
+  const uint16_t* gA = cdfA + ((int64_t)(l * 2 + k) * P.C + chv) * 256;
 
-  const uint64_t o0 = offsets[sidx], o1 = offsets[sidx + 1];
-  BitIn in;
-  in.p = words + o0;
-  in.end = words + (o1 > o0 ? o1 : o0);
-  uint32_t D = in.fetch();
-  in.buf = (uint64_t)in.fetch() << 32;
-  in.avail = 32;
-  in.w1 = in.fetch();
-  in.w2 = in.fetch();
+  const uint64_t total = offsets[P.S];
+  if (total == 0) return;  // no payload at all: nothing can be decoded (uniform)
+  // Bitstream reader state (plain locals so everything stays in registers). The lane consumes
+  // bits from `buf`; whole words move into it from the four-word shift register s0..s3 (always
+  // from s0). Every kEpoch tokens (the same tokens for the whole wave) the h words used since
+  // the last epoch are replaced by the next ones, requested one epoch earlier into t0..t3, and
+  // t0..t3 are requested again. A symbol takes at most 18 bits, so at most one word moves per
+  // token and the shift register never runs dry inside an epoch. Requests are unconditional
+  // loads (reading at most CG_TAIL_WORDS past the payload, which never affects a result), so
+  // every epoch issues the same memory operations and the wait for t0..t3 comes one epoch
+  // after the request instead of at once.
+  const uint64_t o0 = offsets[sidx];
+  const uint32_t* sbase = words + (o0 < total ? o0 : total);
+  uint32_t D = sbase[0];
+  uint64_t buf = (uint64_t)sbase[1] << 32;
+  uint32_t avail = 32;
+  uint32_t s0 = sbase[2], s1 = sbase[3], s2 = sbase[4], s3 = sbase[5];
+  uint32_t hcnt = 0;
+  uint64_t wpos = (o0 < total ? o0 : total) + 6;        // payload index of t0
+  const uint64_t wcap = total;                          // requests start at most here
+  const uint32_t* tq0 = words + (wpos < wcap ? wpos : wcap);
+  uint32_t t0 = tq0[0], t1 = tq0[1], t2 = tq0[2], t3 = tq0[3];
+  settle(D); settle(s0); settle(s1); settle(s2); settle(s3);
+  settle((uint32_t)(buf >> 32));
   uint32_t low = 0u, rm1 = 0xFFFFFFFFu;
 
-  uint16_t* row = out + cg_elem(P, b, l, k, t0, cb * 64);  // wave-uniform row pointer
+  uint16_t* row = out + cg_elem(P, b, l, k, tok0, cb * 64);  // wave-uniform row pointer
+  const int64_t rstride = P.C;
+  uint16_t* obuf = obuf_all + wave * kRows * 64;
+  int r = 0;
   float a = 0.0f;
   int g = 0;
+  int ep = 0;
   for (int j = 0; j < n; ++j) {
-    // 1. estimate of the target
-    const float fr = (float)rm1 + 1.0f;
-    const float fd = (float)D + 1.0f;
-    const float te = fd * (65536.0f * __builtin_amdgcn_rcpf(fr));
-    const uint32_t ti = min((uint32_t)te, 65535u);
-
-    int sym;
-    uint32_t clo, chi;
     const bool anchor = (g == 0);
-    if (anchor) {
-      // fences in LDS: largest f with cum[16 f] <= ti
-      int f = 0;
-      if ((uint32_t)ftab[f + 8] <= ti) f += 8;
-      if ((uint32_t)ftab[f + 4] <= ti) f += 4;
-      if ((uint32_t)ftab[f + 2] <= ti) f += 2;
-      if ((uint32_t)ftab[f + 1] <= ti) f += 1;
-      const uint4* blk = reinterpret_cast<const uint4*>(gA + 16 * f);
-      const uint4 q0 = blk[0], q1 = blk[1];
-      uint32_t v[16] = {q0.x & 0xFFFFu, q0.x >> 16, q0.y & 0xFFFFu, q0.y >> 16,
-                        q0.z & 0xFFFFu, q0.z >> 16, q0.w & 0xFFFFu, q0.w >> 16,
-                        q1.x & 0xFFFFu, q1.x >> 16, q1.y & 0xFFFFu, q1.y >> 16,
-                        q1.z & 0xFFFFu, q1.z >> 16, q1.w & 0xFFFFu, q1.w >> 16};
-      if (f == 15) v[15] = CG_TOTAL;   // symbol 255 does not exist: cum[255] is the implicit top
-      uint32_t lo_v = v[0];
-      uint32_t hi_v = (f == 15) ? CG_TOTAL : (uint32_t)ftab[f + 1];
-      int jj = 0;
-      {  // largest jj in [0, 15] with v[jj] <= ti; track v[jj] and the next value
-        uint32_t cand = v[8];
-        if (cand <= ti) { jj = 8; lo_v = cand; } else { hi_v = cand; }
-        cand = jj ? v[12] : v[4];
-        if (cand <= ti) { jj += 4; lo_v = cand; } else { hi_v = cand; }
-        cand = (jj & 8) ? ((jj & 4) ? v[14] : v[10]) : ((jj & 4) ? v[6] : v[2]);
-        if (cand <= ti) { jj += 2; lo_v = cand; } else { hi_v = cand; }
-        const uint32_t c8 = (jj & 8) ? ((jj & 4) ? ((jj & 2) ? v[15] : v[13]) : ((jj & 2) ? v[11] : v[9]))
-                                     : ((jj & 4) ? ((jj & 2) ? v[7] : v[5]) : ((jj & 2) ? v[3] : v[1]));
-        if (c8 <= ti) { jj += 1; lo_v = c8; } else { hi_v = c8; }
+    if (valid) {
+      if (ep == kEpoch) {
+        // s0..s(3-h) are still unread; positions 4-h..3 take t0..t(h-1)
+        const bool g1 = hcnt >= 1, g2 = hcnt >= 2, g3 = hcnt >= 3, g4 = hcnt >= 4;
+        const uint32_t n3 = g4 ? t3 : (g3 ? t2 : (g2 ? t1 : (g1 ? t0 : s3)));
+        const uint32_t n2 = g4 ? t2 : (g3 ? t1 : (g2 ? t0 : s2));
+        const uint32_t n1 = g4 ? t1 : (g3 ? t0 : s1);
+        const uint32_t n0 = g4 ? t0 : s0;
+        s0 = n0; s1 = n1; s2 = n2; s3 = n3;
+        wpos += hcnt;
+        hcnt = 0;
+        // keep the new requests after the slide: the old t registers are dead by then, so
+        // the loads can write them in place instead of through a copy that would wait
+        __builtin_amdgcn_sched_barrier(0);
+        const uint32_t* tq = words + (wpos < wcap ? wpos : wcap);
+        t0 = tq[0]; t1 = tq[1]; t2 = tq[2]; t3 = tq[3];
+        ep = 0;
       }
-      sym = 16 * f + jj;
-      clo = lo_v;
-      chi = hi_v;
-    } else {
-      // delta: fixed 8-step binary search in LDS for the largest i with cum[i] <= ti
-      const uint16_t* q = dtab;
-      if ((uint32_t)q[128] <= ti) q += 128;
-      if ((uint32_t)q[64] <= ti) q += 64;
-      if ((uint32_t)q[32] <= ti) q += 32;
-      if ((uint32_t)q[16] <= ti) q += 16;
-      if ((uint32_t)q[8] <= ti) q += 8;
-      if ((uint32_t)q[4] <= ti) q += 4;
-      if ((uint32_t)q[2] <= ti) q += 2;
-      if ((uint32_t)q[1] <= ti) q += 1;
-      sym = min((int)(q - dtab), CG_NSYM - 1);
-      clo = dtab[sym];
-      chi = sym == CG_NSYM - 1 ? CG_TOTAL : (uint32_t)dtab[sym + 1];
-    }
+      ++ep;
+      // 1. estimate of the target t = floor(((D + 1) * 2^16 - 1) / (rm1 + 1)); within one
+      const float te = (float)D * (65536.0f * __builtin_amdgcn_rcpf((float)rm1));
+      const uint32_t ti = min((uint32_t)te, 65534u);
 
-    // 2. exact check: (R*clo) >> 16 <= D <= (R*chi >> 16) - 1
-    uint32_t lo_off = (uint32_t)(((uint64_t)rm1 * clo + clo) >> 16);
-    uint32_t hm1 = (uint32_t)((((uint64_t)rm1 * chi + chi) >> 16) - 1ull);
-    if (D < lo_off || D > hm1) {
-      for (int guard = 0; guard < CG_NSYM; ++guard) {
-        sym = (D < lo_off) ? max(sym - 1, 0) : min(sym + 1, CG_NSYM - 1);
-        clo = anchor ? cum_glb(gA, sym) : cum_lds(dtab, sym);
-        chi = anchor ? cum_glb(gA, sym + 1) : cum_lds(dtab, sym + 1);
-        lo_off = (uint32_t)(((uint64_t)rm1 * clo + clo) >> 16);
-        hm1 = (uint32_t)((((uint64_t)rm1 * chi + chi) >> 16) - 1ull);
-        if (D >= lo_off && D <= hm1) break;
+      int sym;
+      uint32_t clo, chi;
+      if (anchor) {
+        // fences in LDS: largest f with cum[16 f] <= ti, then the block from global memory
+        int f = 0;
+        if ((uint32_t)ftab[f + 8] <= ti) f += 8;
+        if ((uint32_t)ftab[f + 4] <= ti) f += 4;
+        if ((uint32_t)ftab[f + 2] <= ti) f += 2;
+        if ((uint32_t)ftab[f + 1] <= ti) f += 1;
+        const uint4* blk = reinterpret_cast<const uint4*>(gA + 16 * f);
+        const uint4 q0 = blk[0], q1 = blk[1];
+        const uint32_t v0 = q0.x & 0xFFFFu, v1 = q0.x >> 16, v2 = q0.y & 0xFFFFu, v3 = q0.y >> 16;
+        const uint32_t v4 = q0.z & 0xFFFFu, v5 = q0.z >> 16, v6 = q0.w & 0xFFFFu, v7 = q0.w >> 16;
+        const uint32_t v8 = q1.x & 0xFFFFu, v9 = q1.x >> 16, v10 = q1.y & 0xFFFFu, v11 = q1.y >> 16;
+        const uint32_t v12 = q1.z & 0xFFFFu, v13 = q1.z >> 16, v14 = q1.w & 0xFFFFu;
+        const uint32_t v15 = f == 15 ? CG_TOTAL : q1.w >> 16;  // symbol 255 does not exist
+        const uint32_t v16 = f == 15 ? CG_TOTAL : (uint32_t)ftab[f + 1];
+        // largest j in [0, 15] with v_j <= ti (v_0 <= ti holds), by selects only
+        const bool c3 = v8 <= ti;
+        const uint32_t x2 = c3 ? v12 : v4;
+        const bool c2 = x2 <= ti;
+        const uint32_t x1 = c3 ? (c2 ? v14 : v10) : (c2 ? v6 : v2);
+        const bool c1 = x1 <= ti;
+        const uint32_t x0 = c3 ? (c2 ? (c1 ? v15 : v13) : (c1 ? v11 : v9))
+                               : (c2 ? (c1 ? v7 : v5) : (c1 ? v3 : v1));
+        const bool c0 = x0 <= ti;
+        const int jj = (c3 ? 8 : 0) + (c2 ? 4 : 0) + (c1 ? 2 : 0) + (c0 ? 1 : 0);
+        // v_jj and v_jj+1: the last probe at or below ti and the last one above it
+        uint32_t lo_v = v0, hi_v = v16;
+        lo_v = c3 ? v8 : lo_v;  hi_v = c3 ? hi_v : v8;
+        lo_v = c2 ? x2 : lo_v;  hi_v = c2 ? hi_v : x2;
+        lo_v = c1 ? x1 : lo_v;  hi_v = c1 ? hi_v : x1;
+        lo_v = c0 ? x0 : lo_v;  hi_v = c0 ? hi_v : x0;
+        sym = 16 * f + jj;
+        clo = lo_v;
+        chi = hi_v;
+      } else {
+        // delta: 4-ary search in LDS for the largest i with cum[i] <= ti (sorted table; three
+        // probes per level, the last level one aligned 8-byte read of cum[i .. i+3])
+        int i;
+        {
+          const uint32_t p1 = dtab[64], p2 = dtab[128], p3 = dtab[192];
+          i = 64 * ((p1 <= ti) + (p2 <= ti) + (p3 <= ti));
+        }
+        {
+          const uint16_t* q = dtab + i;
+          const uint32_t p1 = q[16], p2 = q[32], p3 = q[48];
+          i += 16 * ((p1 <= ti) + (p2 <= ti) + (p3 <= ti));
+        }
+        {
+          const uint16_t* q = dtab + i;
+          const uint32_t p1 = q[4], p2 = q[8], p3 = q[12];
+          i += 4 * ((p1 <= ti) + (p2 <= ti) + (p3 <= ti));
+        }
+        const uint2 quad = *reinterpret_cast<const uint2*>(dtab + i);   // cum[i .. i+3]
+        const uint32_t x0 = quad.x & 0xFFFFu, x1 = quad.x >> 16;
+        const uint32_t x2 = quad.y & 0xFFFFu, x3 = quad.y >> 16;
+        const uint32_t x4 = dtab[i + 4];
+        const bool b1 = x1 <= ti, b2 = x2 <= ti, b3 = x3 <= ti;
+        sym = i + (int)b1 + (int)b2 + (int)b3;
+        clo = b3 ? x3 : (b2 ? x2 : (b1 ? x1 : x0));
+        chi = b3 ? x4 : (b2 ? x3 : (b1 ? x2 : x1));
+        chi = sym == CG_NSYM - 1 ? CG_TOTAL : chi;
       }
-    }
 
-    // 3. interval update and one-step renormalisation
-    low += lo_off;
-    rm1 = hm1 - lo_off;
-    D -= lo_off;
-    const uint32_t high = low + rm1;
-    const uint32_t n1 = __clz(low ^ high);
-    const uint32_t L1 = low << n1, H1 = high << n1;
-    const uint32_t m = L1 & ~H1;
-    const uint32_t n3 = __clz(~(m << 1));
-    low = (L1 & 0x80000000u) | ((L1 << n3) & 0x7FFFFFFFu);
-    const uint32_t nsh = n1 + n3;
-    rm1 = (rm1 << nsh) | ((1u << nsh) - 1u);
-    D = (D << nsh) | in.take(nsh);
+      // 2. exact check: (R*clo) >> 16 <= D <= (R*chi >> 16) - 1; a miss means the estimate
+      //    fell on the other side of a boundary: walk to the neighbour until the check holds
+      uint32_t lo_off = scaled_off(rm1, clo);
+      uint32_t hm1 = scaled_off(rm1, chi) - 1u;
+      if (D < lo_off || D > hm1) {
+        for (int guard = 0; guard < CG_NSYM; ++guard) {
+          sym = (D < lo_off) ? max(sym - 1, 0) : min(sym + 1, CG_NSYM - 1);
+          clo = anchor ? (uint32_t)gA[sym] : (uint32_t)dtab[sym];
+          chi = sym + 1 >= CG_NSYM ? CG_TOTAL
+                                   : (anchor ? (uint32_t)gA[sym + 1] : (uint32_t)dtab[sym + 1]);
+          lo_off = scaled_off(rm1, clo);
+          hm1 = scaled_off(rm1, chi) - 1u;
+          if (D >= lo_off && D <= hm1) break;
+        }
+      }
 
-    // dequantize (step a7) and store
-    const int q = sym - 127;
-    float v;
-    if (anchor) {
-      a = (float)q * s;
-      v = a;
-    } else {
-      const float qw = (float)q * w;
-      v = a + qw;
+      // 3. interval update and one-step renormalisation
+      low += lo_off;
+      rm1 = hm1 - lo_off;
+      D -= lo_off;
+      const uint32_t high = low + rm1;
+      const uint32_t n1 = (uint32_t)__builtin_clz(low ^ high);   // low != high
+      const uint32_t L1 = low << n1, H1 = high << n1;
+      const uint32_t m = L1 & ~H1;
+      const uint32_t n3 = (uint32_t)__builtin_clz(~(m << 1));    // ~(m << 1) is odd
+      low = (L1 & 0x80000000u) | ((L1 << n3) & 0x7FFFFFFFu);
+      const uint32_t nsh = n1 + n3;
+      rm1 = (rm1 << nsh) | ((1u << nsh) - 1u);
+      const uint32_t bits = nsh ? (uint32_t)(buf >> (64 - nsh)) : 0u;
+      buf <<= nsh;
+      avail -= nsh;
+      if (avail < 32) {
+        buf |= (uint64_t)s0 << (32 - avail);
+        avail += 32;
+        s0 = s1; s1 = s2; s2 = s3;
+        ++hcnt;
+      }
+      D = (D << nsh) | bits;
+
+      // dequantize (step a7) into the wave's row buffer
+      const float qf = (float)(sym - 127);
+      float v;
+      if (anchor) {
+        a = qf * s;
+        v = a;
+      } else {
+        const float qw = qf * w;
+        v = a + qw;
+      }
+      obuf[r * 64 + lane] = cg_f2h(v);
     }
-    row[lane] = cg_f2h(v);
-    row += P.C;
     g = (g + 1 == P.G) ? 0 : g + 1;
+    if (++r == kRows || j + 1 == n) {
+      // write the staged rows: lane L stores 16 bytes (8 channels) of row L / 8
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      const int rr = lane >> 3, cc = (lane & 7) * 8;
+      if (rr < r && cb * 64 + cc < P.C) {
+        const uint4 vals = *reinterpret_cast<const uint4*>(obuf + rr * 64 + cc);
+        uint16_t* dst = row + rr * rstride + cc;
+        if (cb * 64 + cc + 8 <= P.C && (reinterpret_cast<uintptr_t>(dst) & 15) == 0) {
+          *reinterpret_cast<uint4*>(dst) = vals;
+        } else {
+          const uint16_t hv[8] = {(uint16_t)(vals.x & 0xFFFFu), (uint16_t)(vals.x >> 16),
+                                  (uint16_t)(vals.y & 0xFFFFu), (uint16_t)(vals.y >> 16),
+                                  (uint16_t)(vals.z & 0xFFFFu), (uint16_t)(vals.z >> 16),
+                                  (uint16_t)(vals.w & 0xFFFFu), (uint16_t)(vals.w >> 16)};
+          for (int e = 0; e < 8; ++e)
+            if (cb * 64 + cc + e < P.C) dst[e] = hv[e];
+        }
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      row += r * rstride;
+      r = 0;
+    }
   }
 }
 
@@ -279,7 +354,8 @@ hipError_t cg_launch_decode(const KParams& P, const uint32_t* words, const uint6
   const int nw = (int)(n_pairs < kMaxWaves ? n_pairs : kMaxWaves);
   const int64_t n_groups = (n_pairs + nw - 1) / nw;
   const int nsets_max = nw < P.NLV ? nw : P.NLV;
-  const size_t lds = (size_t)(64 * kFenceStride + nsets_max * 64 * kTabStride) * sizeof(uint16_t);
+  const size_t lds =
+      (size_t)(64 * kFenceStride + nw * kRows * 64 + nsets_max * 64 * kTabStride) * sizeof(uint16_t);
   hipError_t e = hipFuncSetAttribute((const void*)decode_kernel,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;

@@ -49,7 +49,9 @@ def run_gpu(w: W.Workload, kv_np: np.ndarray, decode_oracle_payload=None):
     if decode_oracle_payload is not None:
         ow, oo, osc, oca, ocd = decode_oracle_payload
         say(f"{w.name}: decode the oracle's payload")
-        tw = torch.from_numpy(np.ascontiguousarray(ow).view(np.int32)).cuda()
+        # the decoder may read CG_TAIL_WORDS (8) words past the payload: pad the exact-size array
+        padded = np.concatenate([np.asarray(ow, np.uint32), np.zeros(8, np.uint32)])
+        tw = torch.from_numpy(padded.view(np.int32)).cuda()
         to = torch.from_numpy(np.ascontiguousarray(oo).view(np.int64)).cuda()
         ts = torch.from_numpy(np.ascontiguousarray(osc)).cuda()
         tca = torch.from_numpy(np.ascontiguousarray(oca).view(np.int16)).cuda()
