@@ -56,6 +56,59 @@ __device__ __forceinline__ uint32_t scaled_off(uint32_t x, uint32_t c) {
 // Make the compiler wait here for a register produced by a load (once, outside the loop).
 __device__ __forceinline__ void settle(uint32_t v) { asm volatile("" ::"v"(v)); }
 
+// Last level of the delta search. q points at cum[i] (8-byte aligned) with cum[i] <= ti; the
+// symbol is i + c with c in [0, 3]. cum[i .. i+3] come in one 8-byte read (x = cum[i] |
+// cum[i+1] << 16, y = cum[i+2] | cum[i+3] << 16), cum[i+4] in a second. The count of entries
+// <= ti uses packed 16-bit math: (ti + 1) - cum saturates to zero exactly when cum > ti,
+// min(., 1) turns each half into 0 / 1 and a dot product with (1, 1) adds the halves; cum[i]
+// always counts, so c = count - 1. Returns c; `pair` = cum[i + c] | cum[i + c + 1] << 16.
+__device__ __forceinline__ uint32_t delta_leaf(const uint16_t* q, uint32_t ti, uint32_t& pair) {
+  const uint2 xy = *reinterpret_cast<const uint2*>(q);
+  const uint32_t x4 = q[4];
+  const uint32_t tt = (ti + 1u) * 0x00010001u;
+  const uint32_t one2 = 0x00010001u;
+  uint32_t ia, ib, c;
+  asm("v_pk_sub_u16 %0, %1, %2 clamp" : "=v"(ia) : "v"(tt), "v"(xy.x));
+  asm("v_pk_sub_u16 %0, %1, %2 clamp" : "=v"(ib) : "v"(tt), "v"(xy.y));
+  asm("v_pk_min_u16 %0, %1, %2" : "=v"(ia) : "v"(ia), "v"(one2));
+  asm("v_pk_min_u16 %0, %1, %2" : "=v"(ib) : "v"(ib), "v"(one2));
+  asm("v_dot2_u32_u16 %0, %1, %2, %3" : "=v"(c) : "v"(ia), "v"(one2), "v"(0xFFFFFFFFu));
+  asm("v_dot2_u32_u16 %0, %1, %2, %3" : "=v"(c) : "v"(ib), "v"(one2), "v"(c));
+  // (cum[i + c], cum[i + c + 1]) is the 32-bit window at 16 c bits of x : y : x4
+  const uint32_t hi2 = (c & 2u) ? x4 : xy.y;
+  const uint32_t lo2 = (c & 2u) ? xy.y : xy.x;
+  pair = __builtin_amdgcn_alignbit(hi2, lo2, (c & 1u) << 4);
+  return c;
+}
+
+// Largest j in [0, 15] with v[j] <= ti, for sorted v[0..16] with v[0] <= ti < v[16]; lo = v[j],
+// hi = v[j + 1]. A binary search by selects on registers: each decision also picks the
+// candidates of the later levels, so the chain is four compare / select steps.
+__device__ __forceinline__ uint32_t select16(const uint32_t (&v)[17], uint32_t ti, uint32_t& lo,
+                                             uint32_t& hi) {
+  const bool c3 = v[8] <= ti;
+  const uint32_t p4 = c3 ? v[12] : v[4];
+  const uint32_t p2a = c3 ? v[10] : v[2], p2b = c3 ? v[14] : v[6];
+  const uint32_t p1a = c3 ? v[9] : v[1], p1b = c3 ? v[11] : v[3];
+  const uint32_t p1c = c3 ? v[13] : v[5], p1d = c3 ? v[15] : v[7];
+  uint32_t l = c3 ? v[8] : v[0], h = c3 ? v[16] : v[8];
+  const bool c2 = p4 <= ti;
+  const uint32_t p2 = c2 ? p2b : p2a;
+  const uint32_t p1e = c2 ? p1c : p1a, p1f = c2 ? p1d : p1b;
+  l = c2 ? p4 : l;
+  h = c2 ? h : p4;
+  const bool c1 = p2 <= ti;
+  const uint32_t p1 = c1 ? p1f : p1e;
+  l = c1 ? p2 : l;
+  h = c1 ? h : p2;
+  const bool c0 = p1 <= ti;
+  l = c0 ? p1 : l;
+  h = c0 ? h : p1;
+  lo = l;
+  hi = h;
+  return (c3 ? 8u : 0u) | (c2 ? 4u : 0u) | (c1 ? 2u : 0u) | (c0 ? 1u : 0u);
+}
+
 __global__ __launch_bounds__(1024) void decode_kernel(
     KParams P, const uint32_t* __restrict__ words, const uint64_t* __restrict__ offsets,
     const float* __restrict__ scales, const uint8_t* __restrict__ chunk_level,
@@ -125,8 +178,11 @@ __global__ __launch_bounds__(1024) void decode_kernel(
 
   if (!active) return;
   const int ch = cb * 64 + lane;
-  const bool valid = ch < P.C;     // lanes past the last channel only help write rows
-  const int chv = valid ? ch : cb * 64;
+  const bool valid = ch < P.C;
+  // Lanes past the last channel (only when C is not a multiple of 64) decode a copy of the
+  // block's first channel, so the whole wave runs the same code; their rows are never stored.
+  const int lsrc = valid ? lane : 0;
+  const int chv = cb * 64 + lsrc;
 
   const int64_t bclk = (((int64_t)b * P.NC + c) * P.L + l) * 2 + k;
   const int64_t sidx = cg_stream(P, bclk, chv);
@@ -135,8 +191,8 @@ __global__ __launch_bounds__(1024) void decode_kernel(
   const float s = scales[sidx];
   const float bw = P.layer_bin[l] * P.level_mult[lv];
   const float w = bw * s;
-  const uint16_t* dtab = tabs + (s_set_of_level[lv] * 64 + lane) * kTabStride;
-  const uint16_t* ftab = fences + lane * kFenceStride;
+  const uint16_t* dtab = tabs + (s_set_of_level[lv] * 64 + lsrc) * kTabStride;
+  const uint16_t* ftab = fences + lsrc * kFenceStride;
   const uint16_t* gA = cdfA + ((int64_t)(l * 2 + k) * P.C + chv) * 256;
 
   const uint64_t total = offsets[P.S];
@@ -171,148 +227,133 @@ __global__ __launch_bounds__(1024) void decode_kernel(
   int r = 0;
   float a = 0.0f;
   int g = 0;
-  int ep = 0;
   for (int j = 0; j < n; ++j) {
-    const bool anchor = (g == 0);
-    if (valid) {
-      if (ep == kEpoch) {
-        // s0..s(3-h) are still unread; positions 4-h..3 take t0..t(h-1)
-        const bool g1 = hcnt >= 1, g2 = hcnt >= 2, g3 = hcnt >= 3, g4 = hcnt >= 4;
-        const uint32_t n3 = g4 ? t3 : (g3 ? t2 : (g2 ? t1 : (g1 ? t0 : s3)));
-        const uint32_t n2 = g4 ? t2 : (g3 ? t1 : (g2 ? t0 : s2));
-        const uint32_t n1 = g4 ? t1 : (g3 ? t0 : s1);
-        const uint32_t n0 = g4 ? t0 : s0;
-        s0 = n0; s1 = n1; s2 = n2; s3 = n3;
-        wpos += hcnt;
-        hcnt = 0;
-        // keep the new requests after the slide: the old t registers are dead by then, so
-        // the loads can write them in place instead of through a copy that would wait
-        __builtin_amdgcn_sched_barrier(0);
-        const uint32_t* tq = words + (wpos < wcap ? wpos : wcap);
-        t0 = tq[0]; t1 = tq[1]; t2 = tq[2]; t3 = tq[3];
-        ep = 0;
-      }
-      ++ep;
-      // 1. estimate of the target t = floor(((D + 1) * 2^16 - 1) / (rm1 + 1)); within one
-      const float te = (float)D * (65536.0f * __builtin_amdgcn_rcpf((float)rm1));
-      const uint32_t ti = min((uint32_t)te, 65534u);
-
-      int sym;
-      uint32_t clo, chi;
-      if (anchor) {
-        // fences in LDS: largest f with cum[16 f] <= ti, then the block from global memory
-        int f = 0;
-        if ((uint32_t)ftab[f + 8] <= ti) f += 8;
-        if ((uint32_t)ftab[f + 4] <= ti) f += 4;
-        if ((uint32_t)ftab[f + 2] <= ti) f += 2;
-        if ((uint32_t)ftab[f + 1] <= ti) f += 1;
-        const uint4* blk = reinterpret_cast<const uint4*>(gA + 16 * f);
-        const uint4 q0 = blk[0], q1 = blk[1];
-        const uint32_t v0 = q0.x & 0xFFFFu, v1 = q0.x >> 16, v2 = q0.y & 0xFFFFu, v3 = q0.y >> 16;
-        const uint32_t v4 = q0.z & 0xFFFFu, v5 = q0.z >> 16, v6 = q0.w & 0xFFFFu, v7 = q0.w >> 16;
-        const uint32_t v8 = q1.x & 0xFFFFu, v9 = q1.x >> 16, v10 = q1.y & 0xFFFFu, v11 = q1.y >> 16;
-        const uint32_t v12 = q1.z & 0xFFFFu, v13 = q1.z >> 16, v14 = q1.w & 0xFFFFu;
-        const uint32_t v15 = f == 15 ? CG_TOTAL : q1.w >> 16;  // symbol 255 does not exist
-        const uint32_t v16 = f == 15 ? CG_TOTAL : (uint32_t)ftab[f + 1];
-        // largest j in [0, 15] with v_j <= ti (v_0 <= ti holds), by selects only
-        const bool c3 = v8 <= ti;
-        const uint32_t x2 = c3 ? v12 : v4;
-        const bool c2 = x2 <= ti;
-        const uint32_t x1 = c3 ? (c2 ? v14 : v10) : (c2 ? v6 : v2);
-        const bool c1 = x1 <= ti;
-        const uint32_t x0 = c3 ? (c2 ? (c1 ? v15 : v13) : (c1 ? v11 : v9))
-                               : (c2 ? (c1 ? v7 : v5) : (c1 ? v3 : v1));
-        const bool c0 = x0 <= ti;
-        const int jj = (c3 ? 8 : 0) + (c2 ? 4 : 0) + (c1 ? 2 : 0) + (c0 ? 1 : 0);
-        // v_jj and v_jj+1: the last probe at or below ti and the last one above it
-        uint32_t lo_v = v0, hi_v = v16;
-        lo_v = c3 ? v8 : lo_v;  hi_v = c3 ? hi_v : v8;
-        lo_v = c2 ? x2 : lo_v;  hi_v = c2 ? hi_v : x2;
-        lo_v = c1 ? x1 : lo_v;  hi_v = c1 ? hi_v : x1;
-        lo_v = c0 ? x0 : lo_v;  hi_v = c0 ? hi_v : x0;
-        sym = 16 * f + jj;
-        clo = lo_v;
-        chi = hi_v;
-      } else {
-        // delta: 4-ary search in LDS for the largest i with cum[i] <= ti (sorted table; three
-        // probes per level, the last level one aligned 8-byte read of cum[i .. i+3])
-        int i;
-        {
-          const uint32_t p1 = dtab[64], p2 = dtab[128], p3 = dtab[192];
-          i = 64 * ((p1 <= ti) + (p2 <= ti) + (p3 <= ti));
-        }
-        {
-          const uint16_t* q = dtab + i;
-          const uint32_t p1 = q[16], p2 = q[32], p3 = q[48];
-          i += 16 * ((p1 <= ti) + (p2 <= ti) + (p3 <= ti));
-        }
-        {
-          const uint16_t* q = dtab + i;
-          const uint32_t p1 = q[4], p2 = q[8], p3 = q[12];
-          i += 4 * ((p1 <= ti) + (p2 <= ti) + (p3 <= ti));
-        }
-        const uint2 quad = *reinterpret_cast<const uint2*>(dtab + i);   // cum[i .. i+3]
-        const uint32_t x0 = quad.x & 0xFFFFu, x1 = quad.x >> 16;
-        const uint32_t x2 = quad.y & 0xFFFFu, x3 = quad.y >> 16;
-        const uint32_t x4 = dtab[i + 4];
-        const bool b1 = x1 <= ti, b2 = x2 <= ti, b3 = x3 <= ti;
-        sym = i + (int)b1 + (int)b2 + (int)b3;
-        clo = b3 ? x3 : (b2 ? x2 : (b1 ? x1 : x0));
-        chi = b3 ? x4 : (b2 ? x3 : (b1 ? x2 : x1));
-        chi = sym == CG_NSYM - 1 ? CG_TOTAL : chi;
-      }
-
-      // 2. exact check: (R*clo) >> 16 <= D <= (R*chi >> 16) - 1; a miss means the estimate
-      //    fell on the other side of a boundary: walk to the neighbour until the check holds
-      uint32_t lo_off = scaled_off(rm1, clo);
-      uint32_t hm1 = scaled_off(rm1, chi) - 1u;
-      if (D < lo_off || D > hm1) {
-        for (int guard = 0; guard < CG_NSYM; ++guard) {
-          sym = (D < lo_off) ? max(sym - 1, 0) : min(sym + 1, CG_NSYM - 1);
-          clo = anchor ? (uint32_t)gA[sym] : (uint32_t)dtab[sym];
-          chi = sym + 1 >= CG_NSYM ? CG_TOTAL
-                                   : (anchor ? (uint32_t)gA[sym + 1] : (uint32_t)dtab[sym + 1]);
-          lo_off = scaled_off(rm1, clo);
-          hm1 = scaled_off(rm1, chi) - 1u;
-          if (D >= lo_off && D <= hm1) break;
-        }
-      }
-
-      // 3. interval update and one-step renormalisation
-      low += lo_off;
-      rm1 = hm1 - lo_off;
-      D -= lo_off;
-      const uint32_t high = low + rm1;
-      const uint32_t n1 = (uint32_t)__builtin_clz(low ^ high);   // low != high
-      const uint32_t L1 = low << n1, H1 = high << n1;
-      const uint32_t m = L1 & ~H1;
-      const uint32_t n3 = (uint32_t)__builtin_clz(~(m << 1));    // ~(m << 1) is odd
-      low = (L1 & 0x80000000u) | ((L1 << n3) & 0x7FFFFFFFu);
-      const uint32_t nsh = n1 + n3;
-      rm1 = (rm1 << nsh) | ((1u << nsh) - 1u);
-      const uint32_t bits = nsh ? (uint32_t)(buf >> (64 - nsh)) : 0u;
-      buf <<= nsh;
-      avail -= nsh;
-      if (avail < 32) {
-        buf |= (uint64_t)s0 << (32 - avail);
-        avail += 32;
-        s0 = s1; s1 = s2; s2 = s3;
-        ++hcnt;
-      }
-      D = (D << nsh) | bits;
-
-      // dequantize (step a7) into the wave's row buffer
-      const float qf = (float)(sym - 127);
-      float v;
-      if (anchor) {
-        a = qf * s;
-        v = a;
-      } else {
-        const float qw = qf * w;
-        v = a + qw;
-      }
-      obuf[r * 64 + lane] = cg_f2h(v);
+    if ((j & (kEpoch - 1)) == 0 && j != 0) {
+      // s0..s(3-h) are still unread; positions 4-h..3 take t0..t(h-1)
+      const bool g1 = hcnt >= 1, g2 = hcnt >= 2, g3 = hcnt >= 3, g4 = hcnt >= 4;
+      const uint32_t n3 = g4 ? t3 : (g3 ? t2 : (g2 ? t1 : (g1 ? t0 : s3)));
+      const uint32_t n2 = g4 ? t2 : (g3 ? t1 : (g2 ? t0 : s2));
+      const uint32_t n1 = g4 ? t1 : (g3 ? t0 : s1);
+      const uint32_t n0 = g4 ? t0 : s0;
+      s0 = n0; s1 = n1; s2 = n2; s3 = n3;
+      wpos += hcnt;
+      hcnt = 0;
+      // keep the new requests after the slide: the old t registers are dead by then, so
+      // the loads can write them in place instead of through a copy that would wait
+      __builtin_amdgcn_sched_barrier(0);
+      const uint32_t* tq = words + (wpos < wcap ? wpos : wcap);
+      t0 = tq[0]; t1 = tq[1]; t2 = tq[2]; t3 = tq[3];
     }
+    // 1. estimate of the target t = floor(((D + 1) * 2^16 - 1) / (rm1 + 1)); within one
+    const float te = (float)D * (65536.0f * __builtin_amdgcn_rcpf((float)rm1));
+    const uint32_t ti = min((uint32_t)te, 65534u);
+    const uint32_t kneg = ~ti;   // p + kneg has its top bit set exactly when p <= ti
+
+    int sym;
+    uint32_t clo, chi;
+    const bool anchor = (g == 0);
+    if (anchor) {
+      // fences in LDS: largest f with cum[16 f] <= ti, then the block from global memory
+      int f = 0;
+      if ((uint32_t)ftab[f + 8] <= ti) f += 8;
+      if ((uint32_t)ftab[f + 4] <= ti) f += 4;
+      if ((uint32_t)ftab[f + 2] <= ti) f += 2;
+      if ((uint32_t)ftab[f + 1] <= ti) f += 1;
+      const uint4* blk = reinterpret_cast<const uint4*>(gA + 16 * f);
+      const uint4 q0 = blk[0], q1 = blk[1];
+      const uint32_t v0 = q0.x & 0xFFFFu, v1 = q0.x >> 16, v2 = q0.y & 0xFFFFu, v3 = q0.y >> 16;
+      const uint32_t v4 = q0.z & 0xFFFFu, v5 = q0.z >> 16, v6 = q0.w & 0xFFFFu, v7 = q0.w >> 16;
+      const uint32_t v8 = q1.x & 0xFFFFu, v9 = q1.x >> 16, v10 = q1.y & 0xFFFFu, v11 = q1.y >> 16;
+      const uint32_t v12 = q1.z & 0xFFFFu, v13 = q1.z >> 16, v14 = q1.w & 0xFFFFu;
+      const uint32_t v15 = f == 15 ? CG_TOTAL : q1.w >> 16;  // symbol 255 does not exist
+      const uint32_t v16 = f == 15 ? CG_TOTAL : (uint32_t)ftab[f + 1];
+      // largest j in [0, 15] with v_j <= ti (v_0 <= ti holds), by selects only
+      const bool c3 = v8 <= ti;
+      const uint32_t x2 = c3 ? v12 : v4;
+      const bool c2 = x2 <= ti;
+      const uint32_t x1 = c3 ? (c2 ? v14 : v10) : (c2 ? v6 : v2);
+      const bool c1 = x1 <= ti;
+      const uint32_t x0 = c3 ? (c2 ? (c1 ? v15 : v13) : (c1 ? v11 : v9))
+                             : (c2 ? (c1 ? v7 : v5) : (c1 ? v3 : v1));
+      const bool c0 = x0 <= ti;
+      const int jj = (c3 ? 8 : 0) + (c2 ? 4 : 0) + (c1 ? 2 : 0) + (c0 ? 1 : 0);
+      // v_jj and v_jj+1: the last probe at or below ti and the last one above it
+      uint32_t lo_v = v0, hi_v = v16;
+      lo_v = c3 ? v8 : lo_v;  hi_v = c3 ? hi_v : v8;
+      lo_v = c2 ? x2 : lo_v;  hi_v = c2 ? hi_v : x2;
+      lo_v = c1 ? x1 : lo_v;  hi_v = c1 ? hi_v : x1;
+      lo_v = c0 ? x0 : lo_v;  hi_v = c0 ? hi_v : x0;
+      sym = 16 * f + jj;
+      clo = lo_v;
+      chi = hi_v;
+    } else {
+      // delta: 4-ary search in LDS for the largest i with cum[i] <= ti (sorted table; three
+      // probes per level counted by sign bits, the last level one aligned 8-byte read)
+      const uint16_t* q = dtab;
+      q += 64 * ((((uint32_t)q[64] + kneg) >> 31) + (((uint32_t)q[128] + kneg) >> 31) +
+                 (((uint32_t)q[192] + kneg) >> 31));
+      q += 16 * ((((uint32_t)q[16] + kneg) >> 31) + (((uint32_t)q[32] + kneg) >> 31) +
+                 (((uint32_t)q[48] + kneg) >> 31));
+      q += 4 * ((((uint32_t)q[4] + kneg) >> 31) + (((uint32_t)q[8] + kneg) >> 31) +
+                (((uint32_t)q[12] + kneg) >> 31));
+      uint32_t pr;
+      const uint32_t cc = delta_leaf(q, ti, pr);
+      sym = (int)((((uint32_t)(uintptr_t)q - (uint32_t)(uintptr_t)dtab) >> 1) + cc);
+      clo = pr & 0xFFFFu;
+      chi = sym == CG_NSYM - 1 ? CG_TOTAL : pr >> 16;
+    }
+
+    // 2. exact check: (R*clo) >> 16 <= D <= (R*chi >> 16) - 1; a miss means the estimate
+    //    fell on the other side of a boundary: walk to the neighbour until the check holds
+    uint32_t lo_off = scaled_off(rm1, clo);
+    uint32_t hm1 = scaled_off(rm1, chi) - 1u;
+    if (D < lo_off || D > hm1) {
+      for (int guard = 0; guard < CG_NSYM; ++guard) {
+        sym = (D < lo_off) ? max(sym - 1, 0) : min(sym + 1, CG_NSYM - 1);
+        clo = anchor ? (uint32_t)gA[sym] : (uint32_t)dtab[sym];
+        chi = sym + 1 >= CG_NSYM ? CG_TOTAL
+                                 : (anchor ? (uint32_t)gA[sym + 1] : (uint32_t)dtab[sym + 1]);
+        lo_off = scaled_off(rm1, clo);
+        hm1 = scaled_off(rm1, chi) - 1u;
+        if (D >= lo_off && D <= hm1) break;
+      }
+    }
+
+    // 3. interval update and one-step renormalisation
+    low += lo_off;
+    rm1 = hm1 - lo_off;
+    D -= lo_off;
+    const uint32_t high = low + rm1;
+    const uint32_t n1 = (uint32_t)__builtin_clz(low ^ high);   // low != high
+    const uint32_t L1 = low << n1, H1 = high << n1;
+    const uint32_t m = L1 & ~H1;
+    const uint32_t n3 = (uint32_t)__builtin_clz(~(m << 1));    // ~(m << 1) is odd
+    low = (L1 & 0x80000000u) | ((L1 << n3) & 0x7FFFFFFFu);
+    const uint32_t nsh = n1 + n3;
+    rm1 = (rm1 << nsh) | ((1u << nsh) - 1u);
+    // D takes the next nsh bits: a funnel shift of (D : top word of buf); nsh = 0 keeps D
+    const uint32_t dsh = __builtin_amdgcn_alignbit(D, (uint32_t)(buf >> 32), 32u - nsh);
+    D = nsh ? dsh : D;
+    buf <<= nsh;
+    avail -= nsh;
+    if (avail < 32) {
+      buf |= (uint64_t)s0 << (32 - avail);
+      avail += 32;
+      s0 = s1; s1 = s2; s2 = s3;
+      ++hcnt;
+    }
+
+    // dequantize (step a7) into the wave's row buffer
+    const float qf = (float)(sym - 127);
+    float v;
+    if (anchor) {
+      a = qf * s;
+      v = a;
+    } else {
+      const float qw = qf * w;
+      v = a + qw;
+    }
+    obuf[r * 64 + lane] = cg_f2h(v);
     g = (g + 1 == P.G) ? 0 : g + 1;
     if (++r == kRows || j + 1 == n) {
       // write the staged rows: lane L stores 16 bytes (8 channels) of row L / 8
@@ -343,6 +384,326 @@ __global__ __launch_bounds__(1024) void decode_kernel(
   }
 }
 
+
+// ---- group size 10: the schedule of a group is fixed at compile time -------------------------
+// Same decoder, same results, for the paper's group of 10 tokens (one anchor, nine deltas):
+//   * the anchor / delta choice, the row of the staging buffer and the bitstream epochs are
+//     compile-time per token, so no per-token bookkeeping is left;
+//   * the 15 fences cum[16 f] of the lane's anchor and delta tables sit in registers, so both
+//     searches start with a 4-step select search (no memory round trip); the delta search then
+//     needs two LDS round trips (one 4-ary level, the leaf), the anchor search one global block;
+//   * epoch boundaries come after tokens 0, 3 and 6 of each group: the requests issued after
+//     token 6 are four tokens old when the next anchor waits for its block (a wait for the
+//     youngest global load also waits for every older one), and the staged rows of a group
+//     are stored after token 9.
+constexpr int kG10 = 10;
+
+// Per-lane decoder state of the group-of-10 kernel (plain scalars: it lives in registers).
+struct G10Lane {
+  uint32_t D, low, rm1;          // code value - low, low, high - low
+  uint64_t buf;                  // bit buffer, `avail` valid bits from the top
+  uint32_t avail;
+  uint32_t s0, s1, s2, s3;       // shift register of unread words
+  uint32_t t0, t1, t2, t3;       // the next four words, requested one epoch ahead
+  uint32_t hcnt;                 // words moved from s0 into buf since the last epoch
+  uint64_t wpos;                 // payload index of t0
+  float a;                       // dequantized anchor of the current group
+};
+
+// Epoch boundary: drop the hcnt words used since the last boundary from the shift register,
+// append as many requested words, and request the next four.
+__device__ __forceinline__ void g10_epoch(G10Lane& st, const uint32_t* __restrict__ words,
+                                          uint64_t wcap) {
+  const uint32_t h = st.hcnt;
+  // register copies behind an empty asm: selects between the fields themselves could be
+  // turned into a select of their addresses, which would move the state to scratch memory
+  uint32_t t0 = st.t0, t1 = st.t1, t2 = st.t2, t3 = st.t3;
+  uint32_t s0 = st.s0, s1 = st.s1, s2 = st.s2, s3 = st.s3;
+  asm("" : "+v"(t0), "+v"(t1), "+v"(t2), "+v"(t3), "+v"(s0), "+v"(s1), "+v"(s2), "+v"(s3));
+  const bool g1 = h >= 1, g2 = h >= 2, g3 = h >= 3, g4 = h >= 4;
+  const uint32_t n3 = g4 ? t3 : (g3 ? t2 : (g2 ? t1 : (g1 ? t0 : s3)));
+  const uint32_t n2 = g4 ? t2 : (g3 ? t1 : (g2 ? t0 : s2));
+  const uint32_t n1 = g4 ? t1 : (g3 ? t0 : s1);
+  const uint32_t n0 = g4 ? t0 : s0;
+  st.s0 = n0;
+  st.s1 = n1;
+  st.s2 = n2;
+  st.s3 = n3;
+  st.wpos += h;
+  st.hcnt = 0;
+  __builtin_amdgcn_sched_barrier(0);
+  const uint32_t* tq = words + (st.wpos < wcap ? st.wpos : wcap);
+  st.t0 = tq[0];
+  st.t1 = tq[1];
+  st.t2 = tq[2];
+  st.t3 = tq[3];
+}
+
+// One token: decode the symbol at row r of the group (the anchor when kAnchor) and stage its
+// fp16 value in the wave's row buffer.
+template <bool kAnchor>
+__device__ __forceinline__ void g10_token(G10Lane& st, const uint32_t (&fA)[17],
+                                          const uint32_t (&fD)[17], const uint16_t* dtab,
+                                          const uint16_t* __restrict__ gA, float s, float w,
+                                          uint16_t* obuf, int r, int lane) {
+  const float te = (float)st.D * (65536.0f * __builtin_amdgcn_rcpf((float)st.rm1));
+  const uint32_t ti = min((uint32_t)te, 65534u);
+  const uint32_t kneg = ~ti;
+  int sym;
+  uint32_t clo, chi;
+  if constexpr (kAnchor) {
+    uint32_t flo, fhi;
+    const uint32_t f = select16(fA, ti, flo, fhi);
+    const uint4* blk = reinterpret_cast<const uint4*>(gA + 16 * f);
+    const uint4 q0 = blk[0], q1 = blk[1];
+    uint32_t v[17];
+    v[0] = q0.x & 0xFFFFu;  v[1] = q0.x >> 16;  v[2] = q0.y & 0xFFFFu;  v[3] = q0.y >> 16;
+    v[4] = q0.z & 0xFFFFu;  v[5] = q0.z >> 16;  v[6] = q0.w & 0xFFFFu;  v[7] = q0.w >> 16;
+    v[8] = q1.x & 0xFFFFu;  v[9] = q1.x >> 16;  v[10] = q1.y & 0xFFFFu; v[11] = q1.y >> 16;
+    v[12] = q1.z & 0xFFFFu; v[13] = q1.z >> 16; v[14] = q1.w & 0xFFFFu;
+    v[15] = f == 15 ? CG_TOTAL : q1.w >> 16;   // symbol 255 does not exist
+    v[16] = fhi;
+    const uint32_t jj = select16(v, ti, clo, chi);
+    sym = (int)(16 * f + jj);
+  } else {
+    uint32_t flo, fhi;
+    const uint32_t f = select16(fD, ti, flo, fhi);
+    const uint16_t* q = dtab + 16 * f;
+    q += 4 * ((((uint32_t)q[4] + kneg) >> 31) + (((uint32_t)q[8] + kneg) >> 31) +
+              (((uint32_t)q[12] + kneg) >> 31));
+    uint32_t pr;
+    const uint32_t cc = delta_leaf(q, ti, pr);
+    sym = (int)((((uint32_t)(uintptr_t)q - (uint32_t)(uintptr_t)dtab) >> 1) + cc);
+    clo = pr & 0xFFFFu;
+    chi = sym == CG_NSYM - 1 ? CG_TOTAL : pr >> 16;
+  }
+  const uint32_t D = st.D, rm1 = st.rm1;
+  uint32_t lo_off = scaled_off(rm1, clo);
+  uint32_t hm1 = scaled_off(rm1, chi) - 1u;
+  if (D < lo_off || D > hm1) {
+    for (int guard = 0; guard < CG_NSYM; ++guard) {
+      sym = (D < lo_off) ? max(sym - 1, 0) : min(sym + 1, CG_NSYM - 1);
+      clo = kAnchor ? (uint32_t)gA[sym] : (uint32_t)dtab[sym];
+      chi = sym + 1 >= CG_NSYM ? CG_TOTAL
+                               : (kAnchor ? (uint32_t)gA[sym + 1] : (uint32_t)dtab[sym + 1]);
+      lo_off = scaled_off(rm1, clo);
+      hm1 = scaled_off(rm1, chi) - 1u;
+      if (D >= lo_off && D <= hm1) break;
+    }
+  }
+  uint32_t low = st.low + lo_off;
+  uint32_t r1 = hm1 - lo_off;
+  uint32_t d = D - lo_off;
+  const uint32_t high = low + r1;
+  const uint32_t n1 = (uint32_t)__builtin_clz(low ^ high);
+  const uint32_t L1 = low << n1, H1 = high << n1;
+  const uint32_t m = L1 & ~H1;
+  const uint32_t n3 = (uint32_t)__builtin_clz(~(m << 1));
+  st.low = (L1 & 0x80000000u) | ((L1 << n3) & 0x7FFFFFFFu);
+  const uint32_t nsh = n1 + n3;
+  st.rm1 = (r1 << nsh) | ((1u << nsh) - 1u);
+  const uint32_t dsh = __builtin_amdgcn_alignbit(d, (uint32_t)(st.buf >> 32), 32u - nsh);
+  st.D = nsh ? dsh : d;
+  st.buf <<= nsh;
+  st.avail -= nsh;
+  if (st.avail < 32) {
+    st.buf |= (uint64_t)st.s0 << (32 - st.avail);
+    st.avail += 32;
+    st.s0 = st.s1;
+    st.s1 = st.s2;
+    st.s2 = st.s3;
+    ++st.hcnt;
+  }
+  const float qf = (float)(sym - 127);
+  float v;
+  if constexpr (kAnchor) {
+    st.a = qf * s;
+    v = st.a;
+  } else {
+    v = st.a + qf * w;
+  }
+  obuf[r * 64 + lane] = cg_f2h(v);
+}
+
+// Store rows 0 .. rows-1 of the staged group: lane L stores 16 bytes (8 channels) of row L / 8,
+// then lanes 0..15 rows 8 and 9.
+__device__ __forceinline__ void g10_flush(const uint16_t* obuf, uint16_t* row, int64_t rstride,
+                                          int rows, int lane, int cbase, int C) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+  for (int part = 0; part < 2; ++part) {
+    const int rr = part * 8 + (lane >> 3), cc = (lane & 7) * 8;
+    if (rr < rows && cbase + cc < C) {
+      const uint4 vals = *reinterpret_cast<const uint4*>(obuf + rr * 64 + cc);
+      uint16_t* dst = row + rr * rstride + cc;
+      if (cbase + cc + 8 <= C && (reinterpret_cast<uintptr_t>(dst) & 15) == 0) {
+        *reinterpret_cast<uint4*>(dst) = vals;
+      } else {
+        const uint16_t hv[8] = {(uint16_t)(vals.x & 0xFFFFu), (uint16_t)(vals.x >> 16),
+                                (uint16_t)(vals.y & 0xFFFFu), (uint16_t)(vals.y >> 16),
+                                (uint16_t)(vals.z & 0xFFFFu), (uint16_t)(vals.z >> 16),
+                                (uint16_t)(vals.w & 0xFFFFu), (uint16_t)(vals.w >> 16)};
+        for (int e = 0; e < 8; ++e)
+          if (cbase + cc + e < C) dst[e] = hv[e];
+      }
+    }
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__global__ __launch_bounds__(1024) void decode_g10_kernel(
+    KParams P, const uint32_t* __restrict__ words, const uint64_t* __restrict__ offsets,
+    const float* __restrict__ scales, const uint8_t* __restrict__ chunk_level,
+    const uint16_t* __restrict__ cdfA, const uint16_t* __restrict__ cdfD, int c_begin,
+    int c_end, int nw, uint16_t* __restrict__ out) {
+  extern __shared__ uint16_t smem[];
+  __shared__ uint32_t s_mask;
+  __shared__ int s_set_of_level[CG_MAX_LEVELS];
+  __shared__ int s_level_of_set[CG_MAX_LEVELS];
+  __shared__ int s_nsets;
+  uint16_t* obuf_all = smem;                      // [nw][kG10][64] decoded rows per wave
+  uint16_t* tabs = obuf_all + nw * kG10 * 64;     // [nsets][64][kTabStride]
+
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int nwaves = blockDim.x >> 6;
+  const int ncr = c_end - c_begin;
+  const int n_pairs = P.B * ncr;
+  const int n_groups = (n_pairs + nw - 1) / nw;
+  const int grp = blockIdx.x % n_groups;
+  int rest = blockIdx.x / n_groups;
+  const int cb = rest % P.nblk;
+  rest /= P.nblk;
+  const int k = rest & 1, l = rest >> 1;
+
+  const int pair = uni(grp * nw + wave);
+  const bool active = pair < n_pairs;
+  const int b = uni(active ? pair / ncr : 0);
+  const int c = uni(active ? c_begin + pair % ncr : 0);
+  const int lv = uni(active ? min((int)chunk_level[(int64_t)b * P.NC + c], P.NLV - 1) : 0);
+
+  if (threadIdx.x == 0) s_mask = 0u;
+  __syncthreads();
+  if (active && lane == 0) atomicOr(&s_mask, 1u << lv);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int n = 0;
+    for (int v = 0; v < P.NLV; ++v)
+      if ((s_mask >> v) & 1u) { s_set_of_level[v] = n; s_level_of_set[n] = v; ++n; }
+    s_nsets = n;
+  }
+  __syncthreads();
+  const int nsets = s_nsets;
+  for (int idx = wave; idx < nsets * 64; idx += nwaves) {
+    const int st = idx >> 6, t = idx & 63;
+    const int ch = cb * 64 + t;
+    if (ch >= P.C) continue;
+    const uint32_t* src = reinterpret_cast<const uint32_t*>(
+        cdfD + ((((int64_t)s_level_of_set[st] * P.L + l) * 2 + k) * P.C + ch) * 256);
+    uint32_t* dst = reinterpret_cast<uint32_t*>(tabs + (st * 64 + t) * kTabStride);
+    const uint32_t v0 = src[lane];
+    uint32_t v1 = src[lane + 64];
+    if (lane == 63) v1 = (v1 & 0xFFFFu) | 0xFFFF0000u;  // entry 255: sentinel above any target
+    dst[lane] = v0;
+    dst[lane + 64] = v1;
+    if (lane < 2) dst[128 + lane] = 0xFFFFFFFFu;        // entries 256..259: sentinels
+  }
+  __syncthreads();
+
+  if (!active) return;
+  const int ch = cb * 64 + lane;
+  const bool valid = ch < P.C;
+  const int lsrc = valid ? lane : 0;   // lanes past C decode a copy of the block's first channel
+  const int chv = cb * 64 + lsrc;
+
+  const int64_t bclk = (((int64_t)b * P.NC + c) * P.L + l) * 2 + k;
+  const int64_t sidx = cg_stream(P, bclk, chv);
+  const int tok0 = c * P.CL;
+  const int n = uni(min(P.CL, P.T - tok0));
+  const float s = scales[sidx];
+  const float w = P.layer_bin[l] * P.level_mult[lv] * s;
+  const uint16_t* dtab = tabs + (s_set_of_level[lv] * 64 + lsrc) * kTabStride;
+  const uint16_t* gA = cdfA + ((int64_t)(l * 2 + k) * P.C + chv) * 256;
+
+  // fences cum[16 f], f = 0..16 (cum[256] = total), of both tables
+  uint32_t fD[17], fA[17];
+  fD[0] = 0u;
+  fA[0] = 0u;
+  fD[16] = CG_TOTAL;
+  fA[16] = CG_TOTAL;
+#pragma unroll
+  for (int f = 1; f < 16; ++f) {
+    fD[f] = dtab[16 * f];
+    fA[f] = gA[16 * f];
+  }
+
+  const uint64_t total = offsets[P.S];
+  if (total == 0) return;
+  // bitstream reader: as in the generic kernel (64-bit bit buffer, four-word shift register,
+  // the next four words requested one epoch ahead; at most one word moves per token and at
+  // most four tokens separate two epoch boundaries)
+  G10Lane st;
+  const uint64_t o0 = offsets[sidx];
+  const uint32_t* sbase = words + (o0 < total ? o0 : total);
+  st.D = sbase[0];
+  st.buf = (uint64_t)sbase[1] << 32;
+  st.avail = 32;
+  st.s0 = sbase[2];
+  st.s1 = sbase[3];
+  st.s2 = sbase[4];
+  st.s3 = sbase[5];
+  st.hcnt = 0;
+  st.wpos = (o0 < total ? o0 : total) + 6;
+  const uint64_t wcap = total;
+  const uint32_t* tq0 = words + (st.wpos < wcap ? st.wpos : wcap);
+  st.t0 = tq0[0];
+  st.t1 = tq0[1];
+  st.t2 = tq0[2];
+  st.t3 = tq0[3];
+  settle(st.D); settle(st.s0); settle(st.s1); settle(st.s2); settle(st.s3);
+  settle((uint32_t)(st.buf >> 32));
+  st.low = 0u;
+  st.rm1 = 0xFFFFFFFFu;
+  st.a = 0.0f;
+
+  uint16_t* row = out + cg_elem(P, b, l, k, tok0, cb * 64);
+  const int64_t rstride = P.C;
+  uint16_t* obuf = obuf_all + wave * kG10 * 64;
+  const int cbase = cb * 64;
+
+  const int ngr = n / kG10;
+  for (int gi = 0; gi < ngr; ++gi) {
+    g10_token<true>(st, fA, fD, dtab, gA, s, w, obuf, 0, lane);
+    g10_epoch(st, words, wcap);
+    g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 1, lane);
+    g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 2, lane);
+    g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 3, lane);
+    g10_epoch(st, words, wcap);
+    g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 4, lane);
+    g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 5, lane);
+    g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 6, lane);
+    g10_epoch(st, words, wcap);
+    g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 7, lane);
+    g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 8, lane);
+    g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 9, lane);
+    g10_flush(obuf, row, rstride, kG10, lane, cbase, P.C);
+    row += kG10 * rstride;
+  }
+  const int rem = n - ngr * kG10;   // last, partial group (uniform)
+  if (rem > 0) {
+    g10_token<true>(st, fA, fD, dtab, gA, s, w, obuf, 0, lane);
+    g10_epoch(st, words, wcap);
+    for (int r = 1; r < rem; ++r) {
+      if (r == 4 || r == 7) g10_epoch(st, words, wcap);
+      g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, r, lane);
+    }
+    g10_flush(obuf, row, rstride, rem, lane, cbase, P.C);
+  }
+}
+
 }  // namespace
 
 hipError_t cg_launch_decode(const KParams& P, const uint32_t* words, const uint64_t* offsets,
@@ -354,12 +715,23 @@ hipError_t cg_launch_decode(const KParams& P, const uint32_t* words, const uint6
   const int nw = (int)(n_pairs < kMaxWaves ? n_pairs : kMaxWaves);
   const int64_t n_groups = (n_pairs + nw - 1) / nw;
   const int nsets_max = nw < P.NLV ? nw : P.NLV;
+  const int64_t grid = (int64_t)P.L * 2 * P.nblk * n_groups;
+  const size_t tab_u16 = (size_t)nsets_max * 64 * kTabStride;
+  if (P.G == kG10) {
+    const size_t lds = ((size_t)nw * kG10 * 64 + tab_u16) * sizeof(uint16_t);
+    hipError_t e = hipFuncSetAttribute((const void*)decode_g10_kernel,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(decode_g10_kernel, dim3((unsigned)grid), dim3(64 * nw), lds, st, P,
+                       words, offsets, scales, chunk_level, cdf_anchor, cdf_delta, c_begin, c_end,
+                       nw, out);
+    return hipGetLastError();
+  }
   const size_t lds =
-      (size_t)(64 * kFenceStride + nw * kRows * 64 + nsets_max * 64 * kTabStride) * sizeof(uint16_t);
+      ((size_t)64 * kFenceStride + (size_t)nw * kRows * 64 + tab_u16) * sizeof(uint16_t);
   hipError_t e = hipFuncSetAttribute((const void*)decode_kernel,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  const int64_t grid = (int64_t)P.L * 2 * P.nblk * n_groups;
   hipLaunchKernelGGL(decode_kernel, dim3((unsigned)grid), dim3(64 * nw), lds, st, P, words,
                      offsets, scales, chunk_level, cdf_anchor, cdf_delta, c_begin, c_end, nw,
                      out);
