@@ -193,7 +193,7 @@ def main():
                      "unit": "Tops/s", "frac": round(alu_tops / VALU_PEAK_TOPS, 4),
                      "ops_per_symbol": DECODE_OPS_PER_SYMBOL,
                      "traffic": measured_traffic(w.name),
-                     "kernel": "decode_kernel"},
+                     "kernel": "decode_g10_kernel" if w.group_size == 10 else "decode_kernel"},
         "hbm": {"achieved": round(hbm_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                 "frac": round(hbm_gbps / HBM_PEAK_GBPS, 4),
                 "bytes_per_launch": dec_bytes},

@@ -56,6 +56,25 @@ __device__ __forceinline__ uint32_t scaled_off(uint32_t x, uint32_t c) {
 // Make the compiler wait here for a register produced by a load (once, outside the loop).
 __device__ __forceinline__ void settle(uint32_t v) { asm volatile("" ::"v"(v)); }
 
+// Number of middle-half (E3) steps after the shared leading bits are shifted out: L1 = low and
+// H1 = high shifted left by those bits (so L1 < 2^31 <= H1); the steps are the run of bit
+// positions 30, 29, ... where low has a one and high a zero. With the top bit of (L1 & ~H1)
+// set, that run is the count of bits after the sign bit equal to it, which v_ffbh_i32 gives
+// plus one.
+__device__ __forceinline__ uint32_t e3_run(uint32_t L1, uint32_t H1) {
+  uint32_t n;
+  asm("v_ffbh_i32 %0, %1" : "=v"(n) : "v"((L1 & ~H1) | 0x80000000u));
+  return n - 1u;
+}
+
+// 16-byte store of decoded fp16 that is not read again by this kernel (non-temporal, so the
+// output stream does not push the anchor tables out of the L2).
+__device__ __forceinline__ void store_row16(uint16_t* dst, const uint4& v) {
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 vv = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(vv, reinterpret_cast<u32x4*>(dst));
+}
+
 // Last level of the delta search. q points at cum[i] (8-byte aligned) with cum[i] <= ti; the
 // symbol is i + c with c in [0, 3]. cum[i .. i+3] come in one 8-byte read (x = cum[i] |
 // cum[i+1] << 16, y = cum[i+2] | cum[i+3] << 16), cum[i+4] in a second. The count of entries
@@ -326,9 +345,8 @@ __global__ __launch_bounds__(1024) void decode_kernel(
     const uint32_t high = low + rm1;
     const uint32_t n1 = (uint32_t)__builtin_clz(low ^ high);   // low != high
     const uint32_t L1 = low << n1, H1 = high << n1;
-    const uint32_t m = L1 & ~H1;
-    const uint32_t n3 = (uint32_t)__builtin_clz(~(m << 1));    // ~(m << 1) is odd
-    low = (L1 & 0x80000000u) | ((L1 << n3) & 0x7FFFFFFFu);
+    const uint32_t n3 = e3_run(L1, H1);
+    low = (L1 << n3) & 0x7FFFFFFFu;   // L1 has a clear top bit
     const uint32_t nsh = n1 + n3;
     rm1 = (rm1 << nsh) | ((1u << nsh) - 1u);
     // D takes the next nsh bits: a funnel shift of (D : top word of buf); nsh = 0 keeps D
@@ -365,7 +383,7 @@ __global__ __launch_bounds__(1024) void decode_kernel(
         const uint4 vals = *reinterpret_cast<const uint4*>(obuf + rr * 64 + cc);
         uint16_t* dst = row + rr * rstride + cc;
         if (cb * 64 + cc + 8 <= P.C && (reinterpret_cast<uintptr_t>(dst) & 15) == 0) {
-          *reinterpret_cast<uint4*>(dst) = vals;
+          store_row16(dst, vals);
         } else {
           const uint16_t hv[8] = {(uint16_t)(vals.x & 0xFFFFu), (uint16_t)(vals.x >> 16),
                                   (uint16_t)(vals.y & 0xFFFFu), (uint16_t)(vals.y >> 16),
@@ -497,9 +515,8 @@ __device__ __forceinline__ void g10_token(G10Lane& st, const uint32_t (&fA)[17],
   const uint32_t high = low + r1;
   const uint32_t n1 = (uint32_t)__builtin_clz(low ^ high);
   const uint32_t L1 = low << n1, H1 = high << n1;
-  const uint32_t m = L1 & ~H1;
-  const uint32_t n3 = (uint32_t)__builtin_clz(~(m << 1));
-  st.low = (L1 & 0x80000000u) | ((L1 << n3) & 0x7FFFFFFFu);
+  const uint32_t n3 = e3_run(L1, H1);
+  st.low = (L1 << n3) & 0x7FFFFFFFu;   // L1 has a clear top bit
   const uint32_t nsh = n1 + n3;
   st.rm1 = (r1 << nsh) | ((1u << nsh) - 1u);
   const uint32_t dsh = __builtin_amdgcn_alignbit(d, (uint32_t)(st.buf >> 32), 32u - nsh);
@@ -539,7 +556,7 @@ __device__ __forceinline__ void g10_flush(const uint16_t* obuf, uint16_t* row, i
       const uint4 vals = *reinterpret_cast<const uint4*>(obuf + rr * 64 + cc);
       uint16_t* dst = row + rr * rstride + cc;
       if (cbase + cc + 8 <= C && (reinterpret_cast<uintptr_t>(dst) & 15) == 0) {
-        *reinterpret_cast<uint4*>(dst) = vals;
+        store_row16(dst, vals);
       } else {
         const uint16_t hv[8] = {(uint16_t)(vals.x & 0xFFFFu), (uint16_t)(vals.x >> 16),
                                 (uint16_t)(vals.y & 0xFFFFu), (uint16_t)(vals.y >> 16),
