@@ -2,19 +2,22 @@
 // distribution per channel-layer for deltas and one for anchors; Sec. 6: frequencies counted
 // over the context's quantized symbols).
 //
-// One workgroup per (layer, K/V, 64-channel block). Its 8 waves walk every (context, chunk)
-// pair of that block; a lane owns one channel and runs the quantizer over the chunk's tokens
-// (one pass for the absmax scale, one to quantize), counting symbols into LDS histograms.
-// Rows are read 64 channels (128 B) at a time, so every load is one coalesced line. After a
-// barrier each wave normalises histograms to 16-bit cumulative tables: per-lane partial sums,
-// a wave reduction for the total, the argmax and the frequency sum, and a wave prefix scan.
+// One workgroup of 16 waves per (layer, K/V, 64-channel block); a lane owns one channel. The
+// workgroup takes the (context, chunk) pairs of that block one after the other and splits each
+// chunk's groups across its waves: every wave first reduces the absmax of its token slice, the
+// slices are combined in LDS into the chunk's scale, then every wave quantizes its slice (groups
+// are independent once the scale is known) and counts the symbols into LDS histograms. Rows
+// are read 64 channels (128 B) at a time, so every load is one coalesced line. Histograms use a
+// 257-word stride so lanes that count the same symbol hit different banks. At the end each
+// wave normalises histograms to 16-bit cumulative tables: per-lane partial sums, a wave
+// reduction for the total, the argmax and the frequency sum, and a wave prefix scan.
 #include "cg_device.h"
 
 namespace {
 
-constexpr int kFitWaves = 8;
+constexpr int kFitWaves = 16;
 constexpr int kFitThreads = kFitWaves * 64;
-constexpr int kHist = 256;  // 255 symbols, padded
+constexpr int kHist = 257;  // 255 symbols, padded; odd stride spreads lanes over the banks
 
 // Normalise one histogram [255] into cum[256] (entry 255 = 0) with one wave.
 __device__ void normalize_wave(const uint32_t* cnt, uint16_t* out) {
@@ -78,7 +81,8 @@ __device__ void normalize_wave(const uint32_t* cnt, uint16_t* out) {
 __global__ __launch_bounds__(kFitThreads) void fit_kernel(KParams P, const uint16_t* __restrict__ kv,
                                                          int level, uint16_t* __restrict__ cdf_anchor,
                                                          uint16_t* __restrict__ cdf_delta) {
-  extern __shared__ uint32_t cnt[];  // [2 kinds][64 channels][256]
+  extern __shared__ uint32_t cnt[];  // [2 kinds][64 channels][kHist]
+  __shared__ float part[kFitWaves][64];
   const int cb = blockIdx.x % P.nblk;
   const int lk = blockIdx.x / P.nblk;
   const int l = lk >> 1, k = lk & 1;
@@ -93,32 +97,46 @@ __global__ __launch_bounds__(kFitThreads) void fit_kernel(KParams P, const uint1
   uint32_t* ha = cnt + lane * kHist;
   uint32_t* hd = cnt + (64 + lane) * kHist;
   const int pairs = P.B * P.NC;
-  for (int pr = wave; pr < pairs; pr += kFitWaves) {
+  const int64_t rs = P.C;
+  for (int pr = 0; pr < pairs; ++pr) {
     const int b = pr / P.NC, c = pr % P.NC;
     const int t0 = c * P.CL;
     const int n = min(P.CL, P.T - t0);
-    if (!act) continue;
-    const uint16_t* x = kv + cg_elem(P, b, l, k, t0, ch);
+    const int ng = (n + P.G - 1) / P.G;                 // groups in the chunk
+    const int gpw = (ng + kFitWaves - 1) / kFitWaves;   // groups per wave
+    const int j0 = min(n, wave * gpw * P.G), j1 = min(n, (wave + 1) * gpw * P.G);
+    const uint16_t* x = kv + cg_elem(P, b, l, k, t0, act ? ch : cb * 64);
+    // pass 1: absmax of this wave's slice, combined over the waves in LDS
     float m = 0.0f;
-    for (int j = 0; j < n; ++j) m = fmaxf(m, fabsf(cg_h2f(x[(int64_t)j * P.C])));
+#pragma unroll 8
+    for (int j = j0; j < j1; ++j) m = fmaxf(m, fabsf(cg_h2f(x[(int64_t)j * rs])));
+    part[wave][lane] = m;
+    __syncthreads();
+    m = 0.0f;
+#pragma unroll
+    for (int v = 0; v < kFitWaves; ++v) m = fmaxf(m, part[v][lane]);
     const float s = (m == 0.0f) ? 1.0f : m / 127.0f;
     const float w = wfac * s;
-    float a = 0.0f;
-    int g = 0;
-    for (int j = 0; j < n; ++j) {
-      const float v = cg_h2f(x[(int64_t)j * P.C]);
-      if (g == 0) {
-        const int q = cg_quant(v, s);
-        a = (float)q * s;
-        atomicAdd(&ha[q + 127], 1u);
-      } else {
-        const int q = cg_quant(v - a, w);
-        atomicAdd(&hd[q + 127], 1u);
+    // pass 2: quantize the slice (it starts on a group boundary) and count
+    if (act) {
+      float a = 0.0f;
+      int g = 0;
+#pragma unroll 4
+      for (int j = j0; j < j1; ++j) {
+        const float v = cg_h2f(x[(int64_t)j * rs]);
+        if (g == 0) {
+          const int q = cg_quant(v, s);
+          a = (float)q * s;
+          atomicAdd(&ha[q + 127], 1u);
+        } else {
+          const int q = cg_quant(v - a, w);
+          atomicAdd(&hd[q + 127], 1u);
+        }
+        g = (g + 1 == P.G) ? 0 : g + 1;
       }
-      g = (g + 1 == P.G) ? 0 : g + 1;
     }
+    __syncthreads();   // `part` is reused by the next pair
   }
-  __syncthreads();
 
   for (int tb = wave; tb < 128; tb += kFitWaves) {
     const int kind = tb >> 6, cl = tb & 63;
