@@ -213,6 +213,8 @@ __global__ __launch_bounds__(1024) void decode_kernel(
   const uint16_t* dtab = tabs + (s_set_of_level[lv] * 64 + lsrc) * kTabStride;
   const uint16_t* ftab = fences + lsrc * kFenceStride;
   const uint16_t* gA = cdfA + ((int64_t)(l * 2 + k) * P.C + chv) * 256;
+  cg_glb_u16* gA1 = (cg_glb_u16*)gA;
+  cg_lds_u16* dtab3 = (cg_lds_u16*)dtab;
 
   const uint64_t total = offsets[P.S];
   if (total == 0) return;  // no payload at all: nothing can be decoded (uniform)
@@ -329,9 +331,10 @@ __global__ __launch_bounds__(1024) void decode_kernel(
     if (D < lo_off || D > hm1) {
       for (int guard = 0; guard < CG_NSYM; ++guard) {
         sym = (D < lo_off) ? max(sym - 1, 0) : min(sym + 1, CG_NSYM - 1);
-        clo = anchor ? (uint32_t)gA[sym] : (uint32_t)dtab[sym];
-        chi = sym + 1 >= CG_NSYM ? CG_TOTAL
-                                 : (anchor ? (uint32_t)gA[sym + 1] : (uint32_t)dtab[sym + 1]);
+        const int s1 = min(sym + 1, CG_NSYM - 1);
+        clo = anchor ? (uint32_t)gA1[sym] : (uint32_t)dtab3[sym];
+        chi = anchor ? (uint32_t)gA1[s1] : (uint32_t)dtab3[s1];
+        chi = sym + 1 >= CG_NSYM ? CG_TOTAL : chi;
         lo_off = scaled_off(rm1, clo);
         hm1 = scaled_off(rm1, chi) - 1u;
         if (D >= lo_off && D <= hm1) break;
@@ -501,9 +504,15 @@ __device__ __forceinline__ void g10_token(G10Lane& st, const uint32_t (&fA)[17],
   if (D < lo_off || D > hm1) {
     for (int guard = 0; guard < CG_NSYM; ++guard) {
       sym = (D < lo_off) ? max(sym - 1, 0) : min(sym + 1, CG_NSYM - 1);
-      clo = kAnchor ? (uint32_t)gA[sym] : (uint32_t)dtab[sym];
-      chi = sym + 1 >= CG_NSYM ? CG_TOTAL
-                               : (kAnchor ? (uint32_t)gA[sym + 1] : (uint32_t)dtab[sym + 1]);
+      const int s1 = min(sym + 1, CG_NSYM - 1);
+      if constexpr (kAnchor) {
+        clo = gA[sym];
+        chi = gA[s1];
+      } else {
+        clo = dtab[sym];
+        chi = dtab[s1];
+      }
+      chi = sym + 1 >= CG_NSYM ? CG_TOTAL : chi;
       lo_off = scaled_off(rm1, clo);
       hm1 = scaled_off(rm1, chi) - 1u;
       if (D >= lo_off && D <= hm1) break;

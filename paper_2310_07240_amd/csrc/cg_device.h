@@ -13,6 +13,13 @@
 #define CG_NSYM 255
 #define CG_TOTAL 65536u
 
+// Table pointers typed by address space. Where one expression may read either an LDS table or a
+// global one, the loads stay separate LDS and global loads instead of being merged into one
+// generic (flat) load through a selected pointer: such a load costs more, and its base (before
+// the instruction's immediate offset) can fall outside the LDS aperture, which faults.
+typedef __attribute__((address_space(3))) const uint16_t cg_lds_u16;
+typedef __attribute__((address_space(1))) const uint16_t cg_glb_u16;
+
 // Parameters as the kernels see them. Passed by value (kernel argument segment, < 4 KiB).
 struct KParams {
   int32_t B, L, T, C;      // contexts, layers, tokens, channels per K and per V

@@ -26,7 +26,8 @@
 
 namespace {
 
-constexpr int kEncThreads = 256;
+constexpr int kEncMaxWaves = 16;
+constexpr int kEncTabStride = 258;   // u16 per delta table in LDS (odd word stride: lanes spread over banks)
 constexpr int kScanThreads = 256;
 constexpr int kScanItems = 16;
 constexpr int kScanBlock = kScanThreads * kScanItems;  // 4096 streams per scan block
@@ -35,7 +36,7 @@ struct BitSink {
   uint32_t* out;    // slot base
   uint32_t cap;     // slot capacity in words
   uint32_t nwords;  // words produced
-  uint64_t acc;     // output bits not yet in a word, right-aligned
+  uint64_t acc;     // output bits not yet in a word: the low nacc bits (higher bits ignored)
   uint32_t nacc;    // number of bits in acc, < 32 between calls
 
   __device__ __forceinline__ void put(uint32_t bits, uint32_t nb) {  // nb <= 32
@@ -71,17 +72,34 @@ __device__ __forceinline__ void enc_symbol(EncState& e, BitSink& o, uint32_t clo
   const uint32_t rm1 = hm1 - lo_off;
   const uint32_t high = low + rm1;
   const uint32_t n1 = __clz(low ^ high);  // high > low, so n1 <= 31
-  if (n1) {
+  const uint32_t P = e.pending;
+  if (n1 != 0 && P + n1 <= 32) {
+    // the n1 shared leading bits H, the first of them followed by P opposite bits: as one
+    // number of P + n1 bits this is H + ((2^P - 1) << (n1 - 1))
+    const uint32_t H = low >> (32 - n1);
+    const uint32_t E = P + n1;
+    const uint32_t val = H + ((uint32_t)((1ull << P) - 1ull) << (n1 - 1));
+    o.acc = (o.acc << E) | val;   // bits above the nacc valid ones are never read
+    o.nacc += E;
+    if (o.nacc >= 32) {
+      o.nacc -= 32;
+      const uint32_t wd = (uint32_t)(o.acc >> o.nacc);
+      if (o.nwords < o.cap) o.out[o.nwords] = wd;
+      ++o.nwords;
+    }
+    e.pending = 0;
+  } else if (n1 != 0) {   // more than 32 bits owed (long middle-half runs): bit by bit
     const uint32_t b0 = low >> 31;
     o.put(b0, 1);
-    if (e.pending) { o.run(b0 ^ 1u, e.pending); e.pending = 0; }
+    o.run(b0 ^ 1u, P);
+    e.pending = 0;
     if (n1 > 1) o.put((low << 1) >> (33 - n1), n1 - 1);
   }
   const uint32_t L1 = low << n1, H1 = high << n1;
   const uint32_t m = L1 & ~H1;
   const uint32_t n3 = __clz(~(m << 1));
   e.pending += n3;
-  e.low = (L1 & 0x80000000u) | ((L1 << n3) & 0x7FFFFFFFu);
+  e.low = (L1 << n3) & 0x7FFFFFFFu;   // L1 has a clear top bit
   const uint32_t n = n1 + n3;  // at most 18 (the new range is at least 2^14)
   e.rm1 = (rm1 << n) | ((1u << n) - 1u);
 }
@@ -94,61 +112,144 @@ __device__ __forceinline__ void enc_finish(EncState& e, BitSink& o) {
   if (o.nacc) o.put(0u, 32 - o.nacc);  // zero-pad to a whole word
 }
 
-__global__ __launch_bounds__(kEncThreads) void encode_kernel(
+// Token pipeline of the encoder: the symbols and their table entries do not depend on the
+// coder state, so they are produced ahead of it. Per step of kPipe tokens, the row values of
+// the tokens two steps ahead are requested, the tokens one step ahead are quantized and their
+// (cum[sym], cum[sym + 1]) requested from the tables, and the tokens of this step are coded
+// with the entries requested one step earlier. With the paper's group of 10 a step is one
+// group (kG = 10: the anchor is always the step's first token, so every step issues the same
+// memory operations); other group sizes use steps of 8 tokens (kG = 0).
+
+template <int kG>
+__global__ __launch_bounds__(1024) void encode_kernel(
     KParams P, const uint16_t* __restrict__ kv, const uint8_t* __restrict__ chunk_level,
     const uint16_t* __restrict__ cdfA, const uint16_t* __restrict__ cdfD,
     uint32_t* __restrict__ slots, uint32_t slot_words, uint32_t* __restrict__ lens,
-    float* __restrict__ scales) {
-  const int64_t gw = (int64_t)blockIdx.x * (kEncThreads / 64) + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  const int64_t nrows = (int64_t)P.B * P.NC * P.L * 2;
-  const int64_t bclk = gw / P.nblk;
-  const int cb = (int)(gw % P.nblk);
-  if (bclk >= nrows) return;
+    float* __restrict__ scales, int nw) {
+  // workgroup = (layer, K/V, 64-channel block) x up to kEncMaxWaves (context, chunk) pairs;
+  // the delta tables of the levels those pairs use are staged in LDS once (9 of 10 symbols
+  // look up there); anchor entries come from global memory, requested a pipeline step ahead
+  extern __shared__ uint16_t tabs[];   // [nsets][64][kEncTabStride]
+  __shared__ uint32_t s_mask;
+  __shared__ int s_set_of_level[CG_MAX_LEVELS];
+  __shared__ int s_level_of_set[CG_MAX_LEVELS];
+  __shared__ int s_nsets;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int nwaves = blockDim.x >> 6;
+  const int n_pairs = P.B * P.NC;
+  const int n_groups = (n_pairs + nw - 1) / nw;
+  const int grp = blockIdx.x % n_groups;
+  int rest = blockIdx.x / n_groups;
+  const int cb = rest % P.nblk;
+  rest /= P.nblk;
+  const int k = rest & 1, l = rest >> 1;
+  const int pair = __builtin_amdgcn_readfirstlane(grp * nw + wave);
+  const bool active = pair < n_pairs;
+  const int b = active ? pair / P.NC : 0;
+  const int c = active ? pair % P.NC : 0;
+  const int lv = active ? min((int)chunk_level[(int64_t)b * P.NC + c], P.NLV - 1) : 0;
+
+  if (threadIdx.x == 0) s_mask = 0u;
+  __syncthreads();
+  if (active && lane == 0) atomicOr(&s_mask, 1u << lv);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int m = 0;
+    for (int v = 0; v < P.NLV; ++v)
+      if ((s_mask >> v) & 1u) { s_set_of_level[v] = m; s_level_of_set[m] = v; ++m; }
+    s_nsets = m;
+  }
+  __syncthreads();
+  const int nsets = s_nsets;
+  for (int idx = wave; idx < nsets * 64; idx += nwaves) {
+    const int st = idx >> 6, t = idx & 63;
+    const int chs = cb * 64 + t;
+    if (chs >= P.C) continue;
+    const uint32_t* src = reinterpret_cast<const uint32_t*>(
+        cdfD + ((((int64_t)s_level_of_set[st] * P.L + l) * 2 + k) * P.C + chs) * 256);
+    uint32_t* dst = reinterpret_cast<uint32_t*>(tabs + (st * 64 + t) * kEncTabStride);
+    dst[lane] = src[lane];
+    dst[lane + 64] = src[lane + 64];
+  }
+  __syncthreads();
+  if (!active) return;
   const int ch = cb * 64 + lane;
   if (ch >= P.C) return;
-  const int k = (int)(bclk & 1);
-  int64_t r = bclk >> 1;
-  const int l = (int)(r % P.L);
-  r /= P.L;
-  const int c = (int)(r % P.NC);
-  const int b = (int)(r / P.NC);
-  const int lv = min((int)chunk_level[(int64_t)b * P.NC + c], P.NLV - 1);
+  const int64_t bclk = (((int64_t)b * P.NC + c) * P.L + l) * 2 + k;
   const int t0 = c * P.CL;
   const int n = min(P.CL, P.T - t0);
   const int64_t sidx = cg_stream(P, bclk, ch);
   const uint16_t* x = kv + cg_elem(P, b, l, k, t0, ch);
+  const int64_t rs = P.C;
 
   float mx = 0.0f;
-  for (int j = 0; j < n; ++j) mx = fmaxf(mx, fabsf(cg_h2f(x[(int64_t)j * P.C])));
+#pragma unroll 16
+  for (int j = 0; j < n; ++j) mx = fmaxf(mx, fabsf(cg_h2f(x[(int64_t)j * rs])));
   const float s = (mx == 0.0f) ? 1.0f : mx / 127.0f;
   scales[sidx] = s;
+  constexpr int kPipe = kG > 0 ? kG : 8;
   const float bw = P.layer_bin[l] * P.level_mult[lv];
   const float w = bw * s;
 
-  const uint16_t* tabA = cdfA + ((int64_t)(l * 2 + k) * P.C + ch) * 256;
-  const uint16_t* tabD = cdfD + ((((int64_t)lv * P.L + l) * 2 + k) * P.C + ch) * 256;
+  cg_glb_u16* tabA = (cg_glb_u16*)(cdfA + ((int64_t)(l * 2 + k) * P.C + ch) * 256);
+  cg_lds_u16* tabD = (cg_lds_u16*)(tabs + (s_set_of_level[lv] * 64 + lane) * kEncTabStride);
   EncState e{0u, 0xFFFFFFFFu, 0u};
   BitSink o{slots + (uint64_t)sidx * slot_words, slot_words, 0u, 0ull, 0u};
+
+  // pipeline registers: row values of the step after next, table entries of the next step
+  uint32_t xn[kPipe], clo_n[kPipe], chi_n[kPipe], clo_c[kPipe], chi_c[kPipe];
+  const int last = n - 1;
+#pragma unroll
+  for (int u = 0; u < kPipe; ++u) xn[u] = x[(int64_t)min(u, last) * rs];
   float a = 0.0f;
-  int g = 0;
-  for (int j = 0; j < n; ++j) {
-    const float v = cg_h2f(x[(int64_t)j * P.C]);
-    int q;
-    const uint16_t* tab;
-    if (g == 0) {
-      q = cg_quant(v, s);
-      a = (float)q * s;
-      tab = tabA;
-    } else {
-      q = cg_quant(v - a, w);
-      tab = tabD;
+  int gq = 0;   // group position of the next token to quantize (uniform)
+  // quantize the next kPipe tokens from xv[] and request their table entries
+  auto quantize_step = [&](const uint32_t (&xv)[kPipe], uint32_t (&clo)[kPipe],
+                           uint32_t (&chi)[kPipe]) __attribute__((always_inline)) {
+    // tokens past the chunk end (values clamped to the last row) are quantized too but never
+    // coded; keeping every step's loads unconditional keeps the memory waits exact
+#pragma unroll
+    for (int u = 0; u < kPipe; ++u) {
+      const float v = cg_h2f((uint16_t)xv[u]);
+      const bool anc = kG > 0 ? u == 0 : gq == 0;
+      const int q = anc ? cg_quant(v, s) : cg_quant(v - a, w);
+      if (anc) a = (float)q * s;
+      const int sym = q + 127;
+      const int sym1 = min(sym + 1, CG_NSYM - 1);
+      if (anc) {
+        clo[u] = tabA[sym];
+        chi[u] = tabA[sym1];
+      } else {
+        clo[u] = tabD[sym];
+        chi[u] = tabD[sym1];
+      }
+      chi[u] = sym == CG_NSYM - 1 ? CG_TOTAL : chi[u];
+      if (kG == 0) gq = (gq + 1 == P.G) ? 0 : gq + 1;
     }
-    const int sym = q + 127;
-    const uint32_t clo = tab[sym];
-    const uint32_t chi = sym == 254 ? CG_TOTAL : (uint32_t)tab[sym + 1];
-    enc_symbol(e, o, clo, chi);
-    g = (g + 1 == P.G) ? 0 : g + 1;
+  };
+  {
+    uint32_t xc[kPipe];
+#pragma unroll
+    for (int u = 0; u < kPipe; ++u) xc[u] = xn[u];
+#pragma unroll
+    for (int u = 0; u < kPipe; ++u) xn[u] = x[(int64_t)min(kPipe + u, last) * rs];
+    quantize_step(xc, clo_c, chi_c);
+  }
+  for (int j = 0; j < n; j += kPipe) {
+    uint32_t xq[kPipe];
+#pragma unroll
+    for (int u = 0; u < kPipe; ++u) xq[u] = xn[u];
+#pragma unroll
+    for (int u = 0; u < kPipe; ++u) xn[u] = x[(int64_t)min(j + 2 * kPipe + u, last) * rs];
+    quantize_step(xq, clo_n, chi_n);
+#pragma unroll
+    for (int u = 0; u < kPipe; ++u)
+      if (j + u < n) enc_symbol(e, o, clo_c[u], chi_c[u]);
+#pragma unroll
+    for (int u = 0; u < kPipe; ++u) {
+      clo_c[u] = clo_n[u];
+      chi_c[u] = chi_n[u];
+    }
   }
   enc_finish(e, o);
   // the coder's bound for n symbols; the compaction never writes past the sum of these
@@ -274,11 +375,23 @@ hipError_t cg_launch_encode(const KParams& P, const uint16_t* kv, const uint8_t*
   uint32_t* lens = reinterpret_cast<uint32_t*>(base + lay.lens_off);
   uint64_t* partial = reinterpret_cast<uint64_t*>(base + lay.partial_off);
 
-  const int64_t waves = (int64_t)P.B * P.NC * P.L * 2 * P.nblk;
-  const int64_t g1 = (waves + 3) / 4;
-  hipLaunchKernelGGL(encode_kernel, dim3((unsigned)g1), dim3(kEncThreads), 0, st, P, kv,
-                     chunk_level, cdf_anchor, cdf_delta, slots, slot_words, lens, scales);
-  hipError_t e = hipGetLastError();
+  const int64_t n_pairs = (int64_t)P.B * P.NC;
+  const int nw = (int)(n_pairs < kEncMaxWaves ? n_pairs : kEncMaxWaves);
+  const int64_t n_groups = (n_pairs + nw - 1) / nw;
+  const int nsets_max = nw < P.NLV ? nw : P.NLV;
+  const size_t lds = (size_t)nsets_max * 64 * kEncTabStride * sizeof(uint16_t);
+  const void* kfn = P.G == 10 ? (const void*)encode_kernel<10> : (const void*)encode_kernel<0>;
+  hipError_t e =
+      hipFuncSetAttribute(kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  const int64_t g1 = (int64_t)P.L * 2 * P.nblk * n_groups;
+  if (P.G == 10)
+    hipLaunchKernelGGL(encode_kernel<10>, dim3((unsigned)g1), dim3(64 * nw), lds, st, P, kv,
+                       chunk_level, cdf_anchor, cdf_delta, slots, slot_words, lens, scales, nw);
+  else
+    hipLaunchKernelGGL(encode_kernel<0>, dim3((unsigned)g1), dim3(64 * nw), lds, st, P, kv,
+                       chunk_level, cdf_anchor, cdf_delta, slots, slot_words, lens, scales, nw);
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t nb = (P.S + kScanBlock - 1) / kScanBlock;
   hipLaunchKernelGGL(scan_reduce, dim3((unsigned)nb), dim3(kScanThreads), 0, st, lens, P.S,
