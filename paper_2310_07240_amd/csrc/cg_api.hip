@@ -80,7 +80,7 @@ uint64_t cg_encode_bound_words(const cg_params* p) {
 uint64_t cg_encode_workspace_bytes(const cg_params* p) {
   KParams K;
   if (make_kparams(p, &K) != CG_OK) return 0;
-  return cg_encode_ws_layout(K.S, slot_words_for(K)).total;
+  return cg_encode_ws_layout(K, slot_words_for(K)).total;
 }
 
 int cg_fit_cdf(const cg_params* p, const uint16_t* kv_f16, int32_t level, uint16_t* cdf_anchor,
@@ -113,7 +113,7 @@ int cg_encode(const cg_params* p, const uint16_t* kv_f16, const uint8_t* chunk_l
     return CG_ERR_ARG;
   if (words_cap < cg_encode_bound_words(p)) return CG_ERR_CAPACITY;
   const uint32_t slot = slot_words_for(K);
-  if (workspace_bytes < cg_encode_ws_layout(K.S, slot).total) return CG_ERR_CAPACITY;
+  if (workspace_bytes < cg_encode_ws_layout(K, slot).total) return CG_ERR_CAPACITY;
   return cg_launch_encode(K, kv_f16, chunk_level, cdf_anchor, cdf_delta, words, offsets, scales,
                           workspace, slot, stream) == hipSuccess
              ? CG_OK

@@ -104,4 +104,4 @@ hipError_t cg_launch_check_finite(const uint16_t* kv, int64_t n, uint32_t* flag,
 struct EncWorkspace {
   uint64_t slots_off, lens_off, partial_off, total;
 };
-EncWorkspace cg_encode_ws_layout(int64_t S, uint32_t slot_words);
+EncWorkspace cg_encode_ws_layout(const KParams& P, uint32_t slot_words);

@@ -27,26 +27,57 @@
 namespace {
 
 constexpr int kEncMaxWaves = 16;
+constexpr size_t kEncLdsBudget = 160 * 1024 - 1024;   // dynamic LDS per workgroup (CDNA4: 160 KB)
 constexpr int kEncTabStride = 258;   // u16 per delta table in LDS (odd word stride: lanes spread over banks)
 constexpr int kScanThreads = 256;
 constexpr int kScanItems = 16;
 constexpr int kScanBlock = kScanThreads * kScanItems;  // 4096 streams per scan block
 
+// Output of one stream. Whole words produced by the common path go to a lane-private ring of
+// kRing words in LDS and reach the stream's slot in global memory in one flush per pipeline
+// step, issued right after the step's row values were consumed: stores issued between the
+// pipeline's loads would otherwise make every later wait for those loads wait for the stores
+// too (loads and stores share one in-order counter). The rare paths (long runs of owed bits,
+// the end of the stream) flush the ring and then write directly.
+constexpr int kRing = 8;
+
 struct BitSink {
-  uint32_t* out;    // slot base
+  uint32_t* out;    // slot base: word k of this stream at out[64 k]
   uint32_t cap;     // slot capacity in words
   uint32_t nwords;  // words produced
+  uint32_t flushed; // words already in the slot
   uint64_t acc;     // output bits not yet in a word: the low nacc bits (higher bits ignored)
   uint32_t nacc;    // number of bits in acc, < 32 between calls
+  uint32_t* ring;   // this lane's kRing words in LDS, 64 words apart (bank-conflict free)
 
+  // a finished word on the common path
+  __device__ __forceinline__ void word(uint32_t w) {
+    ring[(nwords & (kRing - 1)) * 64] = w;
+    ++nwords;
+  }
+  // store the ring's words to the slot (at most kRing - 1 are pending)
+  __device__ __forceinline__ void flush() {
+    // read every slot of the ring first (one wait for all of them), then store the pending ones
+    uint32_t v[kRing - 1];
+#pragma unroll
+    for (int i = 0; i < kRing - 1; ++i) v[i] = ring[((flushed + i) & (kRing - 1)) * 64];
+#pragma unroll
+    for (int i = 0; i < kRing - 1; ++i) {
+      const uint32_t wi = flushed + i;
+      if (wi < nwords && wi < cap) out[(uint64_t)wi * 64] = v[i];
+    }
+    flushed = nwords;
+  }
+  // direct output (the ring must be flushed first)
   __device__ __forceinline__ void put(uint32_t bits, uint32_t nb) {  // nb <= 32
     acc = (acc << nb) | bits;
     nacc += nb;
     if (nacc >= 32) {
       nacc -= 32;
       const uint32_t w = (uint32_t)(acc >> nacc);
-      if (nwords < cap) out[nwords] = w;
+      if (nwords < cap) out[(uint64_t)nwords * 64] = w;
       ++nwords;
+      flushed = nwords;
       acc &= (1ull << nacc) - 1ull;
     }
   }
@@ -83,12 +114,11 @@ __device__ __forceinline__ void enc_symbol(EncState& e, BitSink& o, uint32_t clo
     o.nacc += E;
     if (o.nacc >= 32) {
       o.nacc -= 32;
-      const uint32_t wd = (uint32_t)(o.acc >> o.nacc);
-      if (o.nwords < o.cap) o.out[o.nwords] = wd;
-      ++o.nwords;
+      o.word((uint32_t)(o.acc >> o.nacc));
     }
     e.pending = 0;
   } else if (n1 != 0) {   // more than 32 bits owed (long middle-half runs): bit by bit
+    o.flush();
     const uint32_t b0 = low >> 31;
     o.put(b0, 1);
     o.run(b0 ^ 1u, P);
@@ -105,6 +135,7 @@ __device__ __forceinline__ void enc_symbol(EncState& e, BitSink& o, uint32_t clo
 }
 
 __device__ __forceinline__ void enc_finish(EncState& e, BitSink& o) {
+  o.flush();
   e.pending += 1;
   const uint32_t b = e.low >= 0x40000000u ? 1u : 0u;
   o.put(b, 1);
@@ -125,11 +156,11 @@ __global__ __launch_bounds__(1024) void encode_kernel(
     KParams P, const uint16_t* __restrict__ kv, const uint8_t* __restrict__ chunk_level,
     const uint16_t* __restrict__ cdfA, const uint16_t* __restrict__ cdfD,
     uint32_t* __restrict__ slots, uint32_t slot_words, uint32_t* __restrict__ lens,
-    float* __restrict__ scales, int nw) {
+    float* __restrict__ scales, int nw, int nsets_lds) {
   // workgroup = (layer, K/V, 64-channel block) x up to kEncMaxWaves (context, chunk) pairs;
   // the delta tables of the levels those pairs use are staged in LDS once (9 of 10 symbols
   // look up there); anchor entries come from global memory, requested a pipeline step ahead
-  extern __shared__ uint16_t tabs[];   // [nsets][64][kEncTabStride]
+  extern __shared__ uint16_t tabs[];   // [nsets][64][kEncTabStride], then words [nw][kRing][64]
   __shared__ uint32_t s_mask;
   __shared__ int s_set_of_level[CG_MAX_LEVELS];
   __shared__ int s_level_of_set[CG_MAX_LEVELS];
@@ -194,20 +225,26 @@ __global__ __launch_bounds__(1024) void encode_kernel(
   cg_glb_u16* tabA = (cg_glb_u16*)(cdfA + ((int64_t)(l * 2 + k) * P.C + ch) * 256);
   cg_lds_u16* tabD = (cg_lds_u16*)(tabs + (s_set_of_level[lv] * 64 + lane) * kEncTabStride);
   EncState e{0u, 0xFFFFFFFFu, 0u};
-  BitSink o{slots + (uint64_t)sidx * slot_words, slot_words, 0u, 0ull, 0u};
+  uint32_t* rings = reinterpret_cast<uint32_t*>(tabs + nsets_lds * 64 * kEncTabStride);
+  // the slots of a wave's 64 streams are interleaved word by word (word k of lane L at
+  // 64 k + L), so words that neighbouring lanes finish at about the same time share lines
+  const uint64_t slot_group = (uint64_t)bclk * P.nblk + cb;
+  BitSink o{slots + slot_group * slot_words * 64 + lane, slot_words, 0u, 0u, 0ull, 0u,
+            rings + wave * kRing * 64 + lane};
 
-  // pipeline registers: row values of the step after next, table entries of the next step
-  uint32_t xn[kPipe], clo_n[kPipe], chi_n[kPipe], clo_c[kPipe], chi_c[kPipe];
+  // Pipeline buffers, used in turn (steps alternate between set 0 and set 1, and the loop
+  // body is written out for both so no buffer is ever copied: a copy of a register that a
+  // load is still filling would make the copy wait for that load and for every memory
+  // operation issued after it). xr*: row values; lo* / hi*: the table entries of a step.
+  uint32_t xr0[kPipe], xr1[kPipe], lo0[kPipe], hi0[kPipe], lo1[kPipe], hi1[kPipe];
   const int last = n - 1;
-#pragma unroll
-  for (int u = 0; u < kPipe; ++u) xn[u] = x[(int64_t)min(u, last) * rs];
   float a = 0.0f;
   int gq = 0;   // group position of the next token to quantize (uniform)
-  // quantize the next kPipe tokens from xv[] and request their table entries
+  // quantize the next kPipe tokens from xv[] and request their table entries. Tokens past the
+  // chunk end (rows clamped to the last one) are quantized too but never coded, so every step
+  // issues the same memory operations.
   auto quantize_step = [&](const uint32_t (&xv)[kPipe], uint32_t (&clo)[kPipe],
                            uint32_t (&chi)[kPipe]) __attribute__((always_inline)) {
-    // tokens past the chunk end (values clamped to the last row) are quantized too but never
-    // coded; keeping every step's loads unconditional keeps the memory waits exact
 #pragma unroll
     for (int u = 0; u < kPipe; ++u) {
       const float v = cg_h2f((uint16_t)xv[u]);
@@ -227,29 +264,32 @@ __global__ __launch_bounds__(1024) void encode_kernel(
       if (kG == 0) gq = (gq + 1 == P.G) ? 0 : gq + 1;
     }
   };
-  {
-    uint32_t xc[kPipe];
+  auto load_rows = [&](uint32_t (&xv)[kPipe], int step) __attribute__((always_inline)) {
 #pragma unroll
-    for (int u = 0; u < kPipe; ++u) xc[u] = xn[u];
-#pragma unroll
-    for (int u = 0; u < kPipe; ++u) xn[u] = x[(int64_t)min(kPipe + u, last) * rs];
-    quantize_step(xc, clo_c, chi_c);
-  }
-  for (int j = 0; j < n; j += kPipe) {
-    uint32_t xq[kPipe];
-#pragma unroll
-    for (int u = 0; u < kPipe; ++u) xq[u] = xn[u];
-#pragma unroll
-    for (int u = 0; u < kPipe; ++u) xn[u] = x[(int64_t)min(j + 2 * kPipe + u, last) * rs];
-    quantize_step(xq, clo_n, chi_n);
+    for (int u = 0; u < kPipe; ++u) xv[u] = x[(int64_t)min(step * kPipe + u, last) * rs];
+  };
+  auto code_step = [&](const uint32_t (&clo)[kPipe], const uint32_t (&chi)[kPipe], int step)
+                       __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < kPipe; ++u)
-      if (j + u < n) enc_symbol(e, o, clo_c[u], chi_c[u]);
-#pragma unroll
-    for (int u = 0; u < kPipe; ++u) {
-      clo_c[u] = clo_n[u];
-      chi_c[u] = chi_n[u];
-    }
+      if (step * kPipe + u < n) enc_symbol(e, o, clo[u], chi[u]);
+  };
+  load_rows(xr0, 0);
+  load_rows(xr1, 1);
+  quantize_step(xr0, lo0, hi0);
+  load_rows(xr0, 2);
+  for (int st = 0; st * kPipe < n; st += 2) {
+    // step st: quantize step st+1, request the rows of step st+3, code step st
+    quantize_step(xr1, lo1, hi1);
+    o.flush();
+    load_rows(xr1, st + 3);
+    code_step(lo0, hi0, st);
+    if ((st + 1) * kPipe >= n) break;
+    // step st+1: the same with the sets exchanged
+    quantize_step(xr0, lo0, hi0);
+    o.flush();
+    load_rows(xr0, st + 4);
+    code_step(lo1, hi1, st + 1);
   }
   enc_finish(e, o);
   // the coder's bound for n symbols; the compaction never writes past the sum of these
@@ -341,25 +381,32 @@ __global__ __launch_bounds__(256) void compact_kernel(const uint32_t* __restrict
                                                       uint32_t slot_words,
                                                       const uint32_t* __restrict__ lens,
                                                       const uint64_t* __restrict__ offsets,
-                                                      int64_t S, uint32_t* __restrict__ words) {
+                                                      int64_t S, int C, int nblk,
+                                                      uint32_t* __restrict__ words) {
   const int64_t s = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (s >= S) return;
   const int lane = threadIdx.x & 63;
-  const uint32_t* src = slots + (uint64_t)s * slot_words;
+  const int64_t row = s / C;
+  const int ch = (int)(s - row * C);
+  const uint32_t* src =
+      slots + ((uint64_t)row * nblk + (ch >> 6)) * slot_words * 64 + (ch & 63);
   uint32_t* dst = words + offsets[s];
   const uint32_t n = lens[s];
-  for (uint32_t i = lane; i < n; i += 64) dst[i] = src[i];
+  for (uint32_t i = lane; i < n; i += 64) dst[i] = src[(uint64_t)i * 64];
 }
 
 inline uint64_t align256(uint64_t x) { return (x + 255) & ~(uint64_t)255; }
 
 }  // namespace
 
-EncWorkspace cg_encode_ws_layout(int64_t S, uint32_t slot_words) {
+EncWorkspace cg_encode_ws_layout(const KParams& P, uint32_t slot_words) {
   EncWorkspace w;
+  const int64_t S = P.S;
   const int64_t nb = (S + kScanBlock - 1) / kScanBlock;
+  // one slot per lane of every (row, 64-channel block) wave, lanes past C included
+  const uint64_t slot_lanes = (uint64_t)P.B * P.NC * P.L * 2 * P.nblk * 64;
   w.slots_off = 0;
-  w.lens_off = align256((uint64_t)S * slot_words * 4ull);
+  w.lens_off = align256(slot_lanes * slot_words * 4ull);
   w.partial_off = align256(w.lens_off + (uint64_t)S * 4ull);
   w.total = align256(w.partial_off + (uint64_t)(nb > 0 ? nb : 1) * 8ull);
   return w;
@@ -369,17 +416,23 @@ hipError_t cg_launch_encode(const KParams& P, const uint16_t* kv, const uint8_t*
                             const uint16_t* cdf_anchor, const uint16_t* cdf_delta,
                             uint32_t* words, uint64_t* offsets, float* scales, void* ws,
                             uint32_t slot_words, hipStream_t st) {
-  const EncWorkspace lay = cg_encode_ws_layout(P.S, slot_words);
+  const EncWorkspace lay = cg_encode_ws_layout(P, slot_words);
   uint8_t* base = static_cast<uint8_t*>(ws);
   uint32_t* slots = reinterpret_cast<uint32_t*>(base + lay.slots_off);
   uint32_t* lens = reinterpret_cast<uint32_t*>(base + lay.lens_off);
   uint64_t* partial = reinterpret_cast<uint64_t*>(base + lay.partial_off);
 
   const int64_t n_pairs = (int64_t)P.B * P.NC;
-  const int nw = (int)(n_pairs < kEncMaxWaves ? n_pairs : kEncMaxWaves);
+  int nw = (int)(n_pairs < kEncMaxWaves ? n_pairs : kEncMaxWaves);
+  auto lds_for = [&](int w) {
+    const int sets = w < P.NLV ? w : P.NLV;
+    return (size_t)sets * 64 * kEncTabStride * sizeof(uint16_t) +
+           (size_t)w * kRing * 64 * sizeof(uint32_t);
+  };
+  while (nw > 1 && lds_for(nw) > kEncLdsBudget) --nw;
   const int64_t n_groups = (n_pairs + nw - 1) / nw;
   const int nsets_max = nw < P.NLV ? nw : P.NLV;
-  const size_t lds = (size_t)nsets_max * 64 * kEncTabStride * sizeof(uint16_t);
+  const size_t lds = lds_for(nw);
   const void* kfn = P.G == 10 ? (const void*)encode_kernel<10> : (const void*)encode_kernel<0>;
   hipError_t e =
       hipFuncSetAttribute(kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -387,10 +440,12 @@ hipError_t cg_launch_encode(const KParams& P, const uint16_t* kv, const uint8_t*
   const int64_t g1 = (int64_t)P.L * 2 * P.nblk * n_groups;
   if (P.G == 10)
     hipLaunchKernelGGL(encode_kernel<10>, dim3((unsigned)g1), dim3(64 * nw), lds, st, P, kv,
-                       chunk_level, cdf_anchor, cdf_delta, slots, slot_words, lens, scales, nw);
+                       chunk_level, cdf_anchor, cdf_delta, slots, slot_words, lens, scales, nw,
+                       nsets_max);
   else
     hipLaunchKernelGGL(encode_kernel<0>, dim3((unsigned)g1), dim3(64 * nw), lds, st, P, kv,
-                       chunk_level, cdf_anchor, cdf_delta, slots, slot_words, lens, scales, nw);
+                       chunk_level, cdf_anchor, cdf_delta, slots, slot_words, lens, scales, nw,
+                       nsets_max);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t nb = (P.S + kScanBlock - 1) / kScanBlock;
@@ -401,6 +456,6 @@ hipError_t cg_launch_encode(const KParams& P, const uint16_t* kv, const uint8_t*
                      partial, offsets);
   const int64_t g4 = (P.S + 3) / 4;
   hipLaunchKernelGGL(compact_kernel, dim3((unsigned)g4), dim3(256), 0, st, slots, slot_words,
-                     lens, offsets, P.S, words);
+                     lens, offsets, P.S, P.C, P.nblk, words);
   return hipGetLastError();
 }
