@@ -68,6 +68,9 @@ def main():
     ap.add_argument("--workload", default="mistral7b_gqa_t4096")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=0, help="0 = all host cores")
+    ap.add_argument("--no-streamed", action="store_true",
+                    help="skip the chunk-pipelined decode (payload copied from pinned host memory "
+                         "chunk by chunk while earlier chunks decode), run after the timed region")
     ap.add_argument("--no-calib-copy", action="store_true",
                     help="skip the plain copy of known size run after the timed region (it "
                          "calibrates rocprofv3's FETCH_SIZE / WRITE_SIZE counters)")
@@ -199,9 +202,35 @@ def main():
                 "bytes_per_launch": dec_bytes},
     }
 
+    if not args.no_streamed:
+        result["streamed"] = streamed(p, codec, words, offsets, scales, cl, ca, cd, total_words)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, kv_np, args.cpu_threads)
     print(json.dumps(result), flush=True)
+
+
+def streamed(p, codec, words, offsets, scales, cl, ca, cd, total_words):
+    """Chunk-pipelined decode (cg_decode_streamed): the payload arrives chunk by chunk in pinned
+    host memory and is copied to the GPU on one stream while the chunks already copied decode on
+    another. Reported for the host-to-device bus alone and for a 100 Gb/s link; outside the timed
+    region."""
+    import torch
+    from paper_2310_07240_amd.cachegen import cg_decode_streamed
+    tail = 8
+    words_host = torch.empty((total_words + tail,), dtype=torch.int32, pin_memory=True)
+    words_host.copy_(words[:total_words + tail].cpu())
+    off_host = offsets.cpu()
+    words_dev = torch.zeros((total_words + tail,), dtype=torch.int32, device=words.device)
+    out = torch.empty(codec.p.kv_shape, dtype=torch.int16, device=words.device)
+    dec_s, copy_s = torch.cuda.Stream(), torch.cuda.Stream()
+    res = {"payload_MB": round(total_words * 4 / 1e6, 2)}
+    for name, gbps in (("host_to_device", 0.0), ("link_100gbps", 100.0)):
+        cg_decode_streamed(p, words_host, off_host, words_dev, offsets, scales, cl, ca, cd, out,
+                           gbps, dec_s, copy_s)          # warm-up
+        st = cg_decode_streamed(p, words_host, off_host, words_dev, offsets, scales, cl, ca, cd,
+                                out, gbps, dec_s, copy_s)
+        res[name] = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in st.items()}
+    return res
 
 
 def cpu_baseline(w, kv_np, threads):

@@ -159,6 +159,47 @@ int cg_decode(const cg_params* p, const uint32_t* words, const uint64_t* offsets
               int32_t chunk_begin, int32_t chunk_end, uint16_t* kv_out_f16,
               hipStream_t stream);
 
+/* Timings of one cg_decode_streamed call (milliseconds from the call's first copy). */
+typedef struct cg_stream_stats {
+  int32_t n_chunks;        /* chunks decoded (NC) */
+  double transfer_ms;      /* until the last chunk's payload is on the device */
+  double total_ms;         /* until the last chunk is decoded */
+  double decode_sum_ms;    /* sum of the per-chunk decode durations */
+  double hidden_fraction;  /* 1 - (total_ms - transfer_ms) / decode_sum_ms, clamped to [0, 1]:
+                              the share of decoding done while the payload still arrived */
+} cg_stream_stats;
+
+/* Decode the whole cache chunk by chunk while its payload arrives (Sec. 5.3: the cache is
+ * split into chunks that are sent and decoded independently; Sec. 6: decoding is pipelined with
+ * the transmission so that it adds little delay).
+ *   words_host    [offsets[S]] uint32, HOST memory (page-locked, e.g. from hipHostMalloc, or
+ *                 the copies cannot overlap the decode): the payload as cg_encode produced it.
+ *   offsets_host  [S + 1] uint64, HOST memory: the same offsets (the side information that
+ *                 precedes the payload).
+ *   words_dev     device buffer of words_cap words, words_cap >= offsets[S] + CG_TAIL_WORDS,
+ *                 that receives the payload; the other device arguments are as for cg_decode.
+ * offsets_host is checked on the host before anything is issued: it must start at 0, be
+ * non-decreasing at every chunk boundary used for a copy and end within words_cap -
+ * CG_TAIL_WORDS (else CG_ERR_ARG / CG_ERR_CAPACITY).
+ *   link_gbps     rate of the simulated link the payload arrives over, in gigabits per second:
+ *                 chunk c's copy is issued when the bytes of chunks 0..c would have arrived
+ *                 (the host waits). 0 or less: every copy is issued at once (the host-to-device
+ *                 bus is the link).
+ *   decode_stream, copy_stream   two HIP streams (the copies overlap the decodes only if they
+ *                 differ); chunk c's decode waits for chunk c's copy through an event.
+ *   stats         out, host, may be NULL.
+ * Chunk c of every context is copied (one copy per context: chunk c's streams of context b are
+ * contiguous) and decoded with the cg_decode kernels. Creates and destroys HIP events, and
+ * returns after the last decode has finished (synchronous). The result equals cg_decode over
+ * all chunks. */
+int cg_decode_streamed(const cg_params* p, const uint32_t* words_host,
+                       const uint64_t* offsets_host, uint32_t* words_dev, uint64_t words_cap,
+                       const uint64_t* offsets_dev, const float* scales_dev,
+                       const uint8_t* chunk_level_dev, const uint16_t* cdf_anchor_dev,
+                       const uint16_t* cdf_delta_dev, uint16_t* kv_out_dev, double link_gbps,
+                       hipStream_t decode_stream, hipStream_t copy_stream,
+                       cg_stream_stats* stats);
+
 /* Scan kv_f16 [n_elem] for NaN / Inf (fp16 exponent field all ones), using flag_dev, one
  * caller-owned device uint32_t, as scratch. Synchronises `stream`. Returns CG_OK,
  * CG_ERR_NONFINITE, or an error code. The quantizer is defined for finite input only;

@@ -24,7 +24,7 @@ ERRORS = {-1: "CG_ERR_ARG", -2: "CG_ERR_SHAPE", -3: "CG_ERR_CAPACITY", -4: "CG_E
 
 EXPORTS = ("cg_num_chunks", "cg_num_streams", "cg_encode_bound_words",
            "cg_encode_workspace_bytes", "cg_fit_cdf", "cg_encode", "cg_decode",
-           "cg_check_finite", "cg_strerror")
+           "cg_decode_streamed", "cg_check_finite", "cg_strerror")
 
 
 class CodecError(RuntimeError):
@@ -40,6 +40,16 @@ class _CParams(ctypes.Structure):
                 ("n_levels", ctypes.c_int32),
                 ("layer_bin", ctypes.POINTER(ctypes.c_float)),
                 ("level_mult", ctypes.POINTER(ctypes.c_float))]
+
+
+class StreamStats(ctypes.Structure):
+    """cg_stream_stats: timings of one cg_decode_streamed call (milliseconds)."""
+    _fields_ = [("n_chunks", ctypes.c_int32), ("transfer_ms", ctypes.c_double),
+                ("total_ms", ctypes.c_double), ("decode_sum_ms", ctypes.c_double),
+                ("hidden_fraction", ctypes.c_double)]
+
+    def as_dict(self):
+        return {f: getattr(self, f) for f, _ in self._fields_}
 
 
 _LIB = None
@@ -67,6 +77,9 @@ def lib():
         L.cg_encode.restype = ctypes.c_int
         L.cg_decode.argtypes = [PP, _P, _P, _P, _P, _P, _P, ctypes.c_int32, ctypes.c_int32, _P, _P]
         L.cg_decode.restype = ctypes.c_int
+        L.cg_decode_streamed.argtypes = [PP, _P, _P, _P, ctypes.c_uint64, _P, _P, _P, _P, _P, _P,
+                                         ctypes.c_double, _P, _P, ctypes.POINTER(StreamStats)]
+        L.cg_decode_streamed.restype = ctypes.c_int
         L.cg_check_finite.argtypes = [PP, _P, _P, _P]
         L.cg_check_finite.restype = ctypes.c_int
         L.cg_strerror.argtypes = [ctypes.c_int]
@@ -179,6 +192,22 @@ def cg_decode(p: CodecParams, words, offsets, scales, chunk_level, cdf_anchor, c
     _check(lib().cg_decode(ctypes.byref(s), _ptr(words), _ptr(offsets), _ptr(scales),
                            _ptr(chunk_level), _ptr(cdf_anchor), _ptr(cdf_delta), int(chunk_begin),
                            int(chunk_end), _ptr(kv_out), _stream(stream)), "cg_decode")
+
+
+def cg_decode_streamed(p: CodecParams, words_host, offsets_host, words_dev, offsets_dev, scales,
+                       chunk_level, cdf_anchor, cdf_delta, kv_out, link_gbps: float,
+                       decode_stream, copy_stream) -> dict:
+    """Decode chunk by chunk while the payload is copied from (pinned) host memory; returns
+    the call's timings (cg_stream_stats as a dict). Synchronous."""
+    s, keep = p.c()
+    st = StreamStats()
+    _check(lib().cg_decode_streamed(ctypes.byref(s), _ptr(words_host), _ptr(offsets_host),
+                                    _ptr(words_dev), words_dev.numel(), _ptr(offsets_dev),
+                                    _ptr(scales),
+                                    _ptr(chunk_level), _ptr(cdf_anchor), _ptr(cdf_delta),
+                                    _ptr(kv_out), float(link_gbps), _stream(decode_stream),
+                                    _stream(copy_stream), ctypes.byref(st)), "cg_decode_streamed")
+    return st.as_dict()
 
 
 def cg_check_finite(p: CodecParams, kv, flag, stream=None) -> bool:

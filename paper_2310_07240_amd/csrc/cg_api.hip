@@ -3,6 +3,10 @@
 #include <math.h>
 #include <string.h>
 
+#include <chrono>
+#include <thread>
+#include <vector>
+
 #include "../../include/cachegen.h"
 #include "cg_device.h"
 
@@ -138,6 +142,100 @@ int cg_decode(const cg_params* p, const uint32_t* words, const uint64_t* offsets
                           chunk_begin, chunk_end, kv_out_f16, stream) == hipSuccess
              ? CG_OK
              : CG_ERR_HIP;
+}
+
+int cg_decode_streamed(const cg_params* p, const uint32_t* words_host,
+                       const uint64_t* offsets_host, uint32_t* words_dev, uint64_t words_cap,
+                       const uint64_t* offsets_dev, const float* scales_dev,
+                       const uint8_t* chunk_level_dev, const uint16_t* cdf_anchor_dev,
+                       const uint16_t* cdf_delta_dev, uint16_t* kv_out_dev, double link_gbps,
+                       hipStream_t decode_stream, hipStream_t copy_stream,
+                       cg_stream_stats* stats) {
+  KParams K;
+  int rc = make_kparams(p, &K);
+  if (rc != CG_OK) return rc;
+  if (!words_host || !offsets_host || !words_dev || !offsets_dev || !scales_dev ||
+      !chunk_level_dev || !cdf_anchor_dev || !cdf_delta_dev || !kv_out_dev)
+    return CG_ERR_ARG;
+  if (!aligned(cdf_anchor_dev, 16) || !aligned(cdf_delta_dev, 16) || !aligned(offsets_dev, 8) ||
+      !aligned(words_dev, 4) || !aligned(kv_out_dev, 2) || !aligned(words_host, 4) ||
+      !aligned(offsets_host, 8))
+    return CG_ERR_ARG;
+  const int NC = K.NC;
+  const int64_t per_chunk = (int64_t)K.L * 2 * K.C;   // streams of one (context, chunk)
+  // the copies follow offsets_host: check every boundary they use before issuing anything
+  if (offsets_host[0] != 0) return CG_ERR_ARG;
+  for (int64_t i = 0; i < (int64_t)K.B * NC; ++i)
+    if (offsets_host[(i + 1) * per_chunk] < offsets_host[i * per_chunk]) return CG_ERR_ARG;
+  if (words_cap < CG_TAIL_WORDS || offsets_host[K.S] > words_cap - CG_TAIL_WORDS)
+    return CG_ERR_CAPACITY;
+  const double bits_per_ms = link_gbps > 0.0 ? link_gbps * 1.0e6 : 0.0;
+
+  // events: start, then per chunk copy done, decode start, decode done
+  std::vector<hipEvent_t> ev(1 + 3 * (size_t)NC, nullptr);
+  auto cleanup = [&]() {
+    for (hipEvent_t e : ev)
+      if (e) (void)hipEventDestroy(e);
+  };
+  for (hipEvent_t& e : ev)
+    if (hipEventCreate(&e) != hipSuccess) { e = nullptr; cleanup(); return CG_ERR_HIP; }
+  hipEvent_t ev0 = ev[0];
+  auto ev_copy = [&](int c) { return ev[1 + 3 * c]; };
+  auto ev_dbeg = [&](int c) { return ev[2 + 3 * c]; };
+  auto ev_dend = [&](int c) { return ev[3 + 3 * c]; };
+
+  bool ok = hipEventRecord(ev0, copy_stream) == hipSuccess;
+  const auto t0 = std::chrono::steady_clock::now();
+  uint64_t sent_words = 0;
+  for (int c = 0; ok && c < NC; ++c) {
+    uint64_t chunk_words = 0;
+    for (int b = 0; b < K.B; ++b) {
+      const int64_t s0 = ((int64_t)b * NC + c) * per_chunk;
+      chunk_words += offsets_host[s0 + per_chunk] - offsets_host[s0];
+    }
+    if (bits_per_ms > 0.0) {   // the chunk's last byte arrives over the link
+      const double due_ms = (double)(sent_words + chunk_words) * 32.0 / bits_per_ms;
+      std::this_thread::sleep_until(
+          t0 + std::chrono::duration_cast<std::chrono::steady_clock::duration>(
+                   std::chrono::duration<double, std::milli>(due_ms)));
+    }
+    for (int b = 0; ok && b < K.B; ++b) {
+      const int64_t s0 = ((int64_t)b * NC + c) * per_chunk;
+      const uint64_t w0 = offsets_host[s0], w1 = offsets_host[s0 + per_chunk];
+      if (w1 > w0)
+        ok = hipMemcpyAsync(words_dev + w0, words_host + w0, (w1 - w0) * sizeof(uint32_t),
+                            hipMemcpyHostToDevice, copy_stream) == hipSuccess;
+    }
+    ok = ok && hipEventRecord(ev_copy(c), copy_stream) == hipSuccess &&
+         hipStreamWaitEvent(decode_stream, ev_copy(c), 0) == hipSuccess &&
+         hipEventRecord(ev_dbeg(c), decode_stream) == hipSuccess &&
+         cg_launch_decode(K, words_dev, offsets_dev, scales_dev, chunk_level_dev, cdf_anchor_dev,
+                          cdf_delta_dev, c, c + 1, kv_out_dev, decode_stream) == hipSuccess &&
+         hipEventRecord(ev_dend(c), decode_stream) == hipSuccess;
+    sent_words += chunk_words;
+  }
+  // wait for everything issued, whether or not a step failed
+  const bool synced = hipStreamSynchronize(copy_stream) == hipSuccess &&
+                      hipStreamSynchronize(decode_stream) == hipSuccess;
+  bool timed = true;
+  if (ok && synced && stats) {
+    float tx = 0.0f, tot = 0.0f, d = 0.0f;
+    double dsum = 0.0;
+    timed = hipEventElapsedTime(&tx, ev0, ev_copy(NC - 1)) == hipSuccess &&
+            hipEventElapsedTime(&tot, ev0, ev_dend(NC - 1)) == hipSuccess;
+    for (int c = 0; timed && c < NC; ++c) {
+      timed = hipEventElapsedTime(&d, ev_dbeg(c), ev_dend(c)) == hipSuccess;
+      dsum += d;
+    }
+    stats->n_chunks = NC;
+    stats->transfer_ms = tx;
+    stats->total_ms = tot;
+    stats->decode_sum_ms = dsum;
+    double h = dsum > 0.0 ? 1.0 - ((double)tot - (double)tx) / dsum : 1.0;
+    stats->hidden_fraction = h < 0.0 ? 0.0 : (h > 1.0 ? 1.0 : h);
+  }
+  cleanup();
+  return ok && synced && timed ? CG_OK : CG_ERR_HIP;
 }
 
 int cg_check_finite(const cg_params* p, const uint16_t* kv_f16, uint32_t* flag_dev,
