@@ -2,15 +2,17 @@
 // arithmetic coding; Sec. 5.3: each chunk coded independently at its own level).
 //
 // Launches:
-//   encode_kernel   one lane per stream (64 consecutive channels of one (b, c, l, kv) per
-//                   wave, so every token row is one coalesced 128-byte load): absmax scale,
-//                   quantize, arithmetic-code into a worst-case slot of the workspace, record
-//                   the stream's word count;
+//   encode_kernel   workgroup = (layer, K/V, 64-channel block) x up to 16 (context, chunk)
+//                   pairs, one wave per pair and one lane per stream (every token row is one
+//                   coalesced 128-byte load); the delta tables of the levels in use sit in LDS.
+//                   Absmax scale, quantize, arithmetic-code into a worst-case slot of the
+//                   workspace, record the stream's word count;
 //   scan_reduce     per-block totals of the word counts (4096 streams per block);
 //   scan_top        exclusive scan of the block totals (one workgroup);
 //   scan_finish     block-local exclusive scan (wave prefix sums + LDS) plus the block's
 //                   carry -> offsets[S + 1];
-//   compact         one wave per stream copies its words from the slot to offsets[s].
+//   compact         one workgroup per (row, 64-channel block) moves its 64 streams' words
+//                   from the (interleaved) slots to their offsets, through an LDS transpose.
 //
 // Arithmetic coder: Witten-Neal-Cleary integer coder, 32-bit registers, 16-bit frequencies.
 // Renormalisation is done in one step per symbol instead of one bit at a time:
@@ -377,22 +379,61 @@ __global__ __launch_bounds__(kScanThreads) void scan_finish(const uint32_t* __re
   }
 }
 
+// Copy every stream's words from its slot to their place in the payload. One workgroup per
+// (row, 64-channel block): the slots of its 64 streams are interleaved word by word, so tiles of
+// 16 words x 64 streams are read as whole 256-byte rows, transposed through LDS, and written as
+// 16 consecutive words per stream.
 __global__ __launch_bounds__(256) void compact_kernel(const uint32_t* __restrict__ slots,
                                                       uint32_t slot_words,
                                                       const uint32_t* __restrict__ lens,
                                                       const uint64_t* __restrict__ offsets,
-                                                      int64_t S, int C, int nblk,
+                                                      int C, int nblk,
                                                       uint32_t* __restrict__ words) {
-  const int64_t s = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (s >= S) return;
-  const int lane = threadIdx.x & 63;
-  const int64_t row = s / C;
-  const int ch = (int)(s - row * C);
-  const uint32_t* src =
-      slots + ((uint64_t)row * nblk + (ch >> 6)) * slot_words * 64 + (ch & 63);
-  uint32_t* dst = words + offsets[s];
-  const uint32_t n = lens[s];
-  for (uint32_t i = lane; i < n; i += 64) dst[i] = src[(uint64_t)i * 64];
+  __shared__ uint32_t tile[16][65];
+  __shared__ uint32_t s_len[64];
+  __shared__ uint64_t s_off[64];
+  __shared__ uint32_t s_max;
+  const int64_t grp = blockIdx.x;   // row * nblk + block
+  const int64_t row = grp / nblk;
+  const int cb = (int)(grp - row * nblk);
+  const int t = threadIdx.x;
+  if (t == 0) s_max = 0u;
+  __syncthreads();
+  if (t < 64) {
+    const int ch = cb * 64 + t;
+    uint32_t n = 0;
+    uint64_t o = 0;
+    if (ch < C) {
+      const int64_t s = row * C + ch;
+      n = lens[s];
+      o = offsets[s];
+    }
+    s_len[t] = n;
+    s_off[t] = o;
+    atomicMax(&s_max, n);
+  }
+  __syncthreads();
+  const uint32_t K = s_max;
+  const uint32_t* src = slots + (uint64_t)grp * slot_words * 64;
+  for (uint32_t k0 = 0; k0 < K; k0 += 16) {
+    const uint32_t r = k0 + (t >> 4);            // slot row: word r of all 64 streams
+    if (r < K) {
+      const uint4 v = *reinterpret_cast<const uint4*>(src + (uint64_t)r * 64 + (t & 15) * 4);
+      uint32_t* d = &tile[t >> 4][(t & 15) * 4];
+      d[0] = v.x;
+      d[1] = v.y;
+      d[2] = v.z;
+      d[3] = v.w;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int pass = 0; pass < 4; ++pass) {
+      const int L = pass * 16 + (t >> 4), j = t & 15;
+      const uint32_t k = k0 + j;
+      if (k < s_len[L]) words[s_off[L] + k] = tile[j][L];
+    }
+    __syncthreads();
+  }
 }
 
 inline uint64_t align256(uint64_t x) { return (x + 255) & ~(uint64_t)255; }
@@ -454,8 +495,8 @@ hipError_t cg_launch_encode(const KParams& P, const uint16_t* kv, const uint8_t*
   hipLaunchKernelGGL(scan_top, dim3(1), dim3(kScanThreads), 0, st, partial, nb);
   hipLaunchKernelGGL(scan_finish, dim3((unsigned)nb), dim3(kScanThreads), 0, st, lens, P.S,
                      partial, offsets);
-  const int64_t g4 = (P.S + 3) / 4;
-  hipLaunchKernelGGL(compact_kernel, dim3((unsigned)g4), dim3(256), 0, st, slots, slot_words,
-                     lens, offsets, P.S, P.C, P.nblk, words);
+  const int64_t groups = (int64_t)P.B * P.NC * P.L * 2 * P.nblk;
+  hipLaunchKernelGGL(compact_kernel, dim3((unsigned)groups), dim3(256), 0, st, slots,
+                     slot_words, lens, offsets, P.C, P.nblk, words);
   return hipGetLastError();
 }

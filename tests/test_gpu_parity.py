@@ -33,6 +33,25 @@ def test_small_workloads_bit_exact(w):
     assert_same("decode of oracle payload", g["out_from_oracle_payload"], o["out"])
 
 
+# Every remainder of a chunk's token count modulo the group size of 10 (the decoder's last,
+# partial group has its own code path): chunk lengths 12, 13, 15, 19 leave 2, 3, 5, 9 tokens,
+# and the last chunks of these caches leave 1, 6, 7, 8 (0 and 4 come from the cases above).
+TAILS = [
+    W.small(name="tail_c12_t61", n_tokens=61, chunk_len=12, n_channels=64, n_layers=2),
+    W.small(name="tail_c13_t45", n_tokens=45, chunk_len=13, n_channels=65, n_layers=2),
+    W.small(name="tail_c15_t52", n_tokens=52, chunk_len=15, n_channels=64, n_layers=2),
+    W.small(name="tail_c19_t46", n_tokens=46, chunk_len=19, n_channels=64, n_layers=2, n_ctx=2),
+]
+
+
+@pytest.mark.parametrize("w", TAILS, ids=lambda w: w.name)
+def test_group_tails_bit_exact(w):
+    kv = W.generate(w)
+    o = run_oracle(w, kv)
+    g = run_gpu(w, kv)
+    compare_full(w, g, o)
+
+
 @pytest.mark.parametrize("kind", ["zeros", "constant", "subnormal", "ties", "clamp", "signs"])
 def test_edge_inputs_bit_exact(kind):
     w = W.small(name=f"edge_{kind}", n_tokens=64, chunk_len=25, n_channels=80)
