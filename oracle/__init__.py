@@ -84,6 +84,8 @@ def _lib():
             L.cgo_stream_bound_words.restype = _U64
             L.cg_fit_cdf_ref.argtypes = [_P, _P, ctypes.c_int, _P, _P, ctypes.c_int]
             L.cg_fit_cdf_ref.restype = ctypes.c_int
+            L.cg_fit_cdf_global_ref.argtypes = [_P, _P, ctypes.c_int, _P, _P, ctypes.c_int]
+            L.cg_fit_cdf_global_ref.restype = ctypes.c_int
             L.cg_encode_ref.argtypes = [_P, _P, _P, _P, _P, _P, _U64, _P, _P, ctypes.c_int]
             L.cg_encode_ref.restype = _I64
             L.cg_decode_ref.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I64, _I64, _P, ctypes.c_int]
@@ -249,6 +251,19 @@ def fit_cdf(kv: np.ndarray, shape: Shape, level: int, threads: int | None = None
     ps, keep = shape._c()
     _lib().cg_fit_cdf_ref(ctypes.byref(ps), _ptr(kvu), level, _ptr(ca), _ptr(cd),
                           threads or default_threads())
+    return ca, cd
+
+
+def fit_cdf_global(kv: np.ndarray, shape: Shape, level: int, threads: int | None = None):
+    """The ablation baseline: one anchor and one delta distribution pooled over every layer,
+    K/V and channel, written to every table slot: (cdf_anchor, cdf_delta_level)."""
+    kvu = np.ascontiguousarray(kv.view(np.uint16)).reshape(shape.kv_shape())
+    L, C = shape.n_layers, shape.n_channels
+    ca = np.zeros((L, 2, C, 256), np.uint16)
+    cd = np.zeros((L, 2, C, 256), np.uint16)
+    ps, keep = shape._c()
+    _lib().cg_fit_cdf_global_ref(ctypes.byref(ps), _ptr(kvu), level, _ptr(ca), _ptr(cd),
+                                 threads or default_threads())
     return ca, cd
 
 

@@ -258,6 +258,67 @@ int cg_fit_cdf_ref(const cgo_params* p, const uint16_t* kv, int level, uint16_t*
 }
 
 /* ------------------------------------------------------------------------------------------
+ * Ablation baseline: one global symbol distribution (Sec. 5.2 "Arithmetic coding" compares the
+ * per channel-layer distributions against this strawman; Sec. 7.5 "Ablation Study" starts from
+ * it). The counts of every (layer, K/V, channel) are summed into one anchor histogram and one
+ * delta histogram, normalised once like any other table, and the resulting table is written to
+ * every (layer, K/V, channel) slot so the coder uses it everywhere.
+ * ---------------------------------------------------------------------------------------- */
+typedef struct {
+  const cgo_params* p; const uint16_t* kv; int level;
+  int64_t s_begin, s_end;                      /* range of streams for this thread */
+  uint64_t ca[NSYM], cd[NSYM];                 /* this thread's counts */
+} global_job;
+
+static void* global_worker(void* arg) {
+  global_job* J = (global_job*)arg;
+  const cgo_params* p = J->p;
+  int64_t C = p->n_channels, L = p->n_layers;
+  uint8_t* sym = (uint8_t*)malloc((size_t)p->chunk_len);
+  for (int64_t s = J->s_begin; s < J->s_end; ++s) {
+    int64_t l = (s / (2 * C)) % L;
+    stream_t st = locate(p, J->kv, s);
+    float sc = cgo_stream_scale(st.x, st.stride, st.n);
+    float w = bin_width(p, l, J->level, sc);
+    cgo_quantize_stream(st.x, st.stride, st.n, p->group_size, sc, w, sym, NULL);
+    for (int64_t j = 0; j < st.n; ++j) {
+      if (j % p->group_size == 0) J->ca[sym[j]] += 1;
+      else J->cd[sym[j]] += 1;
+    }
+  }
+  free(sym);
+  return NULL;
+}
+
+int cg_fit_cdf_global_ref(const cgo_params* p, const uint16_t* kv, int level,
+                          uint16_t* cdf_anchor, uint16_t* cdf_delta_level, int threads) {
+  int64_t S = cgo_num_streams(p);
+  threads = clamp_threads(threads, S);
+  pthread_t th[256];
+  global_job* jobs = (global_job*)calloc((size_t)threads, sizeof(global_job));
+  for (int i = 0; i < threads; ++i) {
+    jobs[i].p = p; jobs[i].kv = kv; jobs[i].level = level;
+    jobs[i].s_begin = S * i / threads; jobs[i].s_end = S * (i + 1) / threads;
+    pthread_create(&th[i], NULL, global_worker, &jobs[i]);
+  }
+  uint64_t ca[NSYM] = {0}, cd[NSYM] = {0};
+  for (int i = 0; i < threads; ++i) {
+    pthread_join(th[i], NULL);
+    for (int k = 0; k < NSYM; ++k) { ca[k] += jobs[i].ca[k]; cd[k] += jobs[i].cd[k]; }
+  }
+  free(jobs);
+  uint16_t ta[256], td[256];
+  cgo_normalize(ca, ta);
+  cgo_normalize(cd, td);
+  int64_t tables = (int64_t)p->n_layers * 2 * p->n_channels;
+  for (int64_t t = 0; t < tables; ++t) {
+    if (cdf_anchor) memcpy(cdf_anchor + t * 256, ta, sizeof(ta));
+    memcpy(cdf_delta_level + t * 256, td, sizeof(td));
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------------------------
  * Steps a5 / a6: arithmetic coding (Sec. 5.2 "Arithmetic coding"; GPU coding in Sec. 6).
  * The paper names no variant. Reading: the integer arithmetic coder of Witten, Neal and
  * Cleary (CACM 30(6), 1987) with 32-bit code registers and 16-bit cumulative frequencies:

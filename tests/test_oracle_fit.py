@@ -70,3 +70,47 @@ def test_fit_is_thread_count_independent():
     a1, d1 = oracle.fit_cdf(kv, shape, 0, threads=1)
     a2, d2 = oracle.fit_cdf(kv, shape, 0, threads=5)
     assert np.array_equal(a1, a2) and np.array_equal(d1, d2)
+
+
+# ---- the ablation baseline: one global distribution (Sec. 5.2; Sec. 7.5 "Ablation Study") ----
+def test_global_fit_is_the_pooled_histogram():
+    """One anchor and one delta table for the whole cache: the normalisation of the symbol
+    histogram pooled over every layer, K/V, channel, chunk and context, in every slot."""
+    w = W.small(n_ctx=2, n_layers=2, n_tokens=70, n_channels=5, chunk_len=32)
+    kv = W.generate(w)
+    shape = oracle.shape_from(w)
+    ga, gd = oracle.fit_cdf_global(kv, shape, 1, threads=3)
+    cl = np.ones((w.n_ctx, w.n_chunks), np.uint8)
+    hist_a = np.zeros(255, np.int64)
+    hist_d = np.zeros(255, np.int64)
+    for s in range(oracle.shape_from(w).n_streams):
+        sc, sym, _ = oracle.stream_symbols(kv, shape, cl, s)
+        anchor = np.arange(sym.size) % w.group_size == 0
+        hist_a += np.bincount(sym[anchor], minlength=255)
+        hist_d += np.bincount(sym[~anchor], minlength=255)
+    ta, td = oracle.normalize(hist_a), oracle.normalize(hist_d)
+    assert np.array_equal(ga, np.broadcast_to(ta, ga.shape))
+    assert np.array_equal(gd, np.broadcast_to(td, gd.shape))
+
+
+def test_global_fit_of_one_channel_is_the_channel_fit():
+    """Pooling reduces to the per-channel fit when there is nothing to pool: a one-layer,
+    one-channel cache whose V equals its K counts every symbol twice, which normalises to the
+    same table."""
+    w = W.small(n_ctx=1, n_layers=1, n_tokens=90, n_channels=1, chunk_len=40)
+    kv = W.generate(w)
+    kv = kv.reshape(w.kv_shape).copy()
+    kv[:, :, 1] = kv[:, :, 0]                                   # V = K: both counted twice
+    shape = oracle.shape_from(w)
+    ga, gd = oracle.fit_cdf_global(kv, shape, 0)
+    ca, cd = oracle.fit_cdf(kv, shape, 0)
+    assert np.array_equal(ga, ca) and np.array_equal(gd, cd)
+
+
+def test_global_fit_is_thread_count_independent():
+    w = W.small(n_layers=3, n_tokens=64, n_channels=9)
+    kv = W.generate(w)
+    shape = oracle.shape_from(w)
+    a1, d1 = oracle.fit_cdf_global(kv, shape, 0, threads=1)
+    a2, d2 = oracle.fit_cdf_global(kv, shape, 0, threads=7)
+    assert np.array_equal(a1, a2) and np.array_equal(d1, d2)
