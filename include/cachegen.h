@@ -124,6 +124,22 @@ uint64_t cg_encode_workspace_bytes(const cg_params* p);
 int cg_fit_cdf(const cg_params* p, const uint16_t* kv_f16, int32_t level,
                uint16_t* cdf_anchor, uint16_t* cdf_delta_level, hipStream_t stream);
 
+/* Device scratch that cg_fit_cdf_global needs (bytes). */
+#define CG_FIT_GLOBAL_WORKSPACE_BYTES 8192
+
+/* The ablation baseline "one global symbol distribution" (Sec. 5.2 "Arithmetic coding" measures
+ * the per channel-layer distributions against it; the ablation of Sec. 7.5 starts from it):
+ * like cg_fit_cdf, but the counts of every layer, K/V and channel are pooled into one anchor
+ * histogram and one delta histogram, normalised the same way, and that one table is written to
+ * every [l][kv][ch] slot of cdf_anchor (may be NULL) and cdf_delta_level, so cg_encode and
+ * cg_decode use it unchanged.
+ *   workspace    device scratch of workspace_bytes >= CG_FIT_GLOBAL_WORKSPACE_BYTES, 256-byte
+ *                aligned; its contents on entry do not matter.
+ * Asynchronous. */
+int cg_fit_cdf_global(const cg_params* p, const uint16_t* kv_f16, int32_t level,
+                      uint16_t* cdf_anchor, uint16_t* cdf_delta_level, void* workspace,
+                      uint64_t workspace_bytes, hipStream_t stream);
+
 /* Encode the whole KV cache (Sec. 5.2: delta, layer-wise quantization, arithmetic coding;
  * Sec. 5.3: each chunk at its own level).
  *   kv_f16       [B][L][2][T][C] fp16, device.

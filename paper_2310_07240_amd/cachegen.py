@@ -23,8 +23,9 @@ ERRORS = {-1: "CG_ERR_ARG", -2: "CG_ERR_SHAPE", -3: "CG_ERR_CAPACITY", -4: "CG_E
           -5: "CG_ERR_HIP", -6: "CG_ERR_PARAM"}
 
 EXPORTS = ("cg_num_chunks", "cg_num_streams", "cg_encode_bound_words",
-           "cg_encode_workspace_bytes", "cg_fit_cdf", "cg_encode", "cg_decode",
-           "cg_decode_streamed", "cg_check_finite", "cg_strerror")
+           "cg_encode_workspace_bytes", "cg_fit_cdf", "cg_fit_cdf_global", "cg_encode",
+           "cg_decode", "cg_decode_streamed", "cg_check_finite", "cg_strerror")
+CG_FIT_GLOBAL_WORKSPACE_BYTES = 8192
 
 
 class CodecError(RuntimeError):
@@ -72,6 +73,8 @@ def lib():
         L.cg_encode_workspace_bytes.restype = ctypes.c_uint64
         L.cg_fit_cdf.argtypes = [PP, _P, ctypes.c_int32, _P, _P, _P]
         L.cg_fit_cdf.restype = ctypes.c_int
+        L.cg_fit_cdf_global.argtypes = [PP, _P, ctypes.c_int32, _P, _P, _P, ctypes.c_uint64, _P]
+        L.cg_fit_cdf_global.restype = ctypes.c_int
         L.cg_encode.argtypes = [PP, _P, _P, _P, _P, _P, ctypes.c_uint64, _P, _P, _P,
                                 ctypes.c_uint64, _P]
         L.cg_encode.restype = ctypes.c_int
@@ -175,6 +178,16 @@ def cg_fit_cdf(p: CodecParams, kv, level: int, cdf_anchor, cdf_delta_level, stre
     s, keep = p.c()
     _check(lib().cg_fit_cdf(ctypes.byref(s), _ptr(kv), int(level), _ptr(cdf_anchor),
                             _ptr(cdf_delta_level), _stream(stream)), "cg_fit_cdf")
+
+
+def cg_fit_cdf_global(p: CodecParams, kv, level: int, cdf_anchor, cdf_delta_level, workspace,
+                      stream=None):
+    """The one-global-distribution baseline: pooled tables written to every slot."""
+    s, keep = p.c()
+    _check(lib().cg_fit_cdf_global(ctypes.byref(s), _ptr(kv), int(level), _ptr(cdf_anchor),
+                                   _ptr(cdf_delta_level), _ptr(workspace),
+                                   workspace.numel() * workspace.element_size(),
+                                   _stream(stream)), "cg_fit_cdf_global")
 
 
 def cg_encode(p: CodecParams, kv, chunk_level, cdf_anchor, cdf_delta, words, offsets, scales,

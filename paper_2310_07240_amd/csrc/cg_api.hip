@@ -102,6 +102,24 @@ int cg_fit_cdf(const cg_params* p, const uint16_t* kv_f16, int32_t level, uint16
              : CG_ERR_HIP;
 }
 
+int cg_fit_cdf_global(const cg_params* p, const uint16_t* kv_f16, int32_t level,
+                      uint16_t* cdf_anchor, uint16_t* cdf_delta_level, void* workspace,
+                      uint64_t workspace_bytes, hipStream_t stream) {
+  KParams K;
+  int rc = make_kparams(p, &K);
+  if (rc != CG_OK) return rc;
+  if (!kv_f16 || !cdf_delta_level || !workspace) return CG_ERR_ARG;
+  if (level < 0 || level >= K.NLV) return CG_ERR_ARG;
+  if (!aligned(cdf_delta_level, 8) || (cdf_anchor && !aligned(cdf_anchor, 8)) ||
+      !aligned(kv_f16, 2) || !aligned(workspace, 256))
+    return CG_ERR_ARG;
+  if (workspace_bytes < CG_FIT_GLOBAL_WORKSPACE_BYTES) return CG_ERR_CAPACITY;
+  return cg_launch_fit_global(K, kv_f16, level, cdf_anchor, cdf_delta_level, workspace,
+                              stream) == hipSuccess
+             ? CG_OK
+             : CG_ERR_HIP;
+}
+
 int cg_encode(const cg_params* p, const uint16_t* kv_f16, const uint8_t* chunk_level,
               const uint16_t* cdf_anchor, const uint16_t* cdf_delta, uint32_t* words,
               uint64_t words_cap, uint64_t* offsets, float* scales, void* workspace,

@@ -90,6 +90,9 @@ __device__ __forceinline__ uint64_t cg_wave_incl_scan64(uint64_t v) {
 // Launchers (return hipError_t of the launch).
 hipError_t cg_launch_fit(const KParams& P, const uint16_t* kv, int level, uint16_t* cdf_anchor,
                          uint16_t* cdf_delta_level, hipStream_t st);
+hipError_t cg_launch_fit_global(const KParams& P, const uint16_t* kv, int level,
+                                uint16_t* cdf_anchor, uint16_t* cdf_delta_level, void* ws,
+                                hipStream_t st);
 hipError_t cg_launch_encode(const KParams& P, const uint16_t* kv, const uint8_t* chunk_level,
                             const uint16_t* cdf_anchor, const uint16_t* cdf_delta,
                             uint32_t* words, uint64_t* offsets, float* scales, void* ws,

@@ -20,9 +20,10 @@ constexpr int kFitThreads = kFitWaves * 64;
 constexpr int kHist = 257;  // 255 symbols, padded; odd stride spreads lanes over the banks
 
 // Normalise one histogram [255] into cum[256] (entry 255 = 0) with one wave.
-__device__ void normalize_wave(const uint32_t* cnt, uint16_t* out) {
+template <typename CountT>
+__device__ void normalize_wave(const CountT* cnt, uint16_t* out) {
   const int lane = threadIdx.x & 63;
-  uint32_t c[4];
+  uint64_t c[4];
   uint64_t local = 0;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
@@ -37,7 +38,7 @@ __device__ void normalize_wave(const uint32_t* cnt, uint16_t* out) {
     N = CG_NSYM;
   }
   // argmax with the lowest index on ties
-  uint32_t best = 0;
+  uint64_t best = 0;
   int besti = 0x7fffffff;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
@@ -46,7 +47,7 @@ __device__ void normalize_wave(const uint32_t* cnt, uint16_t* out) {
   }
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) {
-    uint32_t ob = __shfl_xor(best, o, 64);
+    uint64_t ob = __shfl_xor(best, o, 64);
     int oi = __shfl_xor(besti, o, 64);
     if (ob > best || (ob == best && oi < besti)) { best = ob; besti = oi; }
   }
@@ -55,7 +56,7 @@ __device__ void normalize_wave(const uint32_t* cnt, uint16_t* out) {
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     int i = lane * 4 + j;
-    f[j] = i < CG_NSYM ? 1u + (uint32_t)(((uint64_t)c[j] * (CG_TOTAL - CG_NSYM)) / N) : 0u;
+    f[j] = i < CG_NSYM ? 1u + (uint32_t)((c[j] * (CG_TOTAL - CG_NSYM)) / N) : 0u;
     fl += f[j];
   }
   uint32_t sumf = cg_wave_sum<uint32_t>(fl);
@@ -78,9 +79,13 @@ __device__ void normalize_wave(const uint32_t* cnt, uint16_t* out) {
   reinterpret_cast<uint64_t*>(out)[lane] = packed;
 }
 
+// kPool: instead of normalising per channel, add the workgroup's counts (summed over its 64
+// channels) to the global counts pool[2][256] (anchor, delta): the one-distribution baseline.
+template <bool kPool>
 __global__ __launch_bounds__(kFitThreads) void fit_kernel(KParams P, const uint16_t* __restrict__ kv,
                                                          int level, uint16_t* __restrict__ cdf_anchor,
-                                                         uint16_t* __restrict__ cdf_delta) {
+                                                         uint16_t* __restrict__ cdf_delta,
+                                                         unsigned long long* __restrict__ pool) {
   extern __shared__ uint32_t cnt[];  // [2 kinds][64 channels][kHist]
   __shared__ float part[kFitWaves][64];
   const int cb = blockIdx.x % P.nblk;
@@ -138,6 +143,15 @@ __global__ __launch_bounds__(kFitThreads) void fit_kernel(KParams P, const uint1
     __syncthreads();   // `part` is reused by the next pair
   }
 
+  if constexpr (kPool) {
+    for (int i = threadIdx.x; i < 2 * CG_NSYM; i += kFitThreads) {
+      const int kind = i / CG_NSYM, sym = i - kind * CG_NSYM;
+      unsigned long long sum = 0;
+      for (int c2 = 0; c2 < 64; ++c2) sum += cnt[(kind * 64 + c2) * kHist + sym];
+      if (sum) atomicAdd(&pool[kind * 256 + sym], sum);
+    }
+    return;
+  }
   for (int tb = wave; tb < 128; tb += kFitWaves) {
     const int kind = tb >> 6, cl = tb & 63;
     const int chx = cb * 64 + cl;
@@ -145,8 +159,35 @@ __global__ __launch_bounds__(kFitThreads) void fit_kernel(KParams P, const uint1
     if (kind == 0 && cdf_anchor == nullptr) continue;
     uint16_t* dst = (kind == 0 ? cdf_anchor : cdf_delta) +
                     ((int64_t)(l * 2 + k) * P.C + chx) * 256;
-    normalize_wave(cnt + tb * kHist, dst);
+    normalize_wave<uint32_t>(cnt + tb * kHist, dst);
   }
+}
+
+__global__ __launch_bounds__(256) void pool_zero(unsigned long long* pool) {
+  for (int i = threadIdx.x; i < 2 * 256; i += 256) pool[i] = 0ull;
+}
+
+// the two pooled tables (wave 0: anchor, wave 1: delta) into tab[2][256]
+__global__ __launch_bounds__(128) void pool_normalize(const unsigned long long* pool,
+                                                      uint16_t* tab) {
+  const int wave = threadIdx.x >> 6;
+  normalize_wave<unsigned long long>(pool + wave * 256, tab + wave * 256);
+}
+
+// copy the pooled tables into every (layer, K/V, channel) slot: one wave per slot and kind
+__global__ __launch_bounds__(256) void pool_broadcast(const uint16_t* __restrict__ tab,
+                                                      int64_t n_tables,
+                                                      uint16_t* __restrict__ cdf_anchor,
+                                                      uint16_t* __restrict__ cdf_delta) {
+  const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (w >= 2 * n_tables) return;
+  const int kind = (int)(w / n_tables);
+  const int64_t t = w - kind * n_tables;
+  uint16_t* dst = kind == 0 ? cdf_anchor : cdf_delta;
+  if (!dst) return;
+  const uint64_t v = reinterpret_cast<const uint64_t*>(tab + kind * 256)[lane];
+  reinterpret_cast<uint64_t*>(dst + t * 256)[lane] = v;
 }
 
 }  // namespace
@@ -154,11 +195,32 @@ __global__ __launch_bounds__(kFitThreads) void fit_kernel(KParams P, const uint1
 hipError_t cg_launch_fit(const KParams& P, const uint16_t* kv, int level, uint16_t* cdf_anchor,
                          uint16_t* cdf_delta_level, hipStream_t st) {
   const size_t lds = 2 * 64 * kHist * sizeof(uint32_t);
-  hipError_t e = hipFuncSetAttribute((const void*)fit_kernel,
+  hipError_t e = hipFuncSetAttribute((const void*)fit_kernel<false>,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   const int64_t grid = (int64_t)P.L * 2 * P.nblk;
-  hipLaunchKernelGGL(fit_kernel, dim3((unsigned)grid), dim3(kFitThreads), lds, st, P, kv, level,
+  hipLaunchKernelGGL(fit_kernel<false>, dim3((unsigned)grid), dim3(kFitThreads), lds, st, P, kv,
+                     level, cdf_anchor, cdf_delta_level, (unsigned long long*)nullptr);
+  return hipGetLastError();
+}
+
+hipError_t cg_launch_fit_global(const KParams& P, const uint16_t* kv, int level,
+                                uint16_t* cdf_anchor, uint16_t* cdf_delta_level, void* ws,
+                                hipStream_t st) {
+  unsigned long long* pool = static_cast<unsigned long long*>(ws);           // [2][256]
+  uint16_t* tab = reinterpret_cast<uint16_t*>(static_cast<uint8_t*>(ws) + 4096);  // [2][256]
+  const size_t lds = 2 * 64 * kHist * sizeof(uint32_t);
+  hipError_t e = hipFuncSetAttribute((const void*)fit_kernel<true>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(pool_zero, dim3(1), dim3(256), 0, st, pool);
+  const int64_t grid = (int64_t)P.L * 2 * P.nblk;
+  hipLaunchKernelGGL(fit_kernel<true>, dim3((unsigned)grid), dim3(kFitThreads), lds, st, P, kv,
+                     level, cdf_anchor, cdf_delta_level, pool);
+  hipLaunchKernelGGL(pool_normalize, dim3(1), dim3(128), 0, st, pool, tab);
+  const int64_t n_tables = (int64_t)P.L * 2 * P.C;
+  const int64_t blocks = (2 * n_tables + 3) / 4;
+  hipLaunchKernelGGL(pool_broadcast, dim3((unsigned)blocks), dim3(256), 0, st, tab, n_tables,
                      cdf_anchor, cdf_delta_level);
   return hipGetLastError();
 }
