@@ -216,6 +216,38 @@ int cg_decode_streamed(const cg_params* p, const uint32_t* words_host,
                        hipStream_t decode_stream, hipStream_t copy_stream,
                        cg_stream_stats* stats);
 
+/* Streaming adaptation (Sec. 5.3 "KV cache streaming adaptation"; App. B, Alg. 1): the
+ * configuration of each chunk — text (the receiver recomputes its KV) or one encoding level — is
+ * chosen while the chunks are sent, so the transfer stays within a time-to-first-token SLO.
+ * Host-only logic; it plans and simulates one context's transfer over a given bandwidth trace.
+ * Levels are ordered by compression loss: level 0 loses least (largest payload). */
+typedef struct cg_adapt_params {
+  int32_t n_chunks;
+  int32_t n_levels;
+  const double* level_bytes;   /* [n_chunks][n_levels] payload bytes of chunk c at level v */
+  const double* text_bytes;    /* [n_chunks] bytes of the chunk's text */
+  const double* recompute_ms;  /* [n_chunks] time to recompute the chunk's KV from its text;
+                                  NULL: text is never chosen */
+  double slo_ms;               /* time-to-first-token objective for the whole context */
+  double prior_gbps;           /* throughput known before the first chunk; <= 0: unknown */
+  int32_t default_level;       /* level of the first chunk when no throughput is known */
+} cg_adapt_params;
+
+/* Plan and simulate: for every chunk in order, with the throughput estimate (the previous
+ * chunk's measured throughput, or prior_gbps / none for the first) and remaining = slo_ms -
+ * elapsed, choose text if the remaining chunks' recompute time fits in remaining (and
+ * recompute_ms is given), else the lowest-loss level whose remaining chunks' bytes at that level
+ * would arrive within remaining at the estimated throughput, else the most compressed level;
+ * the first chunk without an estimate takes default_level (or text if its rule holds). The
+ * chunk is then sent at bandwidth_gbps[c] (its actual rate), which is also the next chunk's
+ * estimate; elapsed grows by its transfer time, plus its recompute time when sent as text.
+ *   bandwidth_gbps  [n_chunks] host, the link rate each chunk experiences (> 0).
+ *   choice_out      [n_chunks] host out: the chosen level, or -1 for text.
+ *   ttft_ms_out     host out: elapsed time after the last chunk (the simulated TTFT).
+ * Returns CG_OK, or CG_ERR_ARG for a null pointer or a non-positive count or rate. */
+int cg_adapt_schedule(const cg_adapt_params* a, const double* bandwidth_gbps,
+                      int32_t* choice_out, double* ttft_ms_out);
+
 /* Scan kv_f16 [n_elem] for NaN / Inf (fp16 exponent field all ones), using flag_dev, one
  * caller-owned device uint32_t, as scratch. Synchronises `stream`. Returns CG_OK,
  * CG_ERR_NONFINITE, or an error code. The quantizer is defined for finite input only;

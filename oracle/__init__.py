@@ -393,3 +393,52 @@ def stream_symbols(kv, shape: Shape, chunk_level, stream_id):
     w = float(np.float32(bw * np.float32(sc)))
     sym, rec = quantize_stream(x, shape.group_size, sc, w)
     return sc, sym, rec
+
+
+# --------------------------------------------------------------------------------------------
+# Streaming adaptation (Sec. 5.3 "KV cache streaming adaptation"; App. B, Alg. 1), plain Python.
+# --------------------------------------------------------------------------------------------
+def adapt_schedule(level_bytes, text_bytes, recompute_ms, slo_ms, prior_gbps, default_level,
+                   bandwidth_gbps):
+    """The streaming adapter of Alg. 1, one chunk at a time, in the algorithm's terms:
+    remaining_time = SLO - time_elapsed; text if time_recompute (of the chunks still to send)
+    fits in remaining_time; else the encoding level with the least compression loss whose size
+    of the chunks still to send, divided by the throughput (the previous chunk's measured one),
+    fits; else the smallest one. The first chunk without a throughput takes the default level.
+    Returns (choices, ttft_ms) with choice -1 for text."""
+    chunks_to_send = list(range(len(text_bytes)))
+    n_levels = len(level_bytes[0])
+    time_elapsed = 0.0
+    throughput = prior_gbps if prior_gbps > 0 else None
+    choices = []
+    while chunks_to_send:
+        c = chunks_to_send[0]
+        remaining_time = slo_ms - time_elapsed
+        choice = None
+        if recompute_ms is not None:
+            time_recompute = 0.0
+            for i in chunks_to_send:
+                time_recompute += recompute_ms[i]
+            if time_recompute <= remaining_time:
+                choice = -1
+        if choice is None:
+            if throughput is None:
+                choice = default_level
+            else:
+                for level in range(n_levels):          # level 0 loses least
+                    size = 0.0
+                    for i in chunks_to_send:
+                        size += level_bytes[i][level]
+                    if size * 8.0 / (throughput * 1.0e6) <= remaining_time:
+                        choice = level
+                        break
+                if choice is None:
+                    choice = n_levels - 1
+        sent = text_bytes[c] if choice < 0 else level_bytes[c][choice]
+        time_elapsed += sent * 8.0 / (bandwidth_gbps[c] * 1.0e6)
+        if choice < 0:
+            time_elapsed += recompute_ms[c]
+        choices.append(choice)
+        throughput = bandwidth_gbps[c]
+        chunks_to_send = chunks_to_send[1:]
+    return choices, time_elapsed

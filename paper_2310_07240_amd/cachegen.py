@@ -24,7 +24,8 @@ ERRORS = {-1: "CG_ERR_ARG", -2: "CG_ERR_SHAPE", -3: "CG_ERR_CAPACITY", -4: "CG_E
 
 EXPORTS = ("cg_num_chunks", "cg_num_streams", "cg_encode_bound_words",
            "cg_encode_workspace_bytes", "cg_fit_cdf", "cg_fit_cdf_global", "cg_encode",
-           "cg_decode", "cg_decode_streamed", "cg_check_finite", "cg_strerror")
+           "cg_decode", "cg_decode_streamed", "cg_adapt_schedule", "cg_check_finite",
+           "cg_strerror")
 CG_FIT_GLOBAL_WORKSPACE_BYTES = 8192
 
 
@@ -41,6 +42,13 @@ class _CParams(ctypes.Structure):
                 ("n_levels", ctypes.c_int32),
                 ("layer_bin", ctypes.POINTER(ctypes.c_float)),
                 ("level_mult", ctypes.POINTER(ctypes.c_float))]
+
+
+class _AdaptParams(ctypes.Structure):
+    _fields_ = [("n_chunks", ctypes.c_int32), ("n_levels", ctypes.c_int32),
+                ("level_bytes", ctypes.c_void_p), ("text_bytes", ctypes.c_void_p),
+                ("recompute_ms", ctypes.c_void_p), ("slo_ms", ctypes.c_double),
+                ("prior_gbps", ctypes.c_double), ("default_level", ctypes.c_int32)]
 
 
 class StreamStats(ctypes.Structure):
@@ -83,6 +91,8 @@ def lib():
         L.cg_decode_streamed.argtypes = [PP, _P, _P, _P, ctypes.c_uint64, _P, _P, _P, _P, _P, _P,
                                          ctypes.c_double, _P, _P, ctypes.POINTER(StreamStats)]
         L.cg_decode_streamed.restype = ctypes.c_int
+        L.cg_adapt_schedule.argtypes = [ctypes.POINTER(_AdaptParams), _P, _P, _P]
+        L.cg_adapt_schedule.restype = ctypes.c_int
         L.cg_check_finite.argtypes = [PP, _P, _P, _P]
         L.cg_check_finite.restype = ctypes.c_int
         L.cg_strerror.argtypes = [ctypes.c_int]
@@ -221,6 +231,24 @@ def cg_decode_streamed(p: CodecParams, words_host, offsets_host, words_dev, offs
                                     _ptr(kv_out), float(link_gbps), _stream(decode_stream),
                                     _stream(copy_stream), ctypes.byref(st)), "cg_decode_streamed")
     return st.as_dict()
+
+
+def cg_adapt_schedule(level_bytes, text_bytes, recompute_ms, slo_ms: float, prior_gbps: float,
+                      default_level: int, bandwidth_gbps):
+    """Streaming adaptation plan for one context (host only): returns (choices, ttft_ms), a
+    choice being the encoding level or -1 for text. level_bytes is [n_chunks][n_levels]."""
+    lb = np.ascontiguousarray(level_bytes, np.float64)
+    tb = np.ascontiguousarray(text_bytes, np.float64)
+    rc = None if recompute_ms is None else np.ascontiguousarray(recompute_ms, np.float64)
+    bw = np.ascontiguousarray(bandwidth_gbps, np.float64)
+    n, v = lb.shape
+    a = _AdaptParams(n, v, lb.ctypes.data, tb.ctypes.data, None if rc is None else rc.ctypes.data,
+                     float(slo_ms), float(prior_gbps), int(default_level))
+    choices = np.zeros(n, np.int32)
+    ttft = ctypes.c_double(0.0)
+    _check(lib().cg_adapt_schedule(ctypes.byref(a), bw.ctypes.data, choices.ctypes.data,
+                                   ctypes.byref(ttft)), "cg_adapt_schedule")
+    return choices.tolist(), ttft.value
 
 
 def cg_check_finite(p: CodecParams, kv, flag, stream=None) -> bool:

@@ -256,6 +256,50 @@ int cg_decode_streamed(const cg_params* p, const uint32_t* words_host,
   return ok && synced && timed ? CG_OK : CG_ERR_HIP;
 }
 
+int cg_adapt_schedule(const cg_adapt_params* a, const double* bandwidth_gbps,
+                      int32_t* choice_out, double* ttft_ms_out) {
+  if (!a || !bandwidth_gbps || !choice_out || !ttft_ms_out || !a->level_bytes || !a->text_bytes)
+    return CG_ERR_ARG;
+  const int N = a->n_chunks, V = a->n_levels;
+  if (N <= 0 || V <= 0 || a->default_level < 0 || a->default_level >= V) return CG_ERR_ARG;
+  for (int c = 0; c < N; ++c)
+    if (!(bandwidth_gbps[c] > 0.0)) return CG_ERR_ARG;
+  // milliseconds to move `bytes` at `gbps`
+  auto ms_at = [](double bytes, double gbps) { return bytes * 8.0 / (gbps * 1.0e6); };
+  double elapsed = 0.0;
+  bool have_est = a->prior_gbps > 0.0;
+  double est = a->prior_gbps;
+  for (int c = 0; c < N; ++c) {
+    const double remaining = a->slo_ms - elapsed;
+    int choice = -2;
+    if (a->recompute_ms) {   // text: the receiver recomputes the remaining chunks' KV
+      double t_text = 0.0;
+      for (int i = c; i < N; ++i) t_text += a->recompute_ms[i];
+      if (t_text <= remaining) choice = -1;
+    }
+    if (choice == -2) {
+      if (!have_est) {
+        choice = a->default_level;
+      } else {
+        for (int v = 0; v < V && choice == -2; ++v) {   // lowest compression loss first
+          double bytes = 0.0;
+          for (int i = c; i < N; ++i) bytes += a->level_bytes[(size_t)i * V + v];
+          if (ms_at(bytes, est) <= remaining) choice = v;
+        }
+        if (choice == -2) choice = V - 1;
+      }
+    }
+    const double bytes = choice < 0 ? a->text_bytes[c] : a->level_bytes[(size_t)c * V + choice];
+    elapsed += ms_at(bytes, bandwidth_gbps[c]);
+    if (choice < 0) elapsed += a->recompute_ms[c];
+    choice_out[c] = choice;
+    est = bandwidth_gbps[c];   // the next chunk's estimate: this chunk's measured throughput
+    have_est = true;
+  }
+  *ttft_ms_out = elapsed;
+  return CG_OK;
+}
+
 int cg_check_finite(const cg_params* p, const uint16_t* kv_f16, uint32_t* flag_dev,
                     hipStream_t stream) {
   KParams K;

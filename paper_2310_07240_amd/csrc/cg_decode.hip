@@ -38,6 +38,7 @@
 namespace {
 
 constexpr int kMaxWaves = 16;
+constexpr size_t kLdsBudget = 160 * 1024 - 1024;   // dynamic LDS per workgroup (CDNA4: 160 KB)
 constexpr int kTabStride = 260;    // u16 per delta table in LDS (256 + 4 pad -> 520 bytes)
 constexpr int kFenceStride = 18;   // u16 per anchor fence row (16 + 2 pad -> 36 bytes)
 constexpr int kEpoch = 4;          // tokens between bitstream requests
@@ -738,13 +739,21 @@ hipError_t cg_launch_decode(const KParams& P, const uint32_t* words, const uint6
                             int c_end, uint16_t* out, hipStream_t st) {
   const int64_t n_pairs = (int64_t)P.B * (c_end - c_begin);
   if (n_pairs == 0) return hipSuccess;
-  const int nw = (int)(n_pairs < kMaxWaves ? n_pairs : kMaxWaves);
+  // LDS of a workgroup of w waves: row buffers plus one delta table set per level its pairs
+  // may use (sized for the worst case, min(w, levels) sets); fewer waves per workgroup when
+  // that exceeds what a CU offers
+  const bool g10 = P.G == kG10;
+  auto lds_for = [&](int w) {
+    const size_t sets = (size_t)(w < P.NLV ? w : P.NLV);
+    const size_t rows = g10 ? (size_t)w * kG10 * 64 : (size_t)64 * kFenceStride + (size_t)w * kRows * 64;
+    return (rows + sets * 64 * kTabStride) * sizeof(uint16_t);
+  };
+  int nw = (int)(n_pairs < kMaxWaves ? n_pairs : kMaxWaves);
+  while (nw > 1 && lds_for(nw) > kLdsBudget) --nw;
   const int64_t n_groups = (n_pairs + nw - 1) / nw;
-  const int nsets_max = nw < P.NLV ? nw : P.NLV;
   const int64_t grid = (int64_t)P.L * 2 * P.nblk * n_groups;
-  const size_t tab_u16 = (size_t)nsets_max * 64 * kTabStride;
-  if (P.G == kG10) {
-    const size_t lds = ((size_t)nw * kG10 * 64 + tab_u16) * sizeof(uint16_t);
+  const size_t lds = lds_for(nw);
+  if (g10) {
     hipError_t e = hipFuncSetAttribute((const void*)decode_g10_kernel,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
@@ -753,8 +762,6 @@ hipError_t cg_launch_decode(const KParams& P, const uint32_t* words, const uint6
                        nw, out);
     return hipGetLastError();
   }
-  const size_t lds =
-      ((size_t)64 * kFenceStride + (size_t)nw * kRows * 64 + tab_u16) * sizeof(uint16_t);
   hipError_t e = hipFuncSetAttribute((const void*)decode_kernel,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;

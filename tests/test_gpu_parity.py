@@ -21,6 +21,12 @@ SMALL = [
             level_mult=(1.0, 2.0, 4.0)),
     W.small(name="long_chunk_1536", n_layers=2, n_tokens=1600, chunk_len=1536, n_channels=65,
             level_mult=(1.0, 8.0)),
+    # eight levels over sixteen chunks: a workgroup's worst-case table sets exceed the LDS of a
+    # CU at sixteen waves, so the launchers use fewer waves per workgroup
+    W.small(name="levels8_chunks16", n_layers=2, n_tokens=160, chunk_len=10, n_channels=64,
+            level_mult=(1.0, 2.0, 4.0, 8.0, 16.0, 32.0, 64.0, 128.0)),
+    W.small(name="levels8_chunks16_g7", n_layers=2, n_tokens=160, chunk_len=10, n_channels=64,
+            group_size=7, level_mult=(1.0, 2.0, 4.0, 8.0, 16.0, 32.0, 64.0, 128.0)),
 ]
 
 
