@@ -14,7 +14,11 @@ reports the payload bits per element and the error of the decoded cache. The con
      (bin 1.0 s in every layer), so the error bound s/2 of configurations 1-2 is kept;
   4. + layer-wise quantization: the workload's per-layer bins (0.5 / 1 / 1.5 s by layer group),
      i.e. CacheGen's encoder;
-  5. CacheGen's encoder with one global distribution instead of per channel-layer ones.
+  5. CacheGen's encoder with one global distribution instead of per channel-layer ones;
+  6. CacheGen's encoder with per channel-layer distributions fitted on another context of the
+     same model (the same generator with another seed): the paper profiles the distributions
+     offline per model and reuses them for every context (Sec. 5.2), while its implementation
+     counts them per context (Sec. 6).
 
 Chunks are all coded at the first encoding level (multiplier level_mult[0]).
 
@@ -35,6 +39,7 @@ LADDER = (
     ("+ change-based encoding (anchor + delta)", 10, "uniform", "channel"),
     ("+ layer-wise quantization (CacheGen)", 10, "layer", "channel"),
     ("CacheGen with one global distribution", 10, "layer", "global"),
+    ("CacheGen with distributions of another context", 10, "layer", "other"),
 )
 
 
@@ -61,6 +66,12 @@ def run(w, device="cuda"):
         if fit == "global":
             ws = torch.empty((CG_FIT_GLOBAL_WORKSPACE_BYTES,), dtype=torch.uint8, device=device)
             cg_fit_cdf_global(p, kv, 0, ca, cd[0], ws)
+        elif fit == "other":
+            other = W.generate(dataclasses.replace(wc, seed=wc.seed + 1000))
+            kv_other = torch.from_numpy(other.view(np.int16)).to(device)
+            cg_fit_cdf(p, kv_other, 0, ca, cd[0])
+            torch.cuda.synchronize()
+            del kv_other
         else:
             cg_fit_cdf(p, kv, 0, ca, cd[0])
         cl = torch.zeros((wc.n_ctx, codec.n_chunks), dtype=torch.uint8, device=device)
