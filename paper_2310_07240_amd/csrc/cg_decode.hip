@@ -1,21 +1,22 @@
 // cg_decode.hip — GPU arithmetic decoding back to fp16 KV (CacheGen Sec. 5.2 "Arithmetic
 // coding"; Sec. 6 "Speed optimization": decoding runs on the GPU, chunk by chunk).
 //
-// Work layout
+// Work layout (both kernels)
 //   One lane per stream. A wave decodes the 64 consecutive channels of one (context, chunk,
 //   layer, K/V), so each decoded token row is one coalesced 128-byte store. A workgroup holds
 //   up to 16 such waves that share (layer, K/V, channel block) and therefore share their
-//   distribution tables, which are staged in LDS once per workgroup:
-//     * delta tables (9 of 10 symbols): the whole 16-bit cumulative table, 256 entries, at a
-//       520-byte stride (8-byte aligned; neighbouring lanes start in different banks), entries
-//       255..259 holding 0xFFFF sentinels. Search: a 4-ary search over four levels (three
-//       probes per level, the same steps in every lane, no divergence), the last level a single
-//       aligned 8-byte read of four neighbouring entries.
-//     * anchor tables (1 of 10 symbols; broad distributions): only 16 fences cum[16 f] per
-//       table stay in LDS (36-byte stride). A 4-step fence search picks the block of 16
-//       symbols, one 32-byte global load brings that block (L2-resident), and a 4-step binary
-//       search over registers finishes. This keeps a workgroup of the Mistral-7B-shaped cache
-//       at 35 KB so every wave of the grid is resident at once.
+//   distribution tables; the delta tables (9 of 10 symbols) of the levels present are staged in
+//   LDS once per workgroup: the whole 16-bit cumulative table, 256 entries, at a 520-byte stride
+//   (8-byte aligned; neighbouring lanes start in different banks), entries 255..259 holding
+//   0xFFFF sentinels. Anchor tables (1 of 10 symbols) stay in global memory; a symbol reads one
+//   32-byte block of 16 entries and finishes with a select search in registers. Fewer waves
+//   per workgroup when the worst-case table sets would not fit in a CU's LDS.
+//
+// decode_kernel (any group size): anchor fences cum[16 f] in LDS; the delta search is a 4-ary
+//   search over four levels in LDS (three probes per level, the last level one aligned 8-byte
+//   read of four neighbouring entries); bitstream epochs every four tokens.
+// decode_g10_kernel (group size 10, the paper's): the token schedule of a group is fixed at
+//   compile time and the fences of both tables sit in registers (see the kernel's comment).
 //
 // Decoder state per lane (Witten-Neal-Cleary decoder, rewritten on differences):
 //   low  - low end of the interval;  rm1 - high - low;  D - code value - low (<= rm1)
