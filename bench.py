@@ -15,6 +15,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -38,8 +39,14 @@ DECODE_SRC = os.path.join(ROOT, "paper_2310_07240_amd", "csrc", "cg_decode.hip")
 
 
 def decode_source_hash() -> str:
-    with open(DECODE_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of the decode kernels' source without comments and blank space, so a profile stays
+    valid across comment edits and goes stale on any code change."""
+    with open(DECODE_SRC) as f:
+        src = f.read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", "", src)
+    src = re.sub(r"\s+", " ", src).strip()
+    return hashlib.sha256(src.encode()).hexdigest()[:16]
 
 
 def measured_traffic(workload: str):
