@@ -47,12 +47,13 @@ constexpr int kRows = 8;           // decoded token rows staged in LDS per wave 
 
 __device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
-// x * c + c2 >> 16 as one 32x32+64 multiply-add. The addend passes through an empty asm so the
-// compiler cannot fold x*c + c into a 64-bit (x + 1) * c.
+// (x * c + c) >> 16 = (x + 1) * c >> 16 with x + 1 up to 2^32, as one 32x32+64 multiply-add
+// (written out so that it is not rewritten as a 64-bit product of x + 1, and so that c can be
+// both the multiplier and the low half of the addend).
 __device__ __forceinline__ uint32_t scaled_off(uint32_t x, uint32_t c) {
-  uint32_t c2 = c;
-  asm volatile("" : "+v"(c2));
-  return (uint32_t)(((uint64_t)x * c + c2) >> 16);
+  uint64_t r, carry;
+  asm("v_mad_u64_u32 %0, %1, %2, %3, %4" : "=v"(r), "=s"(carry) : "v"(x), "v"(c), "v"((uint64_t)c));
+  return (uint32_t)(r >> 16);
 }
 
 // Make the compiler wait here for a register produced by a load (once, outside the loop).
@@ -67,6 +68,13 @@ __device__ __forceinline__ uint32_t e3_run(uint32_t L1, uint32_t H1) {
   uint32_t n;
   asm("v_ffbh_i32 %0, %1" : "=v"(n) : "v"((L1 & ~H1) | 0x80000000u));
   return n - 1u;
+}
+
+// The same run plus one (the v_ffbh_i32 count itself, >= 1).
+__device__ __forceinline__ uint32_t e3_run1(uint32_t L1, uint32_t H1) {
+  uint32_t n;
+  asm("v_ffbh_i32 %0, %1" : "=v"(n) : "v"((L1 & ~H1) | 0x80000000u));
+  return n;
 }
 
 // 16-byte store of decoded fp16 that is not read again by this kernel (non-temporal, so the
@@ -128,6 +136,24 @@ __device__ __forceinline__ uint32_t select16(const uint32_t (&v)[17], uint32_t t
   lo = l;
   hi = h;
   return (c3 ? 8u : 0u) | (c2 ? 4u : 0u) | (c1 ? 2u : 0u) | (c0 ? 1u : 0u);
+}
+
+// 16 j - 127 for the largest j in [0, 15] with v[j] <= ti (sorted v, v[0] <= ti < v[16]): the
+// select search of select16 without the bounds, its index already scaled and biased so that
+// adding the offset of the symbol inside the block gives the quantized value.
+__device__ __forceinline__ int fence_q(const uint32_t (&v)[17], uint32_t ti) {
+  const bool c3 = v[8] <= ti;
+  const uint32_t p4 = c3 ? v[12] : v[4];
+  const uint32_t p2a = c3 ? v[10] : v[2], p2b = c3 ? v[14] : v[6];
+  const uint32_t p1a = c3 ? v[9] : v[1], p1b = c3 ? v[11] : v[3];
+  const uint32_t p1c = c3 ? v[13] : v[5], p1d = c3 ? v[15] : v[7];
+  const bool c2 = p4 <= ti;
+  const uint32_t p2 = c2 ? p2b : p2a;
+  const uint32_t p1e = c2 ? p1c : p1a, p1f = c2 ? p1d : p1b;
+  const bool c1 = p2 <= ti;
+  const uint32_t p1 = c1 ? p1f : p1e;
+  const bool c0 = p1 <= ti;
+  return (c3 ? 1 : -127) + (c2 ? 64 : 0) + (c1 ? 32 : 0) + (c0 ? 16 : 0);
 }
 
 __global__ __launch_bounds__(1024) void decode_kernel(
@@ -422,40 +448,40 @@ __global__ __launch_bounds__(1024) void decode_kernel(
 constexpr int kG10 = 10;
 
 // Per-lane decoder state of the group-of-10 kernel (plain scalars: it lives in registers).
+// Bitstream reader: the 128 bits after the code value's own are held in w0..w3, of which the
+// first `pos` bits of w0 are already consumed. A token takes n <= 18 bits (the interval is
+// wider than 2^30 before a symbol and at least 2^14 after it, and renormalisation doubles it
+// to at most 2^32), so it crosses at most one word boundary and w0 moves up by at most one
+// word; four tokens take at most 72 bits, which never reach past w3 from an epoch start with
+// pos < 32, so at most three words leave between two epoch boundaries.
 struct G10Lane {
   uint32_t D, low, rm1;          // code value - low, low, high - low
-  uint64_t buf;                  // bit buffer, `avail` valid bits from the top
-  uint32_t avail;
-  uint32_t s0, s1, s2, s3;       // shift register of unread words
-  uint32_t t0, t1, t2, t3;       // the next four words, requested one epoch ahead
-  uint32_t hcnt;                 // words moved from s0 into buf since the last epoch
-  uint64_t wpos;                 // payload index of t0
+  uint32_t w0, w1, w2, w3;       // the next stream words, w0 partly consumed
+  uint32_t pos;                  // bits of w0 already taken (< 32)
+  uint32_t t0, t1, t2, t3;       // the four words after w3, requested one epoch ahead
+  uint32_t hcnt;                 // words moved out of w0 since the last epoch (<= 3)
+  uint32_t widx;                 // index of t0's word from the stream's first word
   float a;                       // dequantized anchor of the current group
 };
 
-// Epoch boundary: drop the hcnt words used since the last boundary from the shift register,
-// append as many requested words, and request the next four.
-__device__ __forceinline__ void g10_epoch(G10Lane& st, const uint32_t* __restrict__ words,
-                                          uint64_t wcap) {
+// Epoch boundary: the hcnt words dropped from the front of w0..w3 since the last boundary are
+// replaced at the back by as many requested words, and the next four are requested.
+__device__ __forceinline__ void g10_epoch(G10Lane& st, const uint32_t* __restrict__ sbase,
+                                          uint32_t cap) {
   const uint32_t h = st.hcnt;
   // register copies behind an empty asm: selects between the fields themselves could be
   // turned into a select of their addresses, which would move the state to scratch memory
-  uint32_t t0 = st.t0, t1 = st.t1, t2 = st.t2, t3 = st.t3;
-  uint32_t s0 = st.s0, s1 = st.s1, s2 = st.s2, s3 = st.s3;
-  asm("" : "+v"(t0), "+v"(t1), "+v"(t2), "+v"(t3), "+v"(s0), "+v"(s1), "+v"(s2), "+v"(s3));
-  const bool g1 = h >= 1, g2 = h >= 2, g3 = h >= 3, g4 = h >= 4;
-  const uint32_t n3 = g4 ? t3 : (g3 ? t2 : (g2 ? t1 : (g1 ? t0 : s3)));
-  const uint32_t n2 = g4 ? t2 : (g3 ? t1 : (g2 ? t0 : s2));
-  const uint32_t n1 = g4 ? t1 : (g3 ? t0 : s1);
-  const uint32_t n0 = g4 ? t0 : s0;
-  st.s0 = n0;
-  st.s1 = n1;
-  st.s2 = n2;
-  st.s3 = n3;
-  st.wpos += h;
+  uint32_t t0 = st.t0, t1 = st.t1, t2 = st.t2;
+  uint32_t w1 = st.w1, w2 = st.w2, w3 = st.w3;
+  asm("" : "+v"(t0), "+v"(t1), "+v"(t2), "+v"(w1), "+v"(w2), "+v"(w3));
+  const bool g1 = h >= 1, g2 = h >= 2, g3 = h >= 3;
+  st.w3 = g3 ? t2 : (g2 ? t1 : (g1 ? t0 : w3));
+  st.w2 = g3 ? t1 : (g2 ? t0 : w2);
+  st.w1 = g3 ? t0 : w1;
+  st.widx += h;
   st.hcnt = 0;
   __builtin_amdgcn_sched_barrier(0);
-  const uint32_t* tq = words + (st.wpos < wcap ? st.wpos : wcap);
+  const uint32_t* tq = sbase + (st.widx < cap ? st.widx : cap);
   st.t0 = tq[0];
   st.t1 = tq[1];
   st.t2 = tq[2];
@@ -472,7 +498,8 @@ __device__ __forceinline__ void g10_token(G10Lane& st, const uint32_t (&fA)[17],
   const float te = (float)st.D * (65536.0f * __builtin_amdgcn_rcpf((float)st.rm1));
   const uint32_t ti = min((uint32_t)te, 65534u);
   const uint32_t kneg = ~ti;
-  int sym;
+  const uint16_t* dtab127 = dtab + 127;
+  int qi;   // quantized value = symbol - 127
   uint32_t clo, chi;
   if constexpr (kAnchor) {
     uint32_t flo, fhi;
@@ -487,23 +514,29 @@ __device__ __forceinline__ void g10_token(G10Lane& st, const uint32_t (&fA)[17],
     v[15] = f == 15 ? CG_TOTAL : q1.w >> 16;   // symbol 255 does not exist
     v[16] = fhi;
     const uint32_t jj = select16(v, ti, clo, chi);
-    sym = (int)(16 * f + jj);
+    qi = (int)(16 * f + jj) - 127;
   } else {
-    uint32_t flo, fhi;
-    const uint32_t f = select16(fD, ti, flo, fhi);
-    const uint16_t* q = dtab + 16 * f;
-    q += 4 * ((((uint32_t)q[4] + kneg) >> 31) + (((uint32_t)q[8] + kneg) >> 31) +
-              (((uint32_t)q[12] + kneg) >> 31));
+    const int fq = fence_q(fD, ti);           // 16 f - 127
+    const uint16_t* q = dtab127 + fq;          // the block of cum[16 f]
+    const int l4 = 4 * (int)((((uint32_t)q[4] + kneg) >> 31) + (((uint32_t)q[8] + kneg) >> 31) +
+                             (((uint32_t)q[12] + kneg) >> 31));
+    q += l4;
     uint32_t pr;
     const uint32_t cc = delta_leaf(q, ti, pr);
-    sym = (int)((((uint32_t)(uintptr_t)q - (uint32_t)(uintptr_t)dtab) >> 1) + cc);
+    qi = fq + l4 + (int)cc;
     clo = pr & 0xFFFFu;
-    chi = sym == CG_NSYM - 1 ? CG_TOTAL : pr >> 16;
+    chi = qi == CG_NSYM - 1 - 127 ? CG_TOTAL : pr >> 16;
   }
   const uint32_t D = st.D, rm1 = st.rm1;
+  // offsets of the candidate's interval from low: [lo_off, hoff) (hoff mod 2^32). The candidate
+  // is the symbol iff D - lo_off < hoff - lo_off (unsigned): below lo_off the difference wraps
+  // past the interval's size, which is below 2^32 - lo_off.
   uint32_t lo_off = scaled_off(rm1, clo);
-  uint32_t hm1 = scaled_off(rm1, chi) - 1u;
-  if (D < lo_off || D > hm1) {
+  uint32_t hoff = scaled_off(rm1, chi);
+  uint32_t d = D - lo_off;
+  uint32_t rsz = hoff - lo_off;
+  if (d >= rsz) {
+    int sym = qi + 127;
     for (int guard = 0; guard < CG_NSYM; ++guard) {
       sym = (D < lo_off) ? max(sym - 1, 0) : min(sym + 1, CG_NSYM - 1);
       const int s1 = min(sym + 1, CG_NSYM - 1);
@@ -516,33 +549,38 @@ __device__ __forceinline__ void g10_token(G10Lane& st, const uint32_t (&fA)[17],
       }
       chi = sym + 1 >= CG_NSYM ? CG_TOTAL : chi;
       lo_off = scaled_off(rm1, clo);
-      hm1 = scaled_off(rm1, chi) - 1u;
-      if (D >= lo_off && D <= hm1) break;
+      hoff = scaled_off(rm1, chi);
+      d = D - lo_off;
+      rsz = hoff - lo_off;
+      if (d < rsz) break;
     }
+    qi = sym - 127;
   }
-  uint32_t low = st.low + lo_off;
-  uint32_t r1 = hm1 - lo_off;
-  uint32_t d = D - lo_off;
-  const uint32_t high = low + r1;
+  // renormalisation: n1 shared leading bits of low and high, then the middle-half run of
+  // n3 = f - 1 steps; the new low is L1 << n3 without its top bit
+  const uint32_t low = st.low + lo_off;
+  const uint32_t high = st.low + hoff - 1u;
   const uint32_t n1 = (uint32_t)__builtin_clz(low ^ high);
   const uint32_t L1 = low << n1, H1 = high << n1;
-  const uint32_t n3 = e3_run(L1, H1);
-  st.low = (L1 << n3) & 0x7FFFFFFFu;   // L1 has a clear top bit
-  const uint32_t nsh = n1 + n3;
-  st.rm1 = (r1 << nsh) | ((1u << nsh) - 1u);
-  const uint32_t dsh = __builtin_amdgcn_alignbit(d, (uint32_t)(st.buf >> 32), 32u - nsh);
-  st.D = nsh ? dsh : d;
-  st.buf <<= nsh;
-  st.avail -= nsh;
-  if (st.avail < 32) {
-    st.buf |= (uint64_t)st.s0 << (32 - st.avail);
-    st.avail += 32;
-    st.s0 = st.s1;
-    st.s1 = st.s2;
-    st.s2 = st.s3;
-    ++st.hcnt;
-  }
-  const float qf = (float)(sym - 127);
+  const uint32_t f = e3_run1(L1, H1);
+  st.low = (L1 << f) >> 1;
+  const uint32_t nsh = n1 + f - 1u;
+  // high - low + 1 scales by 2^nsh (a result of 2^32 wraps to 0, giving rm1 = 2^32 - 1)
+  st.rm1 = (rsz << nsh) - 1u;
+  // D takes the next nsh stream bits: the 32 bits at `pos` of w0:w1, then a 64-bit shift
+  const uint64_t wp = ((uint64_t)st.w0 << 32) | st.w1;
+  const uint32_t win = (uint32_t)((wp << st.pos) >> 32);
+  uint32_t Dn = (uint32_t)(((((uint64_t)d) << 32) | win) << nsh >> 32);
+  asm("" : "+v"(Dn));   // keep D a 32-bit value (not the top half of a 64-bit one)
+  st.D = Dn;
+  const uint32_t p2 = st.pos + nsh;
+  const bool adv = p2 >= 32u;
+  st.w0 = adv ? st.w1 : st.w0;
+  st.w1 = adv ? st.w2 : st.w1;
+  st.w2 = adv ? st.w3 : st.w2;
+  st.pos = p2 & 31u;
+  st.hcnt += adv ? 1u : 0u;
+  const float qf = (float)qi;
   float v;
   if constexpr (kAnchor) {
     st.a = qf * s;
@@ -670,29 +708,28 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
 
   const uint64_t total = offsets[P.S];
   if (total == 0) return;
-  // bitstream reader: as in the generic kernel (64-bit bit buffer, four-word shift register,
-  // the next four words requested one epoch ahead; at most one word moves per token and at
-  // most four tokens separate two epoch boundaries)
+  // bitstream reader: the code value, w0..w3 and the four requested words t0..t3 are the
+  // stream's first 13 words; every read stays below offsets[S] + 4 (the requests are clamped
+  // to it), inside the readable tail
   G10Lane st;
   const uint64_t o0 = offsets[sidx];
-  const uint32_t* sbase = words + (o0 < total ? o0 : total);
+  const uint64_t ob = o0 < total ? o0 : total;
+  const uint32_t* sbase = words + ob;
+  const uint32_t cap = (uint32_t)((total - ob) < 0xFFFFFFF0ull ? (total - ob) : 0xFFFFFFF0ull);
   st.D = sbase[0];
-  st.buf = (uint64_t)sbase[1] << 32;
-  st.avail = 32;
-  st.s0 = sbase[2];
-  st.s1 = sbase[3];
-  st.s2 = sbase[4];
-  st.s3 = sbase[5];
+  st.w0 = sbase[1];
+  st.w1 = sbase[2];
+  st.w2 = sbase[3];
+  st.w3 = sbase[4];
+  st.pos = 0;
   st.hcnt = 0;
-  st.wpos = (o0 < total ? o0 : total) + 6;
-  const uint64_t wcap = total;
-  const uint32_t* tq0 = words + (st.wpos < wcap ? st.wpos : wcap);
+  st.widx = 5;
+  const uint32_t* tq0 = sbase + (5u < cap ? 5u : cap);
   st.t0 = tq0[0];
   st.t1 = tq0[1];
   st.t2 = tq0[2];
   st.t3 = tq0[3];
-  settle(st.D); settle(st.s0); settle(st.s1); settle(st.s2); settle(st.s3);
-  settle((uint32_t)(st.buf >> 32));
+  settle(st.D); settle(st.w0); settle(st.w1); settle(st.w2); settle(st.w3);
   st.low = 0u;
   st.rm1 = 0xFFFFFFFFu;
   st.a = 0.0f;
@@ -705,15 +742,15 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   const int ngr = n / kG10;
   for (int gi = 0; gi < ngr; ++gi) {
     g10_token<true>(st, fA, fD, dtab, gA, s, w, obuf, 0, lane);
-    g10_epoch(st, words, wcap);
+    g10_epoch(st, sbase, cap);
     g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 1, lane);
     g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 2, lane);
     g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 3, lane);
-    g10_epoch(st, words, wcap);
+    g10_epoch(st, sbase, cap);
     g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 4, lane);
     g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 5, lane);
     g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 6, lane);
-    g10_epoch(st, words, wcap);
+    g10_epoch(st, sbase, cap);
     g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 7, lane);
     g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 8, lane);
     g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 9, lane);
@@ -723,9 +760,9 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   const int rem = n - ngr * kG10;   // last, partial group (uniform)
   if (rem > 0) {
     g10_token<true>(st, fA, fD, dtab, gA, s, w, obuf, 0, lane);
-    g10_epoch(st, words, wcap);
+    g10_epoch(st, sbase, cap);
     for (int r = 1; r < rem; ++r) {
-      if (r == 4 || r == 7) g10_epoch(st, words, wcap);
+      if (r == 4 || r == 7) g10_epoch(st, sbase, cap);
       g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, r, lane);
     }
     g10_flush(obuf, row, rstride, rem, lane, cbase, P.C);
