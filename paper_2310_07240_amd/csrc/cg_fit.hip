@@ -7,7 +7,12 @@
 // chunk's groups across its waves: every wave first reduces the absmax of its token slice, the
 // slices are combined in LDS into the chunk's scale, then every wave quantizes its slice (groups
 // are independent once the scale is known) and counts the symbols into LDS histograms. Rows
-// are read 64 channels (128 B) at a time, so every load is one coalesced line. Histograms use a
+// are read 64 channels (128 B) at a time, so every load is one coalesced line. When the channel
+// count is a multiple of 64 and half of a wave's slice is at most kHalf tokens (the paper's
+// 1.5K-token chunks: 48-50), a lane takes two neighbouring channels (one dword per token) over
+// half of the wave's groups; the slice is read once, into registers, with all its loads in
+// flight together, and both passes work from the registers. Otherwise the rows are read once
+// per pass, a lane per channel. Histograms use a
 // 257-word stride so lanes that count the same symbol hit different banks. At the end each
 // wave normalises histograms to 16-bit cumulative tables: per-lane partial sums, a wave
 // reduction for the total, the argmax and the frequency sum, and a wave prefix scan.
@@ -18,6 +23,7 @@ namespace {
 constexpr int kFitWaves = 16;
 constexpr int kFitThreads = kFitWaves * 64;
 constexpr int kHist = 257;  // 255 symbols, padded; odd stride spreads lanes over the banks
+constexpr int kHalf = 56;   // longest half slice per lane held in registers (one dword per token)
 
 // Normalise one histogram [255] into cum[256] (entry 255 = 0) with one wave.
 template <typename CountT>
@@ -81,7 +87,21 @@ __device__ void normalize_wave(const CountT* cnt, uint16_t* out) {
 
 // kPool: instead of normalising per channel, add the workgroup's counts (summed over its 64
 // channels) to the global counts pool[2][256] (anchor, delta): the one-distribution baseline.
-template <bool kPool>
+// Count one quantized token of a slice: the anchor (group position g == 0) under the 8-bit
+// step s, the others as the delta to the dequantized anchor under step w.
+__device__ __forceinline__ void fit_count(float v, int g, float s, float w, float& a,
+                                          uint32_t* ha, uint32_t* hd) {
+  if (g == 0) {
+    const int q = cg_quant(v, s);
+    a = (float)q * s;
+    atomicAdd(&ha[q + 127], 1u);
+  } else {
+    const int q = cg_quant(v - a, w);
+    atomicAdd(&hd[q + 127], 1u);
+  }
+}
+
+template <bool kPool, bool kRegs>
 __global__ __launch_bounds__(kFitThreads) void fit_kernel(KParams P, const uint16_t* __restrict__ kv,
                                                          int level, uint16_t* __restrict__ cdf_anchor,
                                                          uint16_t* __restrict__ cdf_delta,
@@ -111,33 +131,79 @@ __global__ __launch_bounds__(kFitThreads) void fit_kernel(KParams P, const uint1
     const int gpw = (ng + kFitWaves - 1) / kFitWaves;   // groups per wave
     const int j0 = min(n, wave * gpw * P.G), j1 = min(n, (wave + 1) * gpw * P.G);
     const uint16_t* x = kv + cg_elem(P, b, l, k, t0, act ? ch : cb * 64);
-    // pass 1: absmax of this wave's slice, combined over the waves in LDS
-    float m = 0.0f;
-#pragma unroll 8
-    for (int j = j0; j < j1; ++j) m = fmaxf(m, fabsf(cg_h2f(x[(int64_t)j * rs])));
-    part[wave][lane] = m;
-    __syncthreads();
-    m = 0.0f;
+    if constexpr (kRegs) {
+      // lane = (channel pair cp, token half th): channels cb*64 + 2 cp and + 1, read as one
+      // dword per token (64-channel blocks are whole and dword aligned on this path), over the
+      // th-th half of the wave's groups; each half (at most kHalf tokens, each half's own
+      // length) goes into registers with every load in flight at once
+      const int cp = lane & 31, th = lane >> 5;
+      const int gh = (gpw + 1) >> 1;
+      const int h0 = min(j1, j0 + th * gh * P.G), h1 = min(j1, j0 + (th + 1) * gh * P.G);
+      const int len = h1 - h0;
+      typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+      const half2_t* xw = reinterpret_cast<const half2_t*>(kv + cg_elem(P, b, l, k, t0, cb * 64)) + cp;
+      const int64_t rw = P.C >> 1;
+      half2_t pk[kHalf];
 #pragma unroll
-    for (int v = 0; v < kFitWaves; ++v) m = fmaxf(m, part[v][lane]);
-    const float s = (m == 0.0f) ? 1.0f : m / 127.0f;
-    const float w = wfac * s;
-    // pass 2: quantize the slice (it starts on a group boundary) and count
-    if (act) {
-      float a = 0.0f;
+      for (int u = 0; u < kHalf; ++u) pk[u] = xw[(int64_t)min(h0 + u, n - 1) * rw];
+      float m0 = 0.0f, m1 = 0.0f;
+#pragma unroll
+      for (int u = 0; u < kHalf; ++u) {
+        if (u < len) {
+          m0 = fmaxf(m0, fabsf((float)pk[u].x));
+          m1 = fmaxf(m1, fabsf((float)pk[u].y));
+        }
+      }
+      m0 = fmaxf(m0, __shfl_xor(m0, 32, 64));
+      m1 = fmaxf(m1, __shfl_xor(m1, 32, 64));
+      if (th == 0) {
+        part[wave][2 * cp] = m0;
+        part[wave][2 * cp + 1] = m1;
+      }
+      __syncthreads();
+      m0 = 0.0f;
+      m1 = 0.0f;
+#pragma unroll
+      for (int v = 0; v < kFitWaves; ++v) {
+        m0 = fmaxf(m0, part[v][2 * cp]);
+        m1 = fmaxf(m1, part[v][2 * cp + 1]);
+      }
+      const float s0 = (m0 == 0.0f) ? 1.0f : m0 / 127.0f;
+      const float s1 = (m1 == 0.0f) ? 1.0f : m1 / 127.0f;
+      const float w0 = wfac * s0, w1 = wfac * s1;
+      uint32_t* ha0 = cnt + (2 * cp) * kHist;
+      uint32_t* hd0 = cnt + (64 + 2 * cp) * kHist;
+      float a0 = 0.0f, a1 = 0.0f;
       int g = 0;
-#pragma unroll 4
-      for (int j = j0; j < j1; ++j) {
-        const float v = cg_h2f(x[(int64_t)j * rs]);
-        if (g == 0) {
-          const int q = cg_quant(v, s);
-          a = (float)q * s;
-          atomicAdd(&ha[q + 127], 1u);
-        } else {
-          const int q = cg_quant(v - a, w);
-          atomicAdd(&hd[q + 127], 1u);
+#pragma unroll
+      for (int u = 0; u < kHalf; ++u) {
+        if (u < len) {
+          fit_count((float)pk[u].x, g, s0, w0, a0, ha0, hd0);
+          fit_count((float)pk[u].y, g, s1, w1, a1, ha0 + kHist, hd0 + kHist);
         }
         g = (g + 1 == P.G) ? 0 : g + 1;
+      }
+    } else {
+      // pass 1: absmax of this wave's slice, combined over the waves in LDS
+      float m = 0.0f;
+#pragma unroll 8
+      for (int j = j0; j < j1; ++j) m = fmaxf(m, fabsf(cg_h2f(x[(int64_t)j * rs])));
+      part[wave][lane] = m;
+      __syncthreads();
+      m = 0.0f;
+#pragma unroll
+      for (int v = 0; v < kFitWaves; ++v) m = fmaxf(m, part[v][lane]);
+      const float s = (m == 0.0f) ? 1.0f : m / 127.0f;
+      const float w = wfac * s;
+      // pass 2: quantize the slice (it starts on a group boundary) and count
+      if (act) {
+        float a = 0.0f;
+        int g = 0;
+#pragma unroll 4
+        for (int j = j0; j < j1; ++j) {
+          fit_count(cg_h2f(x[(int64_t)j * rs]), g, s, w, a, ha, hd);
+          g = (g + 1 == P.G) ? 0 : g + 1;
+        }
       }
     }
     __syncthreads();   // `part` is reused by the next pair
@@ -192,16 +258,39 @@ __global__ __launch_bounds__(256) void pool_broadcast(const uint16_t* __restrict
 
 }  // namespace
 
-hipError_t cg_launch_fit(const KParams& P, const uint16_t* kv, int level, uint16_t* cdf_anchor,
-                         uint16_t* cdf_delta_level, hipStream_t st) {
+namespace {
+// Whether the register path applies: whole 64-channel blocks, and half of every wave's slice
+// within kHalf tokens (the longest chunk has ceil(n / G) groups, a wave takes ceil(groups / 16)
+// of them, a lane half of those).
+bool fit_slice_in_registers(const KParams& P) {
+  const int64_t n = P.CL < P.T ? P.CL : P.T;
+  const int64_t ng = (n + P.G - 1) / P.G;
+  const int64_t gpw = (ng + kFitWaves - 1) / kFitWaves;
+  return P.C % 64 == 0 && ((gpw + 1) / 2) * P.G <= kHalf;
+}
+
+template <bool kPool, bool kRegs>
+hipError_t launch_fit_kernel(const KParams& P, const uint16_t* kv, int level,
+                             uint16_t* cdf_anchor, uint16_t* cdf_delta_level,
+                             unsigned long long* pool, hipStream_t st) {
   const size_t lds = 2 * 64 * kHist * sizeof(uint32_t);
-  hipError_t e = hipFuncSetAttribute((const void*)fit_kernel<false>,
+  hipError_t e = hipFuncSetAttribute((const void*)fit_kernel<kPool, kRegs>,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   const int64_t grid = (int64_t)P.L * 2 * P.nblk;
-  hipLaunchKernelGGL(fit_kernel<false>, dim3((unsigned)grid), dim3(kFitThreads), lds, st, P, kv,
-                     level, cdf_anchor, cdf_delta_level, (unsigned long long*)nullptr);
+  hipLaunchKernelGGL((fit_kernel<kPool, kRegs>), dim3((unsigned)grid), dim3(kFitThreads), lds,
+                     st, P, kv, level, cdf_anchor, cdf_delta_level, pool);
   return hipGetLastError();
+}
+}  // namespace
+
+hipError_t cg_launch_fit(const KParams& P, const uint16_t* kv, int level, uint16_t* cdf_anchor,
+                         uint16_t* cdf_delta_level, hipStream_t st) {
+  return fit_slice_in_registers(P)
+             ? launch_fit_kernel<false, true>(P, kv, level, cdf_anchor, cdf_delta_level,
+                                              nullptr, st)
+             : launch_fit_kernel<false, false>(P, kv, level, cdf_anchor, cdf_delta_level,
+                                               nullptr, st);
 }
 
 hipError_t cg_launch_fit_global(const KParams& P, const uint16_t* kv, int level,
@@ -209,14 +298,13 @@ hipError_t cg_launch_fit_global(const KParams& P, const uint16_t* kv, int level,
                                 hipStream_t st) {
   unsigned long long* pool = static_cast<unsigned long long*>(ws);           // [2][256]
   uint16_t* tab = reinterpret_cast<uint16_t*>(static_cast<uint8_t*>(ws) + 4096);  // [2][256]
-  const size_t lds = 2 * 64 * kHist * sizeof(uint32_t);
-  hipError_t e = hipFuncSetAttribute((const void*)fit_kernel<true>,
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (e != hipSuccess) return e;
   hipLaunchKernelGGL(pool_zero, dim3(1), dim3(256), 0, st, pool);
-  const int64_t grid = (int64_t)P.L * 2 * P.nblk;
-  hipLaunchKernelGGL(fit_kernel<true>, dim3((unsigned)grid), dim3(kFitThreads), lds, st, P, kv,
-                     level, cdf_anchor, cdf_delta_level, pool);
+  hipError_t e = fit_slice_in_registers(P)
+                     ? launch_fit_kernel<true, true>(P, kv, level, cdf_anchor, cdf_delta_level,
+                                                     pool, st)
+                     : launch_fit_kernel<true, false>(P, kv, level, cdf_anchor,
+                                                      cdf_delta_level, pool, st);
+  if (e != hipSuccess) return e;
   hipLaunchKernelGGL(pool_normalize, dim3(1), dim3(128), 0, st, pool, tab);
   const int64_t n_tables = (int64_t)P.L * 2 * P.C;
   const int64_t blocks = (2 * n_tables + 3) / 4;

@@ -21,6 +21,14 @@ SMALL = [
             level_mult=(1.0, 2.0, 4.0)),
     W.small(name="long_chunk_1536", n_layers=2, n_tokens=1600, chunk_len=1536, n_channels=65,
             level_mult=(1.0, 8.0)),
+    # whole 64-channel blocks and the paper's 1536-token chunks: the fit's register path with
+    # full halves (G = 10: 50 tokens per lane; G = 7: 49), and G = 64, which is too long for it
+    W.small(name="c128_chunk_1536", n_layers=1, n_tokens=1600, chunk_len=1536, n_channels=128,
+            level_mult=(1.0, 8.0)),
+    W.small(name="c64_chunk_1536_g7", n_layers=1, n_tokens=1536, chunk_len=1536, n_channels=64,
+            group_size=7),
+    W.small(name="c64_chunk_1536_g64", n_layers=1, n_tokens=1536, chunk_len=1536, n_channels=64,
+            group_size=64),
     # eight levels over sixteen chunks: a workgroup's worst-case table sets exceed the LDS of a
     # CU at sixteen waves, so the launchers use fewer waves per workgroup
     W.small(name="levels8_chunks16", n_layers=2, n_tokens=160, chunk_len=10, n_channels=64,
