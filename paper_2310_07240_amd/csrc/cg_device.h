@@ -48,6 +48,21 @@ __device__ __forceinline__ int cg_quant(float v, float step) {
   return (int)__builtin_rintf(r);
 }
 
+// The same quantizer through a reciprocal: inv = 1 / step, correctly rounded (computed once
+// per stream). r = v * inv is within |q|(2^-23 + 2^-48) of the exact quotient q = v / step,
+// and the correctly rounded quotient within |q| 2^-24 of q, so below |r| = 127 they differ by
+// less than 2.3e-5. rint(clamp(.)) only changes value at the half-integers k + 0.5 inside
+// (-127, 127) (ties round to even), so when the clamped r is farther than 2^-14 from every
+// half-integer, r and the correctly rounded quotient give the same integer; otherwise (about
+// one value in 8000) the division is done as above. Clamped values (|r| >= 127) are 0.5 from
+// the nearest half-integer and give +-127 either way.
+__device__ __forceinline__ int cg_quant_inv(float v, float step, float inv) {
+  const float r = fminf(fmaxf(v * inv, -127.0f), 127.0f);
+  const float fr = r - __builtin_floorf(r);   // exact: |r| < 2^23
+  if (__builtin_fabsf(fr - 0.5f) <= 0x1p-14f) return cg_quant(v, step);
+  return (int)__builtin_rintf(r);
+}
+
 // Stream index of (b, c, l, kv, ch): chunk-major so each chunk's streams are contiguous.
 __device__ __forceinline__ int64_t cg_stream(const KParams& P, int64_t bclk, int ch) {
   return bclk * P.C + ch;

@@ -223,6 +223,7 @@ __global__ __launch_bounds__(1024) void encode_kernel(
   constexpr int kPipe = kG > 0 ? kG : 8;
   const float bw = P.layer_bin[l] * P.level_mult[lv];
   const float w = bw * s;
+  const float is = 1.0f / s, iw = 1.0f / w;
 
   cg_glb_u16* tabA = (cg_glb_u16*)(cdfA + ((int64_t)(l * 2 + k) * P.C + ch) * 256);
   cg_lds_u16* tabD = (cg_lds_u16*)(tabs + (s_set_of_level[lv] * 64 + lane) * kEncTabStride);
@@ -251,7 +252,7 @@ __global__ __launch_bounds__(1024) void encode_kernel(
     for (int u = 0; u < kPipe; ++u) {
       const float v = cg_h2f((uint16_t)xv[u]);
       const bool anc = kG > 0 ? u == 0 : gq == 0;
-      const int q = anc ? cg_quant(v, s) : cg_quant(v - a, w);
+      const int q = anc ? cg_quant_inv(v, s, is) : cg_quant_inv(v - a, w, iw);
       if (anc) a = (float)q * s;
       const int sym = q + 127;
       const int sym1 = min(sym + 1, CG_NSYM - 1);

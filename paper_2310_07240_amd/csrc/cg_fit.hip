@@ -89,14 +89,15 @@ __device__ void normalize_wave(const CountT* cnt, uint16_t* out) {
 // channels) to the global counts pool[2][256] (anchor, delta): the one-distribution baseline.
 // Count one quantized token of a slice: the anchor (group position g == 0) under the 8-bit
 // step s, the others as the delta to the dequantized anchor under step w.
-__device__ __forceinline__ void fit_count(float v, int g, float s, float w, float& a,
-                                          uint32_t* ha, uint32_t* hd) {
+// is = 1 / s and iw = 1 / w (correctly rounded).
+__device__ __forceinline__ void fit_count(float v, int g, float s, float w, float is, float iw,
+                                          float& a, uint32_t* ha, uint32_t* hd) {
   if (g == 0) {
-    const int q = cg_quant(v, s);
+    const int q = cg_quant_inv(v, s, is);
     a = (float)q * s;
     atomicAdd(&ha[q + 127], 1u);
   } else {
-    const int q = cg_quant(v - a, w);
+    const int q = cg_quant_inv(v - a, w, iw);
     atomicAdd(&hd[q + 127], 1u);
   }
 }
@@ -171,6 +172,7 @@ __global__ __launch_bounds__(kFitThreads) void fit_kernel(KParams P, const uint1
       const float s0 = (m0 == 0.0f) ? 1.0f : m0 / 127.0f;
       const float s1 = (m1 == 0.0f) ? 1.0f : m1 / 127.0f;
       const float w0 = wfac * s0, w1 = wfac * s1;
+      const float is0 = 1.0f / s0, is1 = 1.0f / s1, iw0 = 1.0f / w0, iw1 = 1.0f / w1;
       uint32_t* ha0 = cnt + (2 * cp) * kHist;
       uint32_t* hd0 = cnt + (64 + 2 * cp) * kHist;
       float a0 = 0.0f, a1 = 0.0f;
@@ -178,8 +180,8 @@ __global__ __launch_bounds__(kFitThreads) void fit_kernel(KParams P, const uint1
 #pragma unroll
       for (int u = 0; u < kHalf; ++u) {
         if (u < len) {
-          fit_count((float)pk[u].x, g, s0, w0, a0, ha0, hd0);
-          fit_count((float)pk[u].y, g, s1, w1, a1, ha0 + kHist, hd0 + kHist);
+          fit_count((float)pk[u].x, g, s0, w0, is0, iw0, a0, ha0, hd0);
+          fit_count((float)pk[u].y, g, s1, w1, is1, iw1, a1, ha0 + kHist, hd0 + kHist);
         }
         g = (g + 1 == P.G) ? 0 : g + 1;
       }
@@ -195,13 +197,14 @@ __global__ __launch_bounds__(kFitThreads) void fit_kernel(KParams P, const uint1
       for (int v = 0; v < kFitWaves; ++v) m = fmaxf(m, part[v][lane]);
       const float s = (m == 0.0f) ? 1.0f : m / 127.0f;
       const float w = wfac * s;
+      const float is = 1.0f / s, iw = 1.0f / w;
       // pass 2: quantize the slice (it starts on a group boundary) and count
       if (act) {
         float a = 0.0f;
         int g = 0;
 #pragma unroll 4
         for (int j = j0; j < j1; ++j) {
-          fit_count(cg_h2f(x[(int64_t)j * rs]), g, s, w, a, ha, hd);
+          fit_count(cg_h2f(x[(int64_t)j * rs]), g, s, w, is, iw, a, ha, hd);
           g = (g + 1 == P.G) ? 0 : g + 1;
         }
       }
