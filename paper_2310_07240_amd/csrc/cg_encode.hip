@@ -136,6 +136,41 @@ __device__ __forceinline__ void enc_symbol(EncState& e, BitSink& o, uint32_t clo
   e.rm1 = (rm1 << n) | ((1u << n) - 1u);
 }
 
+// The same symbol without branches, for the steps where no lane owes more than 32 bits: the
+// E = P + n1 output bits (none when n1 = 0) go into acc unconditionally, and the ring slot of
+// the next word is always written (with the finished word, or with bits a later word
+// overwrites: that slot holds no pending word, since at most kRing - 1 are pending). `rare` is
+// set when P + n1 > 32; the step is then coded again from its saved state with enc_symbol.
+__device__ __forceinline__ void enc_symbol_fast(EncState& e, BitSink& o, uint32_t clo,
+                                                uint32_t chi, bool& rare) {
+  const uint32_t lo_off = (uint32_t)(((uint64_t)e.rm1 * clo + clo) >> 16);
+  const uint32_t hm1 = (uint32_t)((((uint64_t)e.rm1 * chi + chi) >> 16) - 1ull);
+  const uint32_t low = e.low + lo_off;
+  const uint32_t rm1 = hm1 - lo_off;
+  const uint32_t high = low + rm1;
+  const uint32_t n1 = __clz(low ^ high);
+  const uint32_t P = e.pending;
+  const bool emit = n1 != 0;
+  const uint32_t E = emit ? P + n1 : 0u;
+  rare |= E > 32u;
+  const uint32_t H = low >> ((32u - n1) & 31u);
+  const uint32_t runb = ((1u << (P & 31u)) - 1u) << ((n1 - 1u) & 31u);
+  const uint32_t val = emit ? H + runb : 0u;
+  o.acc = (o.acc << E) | val;   // bits above the nacc valid ones are never read
+  o.nacc += E;
+  const bool full = o.nacc >= 32u;
+  o.nacc -= full ? 32u : 0u;
+  o.ring[(o.nwords & (kRing - 1)) * 64] = (uint32_t)(o.acc >> o.nacc);
+  o.nwords += full ? 1u : 0u;
+  const uint32_t L1 = low << n1, H1 = high << n1;
+  const uint32_t m = L1 & ~H1;
+  const uint32_t n3 = __clz(~(m << 1));
+  e.pending = (emit ? 0u : P) + n3;
+  e.low = (L1 << n3) & 0x7FFFFFFFu;
+  const uint32_t n = n1 + n3;
+  e.rm1 = (rm1 << n) | ((1u << n) - 1u);
+}
+
 __device__ __forceinline__ void enc_finish(EncState& e, BitSink& o) {
   o.flush();
   e.pending += 1;
@@ -271,11 +306,26 @@ __global__ __launch_bounds__(1024) void encode_kernel(
 #pragma unroll
     for (int u = 0; u < kPipe; ++u) xv[u] = x[(int64_t)min(step * kPipe + u, last) * rs];
   };
+  // a step without branches per symbol; if a lane of the wave owed more than 32 bits at some
+  // symbol, the wave codes the step again from the saved state with the branching coder
   auto code_step = [&](const uint32_t (&clo)[kPipe], const uint32_t (&chi)[kPipe], int step)
                        __attribute__((always_inline)) {
+    const EncState e0 = e;
+    const uint64_t acc0 = o.acc;
+    const uint32_t nacc0 = o.nacc, nwords0 = o.nwords;
+    bool rare = false;
 #pragma unroll
     for (int u = 0; u < kPipe; ++u)
-      if (step * kPipe + u < n) enc_symbol(e, o, clo[u], chi[u]);
+      if (step * kPipe + u < n) enc_symbol_fast(e, o, clo[u], chi[u], rare);
+    if (__builtin_amdgcn_ballot_w64(rare) != 0ull) {
+      e = e0;
+      o.acc = acc0;
+      o.nacc = nacc0;
+      o.nwords = nwords0;
+#pragma unroll
+      for (int u = 0; u < kPipe; ++u)
+        if (step * kPipe + u < n) enc_symbol(e, o, clo[u], chi[u]);
+    }
   };
   load_rows(xr0, 0);
   load_rows(xr1, 1);
