@@ -98,6 +98,13 @@ def _lib():
             L.cgo_encode_streams.argtypes = [_P, _P, _P, _P, _P, _P, _I64, _P, _U64, _P, _P,
                                              ctypes.c_int]
             L.cgo_encode_streams.restype = _I64
+            L.cgo_num_token_streams.argtypes = [_P]
+            L.cgo_num_token_streams.restype = _I64
+            L.cg_encode_tokens_ref.argtypes = [_P, _P, _P, _P, _P, _P, _U64, _P, _P,
+                                               ctypes.c_int]
+            L.cg_encode_tokens_ref.restype = _I64
+            L.cg_decode_tokens_ref.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_int]
+            L.cg_decode_tokens_ref.restype = ctypes.c_int
             _LIB = L
     return _LIB
 
@@ -325,6 +332,49 @@ def decode(words, offsets, scales, shape: Shape, chunk_level, cdf_anchor, cdf_de
     ps, keep = shape._c()
     _lib().cg_decode_ref(ctypes.byref(ps), _ptr(w), _ptr(off), _ptr(sc), _ptr(cl), _ptr(ca),
                          _ptr(cd), chunk_begin, chunk_end, _ptr(out), threads or default_threads())
+    return out
+
+
+def n_token_streams(shape: Shape) -> int:
+    """Streams of the token-parallel layout: one per (context, layer, K/V, token)."""
+    return shape.n_ctx * shape.n_layers * 2 * shape.n_tokens
+
+
+def encode_tokens(kv, shape: Shape, chunk_level, cdf_anchor, cdf_delta, threads=None):
+    """Encode in the token-parallel layout (one stream per (context, layer, K/V, token) over
+    the token's channels). Returns (words uint32, offsets uint64 [St+1], scales fp32 [S])."""
+    kvu = np.ascontiguousarray(kv.view(np.uint16)).reshape(shape.kv_shape())
+    cl = np.ascontiguousarray(np.asarray(chunk_level, np.uint8).reshape(shape.n_ctx, shape.n_chunks))
+    ca = np.ascontiguousarray(cdf_anchor, np.uint16)
+    cd = np.ascontiguousarray(cdf_delta, np.uint16)
+    St = n_token_streams(shape)
+    cap = St * int(_lib().cgo_stream_bound_words(shape.n_channels))
+    words = np.zeros(max(cap, 1), np.uint32)
+    offsets = np.zeros(St + 1, np.uint64)
+    scales = np.zeros(shape.n_streams, np.float32)
+    ps, keep = shape._c()
+    total = _lib().cg_encode_tokens_ref(ctypes.byref(ps), _ptr(kvu), _ptr(cl), _ptr(ca),
+                                        _ptr(cd), _ptr(words), cap, _ptr(offsets),
+                                        _ptr(scales), threads or default_threads())
+    assert total >= 0, "oracle token-layout encode overflowed its bound"
+    return words[:total].copy(), offsets, scales
+
+
+def decode_tokens(words, offsets, scales, shape: Shape, chunk_level, cdf_anchor, cdf_delta,
+                  threads=None):
+    """Decode the token-parallel layout: fp16 bit patterns [B, L, 2, T, C] (uint16)."""
+    w = np.ascontiguousarray(words, np.uint32)
+    if w.size == 0:
+        w = np.zeros(1, np.uint32)
+    off = np.ascontiguousarray(offsets, np.uint64)
+    sc = np.ascontiguousarray(scales, np.float32)
+    cl = np.ascontiguousarray(np.asarray(chunk_level, np.uint8).reshape(shape.n_ctx, shape.n_chunks))
+    ca = np.ascontiguousarray(cdf_anchor, np.uint16)
+    cd = np.ascontiguousarray(cdf_delta, np.uint16)
+    out = np.zeros(shape.kv_shape(), np.uint16)
+    ps, keep = shape._c()
+    _lib().cg_decode_tokens_ref(ctypes.byref(ps), _ptr(w), _ptr(off), _ptr(sc), _ptr(cl),
+                                _ptr(ca), _ptr(cd), _ptr(out), threads or default_threads())
     return out
 
 

@@ -643,3 +643,224 @@ int64_t cgo_encode_streams(const cgo_params* p, const uint16_t* kv, const uint8_
   free(slots);
   return failed ? -1 : (int64_t)total;
 }
+
+/* ------------------------------------------------------------------------------------------
+ * Token-parallel stream layout (Sec. 6: the paper's GPU decoder runs one thread per token).
+ * Reading: one stream per (context, layer, K/V, token) over that token's channels in order;
+ * the symbol of channel ch is coded under the (layer, K/V, ch) tables (the anchor table for the
+ * anchor token of a group, the chunk level's delta table otherwise). Quantization, scales and
+ * tables are those of the channel-stream layout above: only the grouping of the same symbols
+ * into streams differs. Stream order keeps each chunk's streams together: inside context b,
+ * chunk c (first token t0, n_c tokens) holds streams (b T + t0) 2L + (2 l + k) n_c + (t - t0).
+ * ---------------------------------------------------------------------------------------- */
+int64_t cgo_num_token_streams(const cgo_params* p) {
+  return (int64_t)p->n_ctx * p->n_layers * 2 * p->n_tokens;
+}
+
+typedef struct { int64_t b, c, l, k, t, t0, n; } tok_stream_t;
+
+static tok_stream_t locate_token(const cgo_params* p, int64_t s) {
+  tok_stream_t r;
+  int64_t L2 = 2 * (int64_t)p->n_layers, T = p->n_tokens;
+  r.b = s / (T * L2);
+  int64_t rem = s - r.b * T * L2;
+  r.c = rem / ((int64_t)p->chunk_len * L2);
+  r.t0 = r.c * p->chunk_len;
+  r.n = (r.t0 + p->chunk_len <= T) ? p->chunk_len : T - r.t0;
+  rem -= r.t0 * L2;
+  int64_t lk = rem / r.n;
+  r.t = r.t0 + (rem - lk * r.n);
+  r.l = lk / 2;
+  r.k = lk % 2;
+  return r;
+}
+
+/* Symbols of the whole cache in [b][l][k][t][ch] order plus the channel streams' scales. */
+typedef struct {
+  const cgo_params* p; const uint16_t* kv; const uint8_t* chunk_level;
+  int64_t s_begin, s_end; uint8_t* sym; float* scales;
+} qall_job;
+
+static void* qall_worker(void* arg) {
+  qall_job* J = (qall_job*)arg;
+  const cgo_params* p = J->p;
+  uint8_t* col = (uint8_t*)malloc((size_t)p->chunk_len);
+  for (int64_t s = J->s_begin; s < J->s_end; ++s) {
+    stream_t st = locate(p, J->kv, s);
+    int lv = level_of(p, J->chunk_level, &st);
+    float sc = cgo_stream_scale(st.x, st.stride, st.n);
+    cgo_quantize_stream(st.x, st.stride, st.n, p->group_size, sc, bin_width(p, st.l, lv, sc),
+                        col, NULL);
+    J->scales[s] = sc;
+    uint8_t* dst = J->sym + (((st.b * p->n_layers + st.l) * 2 + st.k) * p->n_tokens + st.t0) *
+                                p->n_channels + st.ch;
+    for (int64_t j = 0; j < st.n; ++j) dst[j * p->n_channels] = col[j];
+  }
+  free(col);
+  return NULL;
+}
+
+static void quantize_all(const cgo_params* p, const uint16_t* kv, const uint8_t* chunk_level,
+                         uint8_t* sym, float* scales, int threads) {
+  int64_t S = cgo_num_streams(p);
+  threads = clamp_threads(threads, S);
+  pthread_t th[256];
+  qall_job jobs[256];
+  for (int i = 0; i < threads; ++i) {
+    jobs[i] = (qall_job){p, kv, chunk_level, S * i / threads, S * (i + 1) / threads, sym, scales};
+    pthread_create(&th[i], NULL, qall_worker, &jobs[i]);
+  }
+  for (int i = 0; i < threads; ++i) pthread_join(th[i], NULL);
+}
+
+/* The tables of the C symbols of token stream ts. */
+static void token_tables(const cgo_params* p, const uint8_t* chunk_level,
+                         const uint16_t* cdf_anchor, const uint16_t* cdf_delta,
+                         const tok_stream_t* ts, const uint16_t** tabs) {
+  int lv = chunk_level[ts->b * n_chunks(p) + ts->c];
+  lv = lv < p->n_levels ? lv : p->n_levels - 1;
+  int anchor = (ts->t - ts->t0) % p->group_size == 0;
+  for (int64_t ch = 0; ch < p->n_channels; ++ch) {
+    stream_t st = {ts->b, ts->c, ts->l, ts->k, ch, ts->t0, ts->n, NULL, p->n_channels};
+    tabs[ch] = anchor ? anchor_table(p, cdf_anchor, &st) : delta_table(p, cdf_delta, lv, &st);
+  }
+}
+
+typedef struct {
+  const cgo_params* p; const uint8_t* sym; const uint8_t* chunk_level;
+  const uint16_t* cdf_anchor; const uint16_t* cdf_delta;
+  int64_t s_begin, s_end;
+  uint32_t* buf; uint64_t buf_words; uint64_t* lens; int failed;
+} tenc_job;
+
+static void* tenc_worker(void* arg) {
+  tenc_job* J = (tenc_job*)arg;
+  const cgo_params* p = J->p;
+  int64_t C = p->n_channels;
+  uint64_t need = cgo_stream_bound_words(C);
+  uint64_t cap = (uint64_t)(J->s_end - J->s_begin) * need + 1;
+  J->buf = (uint32_t*)calloc((size_t)cap, sizeof(uint32_t));
+  const uint16_t** tabs = (const uint16_t**)malloc((size_t)C * sizeof(*tabs));
+  uint64_t used = 0;
+  for (int64_t s = J->s_begin; s < J->s_end; ++s) {
+    tok_stream_t ts = locate_token(p, s);
+    token_tables(p, J->chunk_level, J->cdf_anchor, J->cdf_delta, &ts, tabs);
+    const uint8_t* row = J->sym + (((ts.b * p->n_layers + ts.l) * 2 + ts.k) * p->n_tokens + ts.t) * C;
+    uint64_t bits = cgo_ac_encode(row, C, tabs, J->buf + used, need);
+    if (bits == UINT64_MAX) { J->failed = 1; break; }
+    J->lens[s] = (bits + 31) / 32;
+    used += J->lens[s];
+  }
+  free(tabs);
+  J->buf_words = used;
+  return NULL;
+}
+
+/* Encode in the token layout. offsets [St + 1] (St token streams); scales [S] of the channel
+ * streams (the side information is the same as in the channel layout). Returns the total word
+ * count, or -1 if cap_words is too small. */
+int64_t cg_encode_tokens_ref(const cgo_params* p, const uint16_t* kv, const uint8_t* chunk_level,
+                             const uint16_t* cdf_anchor, const uint16_t* cdf_delta,
+                             uint32_t* words, uint64_t cap_words, uint64_t* offsets,
+                             float* scales, int threads) {
+  int64_t St = cgo_num_token_streams(p);
+  int64_t n_elem = St * p->n_channels;
+  uint8_t* sym = (uint8_t*)malloc((size_t)(n_elem > 0 ? n_elem : 1));
+  quantize_all(p, kv, chunk_level, sym, scales, threads);
+  threads = clamp_threads(threads, St);
+  uint64_t* lens = (uint64_t*)calloc((size_t)(St > 0 ? St : 1), sizeof(uint64_t));
+  pthread_t th[256];
+  tenc_job jobs[256];
+  for (int i = 0; i < threads; ++i) {
+    jobs[i] = (tenc_job){p, sym, chunk_level, cdf_anchor, cdf_delta,
+                         St * i / threads, St * (i + 1) / threads, NULL, 0, lens, 0};
+    pthread_create(&th[i], NULL, tenc_worker, &jobs[i]);
+  }
+  for (int i = 0; i < threads; ++i) pthread_join(th[i], NULL);
+  int failed = 0;
+  for (int i = 0; i < threads; ++i) failed |= jobs[i].failed;
+  uint64_t total = 0;
+  offsets[0] = 0;
+  for (int64_t s = 0; s < St; ++s) { total += lens[s]; offsets[s + 1] = total; }
+  if (!failed && total <= cap_words) {
+    for (int i = 0; i < threads; ++i)
+      memcpy(words + offsets[jobs[i].s_begin], jobs[i].buf, jobs[i].buf_words * sizeof(uint32_t));
+  }
+  for (int i = 0; i < threads; ++i) free(jobs[i].buf);
+  free(lens);
+  free(sym);
+  return (failed || total > cap_words) ? -1 : (int64_t)total;
+}
+
+typedef struct {
+  const cgo_params* p; const uint32_t* words; const uint64_t* offsets;
+  const uint8_t* chunk_level; const uint16_t* cdf_anchor; const uint16_t* cdf_delta;
+  int64_t s_begin, s_end; uint8_t* sym;
+} tdec_job;
+
+static void* tdec_worker(void* arg) {
+  tdec_job* J = (tdec_job*)arg;
+  const cgo_params* p = J->p;
+  int64_t C = p->n_channels;
+  const uint16_t** tabs = (const uint16_t**)malloc((size_t)C * sizeof(*tabs));
+  for (int64_t s = J->s_begin; s < J->s_end; ++s) {
+    tok_stream_t ts = locate_token(p, s);
+    token_tables(p, J->chunk_level, J->cdf_anchor, J->cdf_delta, &ts, tabs);
+    uint8_t* row = J->sym + (((ts.b * p->n_layers + ts.l) * 2 + ts.k) * p->n_tokens + ts.t) * C;
+    cgo_ac_decode(J->words + J->offsets[s], J->offsets[s + 1] - J->offsets[s], C, tabs, row);
+  }
+  free(tabs);
+  return NULL;
+}
+
+typedef struct {
+  const cgo_params* p; const uint8_t* sym; const float* scales; const uint8_t* chunk_level;
+  int64_t s_begin, s_end; uint16_t* kv_out;
+} tdq_job;
+
+static void* tdq_worker(void* arg) {
+  tdq_job* J = (tdq_job*)arg;
+  const cgo_params* p = J->p;
+  uint8_t* col = (uint8_t*)malloc((size_t)p->chunk_len);
+  for (int64_t s = J->s_begin; s < J->s_end; ++s) {
+    stream_t st = locate(p, NULL, s);
+    int lv = level_of(p, J->chunk_level, &st);
+    int64_t base = (((st.b * p->n_layers + st.l) * 2 + st.k) * p->n_tokens + st.t0) *
+                   p->n_channels + st.ch;
+    for (int64_t j = 0; j < st.n; ++j) col[j] = J->sym[base + j * p->n_channels];
+    float sc = J->scales[s];
+    cgo_dequantize_stream(col, st.n, p->group_size, sc, bin_width(p, st.l, lv, sc),
+                          J->kv_out + base, p->n_channels);
+  }
+  free(col);
+  return NULL;
+}
+
+/* Decode every token stream, then reconstruct each channel stream from its symbols. */
+int cg_decode_tokens_ref(const cgo_params* p, const uint32_t* words, const uint64_t* offsets,
+                         const float* scales, const uint8_t* chunk_level,
+                         const uint16_t* cdf_anchor, const uint16_t* cdf_delta,
+                         uint16_t* kv_out, int threads) {
+  int64_t St = cgo_num_token_streams(p);
+  int64_t n_elem = St * p->n_channels;
+  uint8_t* sym = (uint8_t*)malloc((size_t)(n_elem > 0 ? n_elem : 1));
+  int tt = clamp_threads(threads, St);
+  pthread_t th[256];
+  tdec_job jobs[256];
+  for (int i = 0; i < tt; ++i) {
+    jobs[i] = (tdec_job){p, words, offsets, chunk_level, cdf_anchor, cdf_delta,
+                         St * i / tt, St * (i + 1) / tt, sym};
+    pthread_create(&th[i], NULL, tdec_worker, &jobs[i]);
+  }
+  for (int i = 0; i < tt; ++i) pthread_join(th[i], NULL);
+  int64_t S = cgo_num_streams(p);
+  int tq = clamp_threads(threads, S);
+  tdq_job qj[256];
+  for (int i = 0; i < tq; ++i) {
+    qj[i] = (tdq_job){p, sym, scales, chunk_level, S * i / tq, S * (i + 1) / tq, kv_out};
+    pthread_create(&th[i], NULL, tdq_worker, &qj[i]);
+  }
+  for (int i = 0; i < tq; ++i) pthread_join(th[i], NULL);
+  free(sym);
+  return 0;
+}
