@@ -255,6 +255,49 @@ int cg_adapt_schedule(const cg_adapt_params* a, const double* bandwidth_gbps,
 int cg_check_finite(const cg_params* p, const uint16_t* kv_f16, uint32_t* flag_dev,
                     hipStream_t stream);
 
+/* ---- Token-parallel stream layout (Sec. 6: the paper's GPU decoder runs one thread per
+ * token), for comparison with the channel streams above. One stream per (context, layer,
+ * K/V, token) over the token's C channels in order; the symbol of channel ch is coded under the
+ * (layer, K/V, ch) tables: cdf_anchor on the first token of each group, the chunk level's delta
+ * table otherwise. The quantized symbols and the scales are exactly those of the channel layout
+ * (the same fp16 output comes back); only their grouping into streams changes. Stream order:
+ * inside context b, chunk c (first token t0, n tokens) holds streams
+ * (b T + t0) 2L + (2 l + k) n + (t - t0), so each chunk's streams are contiguous. */
+
+/* Token streams: B * L * 2 * T. 0 if p is invalid. */
+int64_t cg_num_token_streams(const cg_params* p);
+
+/* Capacity of the token-layout payload (words): every token stream at its worst case
+ * ceil((18 C + 2) / 32), plus CG_TAIL_WORDS. */
+uint64_t cg_encode_tokens_bound_words(const cg_params* p);
+
+/* Device scratch of cg_encode_tokens (bytes): the symbol array (one byte per element), a
+ * worst-case slot per token stream, per-stream word counts and scan partials. */
+uint64_t cg_encode_tokens_workspace_bytes(const cg_params* p);
+
+/* Device scratch of cg_decode_tokens (bytes): the symbol array, one byte per element. */
+uint64_t cg_decode_tokens_workspace_bytes(const cg_params* p);
+
+/* Encode in the token layout. Arguments as for cg_encode, except offsets [St + 1] for the St
+ * token streams, words_cap >= cg_encode_tokens_bound_words(p) and workspace_bytes >=
+ * cg_encode_tokens_workspace_bytes(p); scales [S] are the channel streams' (as cg_encode).
+ * Asynchronous. */
+int cg_encode_tokens(const cg_params* p, const uint16_t* kv_f16, const uint8_t* chunk_level,
+                     const uint16_t* cdf_anchor, const uint16_t* cdf_delta, uint32_t* words,
+                     uint64_t words_cap, uint64_t* offsets, float* scales, void* workspace,
+                     uint64_t workspace_bytes, hipStream_t stream);
+
+/* Decode the token layout to fp16 KV [B][L][2][T][C] (every chunk). words, offsets [St + 1],
+ * scales [S], chunk_level, tables: device, as cg_encode_tokens / cg_fit_cdf produced them; the
+ * words buffer must be readable up to offsets[St] + CG_TAIL_WORDS (as for cg_decode: a corrupt
+ * payload gives wrong values, never an out-of-range access). workspace_bytes >=
+ * cg_decode_tokens_workspace_bytes(p). Asynchronous. */
+int cg_decode_tokens(const cg_params* p, const uint32_t* words, const uint64_t* offsets,
+                     const float* scales, const uint8_t* chunk_level,
+                     const uint16_t* cdf_anchor, const uint16_t* cdf_delta,
+                     uint16_t* kv_out_f16, void* workspace, uint64_t workspace_bytes,
+                     hipStream_t stream);
+
 /* Static description of a return code; never NULL. */
 const char* cg_strerror(int code);
 

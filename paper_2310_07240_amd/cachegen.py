@@ -25,7 +25,9 @@ ERRORS = {-1: "CG_ERR_ARG", -2: "CG_ERR_SHAPE", -3: "CG_ERR_CAPACITY", -4: "CG_E
 EXPORTS = ("cg_num_chunks", "cg_num_streams", "cg_encode_bound_words",
            "cg_encode_workspace_bytes", "cg_fit_cdf", "cg_fit_cdf_global", "cg_encode",
            "cg_decode", "cg_decode_streamed", "cg_adapt_schedule", "cg_check_finite",
-           "cg_strerror")
+           "cg_num_token_streams", "cg_encode_tokens_bound_words",
+           "cg_encode_tokens_workspace_bytes", "cg_decode_tokens_workspace_bytes",
+           "cg_encode_tokens", "cg_decode_tokens", "cg_strerror")
 CG_FIT_GLOBAL_WORKSPACE_BYTES = 8192
 
 
@@ -95,6 +97,16 @@ def lib():
         L.cg_adapt_schedule.restype = ctypes.c_int
         L.cg_check_finite.argtypes = [PP, _P, _P, _P]
         L.cg_check_finite.restype = ctypes.c_int
+        for name in ("cg_encode_tokens_bound_words", "cg_encode_tokens_workspace_bytes",
+                     "cg_decode_tokens_workspace_bytes"):
+            getattr(L, name).argtypes = [PP]
+            getattr(L, name).restype = ctypes.c_uint64
+        L.cg_num_token_streams.argtypes = [PP]; L.cg_num_token_streams.restype = ctypes.c_int64
+        L.cg_encode_tokens.argtypes = [PP, _P, _P, _P, _P, _P, ctypes.c_uint64, _P, _P, _P,
+                                       ctypes.c_uint64, _P]
+        L.cg_encode_tokens.restype = ctypes.c_int
+        L.cg_decode_tokens.argtypes = [PP, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_uint64, _P]
+        L.cg_decode_tokens.restype = ctypes.c_int
         L.cg_strerror.argtypes = [ctypes.c_int]
         L.cg_strerror.restype = ctypes.c_char_p
         _LIB = L
@@ -261,6 +273,49 @@ def cg_check_finite(p: CodecParams, kv, flag, stream=None) -> bool:
 
 
 # --------------------------------------------------------------------------------------------
+# token-parallel stream layout (one stream per context, layer, K/V and token)
+# --------------------------------------------------------------------------------------------
+def cg_num_token_streams(p: CodecParams) -> int:
+    s, keep = p.c()
+    return int(lib().cg_num_token_streams(ctypes.byref(s)))
+
+
+def cg_encode_tokens_bound_words(p: CodecParams) -> int:
+    s, keep = p.c()
+    return int(lib().cg_encode_tokens_bound_words(ctypes.byref(s)))
+
+
+def cg_encode_tokens_workspace_bytes(p: CodecParams) -> int:
+    s, keep = p.c()
+    return int(lib().cg_encode_tokens_workspace_bytes(ctypes.byref(s)))
+
+
+def cg_decode_tokens_workspace_bytes(p: CodecParams) -> int:
+    s, keep = p.c()
+    return int(lib().cg_decode_tokens_workspace_bytes(ctypes.byref(s)))
+
+
+def cg_encode_tokens(p: CodecParams, kv, chunk_level, cdf_anchor, cdf_delta, words, offsets,
+                     scales, workspace, stream=None):
+    s, keep = p.c()
+    _check(lib().cg_encode_tokens(ctypes.byref(s), _ptr(kv), _ptr(chunk_level), _ptr(cdf_anchor),
+                                  _ptr(cdf_delta), _ptr(words), words.numel(), _ptr(offsets),
+                                  _ptr(scales), _ptr(workspace),
+                                  workspace.numel() * workspace.element_size(), _stream(stream)),
+           "cg_encode_tokens")
+
+
+def cg_decode_tokens(p: CodecParams, words, offsets, scales, chunk_level, cdf_anchor, cdf_delta,
+                     kv_out, workspace, stream=None):
+    s, keep = p.c()
+    _check(lib().cg_decode_tokens(ctypes.byref(s), _ptr(words), _ptr(offsets), _ptr(scales),
+                                  _ptr(chunk_level), _ptr(cdf_anchor), _ptr(cdf_delta),
+                                  _ptr(kv_out), _ptr(workspace),
+                                  workspace.numel() * workspace.element_size(), _stream(stream)),
+           "cg_decode_tokens")
+
+
+# --------------------------------------------------------------------------------------------
 # convenience: allocate outputs with torch and call the above
 # --------------------------------------------------------------------------------------------
 class Codec:
@@ -319,4 +374,25 @@ class Codec:
             out = self.torch.zeros(self.p.kv_shape, dtype=self.torch.int16, device=self.device)
         cg_decode(self.p, words, offsets, scales, chunk_level, cdf_anchor, cdf_delta,
                   chunk_begin, chunk_end, out, stream)
+        return out
+
+    def encode_tokens(self, kv, chunk_level, cdf_anchor, cdf_delta, stream=None):
+        """Token-parallel layout: (words [bound], offsets [St+1], scales [S])."""
+        t = self.torch
+        words = self._empty((cg_encode_tokens_bound_words(self.p),), t.int32)
+        offsets = self._empty((cg_num_token_streams(self.p) + 1,), t.int64)
+        scales = self._empty((self.n_streams,), t.float32)
+        ws = self._empty((cg_encode_tokens_workspace_bytes(self.p),), t.uint8)
+        cg_encode_tokens(self.p, kv, chunk_level, cdf_anchor, cdf_delta, words, offsets, scales,
+                         ws, stream)
+        return words, offsets, scales
+
+    def decode_tokens(self, words, offsets, scales, chunk_level, cdf_anchor, cdf_delta, out=None,
+                      workspace=None, stream=None):
+        if out is None:
+            out = self.torch.zeros(self.p.kv_shape, dtype=self.torch.int16, device=self.device)
+        if workspace is None:
+            workspace = self._empty((cg_decode_tokens_workspace_bytes(self.p),), self.torch.uint8)
+        cg_decode_tokens(self.p, words, offsets, scales, chunk_level, cdf_anchor, cdf_delta, out,
+                         workspace, stream)
         return out

@@ -162,6 +162,72 @@ int cg_decode(const cg_params* p, const uint32_t* words, const uint64_t* offsets
              : CG_ERR_HIP;
 }
 
+int64_t cg_num_token_streams(const cg_params* p) {
+  KParams K;
+  return make_kparams(p, &K) == CG_OK ? cg_token_streams(K) : 0;
+}
+
+uint64_t cg_encode_tokens_bound_words(const cg_params* p) {
+  KParams K;
+  if (make_kparams(p, &K) != CG_OK) return 0;
+  return (uint64_t)cg_token_streams(K) * cg_token_slot_words(K) + CG_TAIL_WORDS;
+}
+
+uint64_t cg_encode_tokens_workspace_bytes(const cg_params* p) {
+  KParams K;
+  if (make_kparams(p, &K) != CG_OK) return 0;
+  return cg_encode_tokens_ws_layout(K).total;
+}
+
+uint64_t cg_decode_tokens_workspace_bytes(const cg_params* p) {
+  KParams K;
+  if (make_kparams(p, &K) != CG_OK) return 0;
+  return (uint64_t)cg_token_streams(K) * (uint64_t)K.C;
+}
+
+int cg_encode_tokens(const cg_params* p, const uint16_t* kv_f16, const uint8_t* chunk_level,
+                     const uint16_t* cdf_anchor, const uint16_t* cdf_delta, uint32_t* words,
+                     uint64_t words_cap, uint64_t* offsets, float* scales, void* workspace,
+                     uint64_t workspace_bytes, hipStream_t stream) {
+  KParams K;
+  int rc = make_kparams(p, &K);
+  if (rc != CG_OK) return rc;
+  if (!kv_f16 || !chunk_level || !cdf_anchor || !cdf_delta || !words || !offsets || !scales ||
+      !workspace)
+    return CG_ERR_ARG;
+  if (!aligned(workspace, 256) || !aligned(offsets, 8) || !aligned(words, 4) ||
+      !aligned(scales, 4) || !aligned(kv_f16, 2))
+    return CG_ERR_ARG;
+  if (words_cap < cg_encode_tokens_bound_words(p)) return CG_ERR_CAPACITY;
+  if (workspace_bytes < cg_encode_tokens_ws_layout(K).total) return CG_ERR_CAPACITY;
+  return cg_launch_encode_tokens(K, kv_f16, chunk_level, cdf_anchor, cdf_delta, words, offsets,
+                                 scales, workspace, stream) == hipSuccess
+             ? CG_OK
+             : CG_ERR_HIP;
+}
+
+int cg_decode_tokens(const cg_params* p, const uint32_t* words, const uint64_t* offsets,
+                     const float* scales, const uint8_t* chunk_level,
+                     const uint16_t* cdf_anchor, const uint16_t* cdf_delta,
+                     uint16_t* kv_out_f16, void* workspace, uint64_t workspace_bytes,
+                     hipStream_t stream) {
+  KParams K;
+  int rc = make_kparams(p, &K);
+  if (rc != CG_OK) return rc;
+  if (!words || !offsets || !scales || !chunk_level || !cdf_anchor || !cdf_delta ||
+      !kv_out_f16 || !workspace)
+    return CG_ERR_ARG;
+  if (!aligned(cdf_anchor, 16) || !aligned(cdf_delta, 16) || !aligned(offsets, 8) ||
+      !aligned(words, 4) || !aligned(kv_out_f16, 2) || !aligned(workspace, 256))
+    return CG_ERR_ARG;
+  if (workspace_bytes < cg_decode_tokens_workspace_bytes(p)) return CG_ERR_CAPACITY;
+  return cg_launch_decode_tokens(K, words, offsets, scales, chunk_level, cdf_anchor, cdf_delta,
+                                 static_cast<uint8_t*>(workspace), kv_out_f16,
+                                 stream) == hipSuccess
+             ? CG_OK
+             : CG_ERR_HIP;
+}
+
 int cg_decode_streamed(const cg_params* p, const uint32_t* words_host,
                        const uint64_t* offsets_host, uint32_t* words_dev, uint64_t words_cap,
                        const uint64_t* offsets_dev, const float* scales_dev,

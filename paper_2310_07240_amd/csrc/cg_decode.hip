@@ -488,6 +488,36 @@ __device__ __forceinline__ void g10_epoch(G10Lane& st, const uint32_t* __restric
   st.t3 = tq[3];
 }
 
+// Interval update after the symbol [lo_off, hoff) (offsets from low; d = D - lo_off, rsz =
+// hoff - lo_off): one-step renormalisation and the refill of D from the word window.
+__device__ __forceinline__ void g10_advance(G10Lane& st, uint32_t lo_off, uint32_t hoff,
+                                            uint32_t d, uint32_t rsz) {
+  // renormalisation: n1 shared leading bits of low and high, then the middle-half run of
+  // n3 = f - 1 steps; the new low is L1 << n3 without its top bit
+  const uint32_t low = st.low + lo_off;
+  const uint32_t high = st.low + hoff - 1u;
+  const uint32_t n1 = (uint32_t)__builtin_clz(low ^ high);
+  const uint32_t L1 = low << n1, H1 = high << n1;
+  const uint32_t f = e3_run1(L1, H1);
+  st.low = (L1 << f) >> 1;
+  const uint32_t nsh = n1 + f - 1u;
+  // high - low + 1 scales by 2^nsh (a result of 2^32 wraps to 0, giving rm1 = 2^32 - 1)
+  st.rm1 = (rsz << nsh) - 1u;
+  // D takes the next nsh stream bits: the 32 bits at `pos` of w0:w1, then a 64-bit shift
+  const uint64_t wp = ((uint64_t)st.w0 << 32) | st.w1;
+  const uint32_t win = (uint32_t)((wp << st.pos) >> 32);
+  uint32_t Dn = (uint32_t)(((((uint64_t)d) << 32) | win) << nsh >> 32);
+  asm("" : "+v"(Dn));   // keep D a 32-bit value (not the top half of a 64-bit one)
+  st.D = Dn;
+  const uint32_t p2 = st.pos + nsh;
+  const bool adv = p2 >= 32u;
+  st.w0 = adv ? st.w1 : st.w0;
+  st.w1 = adv ? st.w2 : st.w1;
+  st.w2 = adv ? st.w3 : st.w2;
+  st.pos = p2 & 31u;
+  st.hcnt += adv ? 1u : 0u;
+}
+
 // One token: decode the symbol at row r of the group (the anchor when kAnchor) and stage its
 // fp16 value in the wave's row buffer.
 template <bool kAnchor>
@@ -556,30 +586,7 @@ __device__ __forceinline__ void g10_token(G10Lane& st, const uint32_t (&fA)[17],
     }
     qi = sym - 127;
   }
-  // renormalisation: n1 shared leading bits of low and high, then the middle-half run of
-  // n3 = f - 1 steps; the new low is L1 << n3 without its top bit
-  const uint32_t low = st.low + lo_off;
-  const uint32_t high = st.low + hoff - 1u;
-  const uint32_t n1 = (uint32_t)__builtin_clz(low ^ high);
-  const uint32_t L1 = low << n1, H1 = high << n1;
-  const uint32_t f = e3_run1(L1, H1);
-  st.low = (L1 << f) >> 1;
-  const uint32_t nsh = n1 + f - 1u;
-  // high - low + 1 scales by 2^nsh (a result of 2^32 wraps to 0, giving rm1 = 2^32 - 1)
-  st.rm1 = (rsz << nsh) - 1u;
-  // D takes the next nsh stream bits: the 32 bits at `pos` of w0:w1, then a 64-bit shift
-  const uint64_t wp = ((uint64_t)st.w0 << 32) | st.w1;
-  const uint32_t win = (uint32_t)((wp << st.pos) >> 32);
-  uint32_t Dn = (uint32_t)(((((uint64_t)d) << 32) | win) << nsh >> 32);
-  asm("" : "+v"(Dn));   // keep D a 32-bit value (not the top half of a 64-bit one)
-  st.D = Dn;
-  const uint32_t p2 = st.pos + nsh;
-  const bool adv = p2 >= 32u;
-  st.w0 = adv ? st.w1 : st.w0;
-  st.w1 = adv ? st.w2 : st.w1;
-  st.w2 = adv ? st.w3 : st.w2;
-  st.pos = p2 & 31u;
-  st.hcnt += adv ? 1u : 0u;
+  g10_advance(st, lo_off, hoff, d, rsz);
   const float qf = (float)qi;
   float v;
   if constexpr (kAnchor) {
@@ -769,7 +776,212 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   }
 }
 
+// ---- token-parallel layout (Sec. 6: the paper's decoder runs one thread per token) -----------
+// A wave decodes 64 consecutive token streams of one (context, chunk, layer, K/V), a lane per
+// token, symbol by symbol over the channels. Every lane codes channel ch under the tables of
+// (layer, K/V, ch), so per channel the wave stages that channel's anchor and delta tables in LDS
+// (512 bytes each, 16 bytes per lane; the next channel's are loaded while the current one is
+// decoded) and searches them with the channel layout's delta search from the top: three 4-ary
+// levels and the leaf. There are no per-table fences in registers and no table reuse across
+// symbols: that is the price of this layout. Symbols collect in a lane-private LDS row and go
+// to the symbol array [B][L][2][T][C] every 64 channels; tok_dequant_kernel then reconstructs
+// the channel streams exactly as the channel layout does.
+constexpr int kTokTab = 264;   // u16 per staged table: 256 entries + 8 sentinels (528 bytes)
+constexpr int kTokRow = 68;    // bytes per lane's symbol row (64 + 4: rows start in other banks)
+
+// One symbol of a token stream under the staged table `tab` (sentinels from entry 255 on).
+__device__ __forceinline__ uint32_t tok_symbol(G10Lane& st, const uint16_t* tab) {
+  const float te = (float)st.D * (65536.0f * __builtin_amdgcn_rcpf((float)st.rm1));
+  const uint32_t ti = min((uint32_t)te, 65534u);
+  const uint32_t kneg = ~ti;
+  const uint16_t* q = tab;
+  q += 64 * ((((uint32_t)q[64] + kneg) >> 31) + (((uint32_t)q[128] + kneg) >> 31) +
+             (((uint32_t)q[192] + kneg) >> 31));
+  q += 16 * ((((uint32_t)q[16] + kneg) >> 31) + (((uint32_t)q[32] + kneg) >> 31) +
+             (((uint32_t)q[48] + kneg) >> 31));
+  q += 4 * ((((uint32_t)q[4] + kneg) >> 31) + (((uint32_t)q[8] + kneg) >> 31) +
+            (((uint32_t)q[12] + kneg) >> 31));
+  uint32_t pr;
+  const uint32_t cc = delta_leaf(q, ti, pr);
+  int sym = (int)((((uint32_t)(uintptr_t)q - (uint32_t)(uintptr_t)tab) >> 1) + cc);
+  uint32_t clo = pr & 0xFFFFu;
+  uint32_t chi = sym == CG_NSYM - 1 ? CG_TOTAL : pr >> 16;
+  const uint32_t D = st.D, rm1 = st.rm1;
+  uint32_t lo_off = scaled_off(rm1, clo);
+  uint32_t hoff = scaled_off(rm1, chi);
+  uint32_t d = D - lo_off;
+  uint32_t rsz = hoff - lo_off;
+  if (d >= rsz) {
+    for (int guard = 0; guard < CG_NSYM; ++guard) {
+      sym = (D < lo_off) ? max(sym - 1, 0) : min(sym + 1, CG_NSYM - 1);
+      clo = tab[sym];
+      chi = sym + 1 >= CG_NSYM ? CG_TOTAL : (uint32_t)tab[sym + 1];
+      lo_off = scaled_off(rm1, clo);
+      hoff = scaled_off(rm1, chi);
+      d = D - lo_off;
+      rsz = hoff - lo_off;
+      if (d < rsz) break;
+    }
+  }
+  g10_advance(st, lo_off, hoff, d, rsz);
+  return (uint32_t)sym;
+}
+
+__device__ __forceinline__ void wave_sync_lds() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__global__ __launch_bounds__(256) void tok_decode_kernel(
+    KParams P, const uint32_t* __restrict__ words, const uint64_t* __restrict__ offsets,
+    const uint8_t* __restrict__ chunk_level, const uint16_t* __restrict__ cdfA,
+    const uint16_t* __restrict__ cdfD, int nbj, int64_t n_groups, uint8_t* __restrict__ sym) {
+  __shared__ __attribute__((aligned(16))) uint16_t tabs[4][2][2][kTokTab];  // [wave][buffer][anchor, delta]
+  __shared__ __attribute__((aligned(16))) uint8_t rows[4][64 * kTokRow];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t grp = (int64_t)blockIdx.x * 4 + wave;
+  if (grp >= n_groups) return;   // per wave; only wave-level synchronisation below
+  const TokGroup g = tok_group(P, grp, nbj);
+  if (g.jb * 64 >= g.n) return;  // a block past a short last chunk: no streams
+  const int l = g.lk >> 1, k = g.lk & 1;
+  const int t0 = g.c * P.CL;
+  const int j = g.jb * 64 + lane;
+  const bool valid = j < g.n;
+  const int jl = valid ? j : g.n - 1;   // lanes past the chunk decode a copy of its last token
+  const bool anchor = jl % P.G == 0;
+  const int lv = uni(min((int)chunk_level[(int64_t)g.b * P.NC + g.c], P.NLV - 1));
+  const int64_t sidx = tok_stream(P, g.b, g.c, g.lk, jl, g.n);
+  const int64_t St = (int64_t)P.B * P.L * 2 * P.T;
+  uint16_t* tw = &tabs[wave][0][0][0];
+  // sentinels: entries 256..263 of the four staged tables (never overwritten)
+  if (lane < 16) reinterpret_cast<uint32_t*>(tw + (lane >> 2) * kTokTab + 256)[lane & 3] = 0xFFFFFFFFu;
+  // staging: lane L copies bytes 16 (L % 32) .. +16 of table L / 32 (0 anchor, 1 delta); the
+  // lane holding entry 255 replaces it with a sentinel
+  const int kind = lane >> 5, part = lane & 31;
+  const uint16_t* src = (kind ? cdfD + ((int64_t)lv * 2 * P.L + g.lk) * P.C * 256
+                              : cdfA + (int64_t)g.lk * P.C * 256) + part * 8;
+  uint4 v = *reinterpret_cast<const uint4*>(src);
+  if (part == 31) v.w = (v.w & 0xFFFFu) | 0xFFFF0000u;
+  *reinterpret_cast<uint4*>(tw + kind * kTokTab + part * 8) = v;
+  wave_sync_lds();
+
+  const uint64_t total = offsets[St];
+  if (total == 0) return;
+  G10Lane st;
+  const uint64_t o0 = offsets[sidx];
+  const uint64_t ob = o0 < total ? o0 : total;
+  const uint32_t* sbase = words + ob;
+  const uint32_t cap = (uint32_t)((total - ob) < 0xFFFFFFF0ull ? (total - ob) : 0xFFFFFFF0ull);
+  st.D = sbase[0];
+  st.w0 = sbase[1];
+  st.w1 = sbase[2];
+  st.w2 = sbase[3];
+  st.w3 = sbase[4];
+  st.pos = 0;
+  st.hcnt = 0;
+  st.widx = 5;
+  const uint32_t* tq0 = sbase + (5u < cap ? 5u : cap);
+  st.t0 = tq0[0];
+  st.t1 = tq0[1];
+  st.t2 = tq0[2];
+  st.t3 = tq0[3];
+  settle(st.D); settle(st.w0); settle(st.w1); settle(st.w2); settle(st.w3);
+  st.low = 0u;
+  st.rm1 = 0xFFFFFFFFu;
+  st.a = 0.0f;
+
+  uint8_t* myrow = &rows[wave][lane * kTokRow];
+  uint8_t* gout = sym + cg_elem(P, g.b, l, k, t0 + jl, 0);
+  for (int ch = 0; ch < P.C; ++ch) {
+    // bitstream epochs every four symbols (at most 72 bits between two)
+    if ((ch & 3) == 0 && ch != 0) g10_epoch(st, sbase, cap);
+    const bool more = ch + 1 < P.C;
+    if (more) v = *reinterpret_cast<const uint4*>(src + (int64_t)(ch + 1) * 256);
+    const uint32_t sy = tok_symbol(st, tw + ((ch & 1) * 2 + (anchor ? 0 : 1)) * kTokTab);
+    myrow[ch & 63] = (uint8_t)sy;
+    if ((ch & 63) == 63 || !more) {
+      // this lane's row of up to 64 symbols to the symbol array
+      const int c0 = ch & ~63, cnt = ch - c0 + 1;
+      if (valid) {
+        if (cnt == 64 && (reinterpret_cast<uintptr_t>(gout + c0) & 3) == 0) {
+#pragma unroll
+          for (int i = 0; i < 16; ++i)
+            reinterpret_cast<uint32_t*>(gout + c0)[i] = reinterpret_cast<const uint32_t*>(myrow)[i];
+        } else {
+          for (int i = 0; i < cnt; ++i) gout[c0 + i] = myrow[i];
+        }
+      }
+    }
+    if (more) {
+      if (part == 31) v.w = (v.w & 0xFFFFu) | 0xFFFF0000u;
+      *reinterpret_cast<uint4*>(tw + (((ch + 1) & 1) * 2 + kind) * kTokTab + part * 8) = v;
+      wave_sync_lds();
+    }
+  }
+}
+
+// Reconstruct the channel streams from the symbol array (the channel layout's dequantization):
+// one wave per (context, chunk, layer, K/V, 64-channel block), a lane per channel.
+__global__ __launch_bounds__(256) void tok_dequant_kernel(KParams P, const uint8_t* __restrict__ sym,
+                                                          const float* __restrict__ scales,
+                                                          const uint8_t* __restrict__ chunk_level,
+                                                          uint16_t* __restrict__ out) {
+  const int64_t item = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (item >= (int64_t)P.B * P.NC * P.L * 2 * P.nblk) return;
+  const int cb = (int)(item % P.nblk);
+  int64_t r = item / P.nblk;
+  const int k = (int)(r & 1);
+  r >>= 1;
+  const int l = (int)(r % P.L);
+  r /= P.L;
+  const int c = (int)(r % P.NC);
+  const int b = (int)(r / P.NC);
+  const int ch = cb * 64 + lane;
+  if (ch >= P.C) return;
+  const int t0 = c * P.CL;
+  const int n = min(P.CL, P.T - t0);
+  const float s = scales[cg_stream(P, (((int64_t)b * P.NC + c) * P.L + l) * 2 + k, ch)];
+  const int lv = min((int)chunk_level[(int64_t)b * P.NC + c], P.NLV - 1);
+  const float w = P.layer_bin[l] * P.level_mult[lv] * s;
+  const uint8_t* x = sym + cg_elem(P, b, l, k, t0, ch);
+  uint16_t* y = out + cg_elem(P, b, l, k, t0, ch);
+  const int64_t rs = P.C;
+  float a = 0.0f;
+  int g = 0;
+  for (int j = 0; j < n; ++j) {
+    const float qf = (float)((int)x[(int64_t)j * rs] - 127);
+    float v;
+    if (g == 0) {
+      a = qf * s;
+      v = a;
+    } else {
+      v = a + qf * w;
+    }
+    y[(int64_t)j * rs] = cg_f2h(v);
+    g = (g + 1 == P.G) ? 0 : g + 1;
+  }
+}
+
 }  // namespace
+
+hipError_t cg_launch_decode_tokens(const KParams& P, const uint32_t* words,
+                                   const uint64_t* offsets, const float* scales,
+                                   const uint8_t* chunk_level, const uint16_t* cdf_anchor,
+                                   const uint16_t* cdf_delta, uint8_t* sym, uint16_t* out,
+                                   hipStream_t st) {
+  const TokEncWorkspace lay = cg_encode_tokens_ws_layout(P);
+  hipLaunchKernelGGL(tok_decode_kernel, dim3((unsigned)((lay.n_groups + 3) / 4)), dim3(256), 0,
+                     st, P, words, offsets, chunk_level, cdf_anchor, cdf_delta, lay.nbj,
+                     lay.n_groups, sym);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t items = (int64_t)P.B * P.NC * P.L * 2 * P.nblk;
+  hipLaunchKernelGGL(tok_dequant_kernel, dim3((unsigned)((items + 3) / 4)), dim3(256), 0, st, P,
+                     sym, scales, chunk_level, out);
+  return hipGetLastError();
+}
 
 hipError_t cg_launch_decode(const KParams& P, const uint32_t* words, const uint64_t* offsets,
                             const float* scales, const uint8_t* chunk_level,

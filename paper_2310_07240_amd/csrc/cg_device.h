@@ -74,6 +74,31 @@ __device__ __forceinline__ int64_t cg_elem(const KParams& P, int b, int l, int k
   return ((((int64_t)b * P.L + l) * 2 + k) * P.T + t) * P.C + ch;
 }
 
+// Token-parallel layout: a group of 64 consecutive token streams is (context b, chunk c,
+// lk = 2 l + k, block jb of 64 tokens), nbj blocks per (b, c, lk) (enough for the longest
+// chunk); n = tokens of chunk c. Inside context b, chunk c (first token t0) holds the streams
+// (b T + t0) 2L + lk n + (t - t0).
+struct TokGroup {
+  int b, c, lk, jb, n;
+};
+
+__device__ __forceinline__ TokGroup tok_group(const KParams& P, int64_t grp, int nbj) {
+  TokGroup g;
+  g.jb = (int)(grp % nbj);
+  int64_t r = grp / nbj;
+  g.lk = (int)(r % (2 * P.L));
+  r /= 2 * P.L;
+  g.c = (int)(r % P.NC);
+  g.b = (int)(r / P.NC);
+  g.n = P.CL < P.T - g.c * P.CL ? P.CL : P.T - g.c * P.CL;
+  return g;
+}
+
+__device__ __forceinline__ int64_t tok_stream(const KParams& P, int b, int c, int lk, int j,
+                                              int n) {
+  return ((int64_t)b * P.T + (int64_t)c * P.CL) * (2 * P.L) + (int64_t)lk * n + j;
+}
+
 template <typename T>
 __device__ __forceinline__ T cg_wave_sum(T v) {
 #pragma unroll
@@ -123,3 +148,23 @@ struct EncWorkspace {
   uint64_t slots_off, lens_off, partial_off, total;
 };
 EncWorkspace cg_encode_ws_layout(const KParams& P, uint32_t slot_words);
+
+// Token-parallel stream layout: one stream per (context, layer, K/V, token) over the token's
+// channels (streams in chunk-major order; see cg_encode.hip).
+int64_t cg_token_streams(const KParams& P);
+uint32_t cg_token_slot_words(const KParams& P);   // worst-case words of one token stream
+struct TokEncWorkspace {
+  uint64_t sym_off, slots_off, lens_off, partial_off, total;
+  int64_t n_groups;   // slot groups of 64 token streams
+  int nbj;            // 64-token blocks per (context, chunk, layer, K/V)
+};
+TokEncWorkspace cg_encode_tokens_ws_layout(const KParams& P);
+hipError_t cg_launch_encode_tokens(const KParams& P, const uint16_t* kv,
+                                   const uint8_t* chunk_level, const uint16_t* cdf_anchor,
+                                   const uint16_t* cdf_delta, uint32_t* words, uint64_t* offsets,
+                                   float* scales, void* ws, hipStream_t st);
+hipError_t cg_launch_decode_tokens(const KParams& P, const uint32_t* words,
+                                   const uint64_t* offsets, const float* scales,
+                                   const uint8_t* chunk_level, const uint16_t* cdf_anchor,
+                                   const uint16_t* cdf_delta, uint8_t* sym, uint16_t* out,
+                                   hipStream_t st);

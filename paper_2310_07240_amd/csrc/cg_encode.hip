@@ -430,34 +430,151 @@ __global__ __launch_bounds__(kScanThreads) void scan_finish(const uint32_t* __re
   }
 }
 
-// Copy every stream's words from its slot to their place in the payload. One workgroup per
-// (row, 64-channel block): the slots of its 64 streams are interleaved word by word, so tiles of
-// 16 words x 64 streams are read as whole 256-byte rows, transposed through LDS, and written as
-// 16 consecutive words per stream.
-__global__ __launch_bounds__(256) void compact_kernel(const uint32_t* __restrict__ slots,
+// ---- token-parallel layout (Sec. 6: the paper's decoder runs one thread per token) -----------
+// One stream per (context, layer, K/V, token) over the token's channels, each symbol coded under
+// its channel's table (anchor table on a group's first token, the chunk level's delta table
+// otherwise). Quantization and scales are those of the channel layout. Inside context b, chunk
+// c (first token t0, n tokens) holds the streams (b T + t0) 2L + (2 l + k) n + (t - t0).
+
+// Symbols of every channel stream (the channel layout's quantizer and scales) into
+// sym [B][L][2][T][C]: one wave per (context, chunk, layer, K/V, 64-channel block), a lane per
+// channel; each token row is one coalesced 128-byte read and 64-byte write.
+__global__ __launch_bounds__(256) void tok_quantize_kernel(KParams P, const uint16_t* __restrict__ kv,
+                                                           const uint8_t* __restrict__ chunk_level,
+                                                           uint8_t* __restrict__ sym,
+                                                           float* __restrict__ scales) {
+  const int64_t item = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (item >= (int64_t)P.B * P.NC * P.L * 2 * P.nblk) return;
+  const int cb = (int)(item % P.nblk);
+  int64_t r = item / P.nblk;
+  const int k = (int)(r & 1);
+  r >>= 1;
+  const int l = (int)(r % P.L);
+  r /= P.L;
+  const int c = (int)(r % P.NC);
+  const int b = (int)(r / P.NC);
+  const int ch = cb * 64 + lane;
+  if (ch >= P.C) return;
+  const int t0 = c * P.CL;
+  const int n = min(P.CL, P.T - t0);
+  const int64_t rs = P.C;
+  const uint16_t* x = kv + cg_elem(P, b, l, k, t0, ch);
+  float m = 0.0f;
+  for (int j = 0; j < n; ++j) m = fmaxf(m, fabsf(cg_h2f(x[(int64_t)j * rs])));
+  const float s = (m == 0.0f) ? 1.0f : m / 127.0f;
+  scales[cg_stream(P, (((int64_t)b * P.NC + c) * P.L + l) * 2 + k, ch)] = s;
+  const int lv = min((int)chunk_level[(int64_t)b * P.NC + c], P.NLV - 1);
+  const float bw = P.layer_bin[l] * P.level_mult[lv];
+  const float w = bw * s;
+  const float is = 1.0f / s, iw = 1.0f / w;
+  uint8_t* out = sym + cg_elem(P, b, l, k, t0, ch);
+  float a = 0.0f;
+  int g = 0;
+  for (int j = 0; j < n; ++j) {
+    const float v = cg_h2f(x[(int64_t)j * rs]);
+    int q;
+    if (g == 0) {
+      q = cg_quant_inv(v, s, is);
+      a = (float)q * s;
+    } else {
+      q = cg_quant_inv(v - a, w, iw);
+    }
+    out[(int64_t)j * rs] = (uint8_t)(q + 127);
+    g = (g + 1 == P.G) ? 0 : g + 1;
+  }
+}
+
+// Code the token streams: one wave per slot group (64 consecutive tokens of one context, chunk,
+// layer and K/V), a lane per token, the channel layout's coder over the token's channels. Lanes
+// past the chunk's last token code a copy of the last token (read in bounds, never recorded).
+__global__ __launch_bounds__(256) void tok_encode_kernel(KParams P, const uint8_t* __restrict__ sym,
+                                                         const uint8_t* __restrict__ chunk_level,
+                                                         const uint16_t* __restrict__ cdfA,
+                                                         const uint16_t* __restrict__ cdfD,
+                                                         uint32_t* __restrict__ slots,
+                                                         uint32_t slot_words,
+                                                         uint32_t* __restrict__ lens, int nbj,
+                                                         int64_t n_groups) {
+  __shared__ uint32_t rings[4][kRing * 64];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t grp = (int64_t)blockIdx.x * 4 + wave;
+  if (grp >= n_groups) return;   // per wave; no workgroup barriers below
+  const TokGroup g = tok_group(P, grp, nbj);
+  if (g.jb * 64 >= g.n) return;  // a block past a short last chunk: no streams
+  const int l = g.lk >> 1, k = g.lk & 1;
+  const int t0 = g.c * P.CL;
+  const int j = g.jb * 64 + lane;
+  const bool valid = j < g.n;
+  const int jl = valid ? j : g.n - 1;
+  const bool anchor = jl % P.G == 0;
+  const int lv = min((int)chunk_level[(int64_t)g.b * P.NC + g.c], P.NLV - 1);
+  const uint8_t* row = sym + cg_elem(P, g.b, l, k, t0 + jl, 0);
+  const uint16_t* tab = anchor ? cdfA + (int64_t)g.lk * P.C * 256
+                               : cdfD + ((int64_t)lv * P.L * 2 + g.lk) * P.C * 256;
+  EncState e{0u, 0xFFFFFFFFu, 0u};
+  BitSink o{slots + (uint64_t)grp * slot_words * 64 + lane, slot_words, 0u, 0u, 0ull, 0u,
+            rings[wave] + lane};
+  // steps of 8 symbols (at most 8 * 18 bits, so at most 5 ring words pending at a flush)
+  constexpr int kStep = 8;
+  for (int c0 = 0; c0 < P.C; c0 += kStep) {
+    uint32_t lo[kStep], hi[kStep];
+#pragma unroll
+    for (int u = 0; u < kStep; ++u) {
+      const int ch = min(c0 + u, P.C - 1);
+      const int sy = row[ch];
+      const uint16_t* t = tab + (int64_t)ch * 256;
+      lo[u] = t[sy];
+      hi[u] = sy == CG_NSYM - 1 ? CG_TOTAL : (uint32_t)t[sy + 1];
+    }
+#pragma unroll
+    for (int u = 0; u < kStep; ++u)
+      if (c0 + u < P.C) enc_symbol(e, o, lo[u], hi[u]);
+    o.flush();
+  }
+  enc_finish(e, o);
+  const uint32_t own_bound = (uint32_t)((18ull * (uint64_t)P.C + 2ull + 31ull) / 32ull);
+  if (valid) lens[tok_stream(P, g.b, g.c, g.lk, j, g.n)] = min(o.nwords, min(own_bound, slot_words));
+}
+
+// Copy every stream's words from its slot to their place in the payload. One workgroup per slot
+// group of 64 streams: the slots of its streams are interleaved word by word, so tiles of 16
+// words x 64 streams are read as whole 256-byte rows, transposed through LDS, and written as 16
+// consecutive words per stream. Channel layout (kTok false): group = (row, 64-channel block),
+// streams row * C + block * 64 + i. Token layout: group = (context, chunk, layer and K/V,
+// 64-token block), streams tok_stream(...) of the block's tokens.
+template <bool kTok>
+__global__ __launch_bounds__(256) void compact_kernel(KParams P, const uint32_t* __restrict__ slots,
                                                       uint32_t slot_words,
                                                       const uint32_t* __restrict__ lens,
                                                       const uint64_t* __restrict__ offsets,
-                                                      int C, int nblk,
-                                                      uint32_t* __restrict__ words) {
+                                                      int nbj, uint32_t* __restrict__ words) {
   __shared__ uint32_t tile[16][65];
   __shared__ uint32_t s_len[64];
   __shared__ uint64_t s_off[64];
   __shared__ uint32_t s_max;
-  const int64_t grp = blockIdx.x;   // row * nblk + block
-  const int64_t row = grp / nblk;
-  const int cb = (int)(grp - row * nblk);
+  const int64_t grp = blockIdx.x;
+  int64_t base;   // stream of the group's lane 0
+  int count;      // streams in the group
+  if constexpr (kTok) {
+    const TokGroup g = tok_group(P, grp, nbj);
+    base = tok_stream(P, g.b, g.c, g.lk, g.jb * 64, g.n);
+    count = min(64, g.n - g.jb * 64);
+  } else {
+    const int64_t row = grp / P.nblk;
+    const int cb = (int)(grp - row * P.nblk);
+    base = row * P.C + cb * 64;
+    count = min(64, P.C - cb * 64);
+  }
   const int t = threadIdx.x;
   if (t == 0) s_max = 0u;
   __syncthreads();
   if (t < 64) {
-    const int ch = cb * 64 + t;
     uint32_t n = 0;
     uint64_t o = 0;
-    if (ch < C) {
-      const int64_t s = row * C + ch;
-      n = lens[s];
-      o = offsets[s];
+    if (t < count) {
+      n = lens[base + t];
+      o = offsets[base + t];
     }
     s_len[t] = n;
     s_off[t] = o;
@@ -547,7 +664,61 @@ hipError_t cg_launch_encode(const KParams& P, const uint16_t* kv, const uint8_t*
   hipLaunchKernelGGL(scan_finish, dim3((unsigned)nb), dim3(kScanThreads), 0, st, lens, P.S,
                      partial, offsets);
   const int64_t groups = (int64_t)P.B * P.NC * P.L * 2 * P.nblk;
-  hipLaunchKernelGGL(compact_kernel, dim3((unsigned)groups), dim3(256), 0, st, slots,
-                     slot_words, lens, offsets, P.C, P.nblk, words);
+  hipLaunchKernelGGL(compact_kernel<false>, dim3((unsigned)groups), dim3(256), 0, st, P, slots,
+                     slot_words, lens, offsets, 0, words);
+  return hipGetLastError();
+}
+
+// ---- token-parallel layout ----------------------------------------------------------------
+
+int64_t cg_token_streams(const KParams& P) { return (int64_t)P.B * P.L * 2 * P.T; }
+
+uint32_t cg_token_slot_words(const KParams& P) {
+  return (uint32_t)((18ull * (uint64_t)P.C + 2ull + 31ull) / 32ull);
+}
+
+TokEncWorkspace cg_encode_tokens_ws_layout(const KParams& P) {
+  TokEncWorkspace w;
+  const int64_t St = cg_token_streams(P);
+  const int64_t nb = (St + kScanBlock - 1) / kScanBlock;
+  const int nbj = (int)(((P.CL < P.T ? P.CL : P.T) + 63) / 64);
+  w.nbj = nbj;
+  w.n_groups = (int64_t)P.B * P.NC * 2 * P.L * nbj;
+  w.sym_off = 0;
+  w.slots_off = align256((uint64_t)St * P.C);
+  w.lens_off = align256(w.slots_off + (uint64_t)w.n_groups * 64 * cg_token_slot_words(P) * 4ull);
+  w.partial_off = align256(w.lens_off + (uint64_t)St * 4ull);
+  w.total = align256(w.partial_off + (uint64_t)(nb > 0 ? nb : 1) * 8ull);
+  return w;
+}
+
+hipError_t cg_launch_encode_tokens(const KParams& P, const uint16_t* kv,
+                                   const uint8_t* chunk_level, const uint16_t* cdf_anchor,
+                                   const uint16_t* cdf_delta, uint32_t* words, uint64_t* offsets,
+                                   float* scales, void* ws, hipStream_t st) {
+  const TokEncWorkspace lay = cg_encode_tokens_ws_layout(P);
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  uint8_t* sym = base + lay.sym_off;
+  uint32_t* slots = reinterpret_cast<uint32_t*>(base + lay.slots_off);
+  uint32_t* lens = reinterpret_cast<uint32_t*>(base + lay.lens_off);
+  uint64_t* partial = reinterpret_cast<uint64_t*>(base + lay.partial_off);
+  const uint32_t slot_words = cg_token_slot_words(P);
+  const int64_t items = (int64_t)P.B * P.NC * P.L * 2 * P.nblk;
+  hipLaunchKernelGGL(tok_quantize_kernel, dim3((unsigned)((items + 3) / 4)), dim3(256), 0, st, P,
+                     kv, chunk_level, sym, scales);
+  hipLaunchKernelGGL(tok_encode_kernel, dim3((unsigned)((lay.n_groups + 3) / 4)), dim3(256), 0,
+                     st, P, sym, chunk_level, cdf_anchor, cdf_delta, slots, slot_words, lens,
+                     lay.nbj, lay.n_groups);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t St = cg_token_streams(P);
+  const int64_t nb = (St + kScanBlock - 1) / kScanBlock;
+  hipLaunchKernelGGL(scan_reduce, dim3((unsigned)nb), dim3(kScanThreads), 0, st, lens, St,
+                     partial);
+  hipLaunchKernelGGL(scan_top, dim3(1), dim3(kScanThreads), 0, st, partial, nb);
+  hipLaunchKernelGGL(scan_finish, dim3((unsigned)nb), dim3(kScanThreads), 0, st, lens, St,
+                     partial, offsets);
+  hipLaunchKernelGGL(compact_kernel<true>, dim3((unsigned)lay.n_groups), dim3(256), 0, st, P,
+                     slots, slot_words, lens, offsets, lay.nbj, words);
   return hipGetLastError();
 }

@@ -93,3 +93,29 @@ def test_host_validation_before_any_launch():
     assert lib.cg_decode(None, fake, fake, fake, fake, fake, fake, 0, 1, fake, None) == -1
     assert cg.strerror(-3).startswith("output or workspace")
     assert cg.strerror(12345) == "unknown error code"
+
+
+def test_token_layout_size_queries_and_host_validation():
+    """Token-parallel layout: one stream per (context, layer, K/V, token), worst case
+    ceil((18 C + 2) / 32) words each; capacity errors are decided on the host."""
+    lib = cg.lib()
+    p = P()
+    assert cg.cg_num_token_streams(p) == 1 * 2 * 2 * 100
+    per = (18 * 70 + 2 + 31) // 32
+    assert cg.cg_encode_tokens_bound_words(p) == 400 * per + 8
+    assert cg.cg_decode_tokens_workspace_bytes(p) == 1 * 2 * 2 * 100 * 70
+    assert cg.cg_encode_tokens_workspace_bytes(p) > cg.cg_decode_tokens_workspace_bytes(p)
+    assert cg.cg_num_token_streams(P(n_channels=0)) == 0
+    s, keep = p.c()
+    fake = ctypes.c_void_p(1 << 20)
+    bound = cg.cg_encode_tokens_bound_words(p)
+    ws = cg.cg_encode_tokens_workspace_bytes(p)
+    assert lib.cg_encode_tokens(ctypes.byref(s), fake, fake, fake, fake, fake, bound - 1, fake,
+                                fake, fake, ws, None) == -3
+    assert lib.cg_encode_tokens(ctypes.byref(s), fake, fake, fake, fake, fake, bound, fake, fake,
+                                fake, ws - 1, None) == -3
+    dws = cg.cg_decode_tokens_workspace_bytes(p)
+    assert lib.cg_decode_tokens(ctypes.byref(s), fake, fake, fake, fake, fake, fake, fake, fake,
+                                dws - 1, None) == -3
+    assert lib.cg_decode_tokens(ctypes.byref(s), fake, fake, fake, fake, fake, fake, None, fake,
+                                dws, None) == -1
