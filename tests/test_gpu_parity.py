@@ -108,3 +108,40 @@ def test_chunk_range_decode_and_determinism():
         mask = np.ones(w.n_tokens, bool)
         mask[t0:t1] = False
         assert np.all(part[..., mask, :] == 0)
+
+
+@pytest.mark.parametrize("kind", ["random", "ones", "zeros"])
+def test_corrupt_payload_decodes_within_bounds(kind):
+    """The decoder's documented error behaviour: with valid tables and offsets, a corrupt
+    payload gives wrong values but the decode finishes, stays in bounds (the tail after the
+    payload is all it may read) and is deterministic; values are those of some symbols, so they
+    stay finite. Both layouts."""
+    torch = torch_cuda()
+    from paper_2310_07240_amd.cachegen import Codec, CodecParams
+    w = W.small(name=f"corrupt_{kind}", n_tokens=120, chunk_len=50, n_channels=70)
+    codec = Codec(CodecParams.of(w))
+    kv = torch.from_numpy(W.generate(w).view(np.int16)).cuda()
+    cl = torch.from_numpy(w.chunk_levels()).cuda()
+    ca, cd = codec.fit(kv)
+    words, offsets, scales = codec.encode(kv, cl, ca, cd)
+    twords, toffsets, tscales = codec.encode_tokens(kv, cl, ca, cd)
+    rng = np.random.default_rng(5)
+    for name, wds, off, sc, dec in (
+            ("channel", words, offsets, scales,
+             lambda x: codec.decode(x, offsets, scales, cl, ca, cd)),
+            ("token", twords, toffsets, tscales,
+             lambda x: codec.decode_tokens(x, toffsets, tscales, cl, ca, cd))):
+        n = wds.numel()
+        if kind == "random":
+            bad = torch.from_numpy(rng.integers(0, 2**32, n, dtype=np.uint64).astype(np.uint32)
+                                   .view(np.int32)).cuda()
+        elif kind == "ones":
+            bad = torch.full((n,), -1, dtype=torch.int32, device="cuda")
+        else:
+            bad = torch.zeros((n,), dtype=torch.int32, device="cuda")
+        say(f"corrupt payload ({kind}), {name} layout")
+        a = dec(bad).clone()
+        b = dec(bad)
+        torch.cuda.synchronize()
+        assert torch.equal(a, b)
+        assert bool(torch.isfinite(a.view(torch.float16).float()).all())
