@@ -78,6 +78,8 @@ def main():
     ap.add_argument("--no-streamed", action="store_true",
                     help="skip the chunk-pipelined decode (payload copied from pinned host memory "
                          "chunk by chunk while earlier chunks decode), run after the timed region")
+    ap.add_argument("--no-repeated", action="store_true",
+                    help="skip the decode repeated back to back, run after the timed region")
     ap.add_argument("--no-calib-copy", action="store_true",
                     help="skip the plain copy of known size run after the timed region (it "
                          "calibrates rocprofv3's FETCH_SIZE / WRITE_SIZE counters)")
@@ -151,6 +153,20 @@ def main():
         calib.copy_(kv)
         torch.cuda.synchronize()
         del calib
+    repeated = None
+    if not args.no_repeated:
+        # outside the timed region: the same decode repeated back to back, after one untimed run
+        # (the decode's own steady state; inside a step it follows the encode)
+        cg_decode(p, words, offsets, scales, cl, ca, cd, 0, codec.n_chunks, out, stream)
+        rep = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(10)]
+        for e0, e1 in rep:
+            e0.record(stream)
+            cg_decode(p, words, offsets, scales, cl, ca, cd, 0, codec.n_chunks, out, stream)
+            e1.record(stream)
+        torch.cuda.synchronize()
+        rep_ms = sorted(e0.elapsed_time(e1) for e0, e1 in rep)
+        repeated = rep_ms[len(rep_ms) // 2]
     fit_ms = [e[0].elapsed_time(e[1]) for e in events]
     enc_ms = [e[1].elapsed_time(e[2]) for e in events]
     dec_ms = [e[2].elapsed_time(e[3]) for e in events]
@@ -209,6 +225,11 @@ def main():
                 "bytes_per_launch": dec_bytes},
     }
 
+    if repeated is not None:
+        result["decode_repeated"] = {
+            "ms": round(repeated, 4), "GBps": round(fp16_bytes / (repeated * 1e-3) / 1e9, 2),
+            "runs": 10, "what": "median of 10 decodes back to back after the timed steps; "
+                                "`value` is the decode inside each step, right after the encode"}
     if not args.no_streamed:
         result["streamed"] = streamed(p, codec, words, offsets, scales, cl, ca, cd, total_words)
     if not args.no_cpu_baseline:
