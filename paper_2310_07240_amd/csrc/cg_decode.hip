@@ -30,9 +30,13 @@
 //   3. renormalisation in one step: n1 = clz(low ^ high) shared leading bits, then n3
 //      "middle half" steps (run of low = 1 / high = 0 from bit 30 down); D and rm1 both shift
 //      left by n = n1 + n3 taking in n stream bits (D) or ones (rm1).
-// The payload is read through a 64-bit bit buffer fed from words requested one epoch (four
-// tokens) ahead (see the reader state in the kernel). The words buffer must be readable
-// CG_TAIL_WORDS words past offsets[S].
+// The payload is read from words requested one epoch (three or four tokens) ahead: decode_kernel
+// keeps a 64-bit bit buffer refilled from a four-word shift register, decode_g10_kernel and the
+// token-layout decoder a four-word window with a bit position (see G10Lane). The words buffer
+// must be readable CG_TAIL_WORDS words past offsets[S].
+//
+// tok_decode_kernel / tok_dequant_kernel decode the token-parallel layout (one stream per
+// context, layer, K/V and token; see their comment).
 #include "../../include/cachegen.h"
 #include "cg_device.h"
 
