@@ -26,7 +26,7 @@ CASES = [
     W.small(name="tok_chunk150_c64", n_layers=2, n_tokens=300, chunk_len=150, n_channels=64),
     W.small(name="tok_c128_chunk1536", n_layers=1, n_tokens=1600, chunk_len=1536,
             n_channels=128, level_mult=(1.0, 8.0)),
-    # groups longer than a 64-token block: a block's anchors come from another block
+    # groups longer than a 64-token block: some blocks hold no anchor token at all
     W.small(name="tok_g100", group_size=100, n_tokens=250, chunk_len=200, n_channels=64),
 ]
 
