@@ -479,9 +479,14 @@ __device__ __forceinline__ void g10_epoch(G10Lane& st, const uint32_t* __restric
   uint32_t w1 = st.w1, w2 = st.w2, w3 = st.w3;
   asm("" : "+v"(t0), "+v"(t1), "+v"(t2), "+v"(w1), "+v"(w2), "+v"(w3));
   const bool g1 = h >= 1, g2 = h >= 2, g3 = h >= 3;
-  st.w3 = g3 ? t2 : (g2 ? t1 : (g1 ? t0 : w3));
-  st.w2 = g3 ? t1 : (g2 ? t0 : w2);
-  st.w1 = g3 ? t0 : w1;
+  w3 = g3 ? t2 : (g2 ? t1 : (g1 ? t0 : w3));
+  w2 = g3 ? t1 : (g2 ? t0 : w2);
+  w1 = g3 ? t0 : w1;
+  // materialise the window here (else the selects are folded into every token's word shift)
+  asm("" : "+v"(w1), "+v"(w2), "+v"(w3));
+  st.w1 = w1;
+  st.w2 = w2;
+  st.w3 = w3;
   st.widx += h;
   st.hcnt = 0;
   __builtin_amdgcn_sched_barrier(0);
