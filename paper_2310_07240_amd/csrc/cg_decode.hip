@@ -11,6 +11,13 @@
 //   0xFFFF sentinels. Anchor tables (1 of 10 symbols) stay in global memory; a symbol reads one
 //   32-byte block of 16 entries and finishes with a select search in registers. Fewer waves
 //   per workgroup when the worst-case table sets would not fit in a CU's LDS.
+//   decode_g10_kernel puts several such units (layer, K/V, channel block) in one workgroup
+//   while the grid still covers every CU: a CU then runs one workgroup, whose waves the
+//   hardware spreads evenly over the four SIMDs (several small workgroups per CU can land four
+//   waves on one SIMD and two on another, and the kernel waits for the most loaded SIMD). Wave
+//   w of a workgroup decodes pair slot w / units of unit w % units, so each SIMD gets one wave
+//   of every slot; slots follow chunk order, so with one context the last, shorter chunk is
+//   decoded by the youngest waves (older waves issue first).
 //
 // decode_kernel (any group size): anchor fences cum[16 f] in LDS; the delta search is a 4-ary
 //   search over four levels in LDS (three probes per level, the last level one aligned 8-byte
@@ -43,6 +50,7 @@
 namespace {
 
 constexpr int kMaxWaves = 16;
+constexpr int kMaxUnits = 16;   // (layer, K/V, channel block) units per workgroup
 constexpr size_t kLdsBudget = 160 * 1024 - 1024;   // dynamic LDS per workgroup (CDNA4: 160 KB)
 constexpr int kTabStride = 260;    // u16 per delta table in LDS (256 + 4 pad -> 520 bytes)
 constexpr int kFenceStride = 18;   // u16 per anchor fence row (16 + 2 pad -> 36 bytes)
@@ -641,51 +649,57 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     KParams P, const uint32_t* __restrict__ words, const uint64_t* __restrict__ offsets,
     const float* __restrict__ scales, const uint8_t* __restrict__ chunk_level,
     const uint16_t* __restrict__ cdfA, const uint16_t* __restrict__ cdfD, int c_begin,
-    int c_end, int nw, uint16_t* __restrict__ out) {
+    int c_end, int nw, int nu, uint16_t* __restrict__ out) {
   extern __shared__ uint16_t smem[];
-  __shared__ uint32_t s_mask;
-  __shared__ int s_set_of_level[CG_MAX_LEVELS];
-  __shared__ int s_level_of_set[CG_MAX_LEVELS];
-  __shared__ int s_nsets;
-  uint16_t* obuf_all = smem;                      // [nw][kG10][64] decoded rows per wave
-  uint16_t* tabs = obuf_all + nw * kG10 * 64;     // [nsets][64][kTabStride]
+  __shared__ uint32_t s_mask[kMaxUnits];
+  __shared__ int s_set_of_level[kMaxUnits][CG_MAX_LEVELS];
+  __shared__ int s_level_of_set[kMaxUnits][CG_MAX_LEVELS];
+  __shared__ int s_nsets[kMaxUnits];
+  const int msets = nw < P.NLV ? nw : P.NLV;          // table sets a unit may need
+  uint16_t* obuf_all = smem;                          // [nu * nw][kG10][64] rows per wave
+  uint16_t* tabs = obuf_all + nu * nw * kG10 * 64;    // [nu][msets][64][kTabStride]
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int nwaves = blockDim.x >> 6;
+  const int u = wave % nu, j = wave / nu;             // unit and pair slot of this wave
   const int ncr = c_end - c_begin;
   const int n_pairs = P.B * ncr;
   const int n_groups = (n_pairs + nw - 1) / nw;
+  const int n_units = P.L * 2 * P.nblk;
   const int grp = blockIdx.x % n_groups;
-  int rest = blockIdx.x / n_groups;
-  const int cb = rest % P.nblk;
-  rest /= P.nblk;
-  const int k = rest & 1, l = rest >> 1;
+  const int ublk = blockIdx.x / n_groups;
+  const int unit = ublk * nu + u;
+  const int cb = unit % P.nblk;
+  const int k = (unit / P.nblk) & 1, l = (unit / P.nblk) >> 1;
 
-  const int pair = uni(grp * nw + wave);
-  const bool active = pair < n_pairs;
+  const int pair = uni(grp * nw + j);
+  const bool active = unit < n_units && pair < n_pairs;
   const int b = uni(active ? pair / ncr : 0);
   const int c = uni(active ? c_begin + pair % ncr : 0);
   const int lv = uni(active ? min((int)chunk_level[(int64_t)b * P.NC + c], P.NLV - 1) : 0);
 
-  if (threadIdx.x == 0) s_mask = 0u;
+  if (threadIdx.x < nu) s_mask[threadIdx.x] = 0u;
   __syncthreads();
-  if (active && lane == 0) atomicOr(&s_mask, 1u << lv);
+  if (active && lane == 0) atomicOr(&s_mask[u], 1u << lv);
   __syncthreads();
-  if (threadIdx.x == 0) {
+  if (threadIdx.x < nu) {
+    const int uu = threadIdx.x;
     int n = 0;
     for (int v = 0; v < P.NLV; ++v)
-      if ((s_mask >> v) & 1u) { s_set_of_level[v] = n; s_level_of_set[n] = v; ++n; }
-    s_nsets = n;
+      if ((s_mask[uu] >> v) & 1u) { s_set_of_level[uu][v] = n; s_level_of_set[uu][n] = v; ++n; }
+    s_nsets[uu] = n;
   }
   __syncthreads();
-  const int nsets = s_nsets;
-  for (int idx = wave; idx < nsets * 64; idx += nwaves) {
-    const int st = idx >> 6, t = idx & 63;
-    const int ch = cb * 64 + t;
+  for (int idx = wave; idx < nu * msets * 64; idx += nwaves) {
+    const int t = idx & 63, st = (idx >> 6) % msets, uu = (idx >> 6) / msets;
+    const int unit2 = ublk * nu + uu;
+    if (unit2 >= n_units || st >= s_nsets[uu]) continue;
+    const int ch = (unit2 % P.nblk) * 64 + t;
     if (ch >= P.C) continue;
+    const int lk = unit2 / P.nblk;   // l * 2 + k
     const uint32_t* src = reinterpret_cast<const uint32_t*>(
-        cdfD + ((((int64_t)s_level_of_set[st] * P.L + l) * 2 + k) * P.C + ch) * 256);
-    uint32_t* dst = reinterpret_cast<uint32_t*>(tabs + (st * 64 + t) * kTabStride);
+        cdfD + (((int64_t)s_level_of_set[uu][st] * P.L * 2 + lk) * P.C + ch) * 256);
+    uint32_t* dst = reinterpret_cast<uint32_t*>(tabs + ((uu * msets + st) * 64 + t) * kTabStride);
     const uint32_t v0 = src[lane];
     uint32_t v1 = src[lane + 64];
     if (lane == 63) v1 = (v1 & 0xFFFFu) | 0xFFFF0000u;  // entry 255: sentinel above any target
@@ -707,7 +721,7 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   const int n = uni(min(P.CL, P.T - tok0));
   const float s = scales[sidx];
   const float w = P.layer_bin[l] * P.level_mult[lv] * s;
-  const uint16_t* dtab = tabs + (s_set_of_level[lv] * 64 + lsrc) * kTabStride;
+  const uint16_t* dtab = tabs + ((u * msets + s_set_of_level[u][lv]) * 64 + lsrc) * kTabStride;
   const uint16_t* gA = cdfA + ((int64_t)(l * 2 + k) * P.C + chv) * 256;
 
   // fences cum[16 f], f = 0..16 (cum[256] = total), of both tables
@@ -1002,25 +1016,35 @@ hipError_t cg_launch_decode(const KParams& P, const uint32_t* words, const uint6
   // may use (sized for the worst case, min(w, levels) sets); fewer waves per workgroup when
   // that exceeds what a CU offers
   const bool g10 = P.G == kG10;
-  auto lds_for = [&](int w) {
+  auto lds_for = [&](int w, int nu) {
     const size_t sets = (size_t)(w < P.NLV ? w : P.NLV);
-    const size_t rows = g10 ? (size_t)w * kG10 * 64 : (size_t)64 * kFenceStride + (size_t)w * kRows * 64;
-    return (rows + sets * 64 * kTabStride) * sizeof(uint16_t);
+    const size_t rows = g10 ? (size_t)nu * w * kG10 * 64
+                            : (size_t)64 * kFenceStride + (size_t)w * kRows * 64;
+    return (rows + (size_t)nu * sets * 64 * kTabStride) * sizeof(uint16_t);
   };
   int nw = (int)(n_pairs < kMaxWaves ? n_pairs : kMaxWaves);
-  while (nw > 1 && lds_for(nw) > kLdsBudget) --nw;
+  while (nw > 1 && lds_for(nw, 1) > kLdsBudget) --nw;
   const int64_t n_groups = (n_pairs + nw - 1) / nw;
-  const int64_t grid = (int64_t)P.L * 2 * P.nblk * n_groups;
-  const size_t lds = lds_for(nw);
+  const int64_t n_units = (int64_t)P.L * 2 * P.nblk;
   if (g10) {
+    // several units per workgroup while the grid still covers every CU: one workgroup then
+    // holds all of a CU's waves, which the hardware spreads evenly over the SIMDs
+    int nu = 1;
+    while (nu < kMaxUnits && (nu + 1) * nw <= kMaxWaves && lds_for(nw, nu + 1) <= kLdsBudget &&
+           (n_units + nu) / (nu + 1) * n_groups >= 256)
+      ++nu;
+    const int64_t grid = (n_units + nu - 1) / nu * n_groups;
+    const size_t lds = lds_for(nw, nu);
     hipError_t e = hipFuncSetAttribute((const void*)decode_g10_kernel,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(decode_g10_kernel, dim3((unsigned)grid), dim3(64 * nw), lds, st, P,
+    hipLaunchKernelGGL(decode_g10_kernel, dim3((unsigned)grid), dim3(64 * nw * nu), lds, st, P,
                        words, offsets, scales, chunk_level, cdf_anchor, cdf_delta, c_begin, c_end,
-                       nw, out);
+                       nw, nu, out);
     return hipGetLastError();
   }
+  const int64_t grid = n_units * n_groups;
+  const size_t lds = lds_for(nw, 1);
   hipError_t e = hipFuncSetAttribute((const void*)decode_kernel,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
