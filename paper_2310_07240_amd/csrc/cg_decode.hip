@@ -51,6 +51,7 @@ namespace {
 
 constexpr int kMaxWaves = 16;
 constexpr int kMaxUnits = 16;   // (layer, K/V, channel block) units per workgroup
+constexpr int kStageBatch = 8;  // table-staging loads in flight per lane
 constexpr size_t kLdsBudget = 160 * 1024 - 1024;   // dynamic LDS per workgroup (CDNA4: 160 KB)
 constexpr int kTabStride = 260;    // u16 per delta table in LDS (256 + 4 pad -> 520 bytes)
 constexpr int kFenceStride = 18;   // u16 per anchor fence row (16 + 2 pad -> 36 bytes)
@@ -66,6 +67,15 @@ __device__ __forceinline__ uint32_t scaled_off(uint32_t x, uint32_t c) {
   uint64_t r, carry;
   asm("v_mad_u64_u32 %0, %1, %2, %3, %4" : "=v"(r), "=s"(carry) : "v"(x), "v"(c), "v"((uint64_t)c));
   return (uint32_t)(r >> 16);
+}
+
+// Relaxed LDS accesses of a value other waves of the workgroup update (no ordering, no wait
+// beyond the LDS access itself).
+__device__ __forceinline__ int lds_get(int* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+__device__ __forceinline__ void lds_put(int* p, int v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
 // Make the compiler wait here for a register produced by a load (once, outside the loop).
@@ -655,6 +665,8 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   __shared__ int s_set_of_level[kMaxUnits][CG_MAX_LEVELS];
   __shared__ int s_level_of_set[kMaxUnits][CG_MAX_LEVELS];
   __shared__ int s_nsets[kMaxUnits];
+  __shared__ int s_simd[kMaxWaves];            // SIMD of each wave
+  __shared__ int s_left[kMaxWaves];             // tokens each wave has left to decode
   const int msets = nw < P.NLV ? nw : P.NLV;          // table sets a unit may need
   uint16_t* obuf_all = smem;                          // [nu * nw][kG10][64] rows per wave
   uint16_t* tabs = obuf_all + nu * nw * kG10 * 64;    // [nu][msets][64][kTabStride]
@@ -678,8 +690,20 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   const int c = uni(active ? c_begin + pair % ncr : 0);
   const int lv = uni(active ? min((int)chunk_level[(int64_t)b * P.NC + c], P.NLV - 1) : 0);
 
+  const int simd = (int)((__builtin_amdgcn_s_getreg((31 << 11) | 4) >> 4) & 3u);   // HW_ID
   if (threadIdx.x < nu) s_mask[threadIdx.x] = 0u;
+  if (lane == 0) {
+    s_simd[wave] = simd;
+    lds_put(&s_left[wave], active ? min(P.CL, P.T - c * P.CL) : 0);
+  }
   __syncthreads();
+  // the (up to three) other waves of this workgroup on this wave's SIMD
+  int p0 = wave, p1 = wave, p2 = wave, np = 0;
+  for (int w2 = 0; w2 < nwaves; ++w2) {
+    if (w2 == wave || uni(s_simd[w2]) != simd) continue;
+    if (np == 0) p0 = w2; else if (np == 1) p1 = w2; else if (np == 2) p2 = w2;
+    ++np;
+  }
   if (active && lane == 0) atomicOr(&s_mask[u], 1u << lv);
   __syncthreads();
   if (threadIdx.x < nu) {
@@ -690,22 +714,40 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     s_nsets[uu] = n;
   }
   __syncthreads();
-  for (int idx = wave; idx < nu * msets * 64; idx += nwaves) {
-    const int t = idx & 63, st = (idx >> 6) % msets, uu = (idx >> 6) / msets;
-    const int unit2 = ublk * nu + uu;
-    if (unit2 >= n_units || st >= s_nsets[uu]) continue;
-    const int ch = (unit2 % P.nblk) * 64 + t;
-    if (ch >= P.C) continue;
-    const int lk = unit2 / P.nblk;   // l * 2 + k
-    const uint32_t* src = reinterpret_cast<const uint32_t*>(
-        cdfD + (((int64_t)s_level_of_set[uu][st] * P.L * 2 + lk) * P.C + ch) * 256);
-    uint32_t* dst = reinterpret_cast<uint32_t*>(tabs + ((uu * msets + st) * 64 + t) * kTabStride);
-    const uint32_t v0 = src[lane];
-    uint32_t v1 = src[lane + 64];
-    if (lane == 63) v1 = (v1 & 0xFFFFu) | 0xFFFF0000u;  // entry 255: sentinel above any target
-    dst[lane] = v0;
-    dst[lane + 64] = v1;
-    if (lane < 2) dst[128 + lane] = 0xFFFFFFFFu;        // entries 256..259: sentinels
+  // stage the tables: a row (one table, 512 bytes) is 32 lanes x 16 bytes, so a wave moves two
+  // rows per load instruction; kStageBatch loads per lane are in flight before their stores
+  const int n_rows = nu * msets * 64;
+  const int half = lane >> 5, piece = lane & 31;
+  for (int base = wave; base * 2 < n_rows; base += nwaves * kStageBatch) {
+    uint4 v[kStageBatch];
+    int dsto[kStageBatch];
+#pragma unroll
+    for (int i = 0; i < kStageBatch; ++i) {
+      // unconditional loads (a row that is not staged reads the first table instead), so that
+      // all of them are in flight before the first store waits
+      const int rr = (base + i * nwaves) * 2 + half;
+      const int t = rr & 63, st = (rr >> 6) % msets, uu = min((rr >> 6) / msets, nu - 1);
+      const int unit2 = ublk * nu + uu;
+      const int ch = (unit2 % P.nblk) * 64 + t;
+      const int lset = s_level_of_set[uu][st], nset = s_nsets[uu];   // in bounds for any rr
+      const bool ok = (rr < n_rows) & (unit2 < n_units) & (st < nset) & (ch < P.C);
+      const int lk = unit2 / P.nblk;   // l * 2 + k
+      const int64_t row = ok ? ((int64_t)lset * P.L * 2 + lk) * P.C + ch : 0;
+      v[i] = reinterpret_cast<const uint4*>(cdfD + row * 256)[piece];
+      dsto[i] = ok ? ((uu * msets + st) * 64 + t) * kTabStride + piece * 8 : -1;
+    }
+#pragma unroll
+    for (int i = 0; i < kStageBatch; ++i) {
+      if (dsto[i] < 0) continue;
+      uint2* dst = reinterpret_cast<uint2*>(tabs + dsto[i]);   // 8-byte aligned (520-byte rows)
+      uint4 x = v[i];
+      if (piece == 31) {
+        x.w = (x.w & 0xFFFFu) | 0xFFFF0000u;         // entry 255: sentinel above any target
+        dst[2] = make_uint2(0xFFFFFFFFu, 0xFFFFFFFFu);  // entries 256..259: sentinels
+      }
+      dst[0] = make_uint2(x.x, x.y);
+      dst[1] = make_uint2(x.z, x.w);
+    }
   }
   __syncthreads();
 
@@ -771,6 +813,8 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
 
   const int ngr = n / kG10;
   for (int gi = 0; gi < ngr; ++gi) {
+    const int l0 = uni(lds_get(&s_left[p0])), l1 = uni(lds_get(&s_left[p1])),
+              l2 = uni(lds_get(&s_left[p2]));
     g10_token<true>(st, fA, fD, dtab, gA, s, w, obuf, 0, lane);
     g10_epoch(st, sbase, cap);
     g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 1, lane);
@@ -786,6 +830,17 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 9, lane);
     g10_flush(obuf, row, rstride, kG10, lane, cbase, P.C);
     row += kG10 * rstride;
+    // issue priority by remaining work among the waves of this SIMD (most left first), so
+    // they finish together instead of the oldest first
+    const int left = n - (gi + 1) * kG10;
+    lds_put(&s_left[wave], left);
+    const int rank = (p0 != wave && (l0 > left || (l0 == left && p0 < wave))) +
+                     (p1 != wave && (l1 > left || (l1 == left && p1 < wave))) +
+                     (p2 != wave && (l2 > left || (l2 == left && p2 < wave)));
+    if (rank == 0) __builtin_amdgcn_s_setprio(3);
+    else if (rank == 1) __builtin_amdgcn_s_setprio(2);
+    else if (rank == 2) __builtin_amdgcn_s_setprio(1);
+    else __builtin_amdgcn_s_setprio(0);
   }
   const int rem = n - ngr * kG10;   // last, partial group (uniform)
   if (rem > 0) {
