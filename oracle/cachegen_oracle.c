@@ -443,6 +443,17 @@ static int level_of(const cgo_params* p, const uint8_t* chunk_level, const strea
   return lv < p->n_levels ? lv : p->n_levels - 1;
 }
 
+/* The order in which a stream's symbols are coded (reading 14): order[i] is the token (within
+ * the chunk) of the i-th coded symbol. First every anchor (tokens 0, G, 2G, ...), then every
+ * other token, each part in token order. The paper fixes what is coded and under which
+ * distribution (Sec. 5.2), not the order of the symbols inside one bitstream. */
+static void coded_order(int64_t n, int64_t G, int64_t* order) {
+  int64_t i = 0;
+  for (int64_t j = 0; j < n; j += G) order[i++] = j;
+  for (int64_t j = 0; j < n; ++j)
+    if (j % G != 0) order[i++] = j;
+}
+
 uint64_t cgo_stream_bound_words(int64_t n) { return (18ull * (uint64_t)n + 2 + 31) / 32; }
 
 /* Encode one stream s into out (zeroed, cap_words). Also returns its scale and symbols.
@@ -460,8 +471,17 @@ uint64_t cgo_encode_stream(const cgo_params* p, const uint16_t* kv, const uint8_
   cgo_quantize_stream(st.x, st.stride, st.n, p->group_size, sc, w, sym, NULL);
   const uint16_t* ta = anchor_table(p, cdf_anchor, &st);
   const uint16_t* td = delta_table(p, cdf_delta, lv, &st);
-  for (int64_t j = 0; j < st.n; ++j) tabs[j] = (j % p->group_size == 0) ? ta : td;
-  uint64_t bits = cgo_ac_encode(sym, st.n, tabs, out, cap_words);
+  /* coded order (reading 14): the anchors in token order, then the deltas in token order */
+  int64_t* order = (int64_t*)malloc((size_t)st.n * sizeof(int64_t));
+  coded_order(st.n, p->group_size, order);
+  uint8_t* csym = (uint8_t*)malloc((size_t)st.n);
+  for (int64_t i = 0; i < st.n; ++i) {
+    csym[i] = sym[order[i]];
+    tabs[i] = (order[i] % p->group_size == 0) ? ta : td;
+  }
+  uint64_t bits = cgo_ac_encode(csym, st.n, tabs, out, cap_words);
+  free(csym);
+  free(order);
   free(tabs);
   if (!sym_out) free(sym);
   if (scale_out) *scale_out = sc;
@@ -481,8 +501,14 @@ void cgo_decode_stream(const cgo_params* p, const uint32_t* words, uint64_t nwor
   const uint16_t** tabs = (const uint16_t**)malloc((size_t)st.n * sizeof(*tabs));
   const uint16_t* ta = anchor_table(p, cdf_anchor, &st);
   const uint16_t* td = delta_table(p, cdf_delta, lv, &st);
-  for (int64_t j = 0; j < st.n; ++j) tabs[j] = (j % p->group_size == 0) ? ta : td;
-  cgo_ac_decode(words, nwords, st.n, tabs, sym);
+  int64_t* order = (int64_t*)malloc((size_t)st.n * sizeof(int64_t));
+  coded_order(st.n, p->group_size, order);
+  uint8_t* csym = (uint8_t*)malloc((size_t)st.n);
+  for (int64_t i = 0; i < st.n; ++i) tabs[i] = (order[i] % p->group_size == 0) ? ta : td;
+  cgo_ac_decode(words, nwords, st.n, tabs, csym);
+  for (int64_t i = 0; i < st.n; ++i) sym[order[i]] = csym[i];
+  free(csym);
+  free(order);
   if (kv_out) {
     int64_t C = p->n_channels, L = p->n_layers, T = p->n_tokens;
     uint16_t* dst = kv_out + (((st.b * L + st.l) * 2 + st.k) * T + st.t0) * C + st.ch;

@@ -132,36 +132,9 @@ __device__ __forceinline__ uint32_t delta_leaf(const uint16_t* q, uint32_t ti, u
   return c;
 }
 
-// Largest j in [0, 15] with v[j] <= ti, for sorted v[0..16] with v[0] <= ti < v[16]; lo = v[j],
-// hi = v[j + 1]. A binary search by selects on registers: each decision also picks the
-// candidates of the later levels, so the chain is four compare / select steps.
-__device__ __forceinline__ uint32_t select16(const uint32_t (&v)[17], uint32_t ti, uint32_t& lo,
-                                             uint32_t& hi) {
-  const bool c3 = v[8] <= ti;
-  const uint32_t p4 = c3 ? v[12] : v[4];
-  const uint32_t p2a = c3 ? v[10] : v[2], p2b = c3 ? v[14] : v[6];
-  const uint32_t p1a = c3 ? v[9] : v[1], p1b = c3 ? v[11] : v[3];
-  const uint32_t p1c = c3 ? v[13] : v[5], p1d = c3 ? v[15] : v[7];
-  uint32_t l = c3 ? v[8] : v[0], h = c3 ? v[16] : v[8];
-  const bool c2 = p4 <= ti;
-  const uint32_t p2 = c2 ? p2b : p2a;
-  const uint32_t p1e = c2 ? p1c : p1a, p1f = c2 ? p1d : p1b;
-  l = c2 ? p4 : l;
-  h = c2 ? h : p4;
-  const bool c1 = p2 <= ti;
-  const uint32_t p1 = c1 ? p1f : p1e;
-  l = c1 ? p2 : l;
-  h = c1 ? h : p2;
-  const bool c0 = p1 <= ti;
-  l = c0 ? p1 : l;
-  h = c0 ? h : p1;
-  lo = l;
-  hi = h;
-  return (c3 ? 8u : 0u) | (c2 ? 4u : 0u) | (c1 ? 2u : 0u) | (c0 ? 1u : 0u);
-}
-
-// 16 j - 127 for the largest j in [0, 15] with v[j] <= ti (sorted v, v[0] <= ti < v[16]): the
-// select search of select16 without the bounds, its index already scaled and biased so that
+// 16 j - 127 for the largest j in [0, 15] with v[j] <= ti (sorted v, v[0] <= ti < v[16]): a
+// binary search by selects on registers, each decision also picking the candidates of the
+// later levels (a chain of four compare / select steps), its index scaled and biased so that
 // adding the offset of the symbol inside the block gives the quantized value.
 __device__ __forceinline__ int fence_q(const uint32_t (&v)[17], uint32_t ti) {
   const bool c3 = v[8] <= ti;
@@ -295,17 +268,21 @@ __global__ __launch_bounds__(1024) void decode_kernel(
   uint16_t* row = out + cg_elem(P, b, l, k, tok0, cb * 64);  // wave-uniform row pointer
   const int64_t rstride = P.C;
   uint16_t* obuf = obuf_all + wave * kRows * 64;
-  int r = 0;
-  float a = 0.0f;
-  int g = 0;
-  for (int j = 0; j < n; ++j) {
-    if ((j & (kEpoch - 1)) == 0 && j != 0) {
-      // s0..s(3-h) are still unread; positions 4-h..3 take t0..t(h-1)
+  int nsym = 0;   // symbols decoded so far (the bitstream epochs come every kEpoch symbols)
+
+  // One symbol under the lane's anchor (global blocks, fences in LDS) or delta (LDS) table.
+  auto decode_symbol = [&](bool anchor) __attribute__((always_inline)) -> int {
+    if ((nsym & (kEpoch - 1)) == 0 && nsym != 0) {
+      // s0..s(3-h) are still unread; positions 4-h..3 take t0..t(h-1). Selects between
+      // register copies (selects between the captured variables themselves could become
+      // selects of their addresses, which would move the state to scratch memory).
       const bool g1 = hcnt >= 1, g2 = hcnt >= 2, g3 = hcnt >= 3, g4 = hcnt >= 4;
-      const uint32_t n3 = g4 ? t3 : (g3 ? t2 : (g2 ? t1 : (g1 ? t0 : s3)));
-      const uint32_t n2 = g4 ? t2 : (g3 ? t1 : (g2 ? t0 : s2));
-      const uint32_t n1 = g4 ? t1 : (g3 ? t0 : s1);
-      const uint32_t n0 = g4 ? t0 : s0;
+      uint32_t T0 = t0, T1 = t1, T2 = t2, T3 = t3, S0 = s0, S1 = s1, S2 = s2, S3 = s3;
+      asm("" : "+v"(T0), "+v"(T1), "+v"(T2), "+v"(T3), "+v"(S0), "+v"(S1), "+v"(S2), "+v"(S3));
+      const uint32_t n3 = g4 ? T3 : (g3 ? T2 : (g2 ? T1 : (g1 ? T0 : S3)));
+      const uint32_t n2 = g4 ? T2 : (g3 ? T1 : (g2 ? T0 : S2));
+      const uint32_t n1 = g4 ? T1 : (g3 ? T0 : S1);
+      const uint32_t n0 = g4 ? T0 : S0;
       s0 = n0; s1 = n1; s2 = n2; s3 = n3;
       wpos += hcnt;
       hcnt = 0;
@@ -315,6 +292,7 @@ __global__ __launch_bounds__(1024) void decode_kernel(
       const uint32_t* tq = words + (wpos < wcap ? wpos : wcap);
       t0 = tq[0]; t1 = tq[1]; t2 = tq[2]; t3 = tq[3];
     }
+    ++nsym;
     // 1. estimate of the target t = floor(((D + 1) * 2^16 - 1) / (rm1 + 1)); within one
     const float te = (float)D * (65536.0f * __builtin_amdgcn_rcpf((float)rm1));
     const uint32_t ti = min((uint32_t)te, 65534u);
@@ -322,7 +300,6 @@ __global__ __launch_bounds__(1024) void decode_kernel(
 
     int sym;
     uint32_t clo, chi;
-    const bool anchor = (g == 0);
     if (anchor) {
       // fences in LDS: largest f with cum[16 f] <= ti, then the block from global memory
       int f = 0;
@@ -413,16 +390,36 @@ __global__ __launch_bounds__(1024) void decode_kernel(
       s0 = s1; s1 = s2; s2 = s3;
       ++hcnt;
     }
+    return sym - 127;
+  };
 
-    // dequantize (step a7) into the wave's row buffer
-    const float qf = (float)(sym - 127);
+  // anchor phase: the chunk's anchors come first in the stream. Each one's fp16 value goes to
+  // its row; its quantized value q goes to the group's first delta row (when there is one),
+  // where the delta phase reads it back before the decoded delta replaces it.
+  uint16_t* col = row + lsrc;
+  const int na = (n + P.G - 1) / P.G;
+  for (int g = 0; g < na; ++g) {
+    const int qi = decode_symbol(true);
+    uint16_t* ra = col + (int64_t)g * P.G * rstride;
+    if (g * P.G + 1 < n && P.G > 1) ra[rstride] = (uint16_t)qi;
+    ra[0] = cg_f2h((float)qi * s);
+  }
+  if (P.G == 1) return;   // every token is an anchor
+
+  // delta phase: rows are staged in LDS as before; an anchor row takes the value the anchor
+  // phase stored (read back from its row)
+  int r = 0;
+  float a = 0.0f;
+  int g = 0;
+  for (int j = 0; j < n; ++j) {
     float v;
-    if (anchor) {
-      a = qf * s;
-      v = a;
+    if (g == 0) {
+      const uint16_t* ra = col + (int64_t)j * rstride;
+      if (j + 1 < n) a = (float)(int)(int16_t)ra[rstride] * s;
+      v = cg_h2f(ra[0]);
     } else {
-      const float qw = qf * w;
-      v = a + qw;
+      const int qi = decode_symbol(false);
+      v = a + (float)qi * w;
     }
     obuf[r * 64 + lane] = cg_f2h(v);
     g = (g + 1 == P.G) ? 0 : g + 1;
@@ -457,17 +454,18 @@ __global__ __launch_bounds__(1024) void decode_kernel(
 
 
 // ---- group size 10: the schedule of a group is fixed at compile time -------------------------
-// Same decoder, same results, for the paper's group of 10 tokens (one anchor, nine deltas):
-//   * the anchor / delta choice, the row of the staging buffer and the bitstream epochs are
-//     compile-time per token, so no per-token bookkeeping is left;
-//   * the 15 fences cum[16 f] of the lane's anchor and delta tables sit in registers, so both
-//     searches start with a 4-step select search (no memory round trip); the delta search then
-//     needs two LDS round trips (one 4-ary level, the leaf), the anchor search one global block;
-//   * epoch boundaries come after tokens 0, 3 and 6 of each group: the requests issued after
-//     token 6 are four tokens old when the next anchor waits for its block (a wait for the
-//     youngest global load also waits for every older one), and the staged rows of a group
-//     are stored after token 9.
+// Same decoder, same results, for the paper's group of 10 tokens (one anchor, nine deltas). A
+// stream holds its chunk's anchors first, then its deltas, so the kernel runs in two phases:
+//   * anchor phase: the anchor tables of the workgroup's units are staged in LDS; each wave
+//     decodes its anchors, kAnchorRun per bitstream epoch, stores each anchor's fp16 value in
+//     its row and keeps the quantized value q in the group's first delta row;
+//   * delta phase: the delta tables replace the anchor tables in LDS; each group reads back its
+//     anchor's q (requested a group ahead), decodes its nine deltas with epochs before deltas
+//     1, 4 and 7, and stores rows 1..9 (over the kept q).
+// Both searches start from the 15 fences cum[16 f] of the table in registers (a 4-step select
+// search, no memory round trip), then take two LDS round trips (one 4-ary level, the leaf).
 constexpr int kG10 = 10;
+constexpr int kAnchorRun = 4;   // anchors per bitstream epoch (a symbol takes <= 18 bits)
 
 // Per-lane decoder state of the group-of-10 kernel (plain scalars: it lives in registers).
 // Bitstream reader: the 128 bits after the code value's own are held in w0..w3, of which the
@@ -545,45 +543,23 @@ __device__ __forceinline__ void g10_advance(G10Lane& st, uint32_t lo_off, uint32
   st.hcnt += adv ? 1u : 0u;
 }
 
-// One token: decode the symbol at row r of the group (the anchor when kAnchor) and stage its
-// fp16 value in the wave's row buffer.
-template <bool kAnchor>
-__device__ __forceinline__ void g10_token(G10Lane& st, const uint32_t (&fA)[17],
-                                          const uint32_t (&fD)[17], const uint16_t* dtab,
-                                          const uint16_t* __restrict__ gA, float s, float w,
-                                          uint16_t* obuf, int r, int lane) {
+// One symbol under the table `tab` (LDS, 256 entries plus sentinels) whose fences cum[16 f]
+// are fT: returns q = symbol - 127 after the interval update and the refill of D.
+__device__ __forceinline__ int g10_symbol(G10Lane& st, const uint32_t (&fT)[17],
+                                          const uint16_t* tab) {
   const float te = (float)st.D * (65536.0f * __builtin_amdgcn_rcpf((float)st.rm1));
   const uint32_t ti = min((uint32_t)te, 65534u);
   const uint32_t kneg = ~ti;
-  const uint16_t* dtab127 = dtab + 127;
-  int qi;   // quantized value = symbol - 127
-  uint32_t clo, chi;
-  if constexpr (kAnchor) {
-    uint32_t flo, fhi;
-    const uint32_t f = select16(fA, ti, flo, fhi);
-    const uint4* blk = reinterpret_cast<const uint4*>(gA + 16 * f);
-    const uint4 q0 = blk[0], q1 = blk[1];
-    uint32_t v[17];
-    v[0] = q0.x & 0xFFFFu;  v[1] = q0.x >> 16;  v[2] = q0.y & 0xFFFFu;  v[3] = q0.y >> 16;
-    v[4] = q0.z & 0xFFFFu;  v[5] = q0.z >> 16;  v[6] = q0.w & 0xFFFFu;  v[7] = q0.w >> 16;
-    v[8] = q1.x & 0xFFFFu;  v[9] = q1.x >> 16;  v[10] = q1.y & 0xFFFFu; v[11] = q1.y >> 16;
-    v[12] = q1.z & 0xFFFFu; v[13] = q1.z >> 16; v[14] = q1.w & 0xFFFFu;
-    v[15] = f == 15 ? CG_TOTAL : q1.w >> 16;   // symbol 255 does not exist
-    v[16] = fhi;
-    const uint32_t jj = select16(v, ti, clo, chi);
-    qi = (int)(16 * f + jj) - 127;
-  } else {
-    const int fq = fence_q(fD, ti);           // 16 f - 127
-    const uint16_t* q = dtab127 + fq;          // the block of cum[16 f]
-    const int l4 = 4 * (int)((((uint32_t)q[4] + kneg) >> 31) + (((uint32_t)q[8] + kneg) >> 31) +
-                             (((uint32_t)q[12] + kneg) >> 31));
-    q += l4;
-    uint32_t pr;
-    const uint32_t cc = delta_leaf(q, ti, pr);
-    qi = fq + l4 + (int)cc;
-    clo = pr & 0xFFFFu;
-    chi = qi == CG_NSYM - 1 - 127 ? CG_TOTAL : pr >> 16;
-  }
+  const int fq = fence_q(fT, ti);          // 16 f - 127
+  const uint16_t* q = tab + 127 + fq;      // the block of cum[16 f]
+  const int l4 = 4 * (int)((((uint32_t)q[4] + kneg) >> 31) + (((uint32_t)q[8] + kneg) >> 31) +
+                           (((uint32_t)q[12] + kneg) >> 31));
+  q += l4;
+  uint32_t pr;
+  const uint32_t cc = delta_leaf(q, ti, pr);
+  int qi = fq + l4 + (int)cc;
+  uint32_t clo = pr & 0xFFFFu;
+  uint32_t chi = qi == CG_NSYM - 1 - 127 ? CG_TOTAL : pr >> 16;
   const uint32_t D = st.D, rm1 = st.rm1;
   // offsets of the candidate's interval from low: [lo_off, hoff) (hoff mod 2^32). The candidate
   // is the symbol iff D - lo_off < hoff - lo_off (unsigned): below lo_off the difference wraps
@@ -597,14 +573,8 @@ __device__ __forceinline__ void g10_token(G10Lane& st, const uint32_t (&fA)[17],
     for (int guard = 0; guard < CG_NSYM; ++guard) {
       sym = (D < lo_off) ? max(sym - 1, 0) : min(sym + 1, CG_NSYM - 1);
       const int s1 = min(sym + 1, CG_NSYM - 1);
-      if constexpr (kAnchor) {
-        clo = gA[sym];
-        chi = gA[s1];
-      } else {
-        clo = dtab[sym];
-        chi = dtab[s1];
-      }
-      chi = sym + 1 >= CG_NSYM ? CG_TOTAL : chi;
+      clo = tab[sym];
+      chi = sym + 1 >= CG_NSYM ? CG_TOTAL : (uint32_t)tab[s1];
       lo_off = scaled_off(rm1, clo);
       hoff = scaled_off(rm1, chi);
       d = D - lo_off;
@@ -614,27 +584,28 @@ __device__ __forceinline__ void g10_token(G10Lane& st, const uint32_t (&fA)[17],
     qi = sym - 127;
   }
   g10_advance(st, lo_off, hoff, d, rsz);
-  const float qf = (float)qi;
-  float v;
-  if constexpr (kAnchor) {
-    st.a = qf * s;
-    v = st.a;
-  } else {
-    v = st.a + qf * w;
-  }
-  obuf[r * 64 + lane] = cg_f2h(v);
+  return qi;
 }
 
-// Store rows 0 .. rows-1 of the staged group: lane L stores 16 bytes (8 channels) of row L / 8,
-// then lanes 0..15 rows 8 and 9.
+// One delta token: its symbol under the delta table, dequantized against the group's anchor
+// into row r of the wave's staging buffer.
+__device__ __forceinline__ void g10_delta(G10Lane& st, const uint32_t (&fD)[17],
+                                          const uint16_t* dtab, float w, uint16_t* obuf, int r,
+                                          int lane) {
+  const int qi = g10_symbol(st, fD, dtab);
+  obuf[r * 64 + lane] = cg_f2h(st.a + (float)qi * w);
+}
+
+// Store rows first .. rows-1 of the staged group: lane L stores 16 bytes (8 channels) of row
+// first + L / 8, then lanes 0..15 rows first + 8 and first + 9.
 __device__ __forceinline__ void g10_flush(const uint16_t* obuf, uint16_t* row, int64_t rstride,
-                                          int rows, int lane, int cbase, int C) {
+                                          int first, int rows, int lane, int cbase, int C) {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
   for (int part = 0; part < 2; ++part) {
-    const int rr = part * 8 + (lane >> 3), cc = (lane & 7) * 8;
+    const int rr = first + part * 8 + (lane >> 3), cc = (lane & 7) * 8;
     if (rr < rows && cbase + cc < C) {
       const uint4 vals = *reinterpret_cast<const uint4*>(obuf + rr * 64 + cc);
       uint16_t* dst = row + rr * rstride + cc;
@@ -665,11 +636,14 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   __shared__ int s_set_of_level[kMaxUnits][CG_MAX_LEVELS];
   __shared__ int s_level_of_set[kMaxUnits][CG_MAX_LEVELS];
   __shared__ int s_nsets[kMaxUnits];
-  __shared__ int s_simd[kMaxWaves];            // SIMD of each wave
-  __shared__ int s_left[kMaxWaves];             // tokens each wave has left to decode
+  __shared__ int s_simd[kMaxWaves];             // SIMD of each wave
+  __shared__ int s_left[kMaxWaves];             // symbols each wave has left in this phase
   const int msets = nw < P.NLV ? nw : P.NLV;          // table sets a unit may need
   uint16_t* obuf_all = smem;                          // [nu * nw][kG10][64] rows per wave
   uint16_t* tabs = obuf_all + nu * nw * kG10 * 64;    // [nu][msets][64][kTabStride]
+
+  const uint64_t total = offsets[P.S];
+  if (total == 0) return;   // no payload at all: nothing to decode (uniform over the grid)
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int nwaves = blockDim.x >> 6;
@@ -689,12 +663,15 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   const int b = uni(active ? pair / ncr : 0);
   const int c = uni(active ? c_begin + pair % ncr : 0);
   const int lv = uni(active ? min((int)chunk_level[(int64_t)b * P.NC + c], P.NLV - 1) : 0);
+  const int tok0 = c * P.CL;
+  const int n = uni(active ? min(P.CL, P.T - tok0) : 0);
+  const int na = (n + kG10 - 1) / kG10;               // anchors (coded first)
 
   const int simd = (int)((__builtin_amdgcn_s_getreg((31 << 11) | 4) >> 4) & 3u);   // HW_ID
   if (threadIdx.x < nu) s_mask[threadIdx.x] = 0u;
   if (lane == 0) {
     s_simd[wave] = simd;
-    lds_put(&s_left[wave], active ? min(P.CL, P.T - c * P.CL) : 0);
+    lds_put(&s_left[wave], na);
   }
   __syncthreads();
   // the (up to three) other waves of this workgroup on this wave's SIMD
@@ -704,135 +681,11 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     if (np == 0) p0 = w2; else if (np == 1) p1 = w2; else if (np == 2) p2 = w2;
     ++np;
   }
-  if (active && lane == 0) atomicOr(&s_mask[u], 1u << lv);
-  __syncthreads();
-  if (threadIdx.x < nu) {
-    const int uu = threadIdx.x;
-    int n = 0;
-    for (int v = 0; v < P.NLV; ++v)
-      if ((s_mask[uu] >> v) & 1u) { s_set_of_level[uu][v] = n; s_level_of_set[uu][n] = v; ++n; }
-    s_nsets[uu] = n;
-  }
-  __syncthreads();
-  // stage the tables: a row (one table, 512 bytes) is 32 lanes x 16 bytes, so a wave moves two
-  // rows per load instruction; kStageBatch loads per lane are in flight before their stores
-  const int n_rows = nu * msets * 64;
-  const int half = lane >> 5, piece = lane & 31;
-  for (int base = wave; base * 2 < n_rows; base += nwaves * kStageBatch) {
-    uint4 v[kStageBatch];
-    int dsto[kStageBatch];
-#pragma unroll
-    for (int i = 0; i < kStageBatch; ++i) {
-      // unconditional loads (a row that is not staged reads the first table instead), so that
-      // all of them are in flight before the first store waits
-      const int rr = (base + i * nwaves) * 2 + half;
-      const int t = rr & 63, st = (rr >> 6) % msets, uu = min((rr >> 6) / msets, nu - 1);
-      const int unit2 = ublk * nu + uu;
-      const int ch = (unit2 % P.nblk) * 64 + t;
-      const int lset = s_level_of_set[uu][st], nset = s_nsets[uu];   // in bounds for any rr
-      const bool ok = (rr < n_rows) & (unit2 < n_units) & (st < nset) & (ch < P.C);
-      const int lk = unit2 / P.nblk;   // l * 2 + k
-      const int64_t row = ok ? ((int64_t)lset * P.L * 2 + lk) * P.C + ch : 0;
-      v[i] = reinterpret_cast<const uint4*>(cdfD + row * 256)[piece];
-      dsto[i] = ok ? ((uu * msets + st) * 64 + t) * kTabStride + piece * 8 : -1;
-    }
-#pragma unroll
-    for (int i = 0; i < kStageBatch; ++i) {
-      if (dsto[i] < 0) continue;
-      uint2* dst = reinterpret_cast<uint2*>(tabs + dsto[i]);   // 8-byte aligned (520-byte rows)
-      uint4 x = v[i];
-      if (piece == 31) {
-        x.w = (x.w & 0xFFFFu) | 0xFFFF0000u;         // entry 255: sentinel above any target
-        dst[2] = make_uint2(0xFFFFFFFFu, 0xFFFFFFFFu);  // entries 256..259: sentinels
-      }
-      dst[0] = make_uint2(x.x, x.y);
-      dst[1] = make_uint2(x.z, x.w);
-    }
-  }
-  __syncthreads();
-
-  if (!active) return;
-  const int ch = cb * 64 + lane;
-  const bool valid = ch < P.C;
-  const int lsrc = valid ? lane : 0;   // lanes past C decode a copy of the block's first channel
-  const int chv = cb * 64 + lsrc;
-
-  const int64_t bclk = (((int64_t)b * P.NC + c) * P.L + l) * 2 + k;
-  const int64_t sidx = cg_stream(P, bclk, chv);
-  const int tok0 = c * P.CL;
-  const int n = uni(min(P.CL, P.T - tok0));
-  const float s = scales[sidx];
-  const float w = P.layer_bin[l] * P.level_mult[lv] * s;
-  const uint16_t* dtab = tabs + ((u * msets + s_set_of_level[u][lv]) * 64 + lsrc) * kTabStride;
-  const uint16_t* gA = cdfA + ((int64_t)(l * 2 + k) * P.C + chv) * 256;
-
-  // fences cum[16 f], f = 0..16 (cum[256] = total), of both tables
-  uint32_t fD[17], fA[17];
-  fD[0] = 0u;
-  fA[0] = 0u;
-  fD[16] = CG_TOTAL;
-  fA[16] = CG_TOTAL;
-#pragma unroll
-  for (int f = 1; f < 16; ++f) {
-    fD[f] = dtab[16 * f];
-    fA[f] = gA[16 * f];
-  }
-
-  const uint64_t total = offsets[P.S];
-  if (total == 0) return;
-  // bitstream reader: the code value, w0..w3 and the four requested words t0..t3 are the
-  // stream's first 13 words; every read stays below offsets[S] + 4 (the requests are clamped
-  // to it), inside the readable tail
-  G10Lane st;
-  const uint64_t o0 = offsets[sidx];
-  const uint64_t ob = o0 < total ? o0 : total;
-  const uint32_t* sbase = words + ob;
-  const uint32_t cap = (uint32_t)((total - ob) < 0xFFFFFFF0ull ? (total - ob) : 0xFFFFFFF0ull);
-  st.D = sbase[0];
-  st.w0 = sbase[1];
-  st.w1 = sbase[2];
-  st.w2 = sbase[3];
-  st.w3 = sbase[4];
-  st.pos = 0;
-  st.hcnt = 0;
-  st.widx = 5;
-  const uint32_t* tq0 = sbase + (5u < cap ? 5u : cap);
-  st.t0 = tq0[0];
-  st.t1 = tq0[1];
-  st.t2 = tq0[2];
-  st.t3 = tq0[3];
-  settle(st.D); settle(st.w0); settle(st.w1); settle(st.w2); settle(st.w3);
-  st.low = 0u;
-  st.rm1 = 0xFFFFFFFFu;
-  st.a = 0.0f;
-
-  uint16_t* row = out + cg_elem(P, b, l, k, tok0, cb * 64);
-  const int64_t rstride = P.C;
-  uint16_t* obuf = obuf_all + wave * kG10 * 64;
-  const int cbase = cb * 64;
-
-  const int ngr = n / kG10;
-  for (int gi = 0; gi < ngr; ++gi) {
+  // issue priority by what is left among the waves of this SIMD (most left first), so that
+  // they finish a phase together instead of the oldest first
+  auto set_priority = [&](int left) __attribute__((always_inline)) {
     const int l0 = uni(lds_get(&s_left[p0])), l1 = uni(lds_get(&s_left[p1])),
               l2 = uni(lds_get(&s_left[p2]));
-    g10_token<true>(st, fA, fD, dtab, gA, s, w, obuf, 0, lane);
-    g10_epoch(st, sbase, cap);
-    g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 1, lane);
-    g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 2, lane);
-    g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 3, lane);
-    g10_epoch(st, sbase, cap);
-    g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 4, lane);
-    g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 5, lane);
-    g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 6, lane);
-    g10_epoch(st, sbase, cap);
-    g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 7, lane);
-    g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 8, lane);
-    g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, 9, lane);
-    g10_flush(obuf, row, rstride, kG10, lane, cbase, P.C);
-    row += kG10 * rstride;
-    // issue priority by remaining work among the waves of this SIMD (most left first), so
-    // they finish together instead of the oldest first
-    const int left = n - (gi + 1) * kG10;
     lds_put(&s_left[wave], left);
     const int rank = (p0 != wave && (l0 > left || (l0 == left && p0 < wave))) +
                      (p1 != wave && (l1 > left || (l1 == left && p1 < wave))) +
@@ -841,16 +694,189 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     else if (rank == 1) __builtin_amdgcn_s_setprio(2);
     else if (rank == 2) __builtin_amdgcn_s_setprio(1);
     else __builtin_amdgcn_s_setprio(0);
+  };
+  if (active && lane == 0) atomicOr(&s_mask[u], 1u << lv);
+  __syncthreads();
+  if (threadIdx.x < nu) {
+    const int uu = threadIdx.x;
+    int m = 0;
+    for (int v = 0; v < P.NLV; ++v)
+      if ((s_mask[uu] >> v) & 1u) { s_set_of_level[uu][v] = m; s_level_of_set[uu][m] = v; ++m; }
+    s_nsets[uu] = m;
+  }
+  __syncthreads();
+
+  // Stage tables into LDS: the anchor table of every unit (set 0), or the delta tables of the
+  // levels each unit's pairs use. A row (one table, 512 bytes) is 32 lanes x 16 bytes, so a
+  // wave moves two rows per load instruction; kStageBatch loads per lane are in flight before
+  // their stores. Entry 255 becomes a sentinel above any target, entries 256..259 too.
+  const int half = lane >> 5, piece = lane & 31;
+  auto stage = [&](bool anchors) __attribute__((always_inline)) {
+    const int sets = anchors ? 1 : msets;
+    const int n_rows = nu * sets * 64;
+    const uint16_t* srcbase = anchors ? cdfA : cdfD;
+    for (int base = wave; base * 2 < n_rows; base += nwaves * kStageBatch) {
+      uint4 v[kStageBatch];
+      int dsto[kStageBatch];
+#pragma unroll
+      for (int i = 0; i < kStageBatch; ++i) {
+        // unconditional loads (a row that is not staged reads the first table instead), so
+        // that all of them are in flight before the first store waits
+        const int rr = (base + i * nwaves) * 2 + half;
+        const int t = rr & 63, st = (rr >> 6) % sets, uu = min((rr >> 6) / sets, nu - 1);
+        const int unit2 = ublk * nu + uu;
+        const int ch = (unit2 % P.nblk) * 64 + t;
+        const int lset = s_level_of_set[uu][st], nset = anchors ? 1 : s_nsets[uu];
+        const bool ok = (rr < n_rows) & (unit2 < n_units) & (st < nset) & (ch < P.C);
+        const int lk = unit2 / P.nblk;   // l * 2 + k
+        const int64_t trow = anchors ? (int64_t)lk * P.C + ch
+                                     : ((int64_t)lset * P.L * 2 + lk) * P.C + ch;
+        v[i] = reinterpret_cast<const uint4*>(srcbase + (ok ? trow : 0) * 256)[piece];
+        dsto[i] = ok ? ((uu * msets + st) * 64 + t) * kTabStride + piece * 8 : -1;
+      }
+#pragma unroll
+      for (int i = 0; i < kStageBatch; ++i) {
+        if (dsto[i] < 0) continue;
+        uint2* dst = reinterpret_cast<uint2*>(tabs + dsto[i]);   // 8-byte aligned (520-byte rows)
+        uint4 x = v[i];
+        if (piece == 31) {
+          x.w = (x.w & 0xFFFFu) | 0xFFFF0000u;
+          dst[2] = make_uint2(0xFFFFFFFFu, 0xFFFFFFFFu);
+        }
+        dst[0] = make_uint2(x.x, x.y);
+        dst[1] = make_uint2(x.z, x.w);
+      }
+    }
+  };
+
+  stage(true);
+  __syncthreads();
+
+  const int ch = cb * 64 + lane;
+  const bool valid = ch < P.C;
+  // Lanes past the last channel (only when C is not a multiple of 64) decode a copy of the
+  // block's first channel, so the whole wave runs the same code; they store into that
+  // channel's column the values its own lane stores, and their staged rows are never stored.
+  const int lsrc = valid ? lane : 0;
+  const int chv = cb * 64 + lsrc;
+  const int64_t rstride = P.C;
+  uint16_t* row0 = out + cg_elem(P, b, l, k, tok0, cb * 64);   // token tok0, channel cb * 64
+  const uint16_t* tab0 = tabs + (u * msets * 64 + lsrc) * kTabStride;   // set 0 of the unit
+  G10Lane st;
+  const uint32_t* sbase = words;
+  uint32_t cap = 0;
+  float s = 1.0f, w = 1.0f;
+
+  // ---- anchor phase: the chunk's anchors, first in the stream ----------------------------
+  if (active) {
+    const int64_t bclk = (((int64_t)b * P.NC + c) * P.L + l) * 2 + k;
+    const int64_t sidx = cg_stream(P, bclk, chv);
+    s = scales[sidx];
+    w = P.layer_bin[l] * P.level_mult[lv] * s;
+    uint32_t fA[17];   // fences cum[16 f] of the anchor table, f = 0..16 (cum[256] = total)
+    fA[0] = 0u;
+    fA[16] = CG_TOTAL;
+#pragma unroll
+    for (int f = 1; f < 16; ++f) fA[f] = tab0[16 * f];
+    // bitstream reader: the code value, w0..w3 and the four requested words t0..t3 are the
+    // stream's first 13 words; every read stays below offsets[S] + 4 (the requests are clamped
+    // to it), inside the readable tail
+    const uint64_t o0 = offsets[sidx];
+    const uint64_t ob = o0 < total ? o0 : total;
+    sbase = words + ob;
+    cap = (uint32_t)((total - ob) < 0xFFFFFFF0ull ? (total - ob) : 0xFFFFFFF0ull);
+    st.D = sbase[0];
+    st.w0 = sbase[1];
+    st.w1 = sbase[2];
+    st.w2 = sbase[3];
+    st.w3 = sbase[4];
+    st.pos = 0;
+    st.hcnt = 0;
+    st.widx = 5;
+    const uint32_t* tq0 = sbase + (5u < cap ? 5u : cap);
+    st.t0 = tq0[0];
+    st.t1 = tq0[1];
+    st.t2 = tq0[2];
+    st.t3 = tq0[3];
+    settle(st.D); settle(st.w0); settle(st.w1); settle(st.w2); settle(st.w3);
+    st.low = 0u;
+    st.rm1 = 0xFFFFFFFFu;
+    st.a = 0.0f;
+
+    // kAnchorRun anchors per epoch. Each stores its fp16 value in its row and its quantized
+    // value q in the group's first delta row (when the group has one; else into its own row
+    // first, which the value then overwrites), both unconditionally
+    uint16_t* col = row0 + lsrc;
+    for (int g0 = 0; g0 < na; g0 += kAnchorRun) {
+      g10_epoch(st, sbase, cap);
+#pragma unroll
+      for (int r = 0; r < kAnchorRun; ++r) {
+        const int g = g0 + r;
+        if (g < na) {
+          const int qi = g10_symbol(st, fA, tab0);
+          uint16_t* ra = col + (int64_t)g * kG10 * rstride;
+          uint16_t* rq = g * kG10 + 1 < n ? ra + rstride : ra;
+          *rq = (uint16_t)qi;
+          *ra = cg_f2h((float)qi * s);
+        }
+      }
+      set_priority(max(na - g0 - kAnchorRun, 0));
+    }
+  }
+
+  // ---- delta phase: the delta tables replace the anchor tables --------------------------
+  __syncthreads();
+  stage(false);
+  __syncthreads();
+  if (!active || n < 2) return;
+  set_priority(n - na);
+  const uint16_t* dtab = tabs + ((u * msets + s_set_of_level[u][lv]) * 64 + lsrc) * kTabStride;
+  uint32_t fD[17];
+  fD[0] = 0u;
+  fD[16] = CG_TOTAL;
+#pragma unroll
+  for (int f = 1; f < 16; ++f) fD[f] = dtab[16 * f];
+
+  uint16_t* obuf = obuf_all + wave * kG10 * 64;
+  const int cbase = cb * 64;
+  const int ngr = n / kG10;
+  const int gmax = (n - 2) / kG10;                    // last group with a delta
+  // the anchor's q of group g (kept in the group's first delta row)
+  const uint16_t* qcol = row0 + lsrc + rstride;
+  auto q_of = [&](int g) __attribute__((always_inline)) {
+    return (uint32_t)qcol[(int64_t)min(g, gmax) * kG10 * rstride];
+  };
+  uint32_t qraw = q_of(0);
+  uint16_t* row = row0;
+  for (int gi = 0; gi < ngr; ++gi) {
+    st.a = (float)(int)(int16_t)qraw * s;
+    g10_epoch(st, sbase, cap);
+    g10_delta(st, fD, dtab, w, obuf, 1, lane);
+    g10_delta(st, fD, dtab, w, obuf, 2, lane);
+    g10_delta(st, fD, dtab, w, obuf, 3, lane);
+    g10_epoch(st, sbase, cap);
+    const uint32_t qnext = q_of(gi + 1);   // requested a group ahead
+    g10_delta(st, fD, dtab, w, obuf, 4, lane);
+    g10_delta(st, fD, dtab, w, obuf, 5, lane);
+    g10_delta(st, fD, dtab, w, obuf, 6, lane);
+    g10_epoch(st, sbase, cap);
+    g10_delta(st, fD, dtab, w, obuf, 7, lane);
+    g10_delta(st, fD, dtab, w, obuf, 8, lane);
+    g10_delta(st, fD, dtab, w, obuf, 9, lane);
+    g10_flush(obuf, row, rstride, 1, kG10, lane, cbase, P.C);
+    row += kG10 * rstride;
+    qraw = qnext;
+    set_priority((ngr - gi - 1) * (kG10 - 1));
   }
   const int rem = n - ngr * kG10;   // last, partial group (uniform)
-  if (rem > 0) {
-    g10_token<true>(st, fA, fD, dtab, gA, s, w, obuf, 0, lane);
+  if (rem > 1) {
+    st.a = (float)(int)(int16_t)qraw * s;
     g10_epoch(st, sbase, cap);
     for (int r = 1; r < rem; ++r) {
       if (r == 4 || r == 7) g10_epoch(st, sbase, cap);
-      g10_token<false>(st, fA, fD, dtab, gA, s, w, obuf, r, lane);
+      g10_delta(st, fD, dtab, w, obuf, r, lane);
     }
-    g10_flush(obuf, row, rstride, rem, lane, cbase, P.C);
+    g10_flush(obuf, row, rstride, 1, rem, lane, cbase, P.C);
   }
 }
 

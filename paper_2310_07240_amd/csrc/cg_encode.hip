@@ -288,17 +288,16 @@ __global__ __launch_bounds__(1024) void encode_kernel(
       const float v = cg_h2f((uint16_t)xv[u]);
       const bool anc = kG > 0 ? u == 0 : gq == 0;
       const int q = anc ? cg_quant_inv(v, s, is) : cg_quant_inv(v - a, w, iw);
-      if (anc) a = (float)q * s;
       const int sym = q + 127;
       const int sym1 = min(sym + 1, CG_NSYM - 1);
-      if (anc) {
-        clo[u] = tabA[sym];
-        chi[u] = tabA[sym1];
+      if (anc) {   // coded in the anchor pass; here only the base of the group's deltas
+        a = (float)q * s;
+        clo[u] = 0u;
+        chi[u] = 0u;
       } else {
         clo[u] = tabD[sym];
-        chi[u] = tabD[sym1];
+        chi[u] = sym == CG_NSYM - 1 ? CG_TOTAL : (uint32_t)tabD[sym1];
       }
-      chi[u] = sym == CG_NSYM - 1 ? CG_TOTAL : chi[u];
       if (kG == 0) gq = (gq + 1 == P.G) ? 0 : gq + 1;
     }
   };
@@ -308,25 +307,85 @@ __global__ __launch_bounds__(1024) void encode_kernel(
   };
   // a step without branches per symbol; if a lane of the wave owed more than 32 bits at some
   // symbol, the wave codes the step again from the saved state with the branching coder
-  auto code_step = [&](const uint32_t (&clo)[kPipe], const uint32_t (&chi)[kPipe], int step)
-                       __attribute__((always_inline)) {
+  // code[u] (uniform) says whether position u of the buffer is coded in this step
+  auto code_run = [&](const auto& clo, const auto& chi, const bool* code)
+                      __attribute__((always_inline)) {
+    constexpr int K = sizeof(clo) / sizeof(clo[0]);
     const EncState e0 = e;
     const uint64_t acc0 = o.acc;
     const uint32_t nacc0 = o.nacc, nwords0 = o.nwords;
     bool rare = false;
 #pragma unroll
-    for (int u = 0; u < kPipe; ++u)
-      if (step * kPipe + u < n) enc_symbol_fast(e, o, clo[u], chi[u], rare);
+    for (int u = 0; u < K; ++u)
+      if (code[u]) enc_symbol_fast(e, o, clo[u], chi[u], rare);
     if (__builtin_amdgcn_ballot_w64(rare) != 0ull) {
       e = e0;
       o.acc = acc0;
       o.nacc = nacc0;
       o.nwords = nwords0;
 #pragma unroll
-      for (int u = 0; u < kPipe; ++u)
-        if (step * kPipe + u < n) enc_symbol(e, o, clo[u], chi[u]);
+      for (int u = 0; u < K; ++u)
+        if (code[u]) enc_symbol(e, o, clo[u], chi[u]);
     }
   };
+  // the deltas of a step of the token pipeline (its anchors were coded in the anchor pass)
+  auto code_step = [&](const uint32_t (&clo)[kPipe], const uint32_t (&chi)[kPipe], int step)
+                       __attribute__((always_inline)) {
+    bool code[kPipe];
+    const int g0 = kG > 0 ? 0 : (step * kPipe) % P.G;
+#pragma unroll
+    for (int u = 0; u < kPipe; ++u) {
+      const bool anc = kG > 0 ? u == 0 : (g0 + u) % P.G == 0;
+      code[u] = step * kPipe + u < n && !anc;
+    }
+    code_run(clo, chi, code);
+  };
+
+  // Anchor pass: the anchors of the chunk in token order (they come first in the stream), in
+  // steps of kPipeA with the same two-step pipeline (rows two steps ahead, anchor-table
+  // entries one step ahead)
+  {
+    constexpr int kPipeA = 8;
+    const int G = kG > 0 ? kG : P.G;
+    const int na = (n + G - 1) / G;
+    uint32_t ya0[kPipeA], ya1[kPipeA], la0[kPipeA], ha0[kPipeA], la1[kPipeA], ha1[kPipeA];
+    auto load_anchor_rows = [&](uint32_t (&xv)[kPipeA], int step) __attribute__((always_inline)) {
+#pragma unroll
+      for (int u = 0; u < kPipeA; ++u)
+        xv[u] = x[(int64_t)min(step * kPipeA + u, na - 1) * G * rs];
+    };
+    auto quantize_anchors = [&](const uint32_t (&xv)[kPipeA], uint32_t (&clo)[kPipeA],
+                                uint32_t (&chi)[kPipeA]) __attribute__((always_inline)) {
+#pragma unroll
+      for (int u = 0; u < kPipeA; ++u) {
+        const int sym = cg_quant_inv(cg_h2f((uint16_t)xv[u]), s, is) + 127;
+        clo[u] = tabA[sym];
+        chi[u] = sym == CG_NSYM - 1 ? CG_TOTAL : (uint32_t)tabA[min(sym + 1, CG_NSYM - 1)];
+      }
+    };
+    auto code_anchors = [&](const uint32_t (&clo)[kPipeA], const uint32_t (&chi)[kPipeA],
+                            int step) __attribute__((always_inline)) {
+      bool code[kPipeA];
+#pragma unroll
+      for (int u = 0; u < kPipeA; ++u) code[u] = step * kPipeA + u < na;
+      code_run(clo, chi, code);
+    };
+    load_anchor_rows(ya0, 0);
+    load_anchor_rows(ya1, 1);
+    quantize_anchors(ya0, la0, ha0);
+    load_anchor_rows(ya0, 2);
+    for (int st = 0; st * kPipeA < na; st += 2) {
+      quantize_anchors(ya1, la1, ha1);
+      o.flush();
+      load_anchor_rows(ya1, st + 3);
+      code_anchors(la0, ha0, st);
+      if ((st + 1) * kPipeA >= na) break;
+      quantize_anchors(ya0, la0, ha0);
+      o.flush();
+      load_anchor_rows(ya0, st + 4);
+      code_anchors(la1, ha1, st + 1);
+    }
+  }
   load_rows(xr0, 0);
   load_rows(xr1, 1);
   quantize_step(xr0, lo0, hi0);

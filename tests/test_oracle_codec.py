@@ -148,3 +148,26 @@ def test_per_channel_tables_beat_one_global_table():
     gd = np.broadcast_to(oracle.normalize(hd), cd.shape).copy()
     wg, og, sg = oracle.encode(kv, shape, cl, ga, gd)
     assert words.size < wg.size
+
+
+@pytest.mark.parametrize("w", [
+    W.small(name="g7", group_size=7, n_tokens=95, chunk_len=40, n_channels=9),
+    W.small(name="g10_levels", n_tokens=61, chunk_len=25, n_channels=5, n_ctx=2),
+    W.small(name="g1", group_size=1, n_tokens=12, chunk_len=5, n_channels=3),
+], ids=lambda w: w.name)
+def test_stream_codes_anchors_then_deltas(w):
+    """Coded order of a stream: the chunk's anchor symbols (token order), then its delta
+    symbols (token order). Each stream's words, decoded by the generic coder with the tables
+    in that order, give the quantizer's symbols in that order."""
+    kv, shape, ca, cd, cl, words, offsets, scales = _codec(w)
+    C, L, NC, G = shape.n_channels, shape.n_layers, shape.n_chunks, w.group_size
+    cl2 = np.asarray(cl, np.uint8).reshape(shape.n_ctx, NC)
+    for s in range(shape.n_streams):
+        _, sym, _ = oracle.stream_symbols(kv, shape, cl, s)
+        ch = s % C; r = s // C; k = r % 2; r //= 2; l = r % L; r //= L; c = r % NC; b = r // NC
+        lv = min(int(cl2[b, c]), shape.n_levels - 1)
+        j = np.arange(sym.size)
+        order = np.concatenate([j[j % G == 0], j[j % G != 0]])
+        tabs = [ca[l, k, ch] if t % G == 0 else cd[lv, l, k, ch] for t in order]
+        got = oracle.ac_decode(words[int(offsets[s]):int(offsets[s + 1])], sym.size, tabs)
+        assert np.array_equal(got, sym[order]), s
