@@ -51,6 +51,10 @@ namespace {
 
 constexpr int kMaxWaves = 16;
 constexpr int kMaxUnits = 16;   // (layer, K/V, channel block) units per workgroup
+// static LDS of the kernel with several units (masks, level maps, SIMD ids, remaining counts);
+// the dynamic LDS budget leaves 1 KB for it
+static_assert(4 * kMaxUnits + 3 * kMaxUnits * CG_MAX_LEVELS + kMaxWaves + 4 * kMaxWaves <= 1024 - 64,
+              "static LDS exceeds the reserve");
 constexpr int kStageBatch = 8;  // table-staging loads in flight per lane
 constexpr size_t kLdsBudget = 160 * 1024 - 1024;   // dynamic LDS per workgroup (CDNA4: 160 KB)
 constexpr int kTabStride = 260;    // u16 per delta table in LDS (256 + 4 pad -> 520 bytes)
@@ -67,15 +71,6 @@ __device__ __forceinline__ uint32_t scaled_off(uint32_t x, uint32_t c) {
   uint64_t r, carry;
   asm("v_mad_u64_u32 %0, %1, %2, %3, %4" : "=v"(r), "=s"(carry) : "v"(x), "v"(c), "v"((uint64_t)c));
   return (uint32_t)(r >> 16);
-}
-
-// Relaxed LDS accesses of a value other waves of the workgroup update (no ordering, no wait
-// beyond the LDS access itself).
-__device__ __forceinline__ int lds_get(int* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-}
-__device__ __forceinline__ void lds_put(int* p, int v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
 // Make the compiler wait here for a register produced by a load (once, outside the loop).
@@ -156,7 +151,7 @@ __global__ __launch_bounds__(1024) void decode_kernel(
     const float* __restrict__ scales, const uint8_t* __restrict__ chunk_level,
     const uint16_t* __restrict__ cdfA, const uint16_t* __restrict__ cdfD, int c_begin,
     int c_end, int nw, uint16_t* __restrict__ out) {
-  extern __shared__ uint16_t smem[];
+  extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   __shared__ uint32_t s_mask;
   __shared__ int s_set_of_level[CG_MAX_LEVELS];
   __shared__ int s_level_of_set[CG_MAX_LEVELS];
@@ -631,12 +626,12 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     const float* __restrict__ scales, const uint8_t* __restrict__ chunk_level,
     const uint16_t* __restrict__ cdfA, const uint16_t* __restrict__ cdfD, int c_begin,
     int c_end, int nw, int nu, uint16_t* __restrict__ out) {
-  extern __shared__ uint16_t smem[];
+  extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   __shared__ uint32_t s_mask[kMaxUnits];
-  __shared__ int s_set_of_level[kMaxUnits][CG_MAX_LEVELS];
-  __shared__ int s_level_of_set[kMaxUnits][CG_MAX_LEVELS];
-  __shared__ int s_nsets[kMaxUnits];
-  __shared__ int s_simd[kMaxWaves];             // SIMD of each wave
+  __shared__ uint8_t s_set_of_level[kMaxUnits][CG_MAX_LEVELS];
+  __shared__ uint8_t s_level_of_set[kMaxUnits][CG_MAX_LEVELS];
+  __shared__ uint8_t s_nsets[kMaxUnits];
+  __shared__ uint8_t s_simd[kMaxWaves];             // SIMD of each wave
   __shared__ int s_left[kMaxWaves];             // symbols each wave has left in this phase
   const int msets = nw < P.NLV ? nw : P.NLV;          // table sets a unit may need
   uint16_t* obuf_all = smem;                          // [nu * nw][kG10][64] rows per wave

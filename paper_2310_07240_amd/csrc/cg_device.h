@@ -31,6 +31,15 @@ struct KParams {
   float level_mult[CG_MAX_LEVELS];
 };
 
+// Relaxed LDS accesses of a value other waves of the workgroup update (no ordering, no wait
+// beyond the LDS access itself).
+__device__ __forceinline__ int lds_get(int* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+__device__ __forceinline__ void lds_put(int* p, int v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
 __device__ __forceinline__ float cg_h2f(uint16_t h) {
   return (float)__builtin_bit_cast(_Float16, h);               // exact widening
 }

@@ -29,6 +29,11 @@
 namespace {
 
 constexpr int kEncMaxWaves = 16;
+constexpr int kEncMaxUnits = 16;   // (layer, K/V, channel block) units per workgroup
+// static LDS of the kernel with several units (masks, level maps, SIMD ids, remaining counts);
+// the dynamic LDS budget leaves 1 KB for it
+static_assert(4 * kEncMaxUnits + 3 * kEncMaxUnits * CG_MAX_LEVELS + kEncMaxWaves + 4 * kEncMaxWaves <= 1024 - 64,
+              "static LDS exceeds the reserve");
 constexpr size_t kEncLdsBudget = 160 * 1024 - 1024;   // dynamic LDS per workgroup (CDNA4: 160 KB)
 constexpr int kEncTabStride = 258;   // u16 per delta table in LDS (odd word stride: lanes spread over banks)
 constexpr int kScanThreads = 256;
@@ -193,59 +198,95 @@ __global__ __launch_bounds__(1024) void encode_kernel(
     KParams P, const uint16_t* __restrict__ kv, const uint8_t* __restrict__ chunk_level,
     const uint16_t* __restrict__ cdfA, const uint16_t* __restrict__ cdfD,
     uint32_t* __restrict__ slots, uint32_t slot_words, uint32_t* __restrict__ lens,
-    float* __restrict__ scales, int nw, int nsets_lds) {
-  // workgroup = (layer, K/V, 64-channel block) x up to kEncMaxWaves (context, chunk) pairs;
-  // the delta tables of the levels those pairs use are staged in LDS once (9 of 10 symbols
-  // look up there); anchor entries come from global memory, requested a pipeline step ahead
-  extern __shared__ uint16_t tabs[];   // [nsets][64][kEncTabStride], then words [nw][kRing][64]
-  __shared__ uint32_t s_mask;
-  __shared__ int s_set_of_level[CG_MAX_LEVELS];
-  __shared__ int s_level_of_set[CG_MAX_LEVELS];
-  __shared__ int s_nsets;
+    float* __restrict__ scales, int nw, int nu, int nsets_lds) {
+  // workgroup = nu units (layer, K/V, 64-channel block) x nw (context, chunk) pairs; wave w
+  // codes pair slot w / nu of unit w % nu (one workgroup per CU where the grid allows, so the
+  // hardware spreads its waves evenly over the SIMDs). The delta tables of the levels a unit's
+  // pairs use are staged in LDS once (9 of 10 symbols look up there); anchor entries come from
+  // global memory, requested a pipeline step ahead.
+  extern __shared__ __attribute__((aligned(16))) uint16_t tabs[];   // [nu][nsets][64][kEncTabStride], then words [nu * nw][kRing][64]
+  __shared__ uint32_t s_mask[kEncMaxUnits];
+  __shared__ uint8_t s_set_of_level[kEncMaxUnits][CG_MAX_LEVELS];
+  __shared__ uint8_t s_level_of_set[kEncMaxUnits][CG_MAX_LEVELS];
+  __shared__ uint8_t s_nsets[kEncMaxUnits];
+  __shared__ uint8_t s_simd[kEncMaxWaves];   // SIMD of each wave
+  __shared__ int s_left[kEncMaxWaves];   // symbols each wave has left to code
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int nwaves = blockDim.x >> 6;
+  const int u = wave % nu, j = wave / nu;
   const int n_pairs = P.B * P.NC;
   const int n_groups = (n_pairs + nw - 1) / nw;
+  const int n_units = P.L * 2 * P.nblk;
   const int grp = blockIdx.x % n_groups;
-  int rest = blockIdx.x / n_groups;
-  const int cb = rest % P.nblk;
-  rest /= P.nblk;
-  const int k = rest & 1, l = rest >> 1;
-  const int pair = __builtin_amdgcn_readfirstlane(grp * nw + wave);
-  const bool active = pair < n_pairs;
+  const int ublk = blockIdx.x / n_groups;
+  const int unit = ublk * nu + u;
+  const int cb = unit % P.nblk;
+  const int k = (unit / P.nblk) & 1, l = (unit / P.nblk) >> 1;
+  const int pair = __builtin_amdgcn_readfirstlane(grp * nw + j);
+  const bool active = unit < n_units && pair < n_pairs;
   const int b = active ? pair / P.NC : 0;
   const int c = active ? pair % P.NC : 0;
   const int lv = active ? min((int)chunk_level[(int64_t)b * P.NC + c], P.NLV - 1) : 0;
+  const int n = active ? min(P.CL, P.T - c * P.CL) : 0;
 
-  if (threadIdx.x == 0) s_mask = 0u;
-  __syncthreads();
-  if (active && lane == 0) atomicOr(&s_mask, 1u << lv);
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int m = 0;
-    for (int v = 0; v < P.NLV; ++v)
-      if ((s_mask >> v) & 1u) { s_set_of_level[v] = m; s_level_of_set[m] = v; ++m; }
-    s_nsets = m;
+  const int simd = (int)((__builtin_amdgcn_s_getreg((31 << 11) | 4) >> 4) & 3u);   // HW_ID
+  if (threadIdx.x < nu) s_mask[threadIdx.x] = 0u;
+  if (lane == 0) {
+    s_simd[wave] = simd;
+    lds_put(&s_left[wave], n);
   }
   __syncthreads();
-  const int nsets = s_nsets;
-  for (int idx = wave; idx < nsets * 64; idx += nwaves) {
-    const int st = idx >> 6, t = idx & 63;
-    const int chs = cb * 64 + t;
+  if (active && lane == 0) atomicOr(&s_mask[u], 1u << lv);
+  __syncthreads();
+  if (threadIdx.x < nu) {
+    const int uu = threadIdx.x;
+    int m = 0;
+    for (int v = 0; v < P.NLV; ++v)
+      if ((s_mask[uu] >> v) & 1u) { s_set_of_level[uu][v] = m; s_level_of_set[uu][m] = v; ++m; }
+    s_nsets[uu] = m;
+  }
+  __syncthreads();
+  for (int idx = wave; idx < nu * nsets_lds * 64; idx += nwaves) {
+    const int t = idx & 63, st = (idx >> 6) % nsets_lds, uu = (idx >> 6) / nsets_lds;
+    const int unit2 = ublk * nu + uu;
+    if (unit2 >= n_units || st >= s_nsets[uu]) continue;
+    const int chs = (unit2 % P.nblk) * 64 + t;
     if (chs >= P.C) continue;
+    const int lk = unit2 / P.nblk;   // l * 2 + k
     const uint32_t* src = reinterpret_cast<const uint32_t*>(
-        cdfD + ((((int64_t)s_level_of_set[st] * P.L + l) * 2 + k) * P.C + chs) * 256);
-    uint32_t* dst = reinterpret_cast<uint32_t*>(tabs + (st * 64 + t) * kEncTabStride);
+        cdfD + (((int64_t)s_level_of_set[uu][st] * P.L * 2 + lk) * P.C + chs) * 256);
+    uint32_t* dst = reinterpret_cast<uint32_t*>(tabs + ((uu * nsets_lds + st) * 64 + t) * kEncTabStride);
     dst[lane] = src[lane];
     dst[lane + 64] = src[lane + 64];
   }
   __syncthreads();
   if (!active) return;
+  // the (up to three) other waves of this workgroup on this wave's SIMD
+  int p0 = wave, p1 = wave, p2 = wave, np = 0;
+  for (int w2 = 0; w2 < nwaves; ++w2) {
+    if (w2 == wave || __builtin_amdgcn_readfirstlane(s_simd[w2]) != simd) continue;
+    if (np == 0) p0 = w2; else if (np == 1) p1 = w2; else if (np == 2) p2 = w2;
+    ++np;
+  }
+  // issue priority by what is left among the waves of this SIMD (most left first), so that
+  // they finish together instead of the oldest first
+  auto set_priority = [&](int left) __attribute__((always_inline)) {
+    const int l0 = __builtin_amdgcn_readfirstlane(lds_get(&s_left[p0]));
+    const int l1 = __builtin_amdgcn_readfirstlane(lds_get(&s_left[p1]));
+    const int l2 = __builtin_amdgcn_readfirstlane(lds_get(&s_left[p2]));
+    lds_put(&s_left[wave], left);
+    const int rank = (p0 != wave && (l0 > left || (l0 == left && p0 < wave))) +
+                     (p1 != wave && (l1 > left || (l1 == left && p1 < wave))) +
+                     (p2 != wave && (l2 > left || (l2 == left && p2 < wave)));
+    if (rank == 0) __builtin_amdgcn_s_setprio(3);
+    else if (rank == 1) __builtin_amdgcn_s_setprio(2);
+    else if (rank == 2) __builtin_amdgcn_s_setprio(1);
+    else __builtin_amdgcn_s_setprio(0);
+  };
   const int ch = cb * 64 + lane;
   if (ch >= P.C) return;
   const int64_t bclk = (((int64_t)b * P.NC + c) * P.L + l) * 2 + k;
   const int t0 = c * P.CL;
-  const int n = min(P.CL, P.T - t0);
   const int64_t sidx = cg_stream(P, bclk, ch);
   const uint16_t* x = kv + cg_elem(P, b, l, k, t0, ch);
   const int64_t rs = P.C;
@@ -261,9 +302,10 @@ __global__ __launch_bounds__(1024) void encode_kernel(
   const float is = 1.0f / s, iw = 1.0f / w;
 
   cg_glb_u16* tabA = (cg_glb_u16*)(cdfA + ((int64_t)(l * 2 + k) * P.C + ch) * 256);
-  cg_lds_u16* tabD = (cg_lds_u16*)(tabs + (s_set_of_level[lv] * 64 + lane) * kEncTabStride);
+  cg_lds_u16* tabD =
+      (cg_lds_u16*)(tabs + ((u * nsets_lds + s_set_of_level[u][lv]) * 64 + lane) * kEncTabStride);
   EncState e{0u, 0xFFFFFFFFu, 0u};
-  uint32_t* rings = reinterpret_cast<uint32_t*>(tabs + nsets_lds * 64 * kEncTabStride);
+  uint32_t* rings = reinterpret_cast<uint32_t*>(tabs + nu * nsets_lds * 64 * kEncTabStride);
   // the slots of a wave's 64 streams are interleaved word by word (word k of lane L at
   // 64 k + L), so words that neighbouring lanes finish at about the same time share lines
   const uint64_t slot_group = (uint64_t)bclk * P.nblk + cb;
@@ -296,7 +338,8 @@ __global__ __launch_bounds__(1024) void encode_kernel(
         chi[u] = 0u;
       } else {
         clo[u] = tabD[sym];
-        chi[u] = sym == CG_NSYM - 1 ? CG_TOTAL : (uint32_t)tabD[sym1];
+        chi[u] = tabD[sym1];
+        chi[u] = sym == CG_NSYM - 1 ? CG_TOTAL : chi[u];
       }
       if (kG == 0) gq = (gq + 1 == P.G) ? 0 : gq + 1;
     }
@@ -359,8 +402,11 @@ __global__ __launch_bounds__(1024) void encode_kernel(
 #pragma unroll
       for (int u = 0; u < kPipeA; ++u) {
         const int sym = cg_quant_inv(cg_h2f((uint16_t)xv[u]), s, is) + 127;
+        // both entries loaded unconditionally (a load under a condition would be waited for
+        // at once), the top symbol's upper bound selected afterwards
         clo[u] = tabA[sym];
-        chi[u] = sym == CG_NSYM - 1 ? CG_TOTAL : (uint32_t)tabA[min(sym + 1, CG_NSYM - 1)];
+        chi[u] = tabA[min(sym + 1, CG_NSYM - 1)];
+        chi[u] = sym == CG_NSYM - 1 ? CG_TOTAL : chi[u];
       }
     };
     auto code_anchors = [&](const uint32_t (&clo)[kPipeA], const uint32_t (&chi)[kPipeA],
@@ -379,11 +425,13 @@ __global__ __launch_bounds__(1024) void encode_kernel(
       o.flush();
       load_anchor_rows(ya1, st + 3);
       code_anchors(la0, ha0, st);
+      set_priority(max(na - (st + 1) * kPipeA, 0) + n - na);
       if ((st + 1) * kPipeA >= na) break;
       quantize_anchors(ya0, la0, ha0);
       o.flush();
       load_anchor_rows(ya0, st + 4);
       code_anchors(la1, ha1, st + 1);
+      set_priority(max(na - (st + 2) * kPipeA, 0) + n - na);
     }
   }
   load_rows(xr0, 0);
@@ -396,12 +444,14 @@ __global__ __launch_bounds__(1024) void encode_kernel(
     o.flush();
     load_rows(xr1, st + 3);
     code_step(lo0, hi0, st);
+    set_priority(max(n - (st + 1) * kPipe, 0));
     if ((st + 1) * kPipe >= n) break;
     // step st+1: the same with the sets exchanged
     quantize_step(xr0, lo0, hi0);
     o.flush();
     load_rows(xr0, st + 4);
     code_step(lo1, hi1, st + 1);
+    set_priority(max(n - (st + 2) * kPipe, 0));
   }
   enc_finish(e, o);
   // the coder's bound for n symbols; the compaction never writes past the sum of these
@@ -692,28 +742,34 @@ hipError_t cg_launch_encode(const KParams& P, const uint16_t* kv, const uint8_t*
 
   const int64_t n_pairs = (int64_t)P.B * P.NC;
   int nw = (int)(n_pairs < kEncMaxWaves ? n_pairs : kEncMaxWaves);
-  auto lds_for = [&](int w) {
+  auto lds_for = [&](int w, int nu) {
     const int sets = w < P.NLV ? w : P.NLV;
-    return (size_t)sets * 64 * kEncTabStride * sizeof(uint16_t) +
-           (size_t)w * kRing * 64 * sizeof(uint32_t);
+    return (size_t)nu * sets * 64 * kEncTabStride * sizeof(uint16_t) +
+           (size_t)nu * w * kRing * 64 * sizeof(uint32_t);
   };
-  while (nw > 1 && lds_for(nw) > kEncLdsBudget) --nw;
+  while (nw > 1 && lds_for(nw, 1) > kEncLdsBudget) --nw;
   const int64_t n_groups = (n_pairs + nw - 1) / nw;
   const int nsets_max = nw < P.NLV ? nw : P.NLV;
-  const size_t lds = lds_for(nw);
+  const int64_t n_units = (int64_t)P.L * 2 * P.nblk;
+  // several units per workgroup while the grid still covers every CU
+  int nu = 1;
+  while (nu < kEncMaxUnits && (nu + 1) * nw <= kEncMaxWaves &&
+         lds_for(nw, nu + 1) <= kEncLdsBudget && (n_units + nu) / (nu + 1) * n_groups >= 256)
+    ++nu;
+  const size_t lds = lds_for(nw, nu);
   const void* kfn = P.G == 10 ? (const void*)encode_kernel<10> : (const void*)encode_kernel<0>;
   hipError_t e =
       hipFuncSetAttribute(kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  const int64_t g1 = (int64_t)P.L * 2 * P.nblk * n_groups;
+  const int64_t g1 = (n_units + nu - 1) / nu * n_groups;
   if (P.G == 10)
-    hipLaunchKernelGGL(encode_kernel<10>, dim3((unsigned)g1), dim3(64 * nw), lds, st, P, kv,
-                       chunk_level, cdf_anchor, cdf_delta, slots, slot_words, lens, scales, nw,
-                       nsets_max);
+    hipLaunchKernelGGL(encode_kernel<10>, dim3((unsigned)g1), dim3(64 * nw * nu), lds, st, P,
+                       kv, chunk_level, cdf_anchor, cdf_delta, slots, slot_words, lens, scales,
+                       nw, nu, nsets_max);
   else
-    hipLaunchKernelGGL(encode_kernel<0>, dim3((unsigned)g1), dim3(64 * nw), lds, st, P, kv,
-                       chunk_level, cdf_anchor, cdf_delta, slots, slot_words, lens, scales, nw,
-                       nsets_max);
+    hipLaunchKernelGGL(encode_kernel<0>, dim3((unsigned)g1), dim3(64 * nw * nu), lds, st, P,
+                       kv, chunk_level, cdf_anchor, cdf_delta, slots, slot_words, lens, scales,
+                       nw, nu, nsets_max);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t nb = (P.S + kScanBlock - 1) / kScanBlock;

@@ -55,6 +55,10 @@ TAILS = [
     W.small(name="tail_c13_t45", n_tokens=45, chunk_len=13, n_channels=65, n_layers=2),
     W.small(name="tail_c15_t52", n_tokens=52, chunk_len=15, n_channels=64, n_layers=2),
     W.small(name="tail_c19_t46", n_tokens=46, chunk_len=19, n_channels=64, n_layers=2, n_ctx=2),
+    # a last group of only its anchor after full groups (its q has no delta row to stay in)
+    W.small(name="tail_c21_t63", n_tokens=63, chunk_len=21, n_channels=70, n_layers=2),
+    W.small(name="tail_g7_c15_t57", group_size=7, n_tokens=57, chunk_len=15, n_channels=64,
+            n_layers=2),
 ]
 
 
