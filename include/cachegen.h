@@ -23,7 +23,10 @@
  *  Token groups restart at every chunk start (chunks decode independently, Sec. 5.3).
  *  One arithmetic-coder stream per (b, c, l, kv, ch) with stream index
  *      s = (((b*NC + c)*L + l)*2 + kv)*C + ch        (S = B*NC*L*2*C streams)
- *  so every chunk's streams are contiguous in the payload.
+ *  so every chunk's streams are contiguous in the payload. Inside a stream the chunk's anchor
+ *  symbols come first, in token order, then its delta symbols, in token order (Sec. 5.2 fixes
+ *  what is coded and under which distribution, not the order inside one bitstream; anchors
+ *  first lets a decoder take every anchor, then every delta, with one table set at hand).
  *  Symbols: a quantized value q in [-127, 127] is symbol q + 127 in [0, 254] (255 symbols).
  *  Scale (per stream): m = max |x| over the chunk's tokens; s = (m == 0) ? 1 : m / 127 (fp32).
  *  Anchor (token j of a chunk with j % G == 0): q = rint(clamp(x / s, -127, 127)); a = q * s.
