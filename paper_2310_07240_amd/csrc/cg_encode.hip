@@ -30,6 +30,7 @@ namespace {
 
 constexpr int kEncMaxWaves = 16;
 constexpr int kEncMaxUnits = 16;   // (layer, K/V, channel block) units per workgroup
+constexpr int kEncStageBatch = 8;  // table-staging loads in flight per lane
 // static LDS of the kernel with several units (masks, level maps, SIMD ids, remaining counts);
 // the dynamic LDS budget leaves 1 KB for it
 static_assert(4 * kEncMaxUnits + 3 * kEncMaxUnits * CG_MAX_LEVELS + kEncMaxWaves + 4 * kEncMaxWaves <= 1024 - 64,
@@ -246,20 +247,78 @@ __global__ __launch_bounds__(1024) void encode_kernel(
     s_nsets[uu] = m;
   }
   __syncthreads();
-  for (int idx = wave; idx < nu * nsets_lds * 64; idx += nwaves) {
-    const int t = idx & 63, st = (idx >> 6) % nsets_lds, uu = (idx >> 6) / nsets_lds;
-    const int unit2 = ublk * nu + uu;
-    if (unit2 >= n_units || st >= s_nsets[uu]) continue;
-    const int chs = (unit2 % P.nblk) * 64 + t;
-    if (chs >= P.C) continue;
-    const int lk = unit2 / P.nblk;   // l * 2 + k
-    const uint32_t* src = reinterpret_cast<const uint32_t*>(
-        cdfD + (((int64_t)s_level_of_set[uu][st] * P.L * 2 + lk) * P.C + chs) * 256);
-    uint32_t* dst = reinterpret_cast<uint32_t*>(tabs + ((uu * nsets_lds + st) * 64 + t) * kEncTabStride);
-    dst[lane] = src[lane];
-    dst[lane + 64] = src[lane + 64];
+  // stage the delta tables: a row (one table, 512 bytes) is 32 lanes x 16 bytes, so a wave
+  // moves two rows per load instruction; kEncStageBatch unconditional loads per lane (a row
+  // that is not staged reads the first table instead) are in flight before their stores
+  {
+    const int n_rows = nu * nsets_lds * 64;
+    const int half = lane >> 5, piece = lane & 31;
+    for (int base = wave; base * 2 < n_rows; base += nwaves * kEncStageBatch) {
+      uint4 v[kEncStageBatch];
+      int dsto[kEncStageBatch];
+#pragma unroll
+      for (int i = 0; i < kEncStageBatch; ++i) {
+        const int rr = (base + i * nwaves) * 2 + half;
+        const int t = rr & 63, st = (rr >> 6) % nsets_lds;
+        const int uu = min((rr >> 6) / nsets_lds, nu - 1);
+        const int unit2 = ublk * nu + uu;
+        const int chs = (unit2 % P.nblk) * 64 + t;
+        const int lset = s_level_of_set[uu][st], nset = s_nsets[uu];   // in bounds for any rr
+        const bool ok = (rr < n_rows) & (unit2 < n_units) & (st < nset) & (chs < P.C);
+        const int lk = unit2 / P.nblk;   // l * 2 + k
+        const int64_t row = ok ? ((int64_t)lset * P.L * 2 + lk) * P.C + chs : 0;
+        v[i] = reinterpret_cast<const uint4*>(cdfD + row * 256)[piece];
+        dsto[i] = ok ? ((uu * nsets_lds + st) * 64 + t) * kEncTabStride + piece * 8 : -1;
+      }
+#pragma unroll
+      for (int i = 0; i < kEncStageBatch; ++i) {
+        if (dsto[i] < 0) continue;
+        uint32_t* dst = reinterpret_cast<uint32_t*>(tabs + dsto[i]);   // 4-byte aligned rows
+        dst[0] = v[i].x;
+        dst[1] = v[i].y;
+        dst[2] = v[i].z;
+        dst[3] = v[i].w;
+      }
+    }
   }
   __syncthreads();
+
+  // Absmax of the streams. When the workgroup holds four channel-contiguous units of one
+  // (layer, K/V) and all its pairs are valid (uniform over the workgroup), the four waves of a
+  // pair split the chunk's rows (wave u takes rows u, u + 4, ...) and read all 256 channels of
+  // a row, 8 bytes (4 channels) per lane; the partial maxima meet in LDS, in the ring area
+  // that coding uses only later. Otherwise every wave reads its own 64 channels row by row.
+  const int cb0 = (ublk * nu) % P.nblk;
+  const bool coop = nu == 4 && (ublk + 1) * nu <= n_units && cb0 + nu <= P.nblk &&
+                    (cb0 + nu) * 64 <= P.C && (grp + 1) * nw <= n_pairs && (P.C & 3) == 0 &&
+                    (reinterpret_cast<uintptr_t>(kv) & 7) == 0;   // 8-byte aligned row loads
+  float mx_coop = 0.0f;
+  if (coop) {
+    float* part = reinterpret_cast<float*>(tabs + nu * nsets_lds * 64 * kEncTabStride);
+    const uint16_t* xr = kv + cg_elem(P, b, l, k, c * P.CL, cb0 * 64) + 4 * lane;
+    const int64_t rs4 = P.C;
+    const int nr = (n - u + 3) / 4;   // rows u, u + 4, ... below n
+    float m0 = 0.0f, m1 = 0.0f, m2 = 0.0f, m3 = 0.0f;
+    for (int i0 = 0; i0 < nr; i0 += 16) {
+      uint2 v[16];
+#pragma unroll
+      for (int q = 0; q < 16; ++q)
+        v[q] = *reinterpret_cast<const uint2*>(xr + (int64_t)(u + 4 * min(i0 + q, nr - 1)) * rs4);
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        m0 = fmaxf(m0, fabsf(cg_h2f((uint16_t)(v[q].x & 0xFFFFu))));
+        m1 = fmaxf(m1, fabsf(cg_h2f((uint16_t)(v[q].x >> 16))));
+        m2 = fmaxf(m2, fabsf(cg_h2f((uint16_t)(v[q].y & 0xFFFFu))));
+        m3 = fmaxf(m3, fabsf(cg_h2f((uint16_t)(v[q].y >> 16))));
+      }
+    }
+    *reinterpret_cast<float4*>(part + (j * nu + u) * 256 + 4 * lane) = make_float4(m0, m1, m2, m3);
+    __syncthreads();
+#pragma unroll
+    for (int u2 = 0; u2 < 4; ++u2) mx_coop = fmaxf(mx_coop, part[(j * nu + u2) * 256 + u * 64 + lane]);
+    __syncthreads();   // the ring area is free again before any wave codes
+  }
+
   if (!active) return;
   // the (up to three) other waves of this workgroup on this wave's SIMD
   int p0 = wave, p1 = wave, p2 = wave, np = 0;
@@ -291,9 +350,11 @@ __global__ __launch_bounds__(1024) void encode_kernel(
   const uint16_t* x = kv + cg_elem(P, b, l, k, t0, ch);
   const int64_t rs = P.C;
 
-  float mx = 0.0f;
+  float mx = mx_coop;
+  if (!coop) {
 #pragma unroll 16
-  for (int j = 0; j < n; ++j) mx = fmaxf(mx, fabsf(cg_h2f(x[(int64_t)j * rs])));
+    for (int t = 0; t < n; ++t) mx = fmaxf(mx, fabsf(cg_h2f(x[(int64_t)t * rs])));
+  }
   const float s = (mx == 0.0f) ? 1.0f : mx / 127.0f;
   scales[sidx] = s;
   constexpr int kPipe = kG > 0 ? kG : 8;
