@@ -160,7 +160,7 @@ __global__ __launch_bounds__(1024) void decode_kernel(
   uint16_t* obuf_all = smem + 64 * kFenceStride; // [nw][kRows][64] decoded rows per wave
   uint16_t* tabs = obuf_all + nw * kRows * 64;   // [nsets][64][kTabStride]
 
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int nwaves = blockDim.x >> 6;
   const int ncr = c_end - c_begin;
   const int n_pairs = P.B * ncr;
@@ -640,7 +640,7 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   const uint64_t total = offsets[P.S];
   if (total == 0) return;   // no payload at all: nothing to decode (uniform over the grid)
 
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int nwaves = blockDim.x >> 6;
   const int u = wave % nu, j = wave / nu;             // unit and pair slot of this wave
   const int ncr = c_end - c_begin;
@@ -801,7 +801,6 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     // kAnchorRun anchors per epoch. Each stores its fp16 value in its row and its quantized
     // value q in the group's first delta row (when the group has one; else into its own row
     // first, which the value then overwrites), both unconditionally
-    uint16_t* col = row0 + lsrc;
     for (int g0 = 0; g0 < na; g0 += kAnchorRun) {
       g10_epoch(st, sbase, cap);
 #pragma unroll
@@ -809,10 +808,11 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
         const int g = g0 + r;
         if (g < na) {
           const int qi = g10_symbol(st, fA, tab0);
-          uint16_t* ra = col + (int64_t)g * kG10 * rstride;
+          // wave-uniform row pointers, the lane's column as the index
+          uint16_t* ra = row0 + (int64_t)g * kG10 * rstride;
           uint16_t* rq = g * kG10 + 1 < n ? ra + rstride : ra;
-          *rq = (uint16_t)qi;
-          *ra = cg_f2h((float)qi * s);
+          rq[lsrc] = (uint16_t)qi;
+          ra[lsrc] = cg_f2h((float)qi * s);
         }
       }
       set_priority(max(na - g0 - kAnchorRun, 0));
@@ -837,9 +837,9 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   const int ngr = n / kG10;
   const int gmax = (n - 2) / kG10;                    // last group with a delta
   // the anchor's q of group g (kept in the group's first delta row)
-  const uint16_t* qcol = row0 + lsrc + rstride;
   auto q_of = [&](int g) __attribute__((always_inline)) {
-    return (uint32_t)qcol[(int64_t)min(g, gmax) * kG10 * rstride];
+    const uint16_t* rq = row0 + ((int64_t)min(g, gmax) * kG10 + 1) * rstride;   // uniform
+    return (uint32_t)rq[lsrc];
   };
   uint32_t qraw = q_of(0);
   uint16_t* row = row0;
@@ -938,7 +938,7 @@ __global__ __launch_bounds__(256) void tok_decode_kernel(
     const uint16_t* __restrict__ cdfD, int nbj, int64_t n_groups, uint8_t* __restrict__ sym) {
   __shared__ __attribute__((aligned(16))) uint16_t tabs[4][2][2][kTokTab];  // [wave][buffer][anchor, delta]
   __shared__ __attribute__((aligned(16))) uint8_t rows[4][64 * kTokRow];
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int64_t grp = (int64_t)blockIdx.x * 4 + wave;
   if (grp >= n_groups) return;   // per wave; only wave-level synchronisation below
   const TokGroup g = tok_group(P, grp, nbj);
@@ -1026,7 +1026,7 @@ __global__ __launch_bounds__(256) void tok_dequant_kernel(KParams P, const uint8
                                                           const float* __restrict__ scales,
                                                           const uint8_t* __restrict__ chunk_level,
                                                           uint16_t* __restrict__ out) {
-  const int64_t item = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int64_t item = (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (item >= (int64_t)P.B * P.NC * P.L * 2 * P.nblk) return;
   const int cb = (int)(item % P.nblk);

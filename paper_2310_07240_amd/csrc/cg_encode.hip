@@ -212,7 +212,7 @@ __global__ __launch_bounds__(1024) void encode_kernel(
   __shared__ uint8_t s_nsets[kEncMaxUnits];
   __shared__ uint8_t s_simd[kEncMaxWaves];   // SIMD of each wave
   __shared__ int s_left[kEncMaxWaves];   // symbols each wave has left to code
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int nwaves = blockDim.x >> 6;
   const int u = wave % nu, j = wave / nu;
   const int n_pairs = P.B * P.NC;
@@ -523,7 +523,7 @@ __global__ __launch_bounds__(1024) void encode_kernel(
 // Block reduction helper: sum of one value per thread of a 256-thread block.
 __device__ __forceinline__ uint64_t block_sum(uint64_t v, uint64_t* sh) {
   v = cg_wave_sum<uint64_t>(v);
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if ((threadIdx.x & 63) == 0) sh[wave] = v;
   __syncthreads();
   uint64_t t = 0;
@@ -558,7 +558,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_top(uint64_t* __restrict__ 
   for (int64_t i = begin; i < end; ++i) local += partial[i];
   // exclusive scan of the thread totals across the block
   const uint64_t incl = cg_wave_incl_scan64(local);
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if ((threadIdx.x & 63) == 63) sh[wave] = incl;
   __syncthreads();
   uint64_t carry = 0;
@@ -586,7 +586,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_finish(const uint32_t* __re
     local += v[i];
   }
   const uint64_t incl = cg_wave_incl_scan64(local);
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if ((threadIdx.x & 63) == 63) sh[wave] = incl;
   __syncthreads();
   uint64_t run = partial[blockIdx.x] + incl - local;
@@ -613,7 +613,7 @@ __global__ __launch_bounds__(256) void tok_quantize_kernel(KParams P, const uint
                                                            const uint8_t* __restrict__ chunk_level,
                                                            uint8_t* __restrict__ sym,
                                                            float* __restrict__ scales) {
-  const int64_t item = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int64_t item = (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (item >= (int64_t)P.B * P.NC * P.L * 2 * P.nblk) return;
   const int cb = (int)(item % P.nblk);
@@ -667,7 +667,7 @@ __global__ __launch_bounds__(256) void tok_encode_kernel(KParams P, const uint8_
                                                          uint32_t* __restrict__ lens, int nbj,
                                                          int64_t n_groups) {
   __shared__ uint32_t rings[4][kRing * 64];
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int64_t grp = (int64_t)blockIdx.x * 4 + wave;
   if (grp >= n_groups) return;   // per wave; no workgroup barriers below
   const TokGroup g = tok_group(P, grp, nbj);

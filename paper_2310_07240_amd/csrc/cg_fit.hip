@@ -112,7 +112,7 @@ __global__ __launch_bounds__(kFitThreads) void fit_kernel(KParams P, const uint1
   const int cb = blockIdx.x % P.nblk;
   const int lk = blockIdx.x / P.nblk;
   const int l = lk >> 1, k = lk & 1;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
 
   for (int i = threadIdx.x; i < 2 * 64 * kHist; i += kFitThreads) cnt[i] = 0;
   __syncthreads();
@@ -239,7 +239,7 @@ __global__ __launch_bounds__(256) void pool_zero(unsigned long long* pool) {
 // the two pooled tables (wave 0: anchor, wave 1: delta) into tab[2][256]
 __global__ __launch_bounds__(128) void pool_normalize(const unsigned long long* pool,
                                                       uint16_t* tab) {
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   normalize_wave<unsigned long long>(pool + wave * 256, tab + wave * 256);
 }
 
@@ -248,7 +248,7 @@ __global__ __launch_bounds__(256) void pool_broadcast(const uint16_t* __restrict
                                                       int64_t n_tables,
                                                       uint16_t* __restrict__ cdf_anchor,
                                                       uint16_t* __restrict__ cdf_delta) {
-  const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int64_t w = (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (w >= 2 * n_tables) return;
   const int kind = (int)(w / n_tables);
