@@ -31,6 +31,7 @@ namespace {
 constexpr int kEncMaxWaves = 16;
 constexpr int kEncMaxUnits = 16;   // (layer, K/V, channel block) units per workgroup
 constexpr int kEncStageBatch = 8;  // table-staging loads in flight per lane
+constexpr int kCompactRows = 64;   // slot rows per pass of the compaction
 // static LDS of the kernel with several units (masks, level maps, SIMD ids, remaining counts);
 // the dynamic LDS budget leaves 1 KB for it
 static_assert(4 * kEncMaxUnits + 3 * kEncMaxUnits * CG_MAX_LEVELS + kEncMaxWaves + 4 * kEncMaxWaves <= 1024 - 64,
@@ -719,7 +720,7 @@ __global__ __launch_bounds__(256) void compact_kernel(KParams P, const uint32_t*
                                                       const uint32_t* __restrict__ lens,
                                                       const uint64_t* __restrict__ offsets,
                                                       int nbj, uint32_t* __restrict__ words) {
-  __shared__ uint32_t tile[16][65];
+  __shared__ uint32_t ctile[kCompactRows][65];
   __shared__ uint32_t s_len[64];
   __shared__ uint64_t s_off[64];
   __shared__ uint32_t s_max;
@@ -753,22 +754,29 @@ __global__ __launch_bounds__(256) void compact_kernel(KParams P, const uint32_t*
   __syncthreads();
   const uint32_t K = s_max;
   const uint32_t* src = slots + (uint64_t)grp * slot_words * 64;
-  for (uint32_t k0 = 0; k0 < K; k0 += 16) {
-    const uint32_t r = k0 + (t >> 4);            // slot row: word r of all 64 streams
-    if (r < K) {
-      const uint4 v = *reinterpret_cast<const uint4*>(src + (uint64_t)r * 64 + (t & 15) * 4);
-      uint32_t* d = &tile[t >> 4][(t & 15) * 4];
-      d[0] = v.x;
-      d[1] = v.y;
-      d[2] = v.z;
-      d[3] = v.w;
+  // kCompactRows slot rows per pass: every thread has four 16-byte loads in flight
+  for (uint32_t k0 = 0; k0 < K; k0 += kCompactRows) {
+    uint4 v[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t r = k0 + (t >> 4) + 16 * i;   // slot row: word r of all 64 streams
+      v[i] = r < K ? *reinterpret_cast<const uint4*>(src + (uint64_t)r * 64 + (t & 15) * 4)
+                   : make_uint4(0u, 0u, 0u, 0u);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      uint32_t* d = &ctile[(t >> 4) + 16 * i][(t & 15) * 4];
+      d[0] = v[i].x;
+      d[1] = v[i].y;
+      d[2] = v[i].z;
+      d[3] = v[i].w;
     }
     __syncthreads();
 #pragma unroll
-    for (int pass = 0; pass < 4; ++pass) {
-      const int L = pass * 16 + (t >> 4), j = t & 15;
-      const uint32_t k = k0 + j;
-      if (k < s_len[L]) words[s_off[L] + k] = tile[j][L];
+    for (int pass = 0; pass < 16; ++pass) {   // 16 lanes write 16 consecutive words of a stream
+      const int L = (pass & 3) * 16 + (t >> 4);
+      const uint32_t kr = (pass >> 2) * 16 + (t & 15), k = k0 + kr;
+      if (k < s_len[L]) words[s_off[L] + k] = ctile[kr][L];
     }
     __syncthreads();
   }
