@@ -248,27 +248,33 @@ __global__ __launch_bounds__(1024) void encode_kernel(
     s_nsets[uu] = m;
   }
   __syncthreads();
-  // stage the delta tables: a row (one table, 512 bytes) is 32 lanes x 16 bytes, so a wave
-  // moves two rows per load instruction; kEncStageBatch unconditional loads per lane (a row
-  // that is not staged reads the first table instead) are in flight before their stores
-  {
-    const int n_rows = nu * nsets_lds * 64;
-    const int half = lane >> 5, piece = lane & 31;
+  // Stage tables into LDS: the anchor table of every unit (set 0; the anchor pass), or the
+  // delta tables of the levels each unit's pairs use (the delta pass). A row (one table, 512
+  // bytes) is 32 lanes x 16 bytes, so a wave moves two rows per load instruction;
+  // kEncStageBatch unconditional loads per lane (a row that is not staged reads the first
+  // table instead) are in flight before their stores.
+  const int half = lane >> 5, piece = lane & 31;
+  auto stage = [&](bool anchors) __attribute__((always_inline)) {
+    const int sets = anchors ? 1 : nsets_lds;
+    const int n_rows = nu * sets * 64;
+    const uint16_t* srcbase = anchors ? cdfA : cdfD;
     for (int base = wave; base * 2 < n_rows; base += nwaves * kEncStageBatch) {
       uint4 v[kEncStageBatch];
       int dsto[kEncStageBatch];
 #pragma unroll
       for (int i = 0; i < kEncStageBatch; ++i) {
         const int rr = (base + i * nwaves) * 2 + half;
-        const int t = rr & 63, st = (rr >> 6) % nsets_lds;
-        const int uu = min((rr >> 6) / nsets_lds, nu - 1);
+        const int t = rr & 63, st = (rr >> 6) % sets;
+        const int uu = min((rr >> 6) / sets, nu - 1);
         const int unit2 = ublk * nu + uu;
         const int chs = (unit2 % P.nblk) * 64 + t;
-        const int lset = s_level_of_set[uu][st], nset = s_nsets[uu];   // in bounds for any rr
+        const int lset = s_level_of_set[uu][st];   // in bounds for any rr
+        const int nset = anchors ? 1 : (int)s_nsets[uu];
         const bool ok = (rr < n_rows) & (unit2 < n_units) & (st < nset) & (chs < P.C);
         const int lk = unit2 / P.nblk;   // l * 2 + k
-        const int64_t row = ok ? ((int64_t)lset * P.L * 2 + lk) * P.C + chs : 0;
-        v[i] = reinterpret_cast<const uint4*>(cdfD + row * 256)[piece];
+        const int64_t trow = anchors ? (int64_t)lk * P.C + chs
+                                     : ((int64_t)lset * P.L * 2 + lk) * P.C + chs;
+        v[i] = reinterpret_cast<const uint4*>(srcbase + (ok ? trow : 0) * 256)[piece];
         dsto[i] = ok ? ((uu * nsets_lds + st) * 64 + t) * kEncTabStride + piece * 8 : -1;
       }
 #pragma unroll
@@ -281,7 +287,8 @@ __global__ __launch_bounds__(1024) void encode_kernel(
         dst[3] = v[i].w;
       }
     }
-  }
+  };
+  stage(true);
   __syncthreads();
 
   // Absmax of the streams. When the workgroup holds four channel-contiguous units of one
@@ -320,7 +327,6 @@ __global__ __launch_bounds__(1024) void encode_kernel(
     __syncthreads();   // the ring area is free again before any wave codes
   }
 
-  if (!active) return;
   // the (up to three) other waves of this workgroup on this wave's SIMD
   int p0 = wave, p1 = wave, p2 = wave, np = 0;
   for (int w2 = 0; w2 < nwaves; ++w2) {
@@ -344,7 +350,8 @@ __global__ __launch_bounds__(1024) void encode_kernel(
     else __builtin_amdgcn_s_setprio(0);
   };
   const int ch = cb * 64 + lane;
-  if (ch >= P.C) return;
+  // lanes that code a stream (the others take part in the barriers between the passes only)
+  const bool lane_ok = active && ch < P.C;
   const int64_t bclk = (((int64_t)b * P.NC + c) * P.L + l) * 2 + k;
   const int t0 = c * P.CL;
   const int64_t sidx = cg_stream(P, bclk, ch);
@@ -352,18 +359,18 @@ __global__ __launch_bounds__(1024) void encode_kernel(
   const int64_t rs = P.C;
 
   float mx = mx_coop;
-  if (!coop) {
+  if (!coop && lane_ok) {
 #pragma unroll 16
     for (int t = 0; t < n; ++t) mx = fmaxf(mx, fabsf(cg_h2f(x[(int64_t)t * rs])));
   }
   const float s = (mx == 0.0f) ? 1.0f : mx / 127.0f;
-  scales[sidx] = s;
+  if (lane_ok) scales[sidx] = s;
   constexpr int kPipe = kG > 0 ? kG : 8;
   const float bw = P.layer_bin[l] * P.level_mult[lv];
   const float w = bw * s;
   const float is = 1.0f / s, iw = 1.0f / w;
 
-  cg_glb_u16* tabA = (cg_glb_u16*)(cdfA + ((int64_t)(l * 2 + k) * P.C + ch) * 256);
+  cg_lds_u16* tabA = (cg_lds_u16*)(tabs + (u * nsets_lds * 64 + lane) * kEncTabStride);   // set 0
   cg_lds_u16* tabD =
       (cg_lds_u16*)(tabs + ((u * nsets_lds + s_set_of_level[u][lv]) * 64 + lane) * kEncTabStride);
   EncState e{0u, 0xFFFFFFFFu, 0u};
@@ -448,8 +455,8 @@ __global__ __launch_bounds__(1024) void encode_kernel(
 
   // Anchor pass: the anchors of the chunk in token order (they come first in the stream), in
   // steps of kPipeA with the same two-step pipeline (rows two steps ahead, anchor-table
-  // entries one step ahead)
-  {
+  // entries, from the anchor tables staged in LDS, one step ahead)
+  if (lane_ok) {
     constexpr int kPipeA = 8;
     const int G = kG > 0 ? kG : P.G;
     const int na = (n + G - 1) / G;
@@ -487,15 +494,20 @@ __global__ __launch_bounds__(1024) void encode_kernel(
       o.flush();
       load_anchor_rows(ya1, st + 3);
       code_anchors(la0, ha0, st);
-      set_priority(max(na - (st + 1) * kPipeA, 0) + n - na);
+      set_priority(max(na - (st + 1) * kPipeA, 0));
       if ((st + 1) * kPipeA >= na) break;
       quantize_anchors(ya0, la0, ha0);
       o.flush();
       load_anchor_rows(ya0, st + 4);
       code_anchors(la1, ha1, st + 1);
-      set_priority(max(na - (st + 2) * kPipeA, 0) + n - na);
+      set_priority(max(na - (st + 2) * kPipeA, 0));
     }
   }
+  // the delta tables replace the anchor tables
+  __syncthreads();
+  stage(false);
+  __syncthreads();
+  if (!lane_ok) return;
   load_rows(xr0, 0);
   load_rows(xr1, 1);
   quantize_step(xr0, lo0, hi0);
