@@ -62,6 +62,25 @@ TAILS = [
 ]
 
 
+# Grids large enough for several (layer, K/V, channel block) units per workgroup: 512, 768 and
+# 1024 units give 2, 3 and 4 units per workgroup in the encoder and the decoder; with 4 the
+# encoder's absmax is shared by the four waves of a pair (channel-contiguous units).
+UNITS = [
+    W.small(name="units2_l8_c2048", n_layers=8, n_channels=2048, n_tokens=40, chunk_len=40),
+    W.small(name="units3_l12_c2048", n_layers=12, n_channels=2048, n_tokens=30, chunk_len=30),
+    W.small(name="units4_l16_c2048_2chunks", n_layers=16, n_channels=2048, n_tokens=47,
+            chunk_len=25, level_mult=(1.0,), random_levels=False),   # one table set per unit
+]
+
+
+@pytest.mark.parametrize("w", UNITS, ids=lambda w: w.name)
+def test_units_per_workgroup_bit_exact(w):
+    kv = W.generate(w)
+    o = run_oracle(w, kv)
+    g = run_gpu(w, kv)
+    compare_full(w, g, o)
+
+
 @pytest.mark.parametrize("w", TAILS, ids=lambda w: w.name)
 def test_group_tails_bit_exact(w):
     kv = W.generate(w)
