@@ -490,14 +490,14 @@ __global__ __launch_bounds__(1024) void encode_kernel(
     quantize_anchors(ya0, la0, ha0);
     load_anchor_rows(ya0, 2);
     for (int st = 0; st * kPipeA < na; st += 2) {
-      quantize_anchors(ya1, la1, ha1);
       o.flush();
+      quantize_anchors(ya1, la1, ha1);
       load_anchor_rows(ya1, st + 3);
       code_anchors(la0, ha0, st);
       set_priority(max(na - (st + 1) * kPipeA, 0));
       if ((st + 1) * kPipeA >= na) break;
-      quantize_anchors(ya0, la0, ha0);
       o.flush();
+      quantize_anchors(ya0, la0, ha0);
       load_anchor_rows(ya0, st + 4);
       code_anchors(la1, ha1, st + 1);
       set_priority(max(na - (st + 2) * kPipeA, 0));
@@ -514,15 +514,15 @@ __global__ __launch_bounds__(1024) void encode_kernel(
   load_rows(xr0, 2);
   for (int st = 0; st * kPipe < n; st += 2) {
     // step st: quantize step st+1, request the rows of step st+3, code step st
-    quantize_step(xr1, lo1, hi1);
     o.flush();
+    quantize_step(xr1, lo1, hi1);
     load_rows(xr1, st + 3);
     code_step(lo0, hi0, st);
     set_priority(max(n - (st + 1) * kPipe, 0));
     if ((st + 1) * kPipe >= n) break;
     // step st+1: the same with the sets exchanged
-    quantize_step(xr0, lo0, hi0);
     o.flush();
+    quantize_step(xr0, lo0, hi0);
     load_rows(xr0, st + 4);
     code_step(lo1, hi1, st + 1);
     set_priority(max(n - (st + 2) * kPipe, 0));
