@@ -538,21 +538,78 @@ __device__ __forceinline__ void g10_advance(G10Lane& st, uint32_t lo_off, uint32
   st.hcnt += adv ? 1u : 0u;
 }
 
-// One symbol under the table `tab` (LDS, 256 entries plus sentinels) whose fences cum[16 f]
-// are fT: returns q = symbol - 127 after the interval update and the refill of D.
+// LDS byte addresses as plain 32-bit integers, so that offsets can be added without the
+// compiler rebuilding a generic pointer.
+typedef __attribute__((address_space(3))) const uint16_t lds_cu16;
+typedef __attribute__((address_space(3))) const uint64_t lds_cu64;
+__device__ __forceinline__ uint32_t lds_addr(const uint16_t* p) {
+  return (uint32_t)(uintptr_t)(lds_cu16*)p;
+}
+__device__ __forceinline__ uint32_t lds_ld16(uint32_t a) { return *(lds_cu16*)(uintptr_t)a; }
+__device__ __forceinline__ uint2 lds_ld64(uint32_t a) {
+  const uint64_t v = *(lds_cu64*)(uintptr_t)a;
+  return make_uint2((uint32_t)v, (uint32_t)(v >> 32));
+}
+
+// Fence registers of a table: cum[16 f] << 16 in the high half, and in the low half the byte
+// offset 32 (f - 1) of block f - 1 from the table's start. A fence is <= ti exactly when it is
+// below (ti + 1) << 16, and the fence the search ends on carries the block address with it.
+// Entries 0 and 16 (cum[0] = 0 and the total) are never compared and stay zero.
+__device__ __forceinline__ void g10_fences(uint32_t (&fT)[17], const uint16_t* tab) {
+  fT[0] = 0u;
+  fT[16] = 0u;
+#pragma unroll
+  for (int f = 1; f < 16; ++f) fT[f] = ((uint32_t)tab[16 * f] << 16) | (32u * (f - 1));
+}
+
+// One symbol under the table at LDS byte address tb (256 entries plus sentinels; `tab` is the
+// same table as a pointer, for the rare correction walk) whose tagged fences are fT; kq =
+// -(tb / 2 + 127). Returns q = symbol - 127 after the interval update and the refill of D.
 __device__ __forceinline__ int g10_symbol(G10Lane& st, const uint32_t (&fT)[17],
-                                          const uint16_t* tab) {
+                                          const uint16_t* tab, uint32_t tb, uint32_t kq) {
   const float te = (float)st.D * (65536.0f * __builtin_amdgcn_rcpf((float)st.rm1));
   const uint32_t ti = min((uint32_t)te, 65534u);
+  const uint32_t th = (ti << 16) + 0x10000u;   // (ti + 1) << 16
+  // binary search over the fences by selects (four compare / select steps)
+  const bool c3 = fT[8] < th;
+  const uint32_t p4 = c3 ? fT[12] : fT[4];
+  const uint32_t p2a = c3 ? fT[10] : fT[2], p2b = c3 ? fT[14] : fT[6];
+  const uint32_t p1a = c3 ? fT[9] : fT[1], p1b = c3 ? fT[11] : fT[3];
+  const uint32_t p1c = c3 ? fT[13] : fT[5], p1d = c3 ? fT[15] : fT[7];
+  const bool c2 = p4 < th;
+  const uint32_t p2 = c2 ? p2b : p2a;
+  const uint32_t p1e = c2 ? p1c : p1a, p1f = c2 ? p1d : p1b;
+  const bool c1 = p2 < th;
+  const uint32_t p1 = c1 ? p1f : p1e;
+  const bool c0 = p1 < th;
+  // block f = (index of p1) - 1 + c0 starts at byte 32 f
+  uint32_t qa;
+  asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 "
+      "src1_sel:DWORD" : "=v"(qa) : "v"(p1), "v"(c0 ? tb + 32u : tb));
+  // 4-ary level: cum[16 f + 4 m], m = 1..3
   const uint32_t kneg = ~ti;
-  const int fq = fence_q(fT, ti);          // 16 f - 127
-  const uint16_t* q = tab + 127 + fq;      // the block of cum[16 f]
-  const int l4 = 4 * (int)((((uint32_t)q[4] + kneg) >> 31) + (((uint32_t)q[8] + kneg) >> 31) +
-                           (((uint32_t)q[12] + kneg) >> 31));
-  q += l4;
-  uint32_t pr;
-  const uint32_t cc = delta_leaf(q, ti, pr);
-  int qi = fq + l4 + (int)cc;
+  const uint32_t qb = qa + 8u * (((lds_ld16(qa + 8u) + kneg) >> 31) +
+                                 ((lds_ld16(qa + 16u) + kneg) >> 31) +
+                                 ((lds_ld16(qa + 24u) + kneg) >> 31));
+  // leaf: cum[i .. i+3], i = (qb - tb) / 2 (as in delta_leaf)
+  const uint2 xy = lds_ld64(qb);
+  const uint32_t x4 = lds_ld16(qb + 8u);
+  const uint32_t tt = (ti + 1u) * 0x00010001u;
+  const uint32_t one2 = 0x00010001u;
+  uint32_t ia, ib, c;
+  asm("v_pk_sub_u16 %0, %1, %2 clamp" : "=v"(ia) : "v"(tt), "v"(xy.x));
+  asm("v_pk_sub_u16 %0, %1, %2 clamp" : "=v"(ib) : "v"(tt), "v"(xy.y));
+  asm("v_pk_min_u16 %0, %1, %2" : "=v"(ia) : "v"(ia), "v"(one2));
+  asm("v_pk_min_u16 %0, %1, %2" : "=v"(ib) : "v"(ib), "v"(one2));
+  asm("v_dot2_u32_u16 %0, %1, %2, %3" : "=v"(c) : "v"(ia), "v"(one2), "v"(0xFFFFFFFFu));
+  asm("v_dot2_u32_u16 %0, %1, %2, %3" : "=v"(c) : "v"(ib), "v"(one2), "v"(c));
+  // (cum[i + c], cum[i + c + 1]) is the 32-bit window at 16 c bits of x : y : x4 (the shift
+  // takes its low five bits: 16 (c & 1))
+  const bool cge2 = c >= 2u;
+  const uint32_t hi2 = cge2 ? x4 : xy.y;
+  const uint32_t lo2 = cge2 ? xy.y : xy.x;
+  const uint32_t pr = __builtin_amdgcn_alignbit(hi2, lo2, c << 4);
+  int qi = (int)((qb >> 1) + c + kq);
   uint32_t clo = pr & 0xFFFFu;
   uint32_t chi = qi == CG_NSYM - 1 - 127 ? CG_TOTAL : pr >> 16;
   const uint32_t D = st.D, rm1 = st.rm1;
@@ -585,9 +642,9 @@ __device__ __forceinline__ int g10_symbol(G10Lane& st, const uint32_t (&fT)[17],
 // One delta token: its symbol under the delta table, dequantized against the group's anchor
 // into row r of the wave's staging buffer.
 __device__ __forceinline__ void g10_delta(G10Lane& st, const uint32_t (&fD)[17],
-                                          const uint16_t* dtab, float w, uint16_t* obuf, int r,
-                                          int lane) {
-  const int qi = g10_symbol(st, fD, dtab);
+                                          const uint16_t* dtab, uint32_t tb, uint32_t kq,
+                                          float w, uint16_t* obuf, int r, int lane) {
+  const int qi = g10_symbol(st, fD, dtab, tb, kq);
   obuf[r * 64 + lane] = cg_f2h(st.a + (float)qi * w);
 }
 
@@ -768,11 +825,9 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     const int64_t sidx = cg_stream(P, bclk, chv);
     s = scales[sidx];
     w = P.layer_bin[l] * P.level_mult[lv] * s;
-    uint32_t fA[17];   // fences cum[16 f] of the anchor table, f = 0..16 (cum[256] = total)
-    fA[0] = 0u;
-    fA[16] = CG_TOTAL;
-#pragma unroll
-    for (int f = 1; f < 16; ++f) fA[f] = tab0[16 * f];
+    uint32_t fA[17];   // tagged fences of the anchor table
+    g10_fences(fA, tab0);
+    const uint32_t tbA = lds_addr(tab0), kqA = 0u - (tbA / 2u + 127u);
     // bitstream reader: the code value, w0..w3 and the four requested words t0..t3 are the
     // stream's first 13 words; every read stays below offsets[S] + 4 (the requests are clamped
     // to it), inside the readable tail
@@ -807,7 +862,7 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
       for (int r = 0; r < kAnchorRun; ++r) {
         const int g = g0 + r;
         if (g < na) {
-          const int qi = g10_symbol(st, fA, tab0);
+          const int qi = g10_symbol(st, fA, tab0, tbA, kqA);
           // wave-uniform row pointers, the lane's column as the index
           uint16_t* ra = row0 + (int64_t)g * kG10 * rstride;
           uint16_t* rq = g * kG10 + 1 < n ? ra + rstride : ra;
@@ -827,10 +882,8 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   set_priority(n - na);
   const uint16_t* dtab = tabs + ((u * msets + s_set_of_level[u][lv]) * 64 + lsrc) * kTabStride;
   uint32_t fD[17];
-  fD[0] = 0u;
-  fD[16] = CG_TOTAL;
-#pragma unroll
-  for (int f = 1; f < 16; ++f) fD[f] = dtab[16 * f];
+  g10_fences(fD, dtab);
+  const uint32_t tbD = lds_addr(dtab), kqD = 0u - (tbD / 2u + 127u);
 
   uint16_t* obuf = obuf_all + wave * kG10 * 64;
   const int cbase = cb * 64;
@@ -846,18 +899,18 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   for (int gi = 0; gi < ngr; ++gi) {
     st.a = (float)(int)(int16_t)qraw * s;
     g10_epoch(st, sbase, cap);
-    g10_delta(st, fD, dtab, w, obuf, 1, lane);
-    g10_delta(st, fD, dtab, w, obuf, 2, lane);
-    g10_delta(st, fD, dtab, w, obuf, 3, lane);
+    g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 1, lane);
+    g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 2, lane);
+    g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 3, lane);
     g10_epoch(st, sbase, cap);
     const uint32_t qnext = q_of(gi + 1);   // requested a group ahead
-    g10_delta(st, fD, dtab, w, obuf, 4, lane);
-    g10_delta(st, fD, dtab, w, obuf, 5, lane);
-    g10_delta(st, fD, dtab, w, obuf, 6, lane);
+    g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 4, lane);
+    g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 5, lane);
+    g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 6, lane);
     g10_epoch(st, sbase, cap);
-    g10_delta(st, fD, dtab, w, obuf, 7, lane);
-    g10_delta(st, fD, dtab, w, obuf, 8, lane);
-    g10_delta(st, fD, dtab, w, obuf, 9, lane);
+    g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 7, lane);
+    g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 8, lane);
+    g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 9, lane);
     g10_flush(obuf, row, rstride, 1, kG10, lane, cbase, P.C);
     row += kG10 * rstride;
     qraw = qnext;
@@ -869,7 +922,7 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     g10_epoch(st, sbase, cap);
     for (int r = 1; r < rem; ++r) {
       if (r == 4 || r == 7) g10_epoch(st, sbase, cap);
-      g10_delta(st, fD, dtab, w, obuf, r, lane);
+      g10_delta(st, fD, dtab, tbD, kqD, w, obuf, r, lane);
     }
     g10_flush(obuf, row, rstride, 1, rem, lane, cbase, P.C);
   }
