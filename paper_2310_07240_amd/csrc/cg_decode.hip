@@ -87,13 +87,6 @@ __device__ __forceinline__ uint32_t e3_run(uint32_t L1, uint32_t H1) {
   return n - 1u;
 }
 
-// The same run plus one (the v_ffbh_i32 count itself, >= 1).
-__device__ __forceinline__ uint32_t e3_run1(uint32_t L1, uint32_t H1) {
-  uint32_t n;
-  asm("v_ffbh_i32 %0, %1" : "=v"(n) : "v"((L1 & ~H1) | 0x80000000u));
-  return n;
-}
-
 // 16-byte store of decoded fp16 that is not read again by this kernel (non-temporal, so the
 // output stream does not push the anchor tables out of the L2).
 __device__ __forceinline__ void store_row16(uint16_t* dst, const uint4& v) {
@@ -513,14 +506,17 @@ __device__ __forceinline__ void g10_epoch(G10Lane& st, const uint32_t* __restric
 __device__ __forceinline__ void g10_advance(G10Lane& st, uint32_t lo_off, uint32_t hoff,
                                             uint32_t d, uint32_t rsz) {
   // renormalisation: n1 shared leading bits of low and high, then the middle-half run of
-  // n3 = f - 1 steps; the new low is L1 << n3 without its top bit
+  // f - 1 steps, read as in e3_run from (low & ~high) << n1 (the same bits as L1 & ~H1, with
+  // L1 = low << n1 and H1 = high << n1); in all nsh = n1 + f - 1 shifts, after which the new
+  // low is low << nsh without its top bit
   const uint32_t low = st.low + lo_off;
   const uint32_t high = st.low + hoff - 1u;
   const uint32_t n1 = (uint32_t)__builtin_clz(low ^ high);
-  const uint32_t L1 = low << n1, H1 = high << n1;
-  const uint32_t f = e3_run1(L1, H1);
-  st.low = (L1 << f) >> 1;
+  uint32_t e, f;
+  asm("v_bfi_b32 %0, %1, 0, %2" : "=v"(e) : "v"(high), "v"(low));   // low & ~high
+  asm("v_ffbh_i32 %0, %1" : "=v"(f) : "v"((e << n1) | 0x80000000u));   // run + 1
   const uint32_t nsh = n1 + f - 1u;
+  st.low = (low << nsh) & 0x7FFFFFFFu;
   // high - low + 1 scales by 2^nsh (a result of 2^32 wraps to 0, giving rm1 = 2^32 - 1)
   st.rm1 = (rsz << nsh) - 1u;
   // D takes the next nsh stream bits: the 32 bits at `pos` of w0:w1, then a 64-bit shift
@@ -591,18 +587,21 @@ __device__ __forceinline__ int g10_symbol(G10Lane& st, const uint32_t (&fT)[17],
   const uint32_t qb = qa + 8u * (((lds_ld16(qa + 8u) + kneg) >> 31) +
                                  ((lds_ld16(qa + 16u) + kneg) >> 31) +
                                  ((lds_ld16(qa + 24u) + kneg) >> 31));
-  // leaf: cum[i .. i+3], i = (qb - tb) / 2 (as in delta_leaf)
+  // leaf: cum[i .. i+3], i = (qb - tb) / 2, in x = cum[i] | cum[i+1] << 16 and y = cum[i+2] |
+  // cum[i+3] << 16, cum[i+4] in x4 (the layout of delta_leaf; here the count takes 32-bit sign
+  // tests, which measured slightly faster than its packed 16-bit forms)
   const uint2 xy = lds_ld64(qb);
   const uint32_t x4 = lds_ld16(qb + 8u);
-  const uint32_t tt = (ti + 1u) * 0x00010001u;
-  const uint32_t one2 = 0x00010001u;
-  uint32_t ia, ib, c;
-  asm("v_pk_sub_u16 %0, %1, %2 clamp" : "=v"(ia) : "v"(tt), "v"(xy.x));
-  asm("v_pk_sub_u16 %0, %1, %2 clamp" : "=v"(ib) : "v"(tt), "v"(xy.y));
-  asm("v_pk_min_u16 %0, %1, %2" : "=v"(ia) : "v"(ia), "v"(one2));
-  asm("v_pk_min_u16 %0, %1, %2" : "=v"(ib) : "v"(ib), "v"(one2));
-  asm("v_dot2_u32_u16 %0, %1, %2, %3" : "=v"(c) : "v"(ia), "v"(one2), "v"(0xFFFFFFFFu));
-  asm("v_dot2_u32_u16 %0, %1, %2, %3" : "=v"(c) : "v"(ib), "v"(one2), "v"(c));
+  // c = [cum[i+1] <= ti] + [cum[i+2] <= ti] + [cum[i+3] <= ti] (cum[i] <= ti always), each a
+  // sign bit of cum + ~ti with the 16-bit entry taken straight from its half of x or y
+  uint32_t e1, e2, e3;
+  asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_1 "
+      "src1_sel:DWORD" : "=v"(e1) : "v"(xy.x), "v"(kneg));
+  asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 "
+      "src1_sel:DWORD" : "=v"(e2) : "v"(xy.y), "v"(kneg));
+  asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_1 "
+      "src1_sel:DWORD" : "=v"(e3) : "v"(xy.y), "v"(kneg));
+  const uint32_t c = (e1 >> 31) + (e2 >> 31) + (e3 >> 31);
   // (cum[i + c], cum[i + c + 1]) is the 32-bit window at 16 c bits of x : y : x4 (the shift
   // takes its low five bits: 16 (c & 1))
   const bool cge2 = c >= 2u;
