@@ -31,7 +31,7 @@ namespace {
 constexpr int kEncMaxWaves = 16;
 constexpr int kEncMaxUnits = 16;   // (layer, K/V, channel block) units per workgroup
 constexpr int kEncStageBatch = 8;  // table-staging loads in flight per lane
-constexpr int kCompactRows = 64;   // slot rows per pass of the compaction
+constexpr int kCompactRows = 128;  // slot rows per pass of the compaction
 // static LDS of the kernel with several units (masks, level maps, SIMD ids, remaining counts);
 // the dynamic LDS budget leaves 1 KB for it
 static_assert(4 * kEncMaxUnits + 3 * kEncMaxUnits * CG_MAX_LEVELS + kEncMaxWaves + 4 * kEncMaxWaves <= 1024 - 64,
@@ -766,17 +766,17 @@ __global__ __launch_bounds__(256) void compact_kernel(KParams P, const uint32_t*
   __syncthreads();
   const uint32_t K = s_max;
   const uint32_t* src = slots + (uint64_t)grp * slot_words * 64;
-  // kCompactRows slot rows per pass: every thread has four 16-byte loads in flight
+  // kCompactRows slot rows per pass: every thread has eight 16-byte loads in flight
   for (uint32_t k0 = 0; k0 < K; k0 += kCompactRows) {
-    uint4 v[4];
+    uint4 v[8];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < 8; ++i) {
       const uint32_t r = k0 + (t >> 4) + 16 * i;   // slot row: word r of all 64 streams
       v[i] = r < K ? *reinterpret_cast<const uint4*>(src + (uint64_t)r * 64 + (t & 15) * 4)
                    : make_uint4(0u, 0u, 0u, 0u);
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < 8; ++i) {
       uint32_t* d = &ctile[(t >> 4) + 16 * i][(t & 15) * 4];
       d[0] = v[i].x;
       d[1] = v[i].y;
@@ -785,7 +785,7 @@ __global__ __launch_bounds__(256) void compact_kernel(KParams P, const uint32_t*
     }
     __syncthreads();
 #pragma unroll
-    for (int pass = 0; pass < 16; ++pass) {   // 16 lanes write 16 consecutive words of a stream
+    for (int pass = 0; pass < 32; ++pass) {   // 16 lanes write 16 consecutive words of a stream
       const int L = (pass & 3) * 16 + (t >> 4);
       const uint32_t kr = (pass >> 2) * 16 + (t & 15), k = k0 + kr;
       if (k < s_len[L]) words[s_off[L] + k] = ctile[kr][L];
