@@ -50,7 +50,7 @@ int make_kparams(const cg_params* p, KParams* K) {
 // Largest slot (in words) any stream can need: ceil((18 n + 2) / 32) for its token count n.
 uint32_t slot_words_for(const KParams& K) {
   const int64_t n = K.CL < K.T ? K.CL : K.T;
-  return (uint32_t)((18ull * (uint64_t)n + 2ull + 31ull) / 32ull);
+  return (uint32_t)(((18ull * (uint64_t)n + 2ull + 31ull) / 32ull + 3ull) & ~3ull);   // whole 16-byte chunks
 }
 
 bool aligned(const void* ptr, size_t a) { return ((uintptr_t)ptr % a) == 0; }

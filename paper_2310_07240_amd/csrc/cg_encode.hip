@@ -12,7 +12,8 @@
 //   scan_finish     block-local exclusive scan (wave prefix sums + LDS) plus the block's
 //                   carry -> offsets[S + 1];
 //   compact         one workgroup per (row, 64-channel block) moves its 64 streams' words
-//                   from the (interleaved) slots to their offsets, through an LDS transpose.
+//                   from the slots (interleaved by 16-byte chunk) to their offsets, through an
+//                   LDS transpose.
 //
 // Arithmetic coder: Witten-Neal-Cleary integer coder, 32-bit registers, 16-bit frequencies.
 // Renormalisation is done in one step per symbol instead of one bit at a time:
@@ -24,6 +25,8 @@
 //     step adds one pending bit;
 //   * high - low grows as rm1 -> (rm1 << n) | (2^n - 1) for n shifts in total.
 // This produces exactly the bits of the one-bit-at-a-time definition.
+#include <type_traits>
+
 #include "cg_device.h"
 
 namespace {
@@ -42,51 +45,64 @@ constexpr int kScanThreads = 256;
 constexpr int kScanItems = 16;
 constexpr int kScanBlock = kScanThreads * kScanItems;  // 4096 streams per scan block
 
-// Output of one stream. Whole words produced by the common path go to a lane-private ring of
-// kRing words in LDS and reach the stream's slot in global memory in one flush per pipeline
-// step, issued right after the step's row values were consumed: stores issued between the
-// pipeline's loads would otherwise make every later wait for those loads wait for the stores
-// too (loads and stores share one in-order counter). The rare paths (long runs of owed bits,
-// the end of the stream) flush the ring and then write directly.
+// Output of one stream. Finished words go to a lane-private ring of kRing words in LDS and reach
+// the stream's slot in global memory as whole 16-byte chunks (four words, 16-byte aligned): a
+// flush stores the oldest four pending words once they are all there. A slot group of 64
+// streams is interleaved by chunk (chunk m of lane L at words (64 m + L) * 4 of the group), so
+// a lane's store is one 16-byte write and a row of chunks is 1 KB for the compaction. Flushes
+// are issued right after a step's row values were consumed and between runs of at most five
+// symbols: stores issued between the pipeline's loads would make every later wait for those
+// loads wait for the stores too (loads and stores share one in-order counter).
+//
+// Ring bound: a run starts with at most 3 pending words. On the common path a symbol emits at
+// most 32 bits and at most 32 + 18 k bits over k symbols (the owed bits it starts with, which
+// are at most 32 when any of them is emitted there, plus at most 18 shifts per symbol), so a
+// run of at most five symbols adds at most 4 words: never more than 7 are pending, and the slot
+// after the last pending word, which the branch-free coder always writes, is free. The rare
+// paths (long runs of owed bits, the end of the stream) put one word at a time and flush after
+// each.
 constexpr int kRing = 8;
 
 struct BitSink {
-  uint32_t* out;    // slot base: word k of this stream at out[64 k]
-  uint32_t cap;     // slot capacity in words
+  uint32_t* out;    // chunk column of this lane: word k at out[256 (k / 4) + k % 4]
+  uint32_t cap;     // slot capacity in words (a multiple of 4)
   uint32_t nwords;  // words produced
-  uint32_t flushed; // words already in the slot
+  uint32_t flushed; // words already in the slot (a multiple of 4)
   uint64_t acc;     // output bits not yet in a word: the low nacc bits (higher bits ignored)
   uint32_t nacc;    // number of bits in acc, < 32 between calls
   uint32_t* ring;   // this lane's kRing words in LDS, 64 words apart (bank-conflict free)
 
-  // a finished word on the common path
+  // a finished word
   __device__ __forceinline__ void word(uint32_t w) {
     ring[(nwords & (kRing - 1)) * 64] = w;
     ++nwords;
   }
-  // store the ring's words to the slot (at most kRing - 1 are pending)
+  // the oldest four pending words as one chunk, once they are all there
   __device__ __forceinline__ void flush() {
-    // read every slot of the ring first (one wait for all of them), then store the pending ones
-    uint32_t v[kRing - 1];
-#pragma unroll
-    for (int i = 0; i < kRing - 1; ++i) v[i] = ring[((flushed + i) & (kRing - 1)) * 64];
-#pragma unroll
-    for (int i = 0; i < kRing - 1; ++i) {
-      const uint32_t wi = flushed + i;
-      if (wi < nwords && wi < cap) out[(uint64_t)wi * 64] = v[i];
-    }
-    flushed = nwords;
+    const uint32_t* r = ring + (flushed & (kRing - 1)) * 64;   // flushed % 8 is 0 or 4
+    const uint4 v = make_uint4(r[0], r[64], r[128], r[192]);
+    const bool full = nwords - flushed >= 4u;
+    if (full && flushed < cap) *reinterpret_cast<uint4*>(out + (uint64_t)(flushed >> 2) * 256) = v;
+    flushed += full ? 4u : 0u;
   }
-  // direct output (the ring must be flushed first)
+  // the last chunk, partly filled (its words past nwords are never read)
+  __device__ __forceinline__ void flush_last() {
+    flush();
+    if (nwords > flushed) {
+      const uint32_t* r = ring + (flushed & (kRing - 1)) * 64;
+      const uint4 v = make_uint4(r[0], r[64], r[128], r[192]);
+      if (flushed < cap) *reinterpret_cast<uint4*>(out + (uint64_t)(flushed >> 2) * 256) = v;
+      flushed = nwords;
+    }
+  }
+  // output of the rare paths: bit by bit into words, a flush after each word
   __device__ __forceinline__ void put(uint32_t bits, uint32_t nb) {  // nb <= 32
     acc = (acc << nb) | bits;
     nacc += nb;
     if (nacc >= 32) {
       nacc -= 32;
-      const uint32_t w = (uint32_t)(acc >> nacc);
-      if (nwords < cap) out[(uint64_t)nwords * 64] = w;
-      ++nwords;
-      flushed = nwords;
+      word((uint32_t)(acc >> nacc));
+      flush();
       acc &= (1ull << nacc) - 1ull;
     }
   }
@@ -185,6 +201,7 @@ __device__ __forceinline__ void enc_finish(EncState& e, BitSink& o) {
   o.put(b, 1);
   o.run(b ^ 1u, e.pending);
   if (o.nacc) o.put(0u, 32 - o.nacc);  // zero-pad to a whole word
+  o.flush_last();
 }
 
 // Token pipeline of the encoder: the symbols and their table entries do not depend on the
@@ -203,9 +220,9 @@ __global__ __launch_bounds__(1024) void encode_kernel(
     float* __restrict__ scales, int nw, int nu, int nsets_lds) {
   // workgroup = nu units (layer, K/V, 64-channel block) x nw (context, chunk) pairs; wave w
   // codes pair slot w / nu of unit w % nu (one workgroup per CU where the grid allows, so the
-  // hardware spreads its waves evenly over the SIMDs). The delta tables of the levels a unit's
-  // pairs use are staged in LDS once (9 of 10 symbols look up there); anchor entries come from
-  // global memory, requested a pipeline step ahead.
+  // hardware spreads its waves evenly over the SIMDs). The anchor tables of the units are
+  // staged in LDS for the anchor pass, then the delta tables of the levels their pairs use for
+  // the delta pass.
   extern __shared__ __attribute__((aligned(16))) uint16_t tabs[];   // [nu][nsets][64][kEncTabStride], then words [nu * nw][kRing][64]
   __shared__ uint32_t s_mask[kEncMaxUnits];
   __shared__ uint8_t s_set_of_level[kEncMaxUnits][CG_MAX_LEVELS];
@@ -375,10 +392,9 @@ __global__ __launch_bounds__(1024) void encode_kernel(
       (cg_lds_u16*)(tabs + ((u * nsets_lds + s_set_of_level[u][lv]) * 64 + lane) * kEncTabStride);
   EncState e{0u, 0xFFFFFFFFu, 0u};
   uint32_t* rings = reinterpret_cast<uint32_t*>(tabs + nu * nsets_lds * 64 * kEncTabStride);
-  // the slots of a wave's 64 streams are interleaved word by word (word k of lane L at
-  // 64 k + L), so words that neighbouring lanes finish at about the same time share lines
+  // the slots of a wave's 64 streams, interleaved by 16-byte chunk
   const uint64_t slot_group = (uint64_t)bclk * P.nblk + cb;
-  BitSink o{slots + slot_group * slot_words * 64 + lane, slot_words, 0u, 0u, 0ull, 0u,
+  BitSink o{slots + slot_group * slot_words * 64 + lane * 4, slot_words, 0u, 0u, 0ull, 0u,
             rings + wave * kRing * 64 + lane};
 
   // Pipeline buffers, used in turn (steps alternate between set 0 and set 1, and the loop
@@ -420,15 +436,17 @@ __global__ __launch_bounds__(1024) void encode_kernel(
   // a step without branches per symbol; if a lane of the wave owed more than 32 bits at some
   // symbol, the wave codes the step again from the saved state with the branching coder
   // code[u] (uniform) says whether position u of the buffer is coded in this step
-  auto code_run = [&](const auto& clo, const auto& chi, const bool* code)
+  // positions [B, E) of the buffers (at most five symbols: the ring bound)
+  auto code_run = [&](const auto& clo, const auto& chi, const bool* code, auto B, auto E)
                       __attribute__((always_inline)) {
-    constexpr int K = sizeof(clo) / sizeof(clo[0]);
+    constexpr int kB = decltype(B)::value, kE = decltype(E)::value;
+    static_assert(kE - kB <= 5, "a run codes at most five symbols");
     const EncState e0 = e;
     const uint64_t acc0 = o.acc;
     const uint32_t nacc0 = o.nacc, nwords0 = o.nwords;
     bool rare = false;
 #pragma unroll
-    for (int u = 0; u < K; ++u)
+    for (int u = kB; u < kE; ++u)
       if (code[u]) enc_symbol_fast(e, o, clo[u], chi[u], rare);
     if (__builtin_amdgcn_ballot_w64(rare) != 0ull) {
       e = e0;
@@ -436,9 +454,18 @@ __global__ __launch_bounds__(1024) void encode_kernel(
       o.nacc = nacc0;
       o.nwords = nwords0;
 #pragma unroll
-      for (int u = 0; u < K; ++u)
+      for (int u = kB; u < kE; ++u)
         if (code[u]) enc_symbol(e, o, clo[u], chi[u]);
     }
+  };
+  // a whole buffer of K positions in two runs, with a flush between them
+  auto code_halves = [&](const auto& clo, const auto& chi, const bool* code)
+                         __attribute__((always_inline)) {
+    constexpr int K = sizeof(clo) / sizeof(clo[0]);
+    constexpr int H = K / 2;
+    code_run(clo, chi, code, std::integral_constant<int, 0>{}, std::integral_constant<int, H>{});
+    o.flush();
+    code_run(clo, chi, code, std::integral_constant<int, H>{}, std::integral_constant<int, K>{});
   };
   // the deltas of a step of the token pipeline (its anchors were coded in the anchor pass)
   auto code_step = [&](const uint32_t (&clo)[kPipe], const uint32_t (&chi)[kPipe], int step)
@@ -450,7 +477,7 @@ __global__ __launch_bounds__(1024) void encode_kernel(
       const bool anc = kG > 0 ? u == 0 : (g0 + u) % P.G == 0;
       code[u] = step * kPipe + u < n && !anc;
     }
-    code_run(clo, chi, code);
+    code_halves(clo, chi, code);
   };
 
   // Anchor pass: the anchors of the chunk in token order (they come first in the stream), in
@@ -483,7 +510,7 @@ __global__ __launch_bounds__(1024) void encode_kernel(
       bool code[kPipeA];
 #pragma unroll
       for (int u = 0; u < kPipeA; ++u) code[u] = step * kPipeA + u < na;
-      code_run(clo, chi, code);
+      code_halves(clo, chi, code);
     };
     load_anchor_rows(ya0, 0);
     load_anchor_rows(ya1, 1);
@@ -696,9 +723,9 @@ __global__ __launch_bounds__(256) void tok_encode_kernel(KParams P, const uint8_
   const uint16_t* tab = anchor ? cdfA + (int64_t)g.lk * P.C * 256
                                : cdfD + ((int64_t)lv * P.L * 2 + g.lk) * P.C * 256;
   EncState e{0u, 0xFFFFFFFFu, 0u};
-  BitSink o{slots + (uint64_t)grp * slot_words * 64 + lane, slot_words, 0u, 0u, 0ull, 0u,
+  BitSink o{slots + (uint64_t)grp * slot_words * 64 + lane * 4, slot_words, 0u, 0u, 0ull, 0u,
             rings[wave] + lane};
-  // steps of 8 symbols (at most 8 * 18 bits, so at most 5 ring words pending at a flush)
+  // steps of 8 symbols, flushed after every 4 (the ring bound of BitSink)
   constexpr int kStep = 8;
   for (int c0 = 0; c0 < P.C; c0 += kStep) {
     uint32_t lo[kStep], hi[kStep];
@@ -711,8 +738,10 @@ __global__ __launch_bounds__(256) void tok_encode_kernel(KParams P, const uint8_
       hi[u] = sy == CG_NSYM - 1 ? CG_TOTAL : (uint32_t)t[sy + 1];
     }
 #pragma unroll
-    for (int u = 0; u < kStep; ++u)
+    for (int u = 0; u < kStep; ++u) {
       if (c0 + u < P.C) enc_symbol(e, o, lo[u], hi[u]);
+      if (u == kStep / 2 - 1) o.flush();   // runs of at most four symbols between flushes
+    }
     o.flush();
   }
   enc_finish(e, o);
@@ -721,8 +750,8 @@ __global__ __launch_bounds__(256) void tok_encode_kernel(KParams P, const uint8_
 }
 
 // Copy every stream's words from its slot to their place in the payload. One workgroup per slot
-// group of 64 streams: the slots of its streams are interleaved word by word, so tiles of 16
-// words x 64 streams are read as whole 256-byte rows, transposed through LDS, and written as 16
+// group of 64 streams: the slots of its streams are interleaved by 16-byte chunk, so tiles of
+// chunks x 64 streams are read as whole 1 KB rows, transposed through LDS, and written as 16
 // consecutive words per stream. Channel layout (kTok false): group = (row, 64-channel block),
 // streams row * C + block * 64 + i. Token layout: group = (context, chunk, layer and K/V,
 // 64-token block), streams tok_stream(...) of the block's tokens.
@@ -766,22 +795,24 @@ __global__ __launch_bounds__(256) void compact_kernel(KParams P, const uint32_t*
   __syncthreads();
   const uint32_t K = s_max;
   const uint32_t* src = slots + (uint64_t)grp * slot_words * 64;
-  // kCompactRows slot rows per pass: every thread has eight 16-byte loads in flight
+  // kCompactRows words of every stream per pass (kCompactRows / 4 chunk rows of 1 KB, a wave
+  // reading whole rows): every thread has eight 16-byte loads in flight
   for (uint32_t k0 = 0; k0 < K; k0 += kCompactRows) {
     uint4 v[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const uint32_t r = k0 + (t >> 4) + 16 * i;   // slot row: word r of all 64 streams
-      v[i] = r < K ? *reinterpret_cast<const uint4*>(src + (uint64_t)r * 64 + (t & 15) * 4)
-                   : make_uint4(0u, 0u, 0u, 0u);
+      const uint32_t cr = (t >> 6) + 4 * i;   // chunk row of this pass: words 4 cr .. 4 cr + 3
+      const uint32_t m = (k0 >> 2) + cr;      // chunk index in the slots
+      v[i] = 4 * m < K ? *reinterpret_cast<const uint4*>(src + ((uint64_t)m * 64 + (t & 63)) * 4)
+                       : make_uint4(0u, 0u, 0u, 0u);
     }
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      uint32_t* d = &ctile[(t >> 4) + 16 * i][(t & 15) * 4];
-      d[0] = v[i].x;
-      d[1] = v[i].y;
-      d[2] = v[i].z;
-      d[3] = v[i].w;
+      const int cr = (t >> 6) + 4 * i;
+      ctile[4 * cr + 0][t & 63] = v[i].x;
+      ctile[4 * cr + 1][t & 63] = v[i].y;
+      ctile[4 * cr + 2][t & 63] = v[i].z;
+      ctile[4 * cr + 3][t & 63] = v[i].w;
     }
     __syncthreads();
 #pragma unroll
@@ -869,8 +900,8 @@ hipError_t cg_launch_encode(const KParams& P, const uint16_t* kv, const uint8_t*
 
 int64_t cg_token_streams(const KParams& P) { return (int64_t)P.B * P.L * 2 * P.T; }
 
-uint32_t cg_token_slot_words(const KParams& P) {
-  return (uint32_t)((18ull * (uint64_t)P.C + 2ull + 31ull) / 32ull);
+uint32_t cg_token_slot_words(const KParams& P) {   // whole 16-byte chunks
+  return (uint32_t)(((18ull * (uint64_t)P.C + 2ull + 31ull) / 32ull + 3ull) & ~3ull);
 }
 
 TokEncWorkspace cg_encode_tokens_ws_layout(const KParams& P) {
