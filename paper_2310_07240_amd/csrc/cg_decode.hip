@@ -449,19 +449,21 @@ __global__ __launch_bounds__(1024) void decode_kernel(
 //     its row and keeps the quantized value q in the group's first delta row;
 //   * delta phase: the delta tables replace the anchor tables in LDS; each group reads back its
 //     anchor's q (requested a group ahead), decodes its nine deltas with epochs before deltas
-//     1, 4 and 7, and stores rows 1..9 (over the kept q).
+//     1 and 6, and stores rows 1..9 (over the kept q).
 // Both searches start from the 15 fences cum[16 f] of the table in registers (a 4-step select
 // search, no memory round trip), then take two LDS round trips (one 4-ary level, the leaf).
 constexpr int kG10 = 10;
-constexpr int kAnchorRun = 4;   // anchors per bitstream epoch (a symbol takes <= 18 bits)
+constexpr int kAnchorRun = 5;   // anchors per bitstream epoch (a symbol takes <= 18 bits)
 
 // Per-lane decoder state of the group-of-10 kernel (plain scalars: it lives in registers).
 // Bitstream reader: the 128 bits after the code value's own are held in w0..w3, of which the
 // first `pos` bits of w0 are already consumed. A token takes n <= 18 bits (the interval is
 // wider than 2^30 before a symbol and at least 2^14 after it, and renormalisation doubles it
 // to at most 2^32), so it crosses at most one word boundary and w0 moves up by at most one
-// word; four tokens take at most 72 bits, which never reach past w3 from an epoch start with
-// pos < 32, so at most three words leave between two epoch boundaries.
+// word; five tokens take at most 90 bits, which from an epoch start with pos < 32 never reach
+// past w3 (31 + 90 < 128), so at most three words leave between two epoch boundaries. (Bits
+// that the 32-bit window read takes past the token's own come from words already moved and are
+// shifted out unused.)
 struct G10Lane {
   uint32_t D, low, rm1;          // code value - low, low, high - low
   uint32_t w0, w1, w2, w3;       // the next stream words, w0 partly consumed
@@ -901,12 +903,11 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 1, lane);
     g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 2, lane);
     g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 3, lane);
-    g10_epoch(st, sbase, cap);
-    const uint32_t qnext = q_of(gi + 1);   // requested a group ahead
     g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 4, lane);
     g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 5, lane);
-    g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 6, lane);
     g10_epoch(st, sbase, cap);
+    const uint32_t qnext = q_of(gi + 1);   // requested a group ahead
+    g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 6, lane);
     g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 7, lane);
     g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 8, lane);
     g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 9, lane);
@@ -920,7 +921,7 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     st.a = (float)(int)(int16_t)qraw * s;
     g10_epoch(st, sbase, cap);
     for (int r = 1; r < rem; ++r) {
-      if (r == 4 || r == 7) g10_epoch(st, sbase, cap);
+      if (r == 6) g10_epoch(st, sbase, cap);
       g10_delta(st, fD, dtab, tbD, kqD, w, obuf, r, lane);
     }
     g10_flush(obuf, row, rstride, 1, rem, lane, cbase, P.C);
