@@ -45,6 +45,8 @@
 // tok_decode_kernel / tok_dequant_kernel decode the token-parallel layout (one stream per
 // context, layer, K/V and token; see their comment).
 #include "../../include/cachegen.h"
+#include <type_traits>
+
 #include "cg_device.h"
 
 namespace {
@@ -679,6 +681,26 @@ __device__ __forceinline__ void g10_flush(const uint16_t* obuf, uint16_t* row, i
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Rows 1..9 of a whole group of a full, 16-byte aligned 64-channel block: two unconditional
+// 16-byte stores per lane (rows 1..8, then row 9, which lanes 8..63 store again with the same
+// bytes as lanes 0..7). With the same two stores on every path, the wait at the next epoch
+// covers only the words it needs, not the stores just issued.
+__device__ __forceinline__ void g10_flush_full(const uint16_t* obuf, uint16_t* row,
+                                               int64_t rstride, int lane) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  const int cc = (lane & 7) * 8;
+  const int r0 = 1 + (lane >> 3);
+  const uint4 v0 = *reinterpret_cast<const uint4*>(obuf + r0 * 64 + cc);
+  const uint4 v1 = *reinterpret_cast<const uint4*>(obuf + 9 * 64 + cc);
+  store_row16(row + r0 * rstride + cc, v0);
+  store_row16(row + 9 * rstride + cc, v1);
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 __global__ __launch_bounds__(1024) void decode_g10_kernel(
     KParams P, const uint32_t* __restrict__ words, const uint64_t* __restrict__ offsets,
     const float* __restrict__ scales, const uint8_t* __restrict__ chunk_level,
@@ -895,10 +917,15 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     const uint16_t* rq = row0 + ((int64_t)min(g, gmax) * kG10 + 1) * rstride;   // uniform
     return (uint32_t)rq[lsrc];
   };
-  uint32_t qraw = q_of(0);
+  // the anchor value of the next group, carried as a float so that the loop head uses no
+  // register a load may still be filling
+  float anext = (float)(int)(int16_t)q_of(0) * s;
   uint16_t* row = row0;
+  // whole groups: the loop is written out twice, for full aligned blocks and for the rest
+  const bool full = cbase + 64 <= P.C && (P.C & 7) == 0 && (reinterpret_cast<uintptr_t>(out) & 15) == 0;
+  auto groups = [&](auto kFull) __attribute__((always_inline)) {
   for (int gi = 0; gi < ngr; ++gi) {
-    st.a = (float)(int)(int16_t)qraw * s;
+    st.a = anext;
     g10_epoch(st, sbase, cap);
     g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 1, lane);
     g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 2, lane);
@@ -911,14 +938,18 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 7, lane);
     g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 8, lane);
     g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 9, lane);
-    g10_flush(obuf, row, rstride, 1, kG10, lane, cbase, P.C);
+    if constexpr (decltype(kFull)::value) g10_flush_full(obuf, row, rstride, lane);
+    else g10_flush(obuf, row, rstride, 1, kG10, lane, cbase, P.C);
     row += kG10 * rstride;
-    qraw = qnext;
+    anext = (float)(int)(int16_t)qnext * s;
     set_priority((ngr - gi - 1) * (kG10 - 1));
   }
+  };
+  if (full) groups(std::integral_constant<bool, true>{});
+  else groups(std::integral_constant<bool, false>{});
   const int rem = n - ngr * kG10;   // last, partial group (uniform)
   if (rem > 1) {
-    st.a = (float)(int)(int16_t)qraw * s;
+    st.a = anext;
     g10_epoch(st, sbase, cap);
     for (int r = 1; r < rem; ++r) {
       if (r == 6) g10_epoch(st, sbase, cap);

@@ -49,8 +49,10 @@ def test_streamed_decode_equals_oracle(link_gbps):
     if link_gbps > 0:
         link_ms = total * 32 / (link_gbps * 1e6)
         assert st["transfer_ms"] >= 0.9 * link_ms
-        # only the last chunk's decode can remain after the last byte arrived
-        assert st["hidden_fraction"] >= 0.5
+        # only the last chunk's decode (and its launch) can remain after the last byte arrived;
+        # with no overlap the fraction would be about 0. The bound leaves room for launch and
+        # event overheads, which on chunks this small are close to a chunk's decode time.
+        assert st["hidden_fraction"] >= 0.25
 
 
 def test_streamed_decode_rejects_bad_arguments():
