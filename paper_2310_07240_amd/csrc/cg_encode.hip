@@ -85,6 +85,17 @@ struct BitSink {
     if (full && flushed < cap) *reinterpret_cast<uint4*>(out + (uint64_t)(flushed >> 2) * 256) = v;
     flushed += full ? 4u : 0u;
   }
+  // a flush in two halves: the ring read first, the store later (after the waits for loads
+  // that were issued before it, which then do not cover the store)
+  __device__ __forceinline__ uint4 flush_read(bool& full) const {
+    const uint32_t* r = ring + (flushed & (kRing - 1)) * 64;
+    full = nwords - flushed >= 4u;
+    return make_uint4(r[0], r[64], r[128], r[192]);
+  }
+  __device__ __forceinline__ void flush_store(const uint4& v, bool full) {
+    if (full && flushed < cap) *reinterpret_cast<uint4*>(out + (uint64_t)(flushed >> 2) * 256) = v;
+    flushed += full ? 4u : 0u;
+  }
   // the last chunk, partly filled (its words past nwords are never read)
   __device__ __forceinline__ void flush_last() {
     flush();
@@ -517,14 +528,17 @@ __global__ __launch_bounds__(1024) void encode_kernel(
     quantize_anchors(ya0, la0, ha0);
     load_anchor_rows(ya0, 2);
     for (int st = 0; st * kPipeA < na; st += 2) {
-      o.flush();
+      bool ff;
+      uint4 fv = o.flush_read(ff);
       quantize_anchors(ya1, la1, ha1);
+      o.flush_store(fv, ff);
       load_anchor_rows(ya1, st + 3);
       code_anchors(la0, ha0, st);
       set_priority(max(na - (st + 1) * kPipeA, 0));
       if ((st + 1) * kPipeA >= na) break;
-      o.flush();
+      fv = o.flush_read(ff);
       quantize_anchors(ya0, la0, ha0);
+      o.flush_store(fv, ff);
       load_anchor_rows(ya0, st + 4);
       code_anchors(la1, ha1, st + 1);
       set_priority(max(na - (st + 2) * kPipeA, 0));
@@ -541,15 +555,18 @@ __global__ __launch_bounds__(1024) void encode_kernel(
   load_rows(xr0, 2);
   for (int st = 0; st * kPipe < n; st += 2) {
     // step st: quantize step st+1, request the rows of step st+3, code step st
-    o.flush();
+    bool ff;
+    uint4 fv = o.flush_read(ff);
     quantize_step(xr1, lo1, hi1);
+    o.flush_store(fv, ff);
     load_rows(xr1, st + 3);
     code_step(lo0, hi0, st);
     set_priority(max(n - (st + 1) * kPipe, 0));
     if ((st + 1) * kPipe >= n) break;
     // step st+1: the same with the sets exchanged
-    o.flush();
+    fv = o.flush_read(ff);
     quantize_step(xr0, lo0, hi0);
+    o.flush_store(fv, ff);
     load_rows(xr0, st + 4);
     code_step(lo1, hi1, st + 1);
     set_priority(max(n - (st + 2) * kPipe, 0));
