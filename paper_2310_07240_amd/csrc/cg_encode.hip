@@ -561,7 +561,6 @@ __global__ __launch_bounds__(1024) void encode_kernel(
     o.flush_store(fv, ff);
     load_rows(xr1, st + 3);
     code_step(lo0, hi0, st);
-    set_priority(max(n - (st + 1) * kPipe, 0));
     if ((st + 1) * kPipe >= n) break;
     // step st+1: the same with the sets exchanged
     fv = o.flush_read(ff);
@@ -569,7 +568,7 @@ __global__ __launch_bounds__(1024) void encode_kernel(
     o.flush_store(fv, ff);
     load_rows(xr0, st + 4);
     code_step(lo1, hi1, st + 1);
-    set_priority(max(n - (st + 2) * kPipe, 0));
+    set_priority(max(n - (st + 2) * kPipe, 0));   // once per two steps (every step: ~1.5 % slower)
   }
   enc_finish(e, o);
   // the coder's bound for n symbols; the compaction never writes past the sum of these
