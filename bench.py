@@ -4,10 +4,14 @@ plus encode throughput and bits per element.
 
 One step = the whole codec over one KV cache resident in HBM: fit the distributions of every
 level (cg_fit_cdf), encode (cg_encode), decode (cg_decode). `value` is the decode throughput
-(fp16 bytes of KV produced per second of cg_decode, HIP events on the launch stream).
+(fp16 bytes of KV produced per second of cg_decode, HIP events on the launch stream) on the
+Mistral-7B-shaped 4K-token cache.
 
-Prints ONE JSON line. Also reports the roofline of the decode kernel, the HBM fraction, and the
-CPU oracle timed on the host's cores on the same workload (a baseline, not the target).
+Prints ONE JSON line. Also reports the roofline of the decode kernel, the HBM fraction, the
+other four workloads (`per_workload`: a few steps each, same kernels), and the CPU oracle timed
+on the host's cores on the same workload (a baseline, not the target). The oracle's payload and
+decoded cache are compared bit for bit with the GPU's (`parity`); a mismatch makes the run exit
+with status 3 after printing the line.
 """
 from __future__ import annotations
 
@@ -29,11 +33,12 @@ METRIC = "AC decode GB/s of fp16 KV (+ encode GB/s, bits/element), 1 MI355X"
 HBM_PEAK_GBPS = 8000.0
 # Integer / fp32 vector issue rate: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz = 39.3 T lane-ops/s.
 VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
-# Algorithmic 32-bit operations of one decode step (one symbol): target 5, binary search over
-# 255 symbols 8, interval update 10, one-step renormalisation with bit refill 20, dequantize 5.
+# A model, not a measurement: algorithmic 32-bit operations of one decode step (one symbol):
+# target 5, binary search over 255 symbols 8, interval update 10, one-step renormalisation with
+# bit refill 20, dequantize 5. The measured instruction count comes from the counter profile.
 DECODE_OPS_PER_SYMBOL = 48
 
-
+MAIN_WORKLOAD = "mistral7b_gqa_t4096"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_traffic_mistral7b_t4096.json")
 DECODE_SRC = os.path.join(ROOT, "paper_2310_07240_amd", "csrc", "cg_decode.hip")
 
@@ -49,10 +54,11 @@ def decode_source_hash() -> str:
     return hashlib.sha256(src.encode()).hexdigest()[:16]
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per decode launch from the committed FETCH_SIZE / WRITE_SIZE profile, scaled
-    by the same counters on a plain copy of known size; None if the decode kernel's source has
-    changed since those counters were taken (or no profile exists for this workload)."""
+def decode_profile(workload: str):
+    """The committed counter profile of the decode kernel (HBM bytes per launch from FETCH_SIZE
+    / WRITE_SIZE scaled by a plain copy of known size; VALU instructions per symbol step), or
+    None if the decode kernel's source has changed since the counters were taken or no profile
+    exists for this workload."""
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
@@ -60,11 +66,132 @@ def measured_traffic(workload: str):
         return None
     if t.get("workload") != workload or t.get("decode_source_sha256_16") != decode_source_hash():
         return None
-    return t.get("decode_bytes_per_launch")
+    return t
 
 
 def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+class Run:
+    """One workload resident on the GPU with its codec buffers."""
+
+    def __init__(self, w, dev, kv_np=None):
+        import torch
+        from paper_2310_07240_amd import workloads as W
+        from paper_2310_07240_amd.cachegen import Codec, CodecParams
+        self.torch = torch
+        self.w = w
+        self.p = CodecParams.of(w)
+        t = time.time()
+        if kv_np is None:
+            kv_np = W.generate(w)
+        log(f"{w.name}: {w.n_elem} elements generated in {time.time() - t:.1f}s")
+        self.codec = Codec(self.p, device=dev)
+        self.kv = torch.from_numpy(kv_np.view(np.int16)).to(dev)
+        self.cl_np = w.chunk_levels()
+        self.cl = torch.from_numpy(self.cl_np).to(dev)
+        L, C, NLV = w.n_layers, w.n_channels, w.n_levels
+        self.ca = torch.empty((L, 2, C, 256), dtype=torch.int16, device=dev)
+        self.cd = torch.empty((NLV, L, 2, C, 256), dtype=torch.int16, device=dev)
+        self.words = torch.empty((self.codec.bound_words,), dtype=torch.int32, device=dev)
+        self.offsets = torch.empty((self.codec.n_streams + 1,), dtype=torch.int64, device=dev)
+        self.scales = torch.empty((self.codec.n_streams,), dtype=torch.float32, device=dev)
+        self.ws = torch.empty((self.codec.ws_bytes,), dtype=torch.uint8, device=dev)
+        self.out = torch.zeros(w.kv_shape, dtype=torch.int16, device=dev)
+        self.stream = torch.cuda.current_stream()
+
+    def fit(self):
+        from paper_2310_07240_amd.cachegen import cg_fit_cdf
+        for lv in range(self.w.n_levels):
+            cg_fit_cdf(self.p, self.kv, lv, self.ca if lv == 0 else None, self.cd[lv],
+                       self.stream)
+
+    def encode(self):
+        from paper_2310_07240_amd.cachegen import cg_encode
+        cg_encode(self.p, self.kv, self.cl, self.ca, self.cd, self.words, self.offsets,
+                  self.scales, self.ws, self.stream)
+
+    def decode(self):
+        from paper_2310_07240_amd.cachegen import cg_decode
+        cg_decode(self.p, self.words, self.offsets, self.scales, self.cl, self.ca, self.cd, 0,
+                  self.codec.n_chunks, self.out, self.stream)
+
+    def step(self, ev=None):
+        if ev:
+            ev[0].record(self.stream)
+        self.fit()
+        if ev:
+            ev[1].record(self.stream)
+        self.encode()
+        if ev:
+            ev[2].record(self.stream)
+        self.decode()
+        if ev:
+            ev[3].record(self.stream)
+
+    def timed(self, steps, warmup):
+        """Warm-up steps, then `steps` timed steps; per-stage times (ms) and the wall time."""
+        torch = self.torch
+        for _ in range(warmup):
+            self.step()
+        torch.cuda.synchronize()
+        events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(steps):
+            self.step(events[i])
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        fit = [e[0].elapsed_time(e[1]) for e in events]
+        enc = [e[1].elapsed_time(e[2]) for e in events]
+        dec = [e[2].elapsed_time(e[3]) for e in events]
+        return fit, enc, dec, wall
+
+    def summary(self, fit, enc, dec):
+        """Throughputs, bits per element and the decode's HBM fraction."""
+        w = self.w
+        L, C = w.n_layers, w.n_channels
+        dec_avg, enc_avg, fit_avg = (sum(x) / len(x) for x in (dec, enc, fit))
+        fp16_bytes = 2 * w.n_elem
+        total_words = int(self.offsets[-1].item())
+        S = self.codec.n_streams
+        levels_used = len(set(int(v) for v in self.cl_np.reshape(-1)))
+        table_bytes = L * 2 * C * 512
+        # decode kernel: algorithmic bytes = fp16 written + payload + side info + the tables of
+        # the levels the chunks use (each table counted once)
+        dec_bytes = fp16_bytes + total_words * 4 + S * (4 + 8) + table_bytes * (1 + levels_used)
+        hbm_gbps = dec_bytes / (dec_avg * 1e-3) / 1e9
+        return {
+            "decode_ms": round(dec_avg, 4),
+            "decode_GBps": round(fp16_bytes / (dec_avg * 1e-3) / 1e9, 2),
+            "encode_ms": round(enc_avg, 4),
+            "encode_GBps": round(fp16_bytes / (enc_avg * 1e-3) / 1e9, 2),
+            "fit_ms": round(fit_avg, 4),
+            "fit_levels": w.n_levels,
+            "bits_per_element": {"payload": round(total_words * 32 / w.n_elem, 4),
+                                 "side_info": round(S * 12 * 8 / w.n_elem, 4),
+                                 "cdf_tables": round(table_bytes * (1 + w.n_levels) * 8
+                                                     / w.n_elem, 4)},
+            "hbm": {"achieved": round(hbm_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                    "frac": round(hbm_gbps / HBM_PEAK_GBPS, 4), "bytes_per_launch": dec_bytes},
+            "alu_frac_model": round(DECODE_OPS_PER_SYMBOL * w.n_elem / (dec_avg * 1e-3) / 1e12
+                                    / VALU_PEAK_TOPS, 4),
+        }
+
+    def host_results(self):
+        """Tables, offsets, scales, payload and decoded cache as numpy bit patterns."""
+        off = self.offsets.cpu().numpy().view(np.uint64)
+        return dict(ca=self.ca.cpu().numpy().view(np.uint16),
+                    cd=self.cd.cpu().numpy().view(np.uint16), offsets=off,
+                    scales=self.scales.cpu().numpy().view(np.uint32),
+                    words=self.words[: int(off[-1])].cpu().numpy().view(np.uint32),
+                    out=self.out.cpu().numpy().view(np.uint16))
+
+    def release(self):
+        for name in ("kv", "cl", "ca", "cd", "words", "offsets", "scales", "ws", "out"):
+            setattr(self, name, None)
+        self.torch.cuda.empty_cache()
 
 
 def main():
@@ -72,8 +199,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="mistral7b_gqa_t4096")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--workload", default=MAIN_WORKLOAD)
+    ap.add_argument("--no-cpu-baseline", action="store_true",
+                    help="skip the oracle (and with it the bit-exactness check of the run)")
     ap.add_argument("--cpu-threads", type=int, default=0, help="0 = all host cores")
     ap.add_argument("--no-streamed", action="store_true",
                     help="skip the chunk-pipelined decode (payload copied from pinned host memory "
@@ -83,6 +211,9 @@ def main():
     ap.add_argument("--no-calib-copy", action="store_true",
                     help="skip the plain copy of known size run after the timed region (it "
                          "calibrates rocprofv3's FETCH_SIZE / WRITE_SIZE counters)")
+    ap.add_argument("--no-per-workload", action="store_true",
+                    help="skip the other workloads (run after the main one, a few steps each)")
+    ap.add_argument("--per-workload-steps", type=int, default=3)
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -94,107 +225,60 @@ def main():
 
     import torch
     from paper_2310_07240_amd import workloads as W
-    from paper_2310_07240_amd.cachegen import (Codec, CodecParams, cg_decode, cg_encode,
-                                               cg_fit_cdf)
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     w = W.WORKLOADS[args.workload]
-    p = CodecParams.of(w)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
 
-    t = time.time()
     kv_np = W.generate(w)
-    log(f"generated {w.name}: {w.n_elem} elements in {time.time() - t:.1f}s")
-    codec = Codec(p, device=dev)
-    kv = torch.from_numpy(kv_np.view(np.int16)).to(dev)
-    cl_np = w.chunk_levels()
-    cl = torch.from_numpy(cl_np).to(dev)
-    L, C, NLV = w.n_layers, w.n_channels, w.n_levels
-    ca = torch.empty((L, 2, C, 256), dtype=torch.int16, device=dev)
-    cd = torch.empty((NLV, L, 2, C, 256), dtype=torch.int16, device=dev)
-    words = torch.empty((codec.bound_words,), dtype=torch.int32, device=dev)
-    offsets = torch.empty((codec.n_streams + 1,), dtype=torch.int64, device=dev)
-    scales = torch.empty((codec.n_streams,), dtype=torch.float32, device=dev)
-    ws = torch.empty((codec.ws_bytes,), dtype=torch.uint8, device=dev)
-    out = torch.zeros(w.kv_shape, dtype=torch.int16, device=dev)
-    stream = torch.cuda.current_stream()
-
-    def step(ev=None):
-        if ev:
-            ev[0].record(stream)
-        for lv in range(NLV):
-            cg_fit_cdf(p, kv, lv, ca if lv == 0 else None, cd[lv], stream)
-        if ev:
-            ev[1].record(stream)
-        cg_encode(p, kv, cl, ca, cd, words, offsets, scales, ws, stream)
-        if ev:
-            ev[2].record(stream)
-        cg_decode(p, words, offsets, scales, cl, ca, cd, 0, codec.n_chunks, out, stream)
-        if ev:
-            ev[3].record(stream)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        step(events[i])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
+    run = Run(w, dev, kv_np)
+    fit, enc, dec, wall = run.timed(args.steps, args.warmup)
     if not args.no_calib_copy:
         # outside the timed region: a plain device-to-device copy of exactly fp16-KV bytes, so a
         # counter profile of this run can scale FETCH_SIZE / WRITE_SIZE to bytes
-        calib = torch.empty_like(kv)
-        calib.copy_(kv)
+        calib = torch.empty_like(run.kv)
+        calib.copy_(run.kv)
         torch.cuda.synchronize()
         del calib
     repeated = None
     if not args.no_repeated:
         # outside the timed region: the same decode repeated back to back, after one untimed run
         # (the decode's own steady state; inside a step it follows the encode)
-        cg_decode(p, words, offsets, scales, cl, ca, cd, 0, codec.n_chunks, out, stream)
+        run.decode()
         rep = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                for _ in range(10)]
         for e0, e1 in rep:
-            e0.record(stream)
-            cg_decode(p, words, offsets, scales, cl, ca, cd, 0, codec.n_chunks, out, stream)
-            e1.record(stream)
+            e0.record(run.stream)
+            run.decode()
+            e1.record(run.stream)
         torch.cuda.synchronize()
         rep_ms = sorted(e0.elapsed_time(e1) for e0, e1 in rep)
         repeated = rep_ms[len(rep_ms) // 2]
-    fit_ms = [e[0].elapsed_time(e[1]) for e in events]
-    enc_ms = [e[1].elapsed_time(e[2]) for e in events]
-    dec_ms = [e[2].elapsed_time(e[3]) for e in events]
-    dec_avg = sum(dec_ms) / len(dec_ms)
-    enc_avg = sum(enc_ms) / len(enc_ms)
-    fit_avg = sum(fit_ms) / len(fit_ms)
 
-    n_elem = w.n_elem
-    fp16_bytes = 2 * n_elem
-    off_np = offsets.cpu().numpy().view(np.uint64)
-    total_words = int(off_np[-1])
-    S = codec.n_streams
-    payload_bits = total_words * 32
-    side_bits = S * (4 + 8) * 8                       # fp32 scale + uint64 offset per stream
-    cdf_bytes = (L * 2 * C * 512) * (1 + NLV)
-    decode_gbps = fp16_bytes / (dec_avg * 1e-3) / 1e9
-    encode_gbps = fp16_bytes / (enc_avg * 1e-3) / 1e9
-    # decode kernel: algorithmic bytes = fp16 written + payload + side info + the CDF tables of
-    # the levels the chunks use (each table counted once)
-    levels_used = len(set(int(v) for v in cl_np.reshape(-1)))
-    dec_bytes = fp16_bytes + total_words * 4 + S * (4 + 8) + L * 2 * C * 512 * (1 + levels_used)
-    hbm_gbps = dec_bytes / (dec_avg * 1e-3) / 1e9
-    ops = DECODE_OPS_PER_SYMBOL * n_elem
-    alu_tops = ops / (dec_avg * 1e-3) / 1e12
+    s = run.summary(fit, enc, dec)
+    dec_avg = s["decode_ms"]
+    fp16_bytes = 2 * w.n_elem
+    alu_tops = DECODE_OPS_PER_SYMBOL * w.n_elem / (dec_avg * 1e-3) / 1e12
+    prof = decode_profile(w.name)
+    roofline = {"bound": "alu", "achieved": round(alu_tops, 3), "peak": round(VALU_PEAK_TOPS, 1),
+                "unit": "Tops/s", "frac": round(alu_tops / VALU_PEAK_TOPS, 4),
+                "ops_per_symbol": DECODE_OPS_PER_SYMBOL,
+                "ops_per_symbol_is": "an algorithmic model (not a measurement)",
+                "traffic": prof.get("decode_bytes_per_launch") if prof else None,
+                "kernel": "decode_g10_kernel" if w.group_size == 10 else "decode_kernel"}
+    if prof:
+        roofline["overfetch"] = round(prof["decode_bytes_per_launch"]
+                                      / s["hbm"]["bytes_per_launch"], 3)
+        for k in ("valu_insts_per_symbol_step", "valu_busy", "waves_per_simd"):
+            if k in prof:
+                roofline[k + "_measured"] = prof[k]
 
     result = {
         "metric": METRIC,
-        "value": round(decode_gbps, 2),
+        "value": s["decode_GBps"],
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -205,65 +289,98 @@ def main():
         "vs_baseline": None,
         "dtype": "u32",
         "data": "synthetic (seeded random-walk KV shaped like the model; no real cache)",
-        "config": {"workload": w.name, "n_ctx": w.n_ctx, "n_layers": L, "n_tokens": w.n_tokens,
-                   "n_channels_per_kv": C, "group_size": w.group_size, "chunk_len": w.chunk_len,
-                   "n_levels": NLV, "streams": S},
-        "decode_ms": round(dec_avg, 4),
-        "encode_ms": round(enc_avg, 4),
-        "fit_ms": round(fit_avg, 4),
-        "encode_GBps": round(encode_gbps, 2),
-        "bits_per_element": {"payload": round(payload_bits / n_elem, 4),
-                             "side_info": round(side_bits / n_elem, 4),
-                             "cdf_tables": round(cdf_bytes * 8 / n_elem, 4)},
-        "roofline": {"bound": "alu", "achieved": round(alu_tops, 3), "peak": round(VALU_PEAK_TOPS, 1),
-                     "unit": "Tops/s", "frac": round(alu_tops / VALU_PEAK_TOPS, 4),
-                     "ops_per_symbol": DECODE_OPS_PER_SYMBOL,
-                     "traffic": measured_traffic(w.name),
-                     "kernel": "decode_g10_kernel" if w.group_size == 10 else "decode_kernel"},
-        "hbm": {"achieved": round(hbm_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                "frac": round(hbm_gbps / HBM_PEAK_GBPS, 4),
-                "bytes_per_launch": dec_bytes},
+        "config": {"workload": w.name, "n_ctx": w.n_ctx, "n_layers": w.n_layers,
+                   "n_tokens": w.n_tokens, "n_channels_per_kv": w.n_channels,
+                   "group_size": w.group_size, "chunk_len": w.chunk_len,
+                   "n_levels": w.n_levels, "streams": run.codec.n_streams},
+        "decode_ms": s["decode_ms"],
+        "encode_ms": s["encode_ms"],
+        "fit_ms": s["fit_ms"],
+        "encode_GBps": s["encode_GBps"],
+        "bits_per_element": s["bits_per_element"],
+        "roofline": roofline,
+        "hbm": s["hbm"],
     }
-
     if repeated is not None:
         result["decode_repeated"] = {
             "ms": round(repeated, 4), "GBps": round(fp16_bytes / (repeated * 1e-3) / 1e9, 2),
             "runs": 10, "what": "median of 10 decodes back to back after the timed steps; "
                                 "`value` is the decode inside each step, right after the encode"}
     if not args.no_streamed:
-        result["streamed"] = streamed(p, codec, words, offsets, scales, cl, ca, cd, total_words)
+        result["streamed"] = streamed(run)
+    gpu_res = run.host_results() if not args.no_cpu_baseline else None
+    run.release()
+    del run
+
+    if not args.no_per_workload:
+        per = {}
+        for name, wo in W.WORKLOADS.items():
+            if name == w.name:
+                continue
+            r = Run(wo, dev)
+            f2, e2, d2, _ = r.timed(args.per_workload_steps, 1)
+            per[name] = r.summary(f2, e2, d2)
+            per[name]["steps"] = args.per_workload_steps
+            log(f"{name}: decode {per[name]['decode_GBps']} GB/s, "
+                f"encode {per[name]['encode_GBps']} GB/s, fit {per[name]['fit_ms']} ms")
+            r.release()
+            del r
+        result["per_workload"] = per
+
+    ok = True
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(w, kv_np, args.cpu_threads)
+        cpu, parity = cpu_baseline(w, kv_np, args.cpu_threads, gpu_res)
+        result["cpu_baseline"] = cpu
+        result["parity"] = parity
+        ok = parity["bit_exact"]
     print(json.dumps(result), flush=True)
+    if not ok:
+        log("GPU results differ from the oracle's: " + json.dumps(parity["mismatches"]))
+        sys.exit(3)
 
 
-def streamed(p, codec, words, offsets, scales, cl, ca, cd, total_words):
+def streamed(run):
     """Chunk-pipelined decode (cg_decode_streamed): the payload arrives chunk by chunk in pinned
     host memory and is copied to the GPU on one stream while the chunks already copied decode on
     another. Reported for the host-to-device bus alone and for a 100 Gb/s link; outside the timed
-    region."""
+    region. `last_chunk_exposed_ms` is the decode time left after the last byte has arrived."""
     import torch
     from paper_2310_07240_amd.cachegen import cg_decode_streamed
     tail = 8
+    total_words = int(run.offsets[-1].item())
     words_host = torch.empty((total_words + tail,), dtype=torch.int32, pin_memory=True)
-    words_host.copy_(words[:total_words + tail].cpu())
-    off_host = offsets.cpu()
-    words_dev = torch.zeros((total_words + tail,), dtype=torch.int32, device=words.device)
-    out = torch.empty(codec.p.kv_shape, dtype=torch.int16, device=words.device)
+    words_host.copy_(run.words[:total_words + tail].cpu())
+    off_host = run.offsets.cpu()
+    words_dev = torch.zeros((total_words + tail,), dtype=torch.int32, device=run.words.device)
+    out = torch.empty(run.w.kv_shape, dtype=torch.int16, device=run.words.device)
     dec_s, copy_s = torch.cuda.Stream(), torch.cuda.Stream()
     res = {"payload_MB": round(total_words * 4 / 1e6, 2)}
     for name, gbps in (("host_to_device", 0.0), ("link_100gbps", 100.0)):
-        cg_decode_streamed(p, words_host, off_host, words_dev, offsets, scales, cl, ca, cd, out,
-                           gbps, dec_s, copy_s)          # warm-up
-        st = cg_decode_streamed(p, words_host, off_host, words_dev, offsets, scales, cl, ca, cd,
-                                out, gbps, dec_s, copy_s)
-        res[name] = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in st.items()}
+        args = (run.p, words_host, off_host, words_dev, run.offsets, run.scales, run.cl, run.ca,
+                run.cd, out, gbps, dec_s, copy_s)
+        cg_decode_streamed(*args)          # warm-up
+        st = cg_decode_streamed(*args)
+        d = {k: (round(v, 4) if isinstance(v, float)
+                 else [round(x, 4) for x in v] if isinstance(v, list) else v)
+             for k, v in st.items()}
+        d["last_chunk_exposed_ms"] = round(st["total_ms"] - st["transfer_ms"], 4)
+        res[name] = d
     return res
 
 
-def cpu_baseline(w, kv_np, threads):
+def _mismatch(name, a, b):
+    a = np.asarray(a).reshape(-1)
+    b = np.asarray(b).reshape(-1)
+    if a.shape != b.shape:
+        return {"what": name, "shape": [list(a.shape), list(b.shape)]}
+    n = int(np.count_nonzero(a != b))
+    return {"what": name, "count": n} if n else None
+
+
+def cpu_baseline(w, kv_np, threads, gpu_res):
     """The CPU oracle's decode of the same workload on the host's cores (it fits and encodes
-    with its own code first, untimed)."""
+    with its own code first, untimed), one core's rate on a two-layer sample, and the
+    comparison of the oracle's tables, payload and decoded cache with the GPU's."""
     import oracle
     threads = threads or oracle.default_threads()
     shape = oracle.shape_from(w)
@@ -273,8 +390,28 @@ def cpu_baseline(w, kv_np, threads):
     words, offsets, scales = oracle.encode(kv_np, shape, cl, ca, cd, threads)
     log(f"oracle fit+encode {time.time() - t:.1f}s on {threads} threads")
     t = time.perf_counter()
-    oracle.decode(words, offsets, scales, shape, cl, ca, cd, threads=threads)
+    out = oracle.decode(words, offsets, scales, shape, cl, ca, cd, threads=threads)
     dt = time.perf_counter() - t
+    mism = [m for m in (_mismatch("cdf_anchor", gpu_res["ca"], ca),
+                        _mismatch("cdf_delta", gpu_res["cd"], cd),
+                        _mismatch("offsets", gpu_res["offsets"], offsets),
+                        _mismatch("scales", gpu_res["scales"], scales.view(np.uint32)),
+                        _mismatch("words", gpu_res["words"], words),
+                        _mismatch("decoded fp16", gpu_res["out"], out)) if m]
+    parity = {"bit_exact": not mism, "mismatches": mism,
+              "compared": "tables, offsets, scales, payload words and the decoded fp16 cache of "
+                          "the timed run against the oracle's, bit for bit"}
+    del out, words
+    # one core: the oracle decodes a sample of the first two layers, from its own payload
+    n_l = min(2, w.n_layers)
+    sub = w.with_(name=w.name + "_sample", n_layers=n_l, layer_bin=tuple(w.layer_bin[:n_l]))
+    sub_kv = np.ascontiguousarray(kv_np[:, :n_l])
+    ssh = oracle.shape_from(sub)
+    sca, scd = oracle.fit_all_levels(sub_kv, ssh, threads)
+    sw, so, ss = oracle.encode(sub_kv, ssh, cl, sca, scd, threads)
+    t = time.perf_counter()
+    oracle.decode(sw, so, ss, ssh, cl, sca, scd, threads=1)
+    dt1 = time.perf_counter() - t
     cpu_model = ""
     try:
         with open("/proc/cpuinfo") as f:
@@ -284,10 +421,15 @@ def cpu_baseline(w, kv_np, threads):
                     break
     except OSError:
         pass
-    return {"value": round(2 * w.n_elem / dt / 1e9, 4), "unit": "GB/s", "cores": threads,
-            "kind": "oracle", "seconds": round(dt, 2), "cpu": cpu_model,
-            "sample": f"the whole {w.name} cache ({w.n_elem} fp16 elements) decoded by the "
-                      f"oracle from its own payload"}
+    cpu = {"value": round(2 * w.n_elem / dt / 1e9, 4), "unit": "GB/s", "cores": threads,
+           "kind": "oracle", "seconds": round(dt, 2), "cpu": cpu_model,
+           "sample": f"the whole {w.name} cache ({w.n_elem} fp16 elements) decoded by the "
+                     f"oracle from its own payload",
+           "single_thread": {"value": round(2 * sub.n_elem / dt1 / 1e9, 4), "unit": "GB/s",
+                             "cores": 1, "seconds": round(dt1, 2),
+                             "sample": f"layers 0-{n_l - 1} of {w.name} ({sub.n_elem} "
+                                       f"elements), decoded on one thread"}}
+    return cpu, parity
 
 
 if __name__ == "__main__":

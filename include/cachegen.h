@@ -74,7 +74,8 @@ enum {
   CG_ERR_SHAPE = -2,      /* a dimension <= 0, group_size < 1, chunk_len < 1, n_levels not
                              in [1, 8], or a size whose index space overflows 64 bits       */
   CG_ERR_CAPACITY = -3,   /* words_cap or workspace_bytes below what the call needs        */
-  CG_ERR_NONFINITE = -4,  /* the KV input holds NaN or +-Inf (reported by cg_check_finite) */
+  CG_ERR_NONFINITE = -4,  /* the KV input holds NaN or +-Inf (reported by cg_get_status after
+                             cg_encode, and by cg_check_finite)                             */
   CG_ERR_HIP = -5,        /* a HIP runtime call or kernel launch failed                     */
   CG_ERR_PARAM = -6       /* a layer_bin or level_mult entry is not finite and > 0          */
 };
@@ -106,8 +107,9 @@ int64_t cg_num_streams(const cg_params* p);
  * invalid. */
 uint64_t cg_encode_bound_words(const cg_params* p);
 
-/* Device scratch that cg_encode needs (bytes): a worst-case slot per stream plus per-stream
- * lengths and the scan's partial sums. 0 if the shape is invalid. */
+/* Device scratch that cg_encode needs (bytes): the status word, per-workgroup non-finite
+ * flags, a worst-case slot per stream, per-stream lengths and the scan's partial sums. 0 if the
+ * shape is invalid. */
 uint64_t cg_encode_workspace_bytes(const cg_params* p);
 
 /* Fit the symbol distributions at encoding level `level` (Sec. 5.2 "Arithmetic coding":
@@ -152,9 +154,14 @@ int cg_fit_cdf_global(const cg_params* p, const uint16_t* kv_f16, int32_t level,
  *   words        out, device, capacity words_cap >= cg_encode_bound_words(p).
  *   offsets      out [S + 1] uint64, device; offsets[S] is the payload length in words.
  *   scales       out [S] fp32, device: the per-stream scale s.
- *   workspace    device scratch of workspace_bytes >= cg_encode_workspace_bytes(p).
+ *   workspace    device scratch of workspace_bytes >= cg_encode_workspace_bytes(p), 256-byte
+ *                aligned; its contents on entry do not matter. After the call its first word
+ *                is the call's status: cg_get_status(workspace, stream) reads it.
  * chunk_level values must be < n_levels (an out-of-range level is clamped to n_levels - 1 on
- * the device). Asynchronous. */
+ * the device). Non-finite input (NaN or +-Inf) is outside the quantizer's domain: the encoder
+ * detects it on the device while it takes the streams' absolute maxima (no extra pass) and
+ * records it in the status word; the payload is then meaningless but every write stays within
+ * the buffers above. Asynchronous. */
 int cg_encode(const cg_params* p, const uint16_t* kv_f16, const uint8_t* chunk_level,
               const uint16_t* cdf_anchor, const uint16_t* cdf_delta,
               uint32_t* words, uint64_t words_cap, uint64_t* offsets, float* scales,
@@ -186,6 +193,11 @@ typedef struct cg_stream_stats {
   double decode_sum_ms;    /* sum of the per-chunk decode durations */
   double hidden_fraction;  /* 1 - (total_ms - transfer_ms) / decode_sum_ms, clamped to [0, 1]:
                               the share of decoding done while the payload still arrived */
+  /* Optional per-chunk event times, host arrays of n_chunks doubles supplied by the caller
+   * (NULL: not reported), in milliseconds from the call's first copy: */
+  double* chunk_copy_done_ms;     /* chunk c's payload is on the device          */
+  double* chunk_decode_begin_ms;  /* chunk c's decode starts                     */
+  double* chunk_decode_end_ms;    /* chunk c's decode ends                       */
 } cg_stream_stats;
 
 /* Decode the whole cache chunk by chunk while its payload arrives (Sec. 5.3: the cache is
@@ -206,7 +218,8 @@ typedef struct cg_stream_stats {
  *                 bus is the link).
  *   decode_stream, copy_stream   two HIP streams (the copies overlap the decodes only if they
  *                 differ); chunk c's decode waits for chunk c's copy through an event.
- *   stats         out, host, may be NULL.
+ *   stats         out, host, may be NULL; its chunk_* pointers are read (NULL or arrays of NC
+ *                 doubles that receive the per-chunk times).
  * Chunk c of every context is copied (one copy per context: chunk c's streams of context b are
  * contiguous) and decoded with the cg_decode kernels. Creates and destroys HIP events, and
  * returns after the last decode has finished (synchronous). The result equals cg_decode over
@@ -250,6 +263,13 @@ typedef struct cg_adapt_params {
  * Returns CG_OK, or CG_ERR_ARG for a null pointer or a non-positive count or rate. */
 int cg_adapt_schedule(const cg_adapt_params* a, const double* bandwidth_gbps,
                       int32_t* choice_out, double* ttft_ms_out);
+
+/* Status of the last cg_encode that used `workspace` (device, the encode workspace): waits for
+ * `stream` (synchronous), then returns CG_OK, or CG_ERR_NONFINITE if the encoded KV held NaN or
+ * +-Inf; CG_ERR_ARG for a null or misaligned workspace, CG_ERR_HIP if the copy fails. The word
+ * is written by every cg_encode, so it never needs clearing; calls that share a workspace on
+ * different streams race. */
+int cg_get_status(const void* workspace, hipStream_t stream);
 
 /* Scan kv_f16 [n_elem] for NaN / Inf (fp16 exponent field all ones), using flag_dev, one
  * caller-owned device uint32_t, as scratch. Synchronises `stream`. Returns CG_OK,

@@ -26,16 +26,28 @@ _LIB = None
 NSYM = 255
 
 
+_FLAGS = ["-std=c11", "-ffp-contract=off", "-fno-fast-math", "-msse2", "-mfpmath=sse", "-fPIC",
+          "-shared", "-pthread"]
+
+
 def build(force: bool = True) -> str:
     """Compile the oracle (gcc, -O2, no fused multiply-add, SSE arithmetic)."""
     if not force and os.path.exists(_LIB_PATH):
         return _LIB_PATH
     tmp = _LIB_PATH + ".tmp%d" % os.getpid()
-    cmd = ["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-msse2",
-           "-mfpmath=sse", "-fPIC", "-shared", "-pthread", _SRC, "-o", tmp, "-lm"]
-    subprocess.run(cmd, check=True)
+    subprocess.run(["gcc", "-O2", *_FLAGS, _SRC, "-o", tmp, "-lm"], check=True)
     os.replace(tmp, _LIB_PATH)
     return _LIB_PATH
+
+
+def build_sanitized(path: str) -> str:
+    """Compile the oracle with AddressSanitizer and UndefinedBehaviorSanitizer (incl. float to
+    integer conversions out of range) into `path`; load it by setting CG_ORACLE_LIB to that path
+    in a process that preloads the ASan runtime."""
+    subprocess.run(["gcc", "-O1", "-g", "-fno-omit-frame-pointer",
+                    "-fsanitize=address,undefined,float-cast-overflow",
+                    "-fno-sanitize-recover=all", *_FLAGS, _SRC, "-o", path, "-lm"], check=True)
+    return path
 
 
 class _Params(ctypes.Structure):
@@ -56,10 +68,11 @@ def _lib():
     global _LIB
     with _LOCK:
         if _LIB is None:
-            if not os.path.exists(_LIB_PATH) or (
-                    os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC)):
+            path = os.environ.get("CG_ORACLE_LIB") or _LIB_PATH
+            if path == _LIB_PATH and (not os.path.exists(_LIB_PATH) or (
+                    os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC))):
                 build()
-            L = ctypes.CDLL(_LIB_PATH)
+            L = ctypes.CDLL(path)
             L.cgo_half_to_float.argtypes = [ctypes.c_uint16]
             L.cgo_half_to_float.restype = ctypes.c_float
             L.cgo_float_to_half.argtypes = [ctypes.c_float]

@@ -27,7 +27,7 @@ EXPORTS = ("cg_num_chunks", "cg_num_streams", "cg_encode_bound_words",
            "cg_decode", "cg_decode_streamed", "cg_adapt_schedule", "cg_check_finite",
            "cg_num_token_streams", "cg_encode_tokens_bound_words",
            "cg_encode_tokens_workspace_bytes", "cg_decode_tokens_workspace_bytes",
-           "cg_encode_tokens", "cg_decode_tokens", "cg_strerror")
+           "cg_encode_tokens", "cg_decode_tokens", "cg_get_status", "cg_strerror")
 CG_FIT_GLOBAL_WORKSPACE_BYTES = 8192
 
 
@@ -57,10 +57,14 @@ class StreamStats(ctypes.Structure):
     """cg_stream_stats: timings of one cg_decode_streamed call (milliseconds)."""
     _fields_ = [("n_chunks", ctypes.c_int32), ("transfer_ms", ctypes.c_double),
                 ("total_ms", ctypes.c_double), ("decode_sum_ms", ctypes.c_double),
-                ("hidden_fraction", ctypes.c_double)]
+                ("hidden_fraction", ctypes.c_double),
+                ("chunk_copy_done_ms", ctypes.POINTER(ctypes.c_double)),
+                ("chunk_decode_begin_ms", ctypes.POINTER(ctypes.c_double)),
+                ("chunk_decode_end_ms", ctypes.POINTER(ctypes.c_double))]
+    SCALARS = ("n_chunks", "transfer_ms", "total_ms", "decode_sum_ms", "hidden_fraction")
 
     def as_dict(self):
-        return {f: getattr(self, f) for f, _ in self._fields_}
+        return {f: getattr(self, f) for f in self.SCALARS}
 
 
 _LIB = None
@@ -97,6 +101,8 @@ def lib():
         L.cg_adapt_schedule.restype = ctypes.c_int
         L.cg_check_finite.argtypes = [PP, _P, _P, _P]
         L.cg_check_finite.restype = ctypes.c_int
+        L.cg_get_status.argtypes = [_P, _P]
+        L.cg_get_status.restype = ctypes.c_int
         for name in ("cg_encode_tokens_bound_words", "cg_encode_tokens_workspace_bytes",
                      "cg_decode_tokens_workspace_bytes"):
             getattr(L, name).argtypes = [PP]
@@ -233,16 +239,27 @@ def cg_decode_streamed(p: CodecParams, words_host, offsets_host, words_dev, offs
                        chunk_level, cdf_anchor, cdf_delta, kv_out, link_gbps: float,
                        decode_stream, copy_stream) -> dict:
     """Decode chunk by chunk while the payload is copied from (pinned) host memory; returns
-    the call's timings (cg_stream_stats as a dict). Synchronous."""
+    the call's timings (cg_stream_stats as a dict, with the per-chunk event times as lists).
+    Synchronous."""
     s, keep = p.c()
+    nc = cg_num_chunks(p)
+    per = [np.zeros(max(nc, 1), np.float64) for _ in range(3)]
     st = StreamStats()
+    dp = ctypes.POINTER(ctypes.c_double)
+    st.chunk_copy_done_ms = per[0].ctypes.data_as(dp)
+    st.chunk_decode_begin_ms = per[1].ctypes.data_as(dp)
+    st.chunk_decode_end_ms = per[2].ctypes.data_as(dp)
     _check(lib().cg_decode_streamed(ctypes.byref(s), _ptr(words_host), _ptr(offsets_host),
                                     _ptr(words_dev), words_dev.numel(), _ptr(offsets_dev),
                                     _ptr(scales),
                                     _ptr(chunk_level), _ptr(cdf_anchor), _ptr(cdf_delta),
                                     _ptr(kv_out), float(link_gbps), _stream(decode_stream),
                                     _stream(copy_stream), ctypes.byref(st)), "cg_decode_streamed")
-    return st.as_dict()
+    d = st.as_dict()
+    d["chunk_copy_done_ms"] = per[0][:nc].tolist()
+    d["chunk_decode_begin_ms"] = per[1][:nc].tolist()
+    d["chunk_decode_end_ms"] = per[2][:nc].tolist()
+    return d
 
 
 def cg_adapt_schedule(level_bytes, text_bytes, recompute_ms, slo_ms: float, prior_gbps: float,
@@ -261,6 +278,15 @@ def cg_adapt_schedule(level_bytes, text_bytes, recompute_ms, slo_ms: float, prio
     _check(lib().cg_adapt_schedule(ctypes.byref(a), bw.ctypes.data, choices.ctypes.data,
                                    ctypes.byref(ttft)), "cg_adapt_schedule")
     return choices.tolist(), ttft.value
+
+
+def cg_get_status(workspace, stream=None) -> int:
+    """Status word of the last cg_encode into `workspace`: 0 (CG_OK) or -4 (CG_ERR_NONFINITE).
+    Synchronises the stream."""
+    rc = lib().cg_get_status(_ptr(workspace), _stream(stream))
+    if rc not in (CG_OK, -4):
+        _check(rc, "cg_get_status")
+    return rc
 
 
 def cg_check_finite(p: CodecParams, kv, flag, stream=None) -> bool:
@@ -333,7 +359,6 @@ class Codec:
         self.bound_words = cg_encode_bound_words(params)
         self.ws_bytes = cg_encode_workspace_bytes(params)
         self._ws = None
-        self._words = None
 
     def _empty(self, shape, dtype):
         return self.torch.empty(shape, dtype=dtype, device=self.device)
@@ -353,13 +378,18 @@ class Codec:
             self._ws = self._empty((self.ws_bytes,), self.torch.uint8)
         return self._ws
 
+    def status(self, stream=None) -> int:
+        """Status of the last encode: 0 (CG_OK) or -4 (CG_ERR_NONFINITE); synchronises."""
+        return cg_get_status(self.workspace(), stream)
+
     def encode(self, kv, chunk_level, cdf_anchor, cdf_delta, stream=None, words=None):
-        """Returns (words [bound], offsets [S+1], scales [S]); offsets[S] is the payload length."""
+        """Returns (words [bound], offsets [S+1], scales [S]); offsets[S] is the payload length.
+        Every call returns new tensors: the payload goes into `words` when given (the caller
+        then owns its reuse), else into a fresh buffer. The encode workspace is kept and
+        reused across calls (its contents do not outlive a call)."""
         t = self.torch
         if words is None:
-            if self._words is None:
-                self._words = self._empty((self.bound_words,), t.int32)
-            words = self._words
+            words = self._empty((self.bound_words,), t.int32)
         offsets = self._empty((self.n_streams + 1,), t.int64)
         scales = self._empty((self.n_streams,), t.float32)
         cg_encode(self.p, kv, chunk_level, cdf_anchor, cdf_delta, words, offsets, scales,

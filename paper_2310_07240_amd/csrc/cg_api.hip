@@ -94,7 +94,7 @@ int cg_fit_cdf(const cg_params* p, const uint16_t* kv_f16, int32_t level, uint16
   if (rc != CG_OK) return rc;
   if (!kv_f16 || !cdf_delta_level) return CG_ERR_ARG;
   if (level < 0 || level >= K.NLV) return CG_ERR_ARG;
-  if (!aligned(cdf_delta_level, 8) || (cdf_anchor && !aligned(cdf_anchor, 8)) ||
+  if (!aligned(cdf_delta_level, 16) || (cdf_anchor && !aligned(cdf_anchor, 16)) ||
       !aligned(kv_f16, 2))
     return CG_ERR_ARG;
   return cg_launch_fit(K, kv_f16, level, cdf_anchor, cdf_delta_level, stream) == hipSuccess
@@ -110,7 +110,7 @@ int cg_fit_cdf_global(const cg_params* p, const uint16_t* kv_f16, int32_t level,
   if (rc != CG_OK) return rc;
   if (!kv_f16 || !cdf_delta_level || !workspace) return CG_ERR_ARG;
   if (level < 0 || level >= K.NLV) return CG_ERR_ARG;
-  if (!aligned(cdf_delta_level, 8) || (cdf_anchor && !aligned(cdf_anchor, 8)) ||
+  if (!aligned(cdf_delta_level, 16) || (cdf_anchor && !aligned(cdf_anchor, 16)) ||
       !aligned(kv_f16, 2) || !aligned(workspace, 256))
     return CG_ERR_ARG;
   if (workspace_bytes < CG_FIT_GLOBAL_WORKSPACE_BYTES) return CG_ERR_CAPACITY;
@@ -131,7 +131,8 @@ int cg_encode(const cg_params* p, const uint16_t* kv_f16, const uint8_t* chunk_l
       !workspace)
     return CG_ERR_ARG;
   if (!aligned(workspace, 256) || !aligned(offsets, 8) || !aligned(words, 4) ||
-      !aligned(scales, 4))
+      !aligned(scales, 4) || !aligned(kv_f16, 2) || !aligned(cdf_anchor, 16) ||
+      !aligned(cdf_delta, 16))
     return CG_ERR_ARG;
   if (words_cap < cg_encode_bound_words(p)) return CG_ERR_CAPACITY;
   const uint32_t slot = slot_words_for(K);
@@ -153,7 +154,7 @@ int cg_decode(const cg_params* p, const uint32_t* words, const uint64_t* offsets
     return CG_ERR_ARG;
   if (chunk_begin < 0 || chunk_end > K.NC || chunk_begin > chunk_end) return CG_ERR_ARG;
   if (!aligned(cdf_anchor, 16) || !aligned(cdf_delta, 16) || !aligned(offsets, 8) ||
-      !aligned(words, 4) || !aligned(kv_out_f16, 2))
+      !aligned(words, 4) || !aligned(scales, 4) || !aligned(kv_out_f16, 2))
     return CG_ERR_ARG;
   if (chunk_begin == chunk_end) return CG_OK;
   return cg_launch_decode(K, words, offsets, scales, chunk_level, cdf_anchor, cdf_delta,
@@ -196,7 +197,8 @@ int cg_encode_tokens(const cg_params* p, const uint16_t* kv_f16, const uint8_t* 
       !workspace)
     return CG_ERR_ARG;
   if (!aligned(workspace, 256) || !aligned(offsets, 8) || !aligned(words, 4) ||
-      !aligned(scales, 4) || !aligned(kv_f16, 2))
+      !aligned(scales, 4) || !aligned(kv_f16, 2) || !aligned(cdf_anchor, 16) ||
+      !aligned(cdf_delta, 16))
     return CG_ERR_ARG;
   if (words_cap < cg_encode_tokens_bound_words(p)) return CG_ERR_CAPACITY;
   if (workspace_bytes < cg_encode_tokens_ws_layout(K).total) return CG_ERR_CAPACITY;
@@ -218,7 +220,8 @@ int cg_decode_tokens(const cg_params* p, const uint32_t* words, const uint64_t* 
       !kv_out_f16 || !workspace)
     return CG_ERR_ARG;
   if (!aligned(cdf_anchor, 16) || !aligned(cdf_delta, 16) || !aligned(offsets, 8) ||
-      !aligned(words, 4) || !aligned(kv_out_f16, 2) || !aligned(workspace, 256))
+      !aligned(words, 4) || !aligned(scales, 4) || !aligned(kv_out_f16, 2) ||
+      !aligned(workspace, 256))
     return CG_ERR_ARG;
   if (workspace_bytes < cg_decode_tokens_workspace_bytes(p)) return CG_ERR_CAPACITY;
   return cg_launch_decode_tokens(K, words, offsets, scales, chunk_level, cdf_anchor, cdf_delta,
@@ -242,8 +245,8 @@ int cg_decode_streamed(const cg_params* p, const uint32_t* words_host,
       !chunk_level_dev || !cdf_anchor_dev || !cdf_delta_dev || !kv_out_dev)
     return CG_ERR_ARG;
   if (!aligned(cdf_anchor_dev, 16) || !aligned(cdf_delta_dev, 16) || !aligned(offsets_dev, 8) ||
-      !aligned(words_dev, 4) || !aligned(kv_out_dev, 2) || !aligned(words_host, 4) ||
-      !aligned(offsets_host, 8))
+      !aligned(words_dev, 4) || !aligned(scales_dev, 4) || !aligned(kv_out_dev, 2) ||
+      !aligned(words_host, 4) || !aligned(offsets_host, 8))
     return CG_ERR_ARG;
   const int NC = K.NC;
   const int64_t per_chunk = (int64_t)K.L * 2 * K.C;   // streams of one (context, chunk)
@@ -310,6 +313,13 @@ int cg_decode_streamed(const cg_params* p, const uint32_t* words_host,
     for (int c = 0; timed && c < NC; ++c) {
       timed = hipEventElapsedTime(&d, ev_dbeg(c), ev_dend(c)) == hipSuccess;
       dsum += d;
+      float tc = 0.0f, tb = 0.0f, te = 0.0f;
+      timed = timed && hipEventElapsedTime(&tc, ev0, ev_copy(c)) == hipSuccess &&
+              hipEventElapsedTime(&tb, ev0, ev_dbeg(c)) == hipSuccess &&
+              hipEventElapsedTime(&te, ev0, ev_dend(c)) == hipSuccess;
+      if (stats->chunk_copy_done_ms) stats->chunk_copy_done_ms[c] = tc;
+      if (stats->chunk_decode_begin_ms) stats->chunk_decode_begin_ms[c] = tb;
+      if (stats->chunk_decode_end_ms) stats->chunk_decode_end_ms[c] = te;
     }
     stats->n_chunks = NC;
     stats->transfer_ms = tx;
@@ -364,6 +374,15 @@ int cg_adapt_schedule(const cg_adapt_params* a, const double* bandwidth_gbps,
   }
   *ttft_ms_out = elapsed;
   return CG_OK;
+}
+
+int cg_get_status(const void* workspace, hipStream_t stream) {
+  if (!workspace || !aligned(workspace, 256)) return CG_ERR_ARG;
+  uint32_t h = 0;
+  if (hipMemcpyAsync(&h, workspace, 4, hipMemcpyDeviceToHost, stream) != hipSuccess)
+    return CG_ERR_HIP;
+  if (hipStreamSynchronize(stream) != hipSuccess) return CG_ERR_HIP;
+  return h ? CG_ERR_NONFINITE : CG_OK;
 }
 
 int cg_check_finite(const cg_params* p, const uint16_t* kv_f16, uint32_t* flag_dev,

@@ -152,9 +152,9 @@ hipError_t cg_launch_decode(const KParams& P, const uint32_t* words, const uint6
                             int c_end, uint16_t* out, hipStream_t st);
 hipError_t cg_launch_check_finite(const uint16_t* kv, int64_t n, uint32_t* flag, hipStream_t st);
 
-// Workspace layout of cg_encode (byte offsets, 256-aligned).
+// Workspace layout of cg_encode (byte offsets, 256-aligned). The status word sits at offset 0.
 struct EncWorkspace {
-  uint64_t slots_off, lens_off, partial_off, total;
+  uint64_t status_off, wflags_off, slots_off, lens_off, partial_off, total;
 };
 EncWorkspace cg_encode_ws_layout(const KParams& P, uint32_t slot_words);
 

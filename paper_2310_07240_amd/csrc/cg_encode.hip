@@ -228,7 +228,7 @@ __global__ __launch_bounds__(1024) void encode_kernel(
     KParams P, const uint16_t* __restrict__ kv, const uint8_t* __restrict__ chunk_level,
     const uint16_t* __restrict__ cdfA, const uint16_t* __restrict__ cdfD,
     uint32_t* __restrict__ slots, uint32_t slot_words, uint32_t* __restrict__ lens,
-    float* __restrict__ scales, int nw, int nu, int nsets_lds) {
+    float* __restrict__ scales, uint32_t* __restrict__ wflags, int nw, int nu, int nsets_lds) {
   // workgroup = nu units (layer, K/V, 64-channel block) x nw (context, chunk) pairs; wave w
   // codes pair slot w / nu of unit w % nu (one workgroup per CU where the grid allows, so the
   // hardware spreads its waves evenly over the SIMDs). The anchor tables of the units are
@@ -241,6 +241,7 @@ __global__ __launch_bounds__(1024) void encode_kernel(
   __shared__ uint8_t s_nsets[kEncMaxUnits];
   __shared__ uint8_t s_simd[kEncMaxWaves];   // SIMD of each wave
   __shared__ int s_left[kEncMaxWaves];   // symbols each wave has left to code
+  __shared__ uint32_t s_bad;               // some stream of the workgroup holds NaN or Inf
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int nwaves = blockDim.x >> 6;
   const int u = wave % nu, j = wave / nu;
@@ -261,6 +262,7 @@ __global__ __launch_bounds__(1024) void encode_kernel(
 
   const int simd = (int)((__builtin_amdgcn_s_getreg((31 << 11) | 4) >> 4) & 3u);   // HW_ID
   if (threadIdx.x < nu) s_mask[threadIdx.x] = 0u;
+  if (threadIdx.x == 0) s_bad = 0u;
   if (lane == 0) {
     s_simd[wave] = simd;
     lds_put(&s_left[wave], n);
@@ -328,13 +330,16 @@ __global__ __launch_bounds__(1024) void encode_kernel(
   const bool coop = nu == 4 && (ublk + 1) * nu <= n_units && cb0 + nu <= P.nblk &&
                     (cb0 + nu) * 64 <= P.C && (grp + 1) * nw <= n_pairs && (P.C & 3) == 0 &&
                     (reinterpret_cast<uintptr_t>(kv) & 7) == 0;   // 8-byte aligned row loads
-  float mx_coop = 0.0f;
+  // The maximum is taken over the magnitude bits (x & 0x7fff) as integers: for finite halves
+  // their order is the order of |x|, and NaN or Inf (exponent all ones) gives a maximum of at
+  // least 0x7c00, which flags the stream as outside the quantizer's domain.
+  uint32_t mx_coop = 0u;
   if (coop) {
-    float* part = reinterpret_cast<float*>(tabs + nu * nsets_lds * 64 * kEncTabStride);
+    uint32_t* part = reinterpret_cast<uint32_t*>(tabs + nu * nsets_lds * 64 * kEncTabStride);
     const uint16_t* xr = kv + cg_elem(P, b, l, k, c * P.CL, cb0 * 64) + 4 * lane;
     const int64_t rs4 = P.C;
     const int nr = (n - u + 3) / 4;   // rows u, u + 4, ... below n
-    float m0 = 0.0f, m1 = 0.0f, m2 = 0.0f, m3 = 0.0f;
+    uint32_t m0 = 0u, m1 = 0u, m2 = 0u, m3 = 0u;
     for (int i0 = 0; i0 < nr; i0 += 16) {
       uint2 v[16];
 #pragma unroll
@@ -342,16 +347,16 @@ __global__ __launch_bounds__(1024) void encode_kernel(
         v[q] = *reinterpret_cast<const uint2*>(xr + (int64_t)(u + 4 * min(i0 + q, nr - 1)) * rs4);
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
-        m0 = fmaxf(m0, fabsf(cg_h2f((uint16_t)(v[q].x & 0xFFFFu))));
-        m1 = fmaxf(m1, fabsf(cg_h2f((uint16_t)(v[q].x >> 16))));
-        m2 = fmaxf(m2, fabsf(cg_h2f((uint16_t)(v[q].y & 0xFFFFu))));
-        m3 = fmaxf(m3, fabsf(cg_h2f((uint16_t)(v[q].y >> 16))));
+        m0 = max(m0, v[q].x & 0x7FFFu);
+        m1 = max(m1, (v[q].x >> 16) & 0x7FFFu);
+        m2 = max(m2, v[q].y & 0x7FFFu);
+        m3 = max(m3, (v[q].y >> 16) & 0x7FFFu);
       }
     }
-    *reinterpret_cast<float4*>(part + (j * nu + u) * 256 + 4 * lane) = make_float4(m0, m1, m2, m3);
+    *reinterpret_cast<uint4*>(part + (j * nu + u) * 256 + 4 * lane) = make_uint4(m0, m1, m2, m3);
     __syncthreads();
 #pragma unroll
-    for (int u2 = 0; u2 < 4; ++u2) mx_coop = fmaxf(mx_coop, part[(j * nu + u2) * 256 + u * 64 + lane]);
+    for (int u2 = 0; u2 < 4; ++u2) mx_coop = max(mx_coop, part[(j * nu + u2) * 256 + u * 64 + lane]);
     __syncthreads();   // the ring area is free again before any wave codes
   }
 
@@ -386,11 +391,14 @@ __global__ __launch_bounds__(1024) void encode_kernel(
   const uint16_t* x = kv + cg_elem(P, b, l, k, t0, ch);
   const int64_t rs = P.C;
 
-  float mx = mx_coop;
+  uint32_t mbits = mx_coop;
   if (!coop && lane_ok) {
 #pragma unroll 16
-    for (int t = 0; t < n; ++t) mx = fmaxf(mx, fabsf(cg_h2f(x[(int64_t)t * rs])));
+    for (int t = 0; t < n; ++t) mbits = max(mbits, (uint32_t)x[(int64_t)t * rs] & 0x7FFFu);
   }
+  if (__builtin_amdgcn_ballot_w64(lane_ok && mbits >= 0x7C00u) != 0ull && lane == 0)
+    atomicOr(&s_bad, 1u);
+  const float mx = cg_h2f((uint16_t)mbits);
   const float s = (mx == 0.0f) ? 1.0f : mx / 127.0f;
   if (lane_ok) scales[sidx] = s;
   constexpr int kPipe = kG > 0 ? kG : 8;
@@ -546,6 +554,7 @@ __global__ __launch_bounds__(1024) void encode_kernel(
   }
   // the delta tables replace the anchor tables
   __syncthreads();
+  if (threadIdx.x == 0) wflags[blockIdx.x] = s_bad;   // every workgroup writes its flag
   stage(false);
   __syncthreads();
   if (!lane_ok) return;
@@ -603,10 +612,21 @@ __global__ __launch_bounds__(kScanThreads) void scan_reduce(const uint32_t* __re
   if (threadIdx.x == 0) partial[blockIdx.x] = t;
 }
 
-// Exclusive scan of nb block totals in place, by one workgroup.
+// Exclusive scan of nb block totals in place, by one workgroup. With `status` given, also the
+// OR of the encode workgroups' n_wg non-finite flags into *status (written unconditionally, so
+// no clearing is needed between calls).
 __global__ __launch_bounds__(kScanThreads) void scan_top(uint64_t* __restrict__ partial,
-                                                         int64_t nb) {
+                                                         int64_t nb,
+                                                         const uint32_t* __restrict__ wflags,
+                                                         int64_t n_wg,
+                                                         uint32_t* __restrict__ status) {
   __shared__ uint64_t sh[kScanThreads / 64];
+  if (status) {
+    uint32_t bad = 0u;
+    for (int64_t i = threadIdx.x; i < n_wg; i += kScanThreads) bad |= wflags[i];
+    bad = __syncthreads_or(bad != 0u);
+    if (threadIdx.x == 0) *status = bad ? 1u : 0u;
+  }
   const int64_t per = (nb + kScanThreads - 1) / kScanThreads;
   const int64_t begin = threadIdx.x * per;
   const int64_t end = min(begin + per, nb);
@@ -843,16 +863,55 @@ __global__ __launch_bounds__(256) void compact_kernel(KParams P, const uint32_t*
 
 inline uint64_t align256(uint64_t x) { return (x + 255) & ~(uint64_t)255; }
 
+
+// Launch geometry of encode_kernel: nw (context, chunk) pairs x nu units per workgroup, g1
+// workgroups, lds bytes of dynamic LDS, nsets delta-table sets per unit.
+struct EncGeom {
+  int nw, nu, nsets;
+  int64_t n_groups, g1;
+  size_t lds;
+};
+
+EncGeom enc_geometry(const KParams& P) {
+  EncGeom g;
+  const int64_t n_pairs = (int64_t)P.B * P.NC;
+  int nw = (int)(n_pairs < kEncMaxWaves ? n_pairs : kEncMaxWaves);
+  auto lds_for = [&](int w, int nu) {
+    const int sets = w < P.NLV ? w : P.NLV;
+    return (size_t)nu * sets * 64 * kEncTabStride * sizeof(uint16_t) +
+           (size_t)nu * w * kRing * 64 * sizeof(uint32_t);
+  };
+  while (nw > 1 && lds_for(nw, 1) > kEncLdsBudget) --nw;
+  const int64_t n_groups = (n_pairs + nw - 1) / nw;
+  const int64_t n_units = (int64_t)P.L * 2 * P.nblk;
+  // several units per workgroup while the grid still covers every CU
+  int nu = 1;
+  while (nu < kEncMaxUnits && (nu + 1) * nw <= kEncMaxWaves &&
+         lds_for(nw, nu + 1) <= kEncLdsBudget && (n_units + nu) / (nu + 1) * n_groups >= 256)
+    ++nu;
+  g.nw = nw;
+  g.nu = nu;
+  g.nsets = nw < P.NLV ? nw : P.NLV;
+  g.n_groups = n_groups;
+  g.g1 = (n_units + nu - 1) / nu * n_groups;
+  g.lds = lds_for(nw, nu);
+  return g;
+}
+
 }  // namespace
 
+// Workspace: the status word (offset 0, read by cg_get_status), the encode workgroups'
+// non-finite flags, one worst-case slot per lane of every (row, 64-channel block) wave (lanes
+// past C included), per-stream word counts, and the scan's block totals.
 EncWorkspace cg_encode_ws_layout(const KParams& P, uint32_t slot_words) {
   EncWorkspace w;
   const int64_t S = P.S;
   const int64_t nb = (S + kScanBlock - 1) / kScanBlock;
-  // one slot per lane of every (row, 64-channel block) wave, lanes past C included
   const uint64_t slot_lanes = (uint64_t)P.B * P.NC * P.L * 2 * P.nblk * 64;
-  w.slots_off = 0;
-  w.lens_off = align256(slot_lanes * slot_words * 4ull);
+  w.status_off = 0;
+  w.wflags_off = 256;
+  w.slots_off = align256(w.wflags_off + (uint64_t)enc_geometry(P).g1 * 4ull);
+  w.lens_off = align256(w.slots_off + slot_lanes * slot_words * 4ull);
   w.partial_off = align256(w.lens_off + (uint64_t)S * 4ull);
   w.total = align256(w.partial_off + (uint64_t)(nb > 0 ? nb : 1) * 8ull);
   return w;
@@ -864,46 +923,32 @@ hipError_t cg_launch_encode(const KParams& P, const uint16_t* kv, const uint8_t*
                             uint32_t slot_words, hipStream_t st) {
   const EncWorkspace lay = cg_encode_ws_layout(P, slot_words);
   uint8_t* base = static_cast<uint8_t*>(ws);
+  uint32_t* status = reinterpret_cast<uint32_t*>(base + lay.status_off);
+  uint32_t* wflags = reinterpret_cast<uint32_t*>(base + lay.wflags_off);
   uint32_t* slots = reinterpret_cast<uint32_t*>(base + lay.slots_off);
   uint32_t* lens = reinterpret_cast<uint32_t*>(base + lay.lens_off);
   uint64_t* partial = reinterpret_cast<uint64_t*>(base + lay.partial_off);
 
-  const int64_t n_pairs = (int64_t)P.B * P.NC;
-  int nw = (int)(n_pairs < kEncMaxWaves ? n_pairs : kEncMaxWaves);
-  auto lds_for = [&](int w, int nu) {
-    const int sets = w < P.NLV ? w : P.NLV;
-    return (size_t)nu * sets * 64 * kEncTabStride * sizeof(uint16_t) +
-           (size_t)nu * w * kRing * 64 * sizeof(uint32_t);
-  };
-  while (nw > 1 && lds_for(nw, 1) > kEncLdsBudget) --nw;
-  const int64_t n_groups = (n_pairs + nw - 1) / nw;
-  const int nsets_max = nw < P.NLV ? nw : P.NLV;
-  const int64_t n_units = (int64_t)P.L * 2 * P.nblk;
-  // several units per workgroup while the grid still covers every CU
-  int nu = 1;
-  while (nu < kEncMaxUnits && (nu + 1) * nw <= kEncMaxWaves &&
-         lds_for(nw, nu + 1) <= kEncLdsBudget && (n_units + nu) / (nu + 1) * n_groups >= 256)
-    ++nu;
-  const size_t lds = lds_for(nw, nu);
+  const EncGeom g = enc_geometry(P);
   const void* kfn = P.G == 10 ? (const void*)encode_kernel<10> : (const void*)encode_kernel<0>;
   hipError_t e =
-      hipFuncSetAttribute(kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      hipFuncSetAttribute(kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)g.lds);
   if (e != hipSuccess) return e;
-  const int64_t g1 = (n_units + nu - 1) / nu * n_groups;
   if (P.G == 10)
-    hipLaunchKernelGGL(encode_kernel<10>, dim3((unsigned)g1), dim3(64 * nw * nu), lds, st, P,
-                       kv, chunk_level, cdf_anchor, cdf_delta, slots, slot_words, lens, scales,
-                       nw, nu, nsets_max);
+    hipLaunchKernelGGL(encode_kernel<10>, dim3((unsigned)g.g1), dim3(64 * g.nw * g.nu), g.lds,
+                       st, P, kv, chunk_level, cdf_anchor, cdf_delta, slots, slot_words, lens,
+                       scales, wflags, g.nw, g.nu, g.nsets);
   else
-    hipLaunchKernelGGL(encode_kernel<0>, dim3((unsigned)g1), dim3(64 * nw * nu), lds, st, P,
-                       kv, chunk_level, cdf_anchor, cdf_delta, slots, slot_words, lens, scales,
-                       nw, nu, nsets_max);
+    hipLaunchKernelGGL(encode_kernel<0>, dim3((unsigned)g.g1), dim3(64 * g.nw * g.nu), g.lds,
+                       st, P, kv, chunk_level, cdf_anchor, cdf_delta, slots, slot_words, lens,
+                       scales, wflags, g.nw, g.nu, g.nsets);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t nb = (P.S + kScanBlock - 1) / kScanBlock;
   hipLaunchKernelGGL(scan_reduce, dim3((unsigned)nb), dim3(kScanThreads), 0, st, lens, P.S,
                      partial);
-  hipLaunchKernelGGL(scan_top, dim3(1), dim3(kScanThreads), 0, st, partial, nb);
+  hipLaunchKernelGGL(scan_top, dim3(1), dim3(kScanThreads), 0, st, partial, nb,
+                     (const uint32_t*)wflags, g.g1, status);
   hipLaunchKernelGGL(scan_finish, dim3((unsigned)nb), dim3(kScanThreads), 0, st, lens, P.S,
                      partial, offsets);
   const int64_t groups = (int64_t)P.B * P.NC * P.L * 2 * P.nblk;
@@ -958,7 +1003,8 @@ hipError_t cg_launch_encode_tokens(const KParams& P, const uint16_t* kv,
   const int64_t nb = (St + kScanBlock - 1) / kScanBlock;
   hipLaunchKernelGGL(scan_reduce, dim3((unsigned)nb), dim3(kScanThreads), 0, st, lens, St,
                      partial);
-  hipLaunchKernelGGL(scan_top, dim3(1), dim3(kScanThreads), 0, st, partial, nb);
+  hipLaunchKernelGGL(scan_top, dim3(1), dim3(kScanThreads), 0, st, partial, nb,
+                     (const uint32_t*)nullptr, (int64_t)0, (uint32_t*)nullptr);
   hipLaunchKernelGGL(scan_finish, dim3((unsigned)nb), dim3(kScanThreads), 0, st, lens, St,
                      partial, offsets);
   hipLaunchKernelGGL(compact_kernel<true>, dim3((unsigned)lay.n_groups), dim3(256), 0, st, P,

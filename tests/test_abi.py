@@ -119,3 +119,39 @@ def test_token_layout_size_queries_and_host_validation():
                                 dws - 1, None) == -3
     assert lib.cg_decode_tokens(ctypes.byref(s), fake, fake, fake, fake, fake, fake, None, fake,
                                 dws, None) == -1
+
+
+def test_alignment_is_checked_the_same_way_everywhere():
+    """Tables need 16-byte alignment in every call that takes them (the fit writes what the
+    decoder later reads with 16-byte loads), scales 4 bytes, offsets 8; decided on the host."""
+    lib = cg.lib()
+    p = P()
+    s, keep = p.c()
+    A = 1 << 20
+    ok, t8, odd2 = ctypes.c_void_p(A), ctypes.c_void_p(A + 8), ctypes.c_void_p(A + 2)
+    # fit: tables 8-byte aligned are rejected (anchor or delta), 16-byte aligned accepted up to
+    # the launch (not reached: the level is out of range)
+    assert lib.cg_fit_cdf(ctypes.byref(s), ok, 0, t8, ok, None) == -1
+    assert lib.cg_fit_cdf(ctypes.byref(s), ok, 0, None, t8, None) == -1
+    assert lib.cg_fit_cdf(ctypes.byref(s), ok, 5, ok, ok, None) == -1
+    ws = ctypes.c_void_p(A)
+    assert lib.cg_fit_cdf_global(ctypes.byref(s), ok, 0, None, t8, ws, 8192, None) == -1
+    # encode: misaligned tables
+    bound = cg.cg_encode_bound_words(p)
+    wsb = cg.cg_encode_workspace_bytes(p)
+    assert lib.cg_encode(ctypes.byref(s), ok, ok, t8, ok, ok, bound, ok, ok, ws, wsb, None) == -1
+    assert lib.cg_encode(ctypes.byref(s), ok, ok, ok, t8, ok, bound, ok, ok, ws, wsb, None) == -1
+    # decode: misaligned scales, tables, offsets
+    assert lib.cg_decode(ctypes.byref(s), ok, ok, odd2, ok, ok, ok, 0, 1, ok, None) == -1
+    assert lib.cg_decode(ctypes.byref(s), ok, ok, ok, ok, t8, ok, 0, 1, ok, None) == -1
+    assert lib.cg_decode(ctypes.byref(s), ok, ctypes.c_void_p(A + 4), ok, ok, ok, ok, 0, 1, ok,
+                         None) == -1
+    # streamed decode: misaligned device scales
+    assert lib.cg_decode_streamed(ctypes.byref(s), ok, ok, ok, 1 << 20, ok, odd2, ok, ok, ok, ok,
+                                  0.0, None, None, None) == -1
+    # token layout decode: misaligned scales
+    dws = cg.cg_decode_tokens_workspace_bytes(p)
+    assert lib.cg_decode_tokens(ctypes.byref(s), ok, ok, odd2, ok, ok, ok, ok, ws, dws, None) == -1
+    # status: null or misaligned workspace
+    assert lib.cg_get_status(None, None) == -1
+    assert lib.cg_get_status(ctypes.c_void_p(A + 16), None) == -1

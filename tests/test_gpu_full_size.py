@@ -1,10 +1,13 @@
 """GPU parity at the benchmark workloads' full sizes, in the launch configuration bench.py times.
 
-The Mistral-7B-shaped cache (268M elements) is compared in full. The three larger caches run in
-full on the GPU; the oracle recomputes every stream of three sampled layers (first, middle and
-last: one per layer group) from a sub-cache holding only those layers. Streams of a layer depend
-only on that layer's slab, its bin width and the chunk levels, so the sub-cache's streams, tables
-and decoded values must equal the full run's, bit for bit.
+Every workload runs in full on the GPU (fit of every level, encode, decode of the whole cache)
+and every result is compared with the oracle: tables, scales, per-stream lengths and offsets,
+payload words and decoded fp16 bit patterns. The Mistral-7B-shaped cache is compared in one
+piece. For the three larger caches the oracle runs on slabs of consecutive layers, so that host
+memory stays bounded: the streams of a layer depend only on that layer's values, its bin width
+and the chunk levels, and the tables of a (layer, K/V, channel) only on that layer's values, so
+a sub-cache holding layers [l0, l1) must reproduce the full run's tables, scales, stream words
+and decoded rows of those layers bit for bit. Together the slabs cover every layer.
 """
 import time
 
@@ -16,6 +19,8 @@ from paper_2310_07240_amd import workloads as W
 from gpu_helpers import assert_same, compare_full, run_gpu, run_oracle, say, torch_cuda
 
 pytestmark = pytest.mark.gpu
+
+SLAB_LAYERS = 8
 
 
 @pytest.mark.timeout(600)
@@ -30,7 +35,8 @@ def test_mistral7b_4k_full_bit_exact():
     say(f"{w.name}: bits/element {g['words'].size * 32 / w.n_elem:.3f}")
 
 
-def _gpu_full_run(w, kv_np, layers):
+def _gpu_full_run(w, kv_np):
+    """Fit, encode and decode the whole cache on the GPU; every result back as numpy."""
     torch = torch_cuda()
     from paper_2310_07240_amd.cachegen import Codec, CodecParams
     codec = Codec(CodecParams.of(w))
@@ -43,55 +49,67 @@ def _gpu_full_run(w, kv_np, layers):
     say(f"{w.name}: encode")
     words, offsets, scales = codec.encode(kv, cl, ca, cd)
     torch.cuda.synchronize()
+    del kv
     say(f"{w.name}: decode")
     out = codec.decode(words, offsets, scales, cl, ca, cd)
     torch.cuda.synchronize()
-    del kv
     say(f"{w.name}: copy back")
     off = offsets.cpu().numpy().view(np.uint64)
-    idx = torch.tensor(layers, device=out.device)
-    res = dict(ca=ca[idx].cpu().numpy().view(np.uint16),
-               cd=cd[:, idx].cpu().numpy().view(np.uint16),
+    res = dict(ca=ca.cpu().numpy().view(np.uint16), cd=cd.cpu().numpy().view(np.uint16),
                offsets=off, scales=scales.cpu().numpy(),
-               words=words[: int(off[-1])].cpu().numpy().view(np.uint32),
-               out=out[:, idx].cpu().numpy().view(np.uint16))
-    del out, words
+               words=words[: int(off[-1])].cpu().numpy().view(np.uint32))
+    res["out"] = out.cpu().numpy().view(np.uint16)
+    del out, words, offsets, scales, ca, cd
     torch.cuda.empty_cache()
     return res
+
+
+def _compare_slab(w, g, o, l0, l1):
+    """The oracle's results on the sub-cache of layers [l0, l1) against the full GPU run."""
+    B, NC, L, C = w.n_ctx, w.n_chunks, w.n_layers, w.n_channels
+    Ls = l1 - l0
+    tag = f"layers {l0}-{l1 - 1}"
+    assert_same(f"cdf_anchor ({tag})", g["ca"][l0:l1], o["ca"])
+    assert_same(f"cdf_delta ({tag})", g["cd"][:, l0:l1], o["cd"])
+    assert_same(f"decoded fp16 ({tag})", g["out"][:, l0:l1], o["out"])
+    goff, ooff = g["offsets"].astype(np.int64), o["offsets"].astype(np.int64)
+    per = Ls * 2 * C                       # streams of one (context, chunk) in the slab
+    for b in range(B):
+        for c in range(NC):
+            s_full = ((b * NC + c) * L + l0) * 2 * C
+            s_sub = (b * NC + c) * per
+            assert_same(f"stream lengths b{b} c{c} ({tag})",
+                        np.diff(goff[s_full:s_full + per + 1]),
+                        np.diff(ooff[s_sub:s_sub + per + 1]))
+            assert_same(f"scales b{b} c{c} ({tag})", g["scales"][s_full:s_full + per],
+                        o["scales"][s_sub:s_sub + per])
+            assert_same(f"words b{b} c{c} ({tag})", g["words"][goff[s_full]:goff[s_full + per]],
+                        o["words"][ooff[s_sub]:ooff[s_sub + per]])
 
 
 @pytest.mark.timeout(900)
 @pytest.mark.parametrize("name", ["llama2_7b_mha_t8192", "llama2_70b_gqa_t16384",
                                   "concurrency_32x_mistral_t2048"])
-def test_large_workload_sampled_layers_bit_exact(name):
+def test_large_workload_every_layer_bit_exact(name):
     w = W.WORKLOADS[name]
-    layers = [0, w.n_layers // 2, w.n_layers - 1]
     t = time.time()
     kv = W.generate(w)
     say(f"{w.name}: generated in {time.time() - t:.1f}s")
-    g = _gpu_full_run(w, kv, layers)
-    sub = w.with_(name=w.name + "_sampled_layers", n_layers=len(layers),
-                  layer_bin=tuple(w.layer_bin[l] for l in layers))
-    kv_sub = np.ascontiguousarray(kv[:, layers])
-    del kv
-    o = run_oracle(sub, kv_sub)
-    assert np.array_equal(sub.chunk_levels(), w.chunk_levels())
-    assert_same("cdf_anchor (sampled layers)", g["ca"], o["ca"])
-    assert_same("cdf_delta (sampled layers)", g["cd"], o["cd"])
-    assert_same("decoded fp16 (sampled layers)", g["out"], o["out"])
-    B, NC, L, C = w.n_ctx, w.n_chunks, w.n_layers, w.n_channels
-    goff, ooff = g["offsets"].astype(np.int64), o["offsets"].astype(np.int64)
-    for b in range(B):
-        for c in range(NC):
-            for li, l in enumerate(layers):
-                for k in range(2):
-                    s_full = (((b * NC + c) * L + l) * 2 + k) * C
-                    s_sub = (((b * NC + c) * len(layers) + li) * 2 + k) * C
-                    assert_same("stream lengths", np.diff(goff[s_full:s_full + C + 1]),
-                                np.diff(ooff[s_sub:s_sub + C + 1]))
-                    assert_same("scales", g["scales"][s_full:s_full + C], o["scales"][s_sub:s_sub + C])
-                    assert_same(f"words b{b} c{c} l{l} k{k}",
-                                g["words"][goff[s_full]:goff[s_full + C]],
-                                o["words"][ooff[s_sub]:ooff[s_sub + C]])
-    total_bits = int(goff[-1]) * 32
-    say(f"{w.name}: bits/element {total_bits / w.n_elem:.3f}")
+    g = _gpu_full_run(w, kv)
+    goff = g["offsets"]
+    assert goff[0] == 0 and np.all(np.diff(goff.astype(np.int64)) > 0)
+    covered = 0
+    for l0 in range(0, w.n_layers, SLAB_LAYERS):
+        l1 = min(w.n_layers, l0 + SLAB_LAYERS)
+        sub = w.with_(name=f"{w.name}_layers_{l0}_{l1}", n_layers=l1 - l0,
+                      layer_bin=tuple(w.layer_bin[l0:l1]))
+        assert np.array_equal(sub.chunk_levels(), w.chunk_levels())
+        kv_sub = np.ascontiguousarray(kv[:, l0:l1])
+        o = run_oracle(sub, kv_sub)
+        del kv_sub
+        _compare_slab(w, g, o, l0, l1)
+        covered += l1 - l0
+        say(f"{w.name}: layers {l0}-{l1 - 1} bit-exact")
+        del o
+    assert covered == w.n_layers
+    say(f"{w.name}: every layer bit-exact; bits/element {int(goff[-1]) * 32 / w.n_elem:.3f}")

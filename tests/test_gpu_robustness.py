@@ -1,0 +1,164 @@
+"""GPU: the codec's failure behaviour through the C ABI.
+
+* Non-finite input (NaN, +-Inf) is outside the quantizer's domain. The encoder detects it while
+  it takes the streams' absolute maxima and records it in the status word of its workspace
+  (cg_get_status); cg_check_finite reports it from a scan of its own. A clean encode that reuses
+  the workspace resets the word. An encode of non-finite input still writes only inside its
+  buffers and its payload stays decodable (the values are meaningless).
+* A decode writes only the token rows of the chunks it is asked for: canary values around the
+  output buffer and in the rows of other chunks stay untouched, for chunk sub-ranges, for an
+  output buffer that is 16-byte aligned or not, and for corrupt payloads.
+"""
+import numpy as np
+import pytest
+
+from paper_2310_07240_amd import workloads as W
+from gpu_helpers import assert_same, run_oracle, say, torch_cuda
+
+pytestmark = pytest.mark.gpu
+
+CANARY = 0x7BAD   # an fp16 bit pattern (a large finite value) the decoder never writes here
+
+NONFINITE = [
+    # (layer of the workload, K/V, token, channel, fp16 bits)
+    ("nan_first_token", 0, 0, 0, 0, 0x7E00),
+    ("nan_mid", 1, 1, 33, 69, 0xFE01),
+    ("pos_inf_anchor", 2, 0, 40, 5, 0x7C00),
+    ("neg_inf_last", 2, 1, 99, 64, 0xFC00),
+]
+
+
+def _codec(w):
+    torch = torch_cuda()
+    from paper_2310_07240_amd.cachegen import Codec, CodecParams
+    return torch, Codec(CodecParams.of(w))
+
+
+@pytest.mark.parametrize("case", NONFINITE, ids=lambda c: c[0])
+def test_nonfinite_input_is_reported(case):
+    name, l, k, t, ch, bits = case
+    w = W.small(name=f"nonfinite_{name}", n_tokens=100, chunk_len=48, n_channels=70)
+    torch, codec = _codec(w)
+    from paper_2310_07240_amd.cachegen import cg_check_finite, cg_get_status
+    kv_np = W.generate(w)
+    bad_np = kv_np.copy().view(np.uint16)
+    bad_np[0, l, k, t, ch] = bits
+    kv = torch.from_numpy(kv_np.view(np.int16)).cuda()
+    bad = torch.from_numpy(bad_np.view(np.int16)).cuda()
+    cl = torch.from_numpy(w.chunk_levels()).cuda()
+    flag = torch.zeros(1, dtype=torch.int32, device="cuda")
+    say(f"{name}: check_finite")
+    assert cg_check_finite(codec.p, kv, flag) is True
+    assert cg_check_finite(codec.p, bad, flag) is False
+    assert cg_check_finite(codec.p, kv, flag) is True
+
+    ca, cd = codec.fit(kv)
+    say(f"{name}: clean encode")
+    words, offsets, scales = codec.encode(kv, cl, ca, cd)
+    assert codec.status() == 0
+    say(f"{name}: encode with a non-finite value")
+    bwords, boffsets, bscales = codec.encode(bad, cl, ca, cd)
+    assert codec.status() == -4 == cg_get_status(codec.workspace())
+    # the payload is still well formed: lengths within the coder's bound, decodable
+    off = boffsets.cpu().numpy().view(np.uint64).astype(np.int64)
+    assert off[0] == 0 and np.all(np.diff(off) > 0) and off[-1] <= codec.bound_words
+    out = codec.decode(bwords, boffsets, bscales, cl, ca, cd)
+    torch.cuda.synchronize()
+    # streams other than the poisoned one decode to the clean cache's values
+    ref = codec.decode(words, offsets, scales, cl, ca, cd).cpu().numpy()
+    got = out.cpu().numpy()
+    c = t // w.chunk_len
+    t0, t1 = c * w.chunk_len, min((c + 1) * w.chunk_len, w.n_tokens)
+    mask = np.ones(ref.shape, bool)
+    mask[0, l, k, t0:t1, ch] = False
+    assert np.array_equal(got[mask], ref[mask])
+    say(f"{name}: a clean encode resets the status")
+    codec.encode(kv, cl, ca, cd)
+    assert codec.status() == 0
+
+
+def test_nonfinite_flag_with_shared_absmax():
+    """Four channel-contiguous units per workgroup: the encoder's waves split the rows of a
+    chunk for the absolute maxima (the other absmax path)."""
+    w = W.small(name="nonfinite_units4", n_layers=16, n_channels=2048, n_tokens=47,
+                chunk_len=25, level_mult=(1.0,), random_levels=False)
+    torch, codec = _codec(w)
+    kv_np = W.generate(w)
+    kv = torch.from_numpy(kv_np.view(np.int16)).cuda()
+    cl = torch.from_numpy(w.chunk_levels()).cuda()
+    ca, cd = codec.fit(kv)
+    codec.encode(kv, cl, ca, cd)
+    assert codec.status() == 0
+    for (l, k, t, ch, bits) in [(15, 1, 46, 2047, 0x7C01), (7, 0, 3, 1000, 0xFC00)]:
+        bad_np = kv_np.copy().view(np.uint16)
+        bad_np[0, l, k, t, ch] = bits
+        bad = torch.from_numpy(bad_np.view(np.int16)).cuda()
+        codec.encode(bad, cl, ca, cd)
+        assert codec.status() == -4
+    codec.encode(kv, cl, ca, cd)
+    assert codec.status() == 0
+
+
+def test_get_status_rejects_bad_workspace():
+    torch = torch_cuda()
+    from paper_2310_07240_amd import cachegen as cg
+    ws = torch.zeros(512, dtype=torch.uint8, device="cuda")
+    import ctypes
+    s = torch.cuda.current_stream()
+    assert cg.lib().cg_get_status(None, ctypes.c_void_p(s.cuda_stream)) == -1
+    assert cg.lib().cg_get_status(ctypes.c_void_p(ws.data_ptr() + 4),
+                                  ctypes.c_void_p(s.cuda_stream)) == -1
+
+
+CANARY_CASES = [
+    W.small(name="canary_c100", n_ctx=2, n_layers=3, n_tokens=130, chunk_len=40, n_channels=100),
+    W.small(name="canary_c128", n_ctx=1, n_layers=2, n_tokens=125, chunk_len=50, n_channels=128),
+]
+
+
+@pytest.mark.parametrize("pad", [64, 65], ids=["aligned", "misaligned"])
+@pytest.mark.parametrize("w", CANARY_CASES, ids=lambda w: w.name)
+def test_decode_writes_only_requested_rows(w, pad):
+    torch, codec = _codec(w)
+    kv_np = W.generate(w)
+    o = run_oracle(w, kv_np)
+    kv = torch.from_numpy(kv_np.view(np.int16)).cuda()
+    cl = torch.from_numpy(w.chunk_levels()).cuda()
+    ca, cd = codec.fit(kv)
+    words, offsets, scales = codec.encode(kv, cl, ca, cd)
+    n = w.n_elem
+    big = torch.empty(pad + n + 4096, dtype=torch.int16, device="cuda")
+    out = big[pad:pad + n].view(w.kv_shape)
+    NC = w.n_chunks
+    ranges = [(0, NC), (0, 1), (1, NC - 1), (NC - 1, NC)]
+    for c0, c1 in ranges:
+        say(f"{w.name} pad {pad}: chunks [{c0}, {c1})")
+        big.fill_(CANARY)
+        codec.decode(words, offsets, scales, cl, ca, cd, c0, c1, out=out)
+        host = big.cpu().numpy().view(np.uint16)
+        assert np.all(host[:pad] == CANARY), "canary before the output overwritten"
+        assert np.all(host[pad + n:] == CANARY), "canary after the output overwritten"
+        got = host[pad:pad + n].reshape(w.kv_shape)
+        t0, t1 = c0 * w.chunk_len, min(c1 * w.chunk_len, w.n_tokens)
+        assert_same(f"chunks {c0}:{c1}", got[..., t0:t1, :], o["out"][..., t0:t1, :])
+        rest = np.ones(w.n_tokens, bool)
+        rest[t0:t1] = False
+        assert np.all(got[..., rest, :] == CANARY), "a row outside the chunk range was written"
+    # corrupt payloads: wrong values, but still only the requested rows
+    rng = np.random.default_rng(17)
+    for kind in ("random", "ones"):
+        nw = words.numel()
+        bad = (torch.from_numpy(rng.integers(0, 2**32, nw, dtype=np.uint64).astype(np.uint32)
+                                .view(np.int32)).cuda() if kind == "random"
+               else torch.full((nw,), -1, dtype=torch.int32, device="cuda"))
+        for c0, c1 in [(0, NC), (1, 2)]:
+            say(f"{w.name} pad {pad}: corrupt payload ({kind}), chunks [{c0}, {c1})")
+            big.fill_(CANARY)
+            codec.decode(bad, offsets, scales, cl, ca, cd, c0, c1, out=out)
+            host = big.cpu().numpy().view(np.uint16)
+            assert np.all(host[:pad] == CANARY) and np.all(host[pad + n:] == CANARY)
+            got = host[pad:pad + n].reshape(w.kv_shape)
+            t0, t1 = c0 * w.chunk_len, min(c1 * w.chunk_len, w.n_tokens)
+            rest = np.ones(w.n_tokens, bool)
+            rest[t0:t1] = False
+            assert np.all(got[..., rest, :] == CANARY)

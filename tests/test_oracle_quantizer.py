@@ -145,3 +145,62 @@ def test_deltas_more_concentrated_than_values():
             return -(p * np.log2(p)).sum()
         ha.append(H(sym)); hd.append(H(sd[np.arange(1536) % 10 != 0]))
     assert np.mean(hd) < np.mean(ha)
+
+
+def test_hand_worked_groups_of_ten():
+    """Hand-worked streams (tests/golden/quant_g10_hand.txt, Sec. 5.2): anchors at 8 bits,
+    deltas against the reconstructed anchor, ties to even, the +-127 clamp."""
+    from conftest import golden_rows
+    rows = golden_rows("quant_g10_hand.txt")
+    for name, bw in (("A", 0.5), ("B", 1.5)):
+        r = [x for x in rows if x[0] == name]
+        assert [int(x[1]) for x in r] == list(range(len(r)))
+        x = np.array([float(v[2]) for v in r], np.float16)
+        assert np.array_equal(x.astype(np.float64), [float(v[2]) for v in r])   # exact fp16
+        s = oracle.stream_scale(x)
+        w = float(np.float32(np.float32(bw) * np.float32(s)))
+        sym, rec = oracle.quantize_stream(x, 10, s, w)
+        assert (sym.astype(int) - 127).tolist() == [int(v[3]) for v in r]
+        assert rec.view(np.float16).astype(np.float64).tolist() == [float(v[4]) for v in r]
+
+
+def _numpy_quantize_g10(x16, s, w):
+    """Group-of-10 quantization in numpy fp32, vectorised over the groups: anchors
+    q = rint(clip(x / s)), a = q * s; deltas q = rint(clip((x - a) / w)); reconstruction
+    fp16(a + q * w) with the product and the sum each rounded to fp32 (numpy never fuses them)."""
+    n = x16.size
+    x = x16.astype(np.float32)
+    s = np.float32(s)
+    w = np.float32(w)
+    j = np.arange(n)
+    g0 = j - j % 10                                    # the group's anchor token
+    # the quantized value is an integer: -0.0 from the rounding becomes 0 (reading of Sec. 5.2:
+    # a decoder sees only q)
+    qa = np.round(np.clip(x[g0] / s, np.float32(-127), np.float32(127))).astype(np.int64)
+    a = (qa.astype(np.float32) * s).astype(np.float32)
+    d = (x - a).astype(np.float32)
+    qd = np.round(np.clip(d / w, np.float32(-127), np.float32(127)))
+    anchor = j % 10 == 0
+    q = np.where(anchor, qa, qd).astype(np.int64)
+    prod = (q.astype(np.float32) * w).astype(np.float32)
+    out = np.where(anchor, a, (a + prod).astype(np.float32))
+    return q, out.astype(np.float16).view(np.uint16)
+
+
+@pytest.mark.parametrize("bw", [0.5, 1.0, 1.5, 4.0, 12.0])
+def test_group_of_ten_reconstruction_matches_numpy_fp32(bw):
+    """Bit-exact against an independent numpy fp32 evaluation on random streams whose scales
+    make the products inexact (a fused multiply-add or another summation order would differ)."""
+    rng = np.random.default_rng(int(bw * 10))
+    for trial in range(40):
+        n = int(rng.integers(1, 400))
+        sc = np.float32(np.exp(rng.uniform(np.log(0.01), np.log(300.0))))
+        x = (sc * (rng.standard_normal() + np.cumsum(rng.standard_normal(n) * 0.2))).astype(np.float16)
+        if trial % 5 == 0:
+            x[rng.integers(0, n, size=max(1, n // 20))] *= np.float16(-30)     # clamped deltas
+        s = oracle.stream_scale(x)
+        w = float(np.float32(np.float32(bw) * np.float32(s)))
+        sym, rec = oracle.quantize_stream(x, 10, s, w)
+        q_ref, rec_ref = _numpy_quantize_g10(x, s, w)
+        assert np.array_equal(sym.astype(np.int64) - 127, q_ref)
+        assert np.array_equal(rec, rec_ref)
