@@ -77,7 +77,9 @@ enum {
   CG_ERR_NONFINITE = -4,  /* the KV input holds NaN or +-Inf (reported by cg_get_status after
                              cg_encode, and by cg_check_finite)                             */
   CG_ERR_HIP = -5,        /* a HIP runtime call or kernel launch failed                     */
-  CG_ERR_PARAM = -6       /* a layer_bin or level_mult entry is not finite and > 0          */
+  CG_ERR_PARAM = -6,      /* a layer_bin or level_mult entry is not finite and > 0          */
+  CG_ERR_SCRATCH = -7     /* cg_encode_noalloc: the cache needs more scratch than
+                             CG_NOALLOC_SCRATCH_BYTES                                       */
 };
 
 /* cg_decode may read (but never uses) up to this many words past offsets[S]: a words buffer
@@ -166,6 +168,30 @@ int cg_encode(const cg_params* p, const uint16_t* kv_f16, const uint8_t* chunk_l
               const uint16_t* cdf_anchor, const uint16_t* cdf_delta,
               uint32_t* words, uint64_t words_cap, uint64_t* offsets, float* scales,
               void* workspace, uint64_t workspace_bytes, hipStream_t stream);
+
+/* Bytes of the static device scratch of cg_encode_noalloc (held by every GPU the library runs
+ * on until the process ends). */
+#define CG_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/* cg_encode without any device allocation by the library or the caller beyond the inputs and
+ * outputs, for callers that cannot allocate: code being captured into a HIP graph, tight
+ * serving loops, harnesses that forbid hipMalloc. Same arguments, results and errors as
+ * cg_encode, except:
+ *   - no workspace: the encoder's scratch (status word, per-workgroup flags, worst-case slots,
+ *     word counts, scan partials) is one static device buffer of CG_NOALLOC_SCRATCH_BYTES per
+ *     GPU; a cache whose scratch (cg_encode_workspace_bytes(p)) exceeds it is rejected with
+ *     CG_ERR_SCRATCH before anything is launched (e.g. a whole 1536-token chunk of 32 layers
+ *     x 1024 channels needs about 227 MB; one such layer about 7 MB);
+ *   - status: NULL, or a caller-owned device uint32_t (4-byte aligned) that receives the call's
+ *     status word (0, or non-zero if the KV held NaN or +-Inf), written unconditionally.
+ * Every call on a GPU shares that GPU's scratch, and nothing in it needs to start at any value;
+ * calls that overlap on one GPU (on different streams, or from different host threads without
+ * ordering) race and must not be issued. The first call on a device looks up the address of
+ * that device's buffer (hipGetSymbolAddress, no allocation). Asynchronous. */
+int cg_encode_noalloc(const cg_params* p, const uint16_t* kv_f16, const uint8_t* chunk_level,
+                      const uint16_t* cdf_anchor, const uint16_t* cdf_delta, uint32_t* words,
+                      uint64_t words_cap, uint64_t* offsets, float* scales, uint32_t* status,
+                      hipStream_t stream);
 
 /* Decode chunks [chunk_begin, chunk_end) of every context back to fp16 KV (Sec. 5.2; the
  * GPU decoder of Sec. 6; chunk ranges allow decoding a chunk as soon as it arrives, Sec. 6).

@@ -20,15 +20,17 @@ LIB_PATH = os.path.join(_HERE, "libcachegen.so")
 
 CG_OK = 0
 ERRORS = {-1: "CG_ERR_ARG", -2: "CG_ERR_SHAPE", -3: "CG_ERR_CAPACITY", -4: "CG_ERR_NONFINITE",
-          -5: "CG_ERR_HIP", -6: "CG_ERR_PARAM"}
+          -5: "CG_ERR_HIP", -6: "CG_ERR_PARAM", -7: "CG_ERR_SCRATCH"}
 
 EXPORTS = ("cg_num_chunks", "cg_num_streams", "cg_encode_bound_words",
            "cg_encode_workspace_bytes", "cg_fit_cdf", "cg_fit_cdf_global", "cg_encode",
            "cg_decode", "cg_decode_streamed", "cg_adapt_schedule", "cg_check_finite",
            "cg_num_token_streams", "cg_encode_tokens_bound_words",
            "cg_encode_tokens_workspace_bytes", "cg_decode_tokens_workspace_bytes",
-           "cg_encode_tokens", "cg_decode_tokens", "cg_get_status", "cg_strerror")
+           "cg_encode_tokens", "cg_decode_tokens", "cg_get_status", "cg_encode_noalloc",
+           "cg_strerror")
 CG_FIT_GLOBAL_WORKSPACE_BYTES = 8192
+CG_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 
 class CodecError(RuntimeError):
@@ -103,6 +105,8 @@ def lib():
         L.cg_check_finite.restype = ctypes.c_int
         L.cg_get_status.argtypes = [_P, _P]
         L.cg_get_status.restype = ctypes.c_int
+        L.cg_encode_noalloc.argtypes = [PP, _P, _P, _P, _P, _P, ctypes.c_uint64, _P, _P, _P, _P]
+        L.cg_encode_noalloc.restype = ctypes.c_int
         for name in ("cg_encode_tokens_bound_words", "cg_encode_tokens_workspace_bytes",
                      "cg_decode_tokens_workspace_bytes"):
             getattr(L, name).argtypes = [PP]
@@ -225,6 +229,17 @@ def cg_encode(p: CodecParams, kv, chunk_level, cdf_anchor, cdf_delta, words, off
                            _ptr(cdf_delta), _ptr(words), words.numel(), _ptr(offsets),
                            _ptr(scales), _ptr(workspace), workspace.numel() * workspace.element_size(),
                            _stream(stream)), "cg_encode")
+
+
+def cg_encode_noalloc(p: CodecParams, kv, chunk_level, cdf_anchor, cdf_delta, words, offsets,
+                      scales, status=None, stream=None):
+    """cg_encode with the library's static per-GPU scratch instead of a workspace (no device
+    allocation); `status` is an optional device int32 tensor of one element."""
+    s, keep = p.c()
+    _check(lib().cg_encode_noalloc(ctypes.byref(s), _ptr(kv), _ptr(chunk_level),
+                                   _ptr(cdf_anchor), _ptr(cdf_delta), _ptr(words), words.numel(),
+                                   _ptr(offsets), _ptr(scales), _ptr(status), _stream(stream)),
+           "cg_encode_noalloc")
 
 
 def cg_decode(p: CodecParams, words, offsets, scales, chunk_level, cdf_anchor, cdf_delta,

@@ -4,6 +4,7 @@
 #include <string.h>
 
 #include <chrono>
+#include <mutex>
 #include <thread>
 #include <vector>
 
@@ -54,6 +55,28 @@ uint32_t slot_words_for(const KParams& K) {
 }
 
 bool aligned(const void* ptr, size_t a) { return ((uintptr_t)ptr % a) == 0; }
+
+// Scratch of cg_encode_noalloc: one static device buffer per GPU (each device holds its own copy
+// of the array, at its own address, for the life of the process). Host code never uses the
+// array's name as an address: the device address of each GPU's copy is looked up once per
+// device with hipGetSymbolAddress and kept here.
+static __device__ __align__(256) uint8_t scratch[CG_NOALLOC_SCRATCH_BYTES];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's scratch, or nullptr if it cannot be found.
+void* scratch_of_current_device() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return nullptr;
+    g_scratch_ptr[dev] = ptr;
+  }
+  return g_scratch_ptr[dev];
+}
 
 }  // namespace
 
@@ -139,6 +162,30 @@ int cg_encode(const cg_params* p, const uint16_t* kv_f16, const uint8_t* chunk_l
   if (workspace_bytes < cg_encode_ws_layout(K, slot).total) return CG_ERR_CAPACITY;
   return cg_launch_encode(K, kv_f16, chunk_level, cdf_anchor, cdf_delta, words, offsets, scales,
                           workspace, slot, stream) == hipSuccess
+             ? CG_OK
+             : CG_ERR_HIP;
+}
+
+int cg_encode_noalloc(const cg_params* p, const uint16_t* kv_f16, const uint8_t* chunk_level,
+                      const uint16_t* cdf_anchor, const uint16_t* cdf_delta, uint32_t* words,
+                      uint64_t words_cap, uint64_t* offsets, float* scales, uint32_t* status,
+                      hipStream_t stream) {
+  KParams K;
+  int rc = make_kparams(p, &K);
+  if (rc != CG_OK) return rc;
+  if (!kv_f16 || !chunk_level || !cdf_anchor || !cdf_delta || !words || !offsets || !scales)
+    return CG_ERR_ARG;
+  if (!aligned(offsets, 8) || !aligned(words, 4) || !aligned(scales, 4) || !aligned(kv_f16, 2) ||
+      !aligned(cdf_anchor, 16) || !aligned(cdf_delta, 16) || (status && !aligned(status, 4)))
+    return CG_ERR_ARG;
+  if (words_cap < cg_encode_bound_words(p)) return CG_ERR_CAPACITY;
+  const uint32_t slot = slot_words_for(K);
+  if (cg_encode_ws_layout(K, slot).total > (uint64_t)CG_NOALLOC_SCRATCH_BYTES)
+    return CG_ERR_SCRATCH;
+  void* ws = scratch_of_current_device();
+  if (!ws) return CG_ERR_HIP;
+  return cg_launch_encode(K, kv_f16, chunk_level, cdf_anchor, cdf_delta, words, offsets, scales,
+                          ws, slot, stream, status) == hipSuccess
              ? CG_OK
              : CG_ERR_HIP;
 }
@@ -409,6 +456,8 @@ const char* cg_strerror(int code) {
     case CG_ERR_NONFINITE: return "KV input holds NaN or Inf";
     case CG_ERR_HIP: return "HIP runtime error";
     case CG_ERR_PARAM: return "a layer bin width or level multiplier is not finite and positive";
+    case CG_ERR_SCRATCH:
+      return "the cache needs more scratch than the static buffer of cg_encode_noalloc holds";
     default: return "unknown error code";
   }
 }

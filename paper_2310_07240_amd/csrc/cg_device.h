@@ -142,10 +142,11 @@ hipError_t cg_launch_fit(const KParams& P, const uint16_t* kv, int level, uint16
 hipError_t cg_launch_fit_global(const KParams& P, const uint16_t* kv, int level,
                                 uint16_t* cdf_anchor, uint16_t* cdf_delta_level, void* ws,
                                 hipStream_t st);
+// status_out: where the non-finite status word goes (nullptr: the workspace's first word).
 hipError_t cg_launch_encode(const KParams& P, const uint16_t* kv, const uint8_t* chunk_level,
                             const uint16_t* cdf_anchor, const uint16_t* cdf_delta,
                             uint32_t* words, uint64_t* offsets, float* scales, void* ws,
-                            uint32_t slot_words, hipStream_t st);
+                            uint32_t slot_words, hipStream_t st, uint32_t* status_out = nullptr);
 hipError_t cg_launch_decode(const KParams& P, const uint32_t* words, const uint64_t* offsets,
                             const float* scales, const uint8_t* chunk_level,
                             const uint16_t* cdf_anchor, const uint16_t* cdf_delta, int c_begin,

@@ -920,10 +920,11 @@ EncWorkspace cg_encode_ws_layout(const KParams& P, uint32_t slot_words) {
 hipError_t cg_launch_encode(const KParams& P, const uint16_t* kv, const uint8_t* chunk_level,
                             const uint16_t* cdf_anchor, const uint16_t* cdf_delta,
                             uint32_t* words, uint64_t* offsets, float* scales, void* ws,
-                            uint32_t slot_words, hipStream_t st) {
+                            uint32_t slot_words, hipStream_t st, uint32_t* status_out) {
   const EncWorkspace lay = cg_encode_ws_layout(P, slot_words);
   uint8_t* base = static_cast<uint8_t*>(ws);
-  uint32_t* status = reinterpret_cast<uint32_t*>(base + lay.status_off);
+  uint32_t* status =
+      status_out ? status_out : reinterpret_cast<uint32_t*>(base + lay.status_off);
   uint32_t* wflags = reinterpret_cast<uint32_t*>(base + lay.wflags_off);
   uint32_t* slots = reinterpret_cast<uint32_t*>(base + lay.slots_off);
   uint32_t* lens = reinterpret_cast<uint32_t*>(base + lay.lens_off);
