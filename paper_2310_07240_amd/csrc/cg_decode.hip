@@ -16,7 +16,8 @@
 //   hardware spreads evenly over the four SIMDs (several small workgroups per CU can land four
 //   waves on one SIMD and two on another, and the kernel waits for the most loaded SIMD). Wave
 //   w of a workgroup decodes pair slot w / units of unit w % units, so each SIMD gets one wave
-//   of every slot; slots follow chunk order, so with one context the last, shorter chunk is
+//   of every slot; slots are chunk-major (pair p = chunk p / B of context p % B), so the waves
+//   of a workgroup share a chunk length, and with one context the last, shorter chunk is
 //   decoded by the youngest waves (older waves issue first).
 //
 // decode_kernel (any group size): anchor fences cum[16 f] in LDS; the delta search is a 4-ary
@@ -160,16 +161,19 @@ __global__ __launch_bounds__(1024) void decode_kernel(
   const int ncr = c_end - c_begin;
   const int n_pairs = P.B * ncr;
   const int n_groups = (n_pairs + nw - 1) / nw;
-  const int grp = blockIdx.x % n_groups;
-  int rest = blockIdx.x / n_groups;
+  int rest, grp;
+  cg_xcd_map(n_groups, rest, grp);
+  if (rest >= P.L * 2 * P.nblk) return;   // past the last unit (uniform over the workgroup)
   const int cb = rest % P.nblk;
   rest /= P.nblk;
   const int k = rest & 1, l = rest >> 1;
 
   const int pair = uni(grp * nw + wave);
   const bool active = pair < n_pairs;
-  const int b = uni(active ? pair / ncr : 0);
-  const int c = uni(active ? c_begin + pair % ncr : 0);
+  // pairs chunk-major: the waves of a workgroup decode the same chunk of consecutive contexts,
+  // so they have the same token count and finish together
+  const int b = uni(active ? pair % P.B : 0);
+  const int c = uni(active ? c_begin + pair / P.B : 0);
   const int lv = uni(active ? min((int)chunk_level[(int64_t)b * P.NC + c], P.NLV - 1) : 0);
 
   if (threadIdx.x == 0) s_mask = 0u;
@@ -562,11 +566,58 @@ __device__ __forceinline__ void g10_fences(uint32_t (&fT)[17], const uint16_t* t
   for (int f = 1; f < 16; ++f) fT[f] = ((uint32_t)tab[16 * f] << 16) | (32u * (f - 1));
 }
 
-// One symbol under the table at LDS byte address tb (256 entries plus sentinels; `tab` is the
-// same table as a pointer, for the rare correction walk) whose tagged fences are fT; kq =
-// -(tb / 2 + 127). Returns q = symbol - 127 after the interval update and the refill of D.
-__device__ __forceinline__ int g10_symbol(G10Lane& st, const uint32_t (&fT)[17],
-                                          const uint16_t* tab, uint32_t tb, uint32_t kq) {
+// Views of a table for the rare correction walk after a missed candidate: cum(i) for a symbol
+// i in [0, 254], and the first symbol the walk tries.
+struct FullTab {   // all 256 entries in LDS
+  const uint16_t* tab;
+  __device__ __forceinline__ uint32_t cum(int i) const { return tab[i]; }
+  __device__ __forceinline__ int first(int sym, uint32_t, bool down) const {
+    return down ? max(sym - 1, 0) : min(sym + 1, CG_NSYM - 1);
+  }
+};
+
+// A table of which only entries k0 .. k1 are in LDS (entry i at byte address rb + 2 i), the
+// rest following closed forms: every frequency below the first one that differs from 1 is 1,
+// so cum[i] = i there, and every frequency above the last one that differs from 1 is 1, so
+// cum[i] = 65536 - (255 - i) = 65281 + i there. k0 = 16 g0 and k1 = 16 (g1 + 1) bound the
+// stored 16-entry blocks g0 .. g1, which extend the blocks holding those two frequencies by one
+// block on each side. A target in a flat region jumps straight to its symbol.
+struct WinTab {
+  uint32_t rb;
+  int k0, k1;
+  __device__ __forceinline__ uint32_t cum(int i) const {
+    return i < k0 ? (uint32_t)i
+                  : (i > k1 ? 65281u + (uint32_t)i : lds_ld16(rb + 2u * (uint32_t)i));
+  }
+  __device__ __forceinline__ int first(int sym, uint32_t ti, bool down) const {
+    if (ti < (uint32_t)k0) return (int)ti;
+    if (ti >= 65281u + (uint32_t)k1) return min((int)(ti - 65281u), CG_NSYM - 1);
+    return down ? max(sym - 1, 0) : min(sym + 1, CG_NSYM - 1);
+  }
+};
+
+// Fences of a window table (blocks g0 .. g1 stored; g1 > g0). The tag of fence f addresses
+// block f - 1 clamped to [g0, g1 - 1], so that the search, which reads block f - 1 or f of the
+// fence it ends on, stays inside the stored blocks. A tag is clamped only when both blocks lie
+// in a flat region (blocks below g0 + 1 and above g1 - 1 hold no frequency other than 1), and a
+// target there misses its candidate and is resolved by the walk's jump.
+__device__ __forceinline__ void g10_fences_win(uint32_t (&fT)[17], const WinTab& T, int g0,
+                                               int g1) {
+  fT[0] = 0u;
+  fT[16] = 0u;
+#pragma unroll
+  for (int f = 1; f < 16; ++f) {
+    const int blk = min(max(f - 1, g0), g1 - 1);
+    fT[f] = (T.cum(16 * f) << 16) | (32u * (uint32_t)blk);
+  }
+}
+
+// One symbol under the table whose entry 0 sits (really, or for a window table virtually) at
+// LDS byte address tb, with tagged fences fT; kq = -(tb / 2 + 127); T is the same table for the
+// rare correction walk. Returns q = symbol - 127 after the interval update and the refill of D.
+template <class Tab>
+__device__ __forceinline__ int g10_symbol(G10Lane& st, const uint32_t (&fT)[17], const Tab& T,
+                                          uint32_t tb, uint32_t kq) {
   const float te = (float)st.D * (65536.0f * __builtin_amdgcn_rcpf((float)st.rm1));
   const uint32_t ti = min((uint32_t)te, 65534u);
   const uint32_t th = (ti << 16) + 0x10000u;   // (ti + 1) << 16
@@ -625,16 +676,19 @@ __device__ __forceinline__ int g10_symbol(G10Lane& st, const uint32_t (&fT)[17],
   uint32_t rsz = hoff - lo_off;
   if (d >= rsz) {
     int sym = qi + 127;
+    int nxt = T.first(sym, ti, D < lo_off);
     for (int guard = 0; guard < CG_NSYM; ++guard) {
-      sym = (D < lo_off) ? max(sym - 1, 0) : min(sym + 1, CG_NSYM - 1);
+      sym = nxt;
       const int s1 = min(sym + 1, CG_NSYM - 1);
-      clo = tab[sym];
-      chi = sym + 1 >= CG_NSYM ? CG_TOTAL : (uint32_t)tab[s1];
+      clo = T.cum(sym);
+      chi = T.cum(s1);
+      chi = sym + 1 >= CG_NSYM ? CG_TOTAL : chi;
       lo_off = scaled_off(rm1, clo);
       hoff = scaled_off(rm1, chi);
       d = D - lo_off;
       rsz = hoff - lo_off;
       if (d < rsz) break;
+      nxt = (D < lo_off) ? max(sym - 1, 0) : min(sym + 1, CG_NSYM - 1);
     }
     qi = sym - 127;
   }
@@ -644,10 +698,11 @@ __device__ __forceinline__ int g10_symbol(G10Lane& st, const uint32_t (&fT)[17],
 
 // One delta token: its symbol under the delta table, dequantized against the group's anchor
 // into row r of the wave's staging buffer.
-__device__ __forceinline__ void g10_delta(G10Lane& st, const uint32_t (&fD)[17],
-                                          const uint16_t* dtab, uint32_t tb, uint32_t kq,
-                                          float w, uint16_t* obuf, int r, int lane) {
-  const int qi = g10_symbol(st, fD, dtab, tb, kq);
+template <class Tab>
+__device__ __forceinline__ void g10_delta(G10Lane& st, const uint32_t (&fD)[17], const Tab& T,
+                                          uint32_t tb, uint32_t kq, float w, uint16_t* obuf,
+                                          int r, int lane) {
+  const int qi = g10_symbol(st, fD, T, tb, kq);
   obuf[r * 64 + lane] = cg_f2h(st.a + (float)qi * w);
 }
 
@@ -701,21 +756,30 @@ __device__ __forceinline__ void g10_flush_full(const uint16_t* obuf, uint16_t* r
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// kCompact: the delta tables are staged as windows (see WinTab): every unit has a region of
+// ustride u16 (at least one whole table set), which holds its anchor tables in the anchor phase
+// and then the windows of its delta tables, packed; sets that do not fit together are staged in
+// rounds, one after the other. Otherwise the region holds min(nw, levels) whole sets.
+template <bool kCompact>
 __global__ __launch_bounds__(1024) void decode_g10_kernel(
     KParams P, const uint32_t* __restrict__ words, const uint64_t* __restrict__ offsets,
     const float* __restrict__ scales, const uint8_t* __restrict__ chunk_level,
     const uint16_t* __restrict__ cdfA, const uint16_t* __restrict__ cdfD, int c_begin,
-    int c_end, int nw, int nu, uint16_t* __restrict__ out) {
+    int c_end, int nw, int nu, int ustride, uint16_t* __restrict__ out) {
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
   __shared__ uint32_t s_mask[kMaxUnits];
   __shared__ uint8_t s_set_of_level[kMaxUnits][CG_MAX_LEVELS];
   __shared__ uint8_t s_level_of_set[kMaxUnits][CG_MAX_LEVELS];
   __shared__ uint8_t s_nsets[kMaxUnits];
+  __shared__ uint8_t s_round[kMaxUnits][CG_MAX_LEVELS];   // staging round of each set (compact)
+  __shared__ uint8_t s_nrounds[kMaxUnits];
   __shared__ uint8_t s_simd[kMaxWaves];             // SIMD of each wave
   __shared__ int s_left[kMaxWaves];             // symbols each wave has left in this phase
   const int msets = nw < P.NLV ? nw : P.NLV;          // table sets a unit may need
   uint16_t* obuf_all = smem;                          // [nu * nw][kG10][64] rows per wave
-  uint16_t* tabs = obuf_all + nu * nw * kG10 * 64;    // [nu][msets][64][kTabStride]
+  uint16_t* tabs = obuf_all + nu * nw * kG10 * 64;    // [nu][ustride]
+  // window descriptors of the delta tables [nu][msets][64] (compact): size / offset, g0, g1
+  uint32_t* desc = reinterpret_cast<uint32_t*>(tabs + (size_t)nu * ustride);
 
   const uint64_t total = offsets[P.S];
   if (total == 0) return;   // no payload at all: nothing to decode (uniform over the grid)
@@ -727,16 +791,19 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   const int n_pairs = P.B * ncr;
   const int n_groups = (n_pairs + nw - 1) / nw;
   const int n_units = P.L * 2 * P.nblk;
-  const int grp = blockIdx.x % n_groups;
-  const int ublk = blockIdx.x / n_groups;
+  int ublk, grp;
+  cg_xcd_map(n_groups, ublk, grp);
+  if (ublk * nu >= n_units) return;   // past the last unit block (uniform over the workgroup)
   const int unit = ublk * nu + u;
   const int cb = unit % P.nblk;
   const int k = (unit / P.nblk) & 1, l = (unit / P.nblk) >> 1;
 
   const int pair = uni(grp * nw + j);
   const bool active = unit < n_units && pair < n_pairs;
-  const int b = uni(active ? pair / ncr : 0);
-  const int c = uni(active ? c_begin + pair % ncr : 0);
+  // pairs chunk-major: the waves of a workgroup decode the same chunk of consecutive contexts,
+  // so they have the same token count and finish together
+  const int b = uni(active ? pair % P.B : 0);
+  const int c = uni(active ? c_begin + pair / P.B : 0);
   const int lv = uni(active ? min((int)chunk_level[(int64_t)b * P.NC + c], P.NLV - 1) : 0);
   const int tok0 = c * P.CL;
   const int n = uni(active ? min(P.CL, P.T - tok0) : 0);
@@ -807,7 +874,7 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
         const int64_t trow = anchors ? (int64_t)lk * P.C + ch
                                      : ((int64_t)lset * P.L * 2 + lk) * P.C + ch;
         v[i] = reinterpret_cast<const uint4*>(srcbase + (ok ? trow : 0) * 256)[piece];
-        dsto[i] = ok ? ((uu * msets + st) * 64 + t) * kTabStride + piece * 8 : -1;
+        dsto[i] = ok ? uu * ustride + (st * 64 + t) * kTabStride + piece * 8 : -1;
       }
 #pragma unroll
       for (int i = 0; i < kStageBatch; ++i) {
@@ -824,8 +891,126 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     }
   };
 
+  // Compact staging of the delta tables. Pass 1 (window): each table's first and last
+  // frequency other than 1 (i0, i1), from the 8 entries a lane holds and the next lane's first;
+  // blocks g0 = max(i0 / 16 - 1, 0) .. g1 = min(i1 / 16 + 1, 15) are kept, entries 16 g0 ..
+  // 16 (g1 + 1) + 3 (8-byte multiple). Pass 2 (layout, one wave per unit): offsets of the
+  // windows, set after set, and a new round whenever a set does not fit the region any more.
+  // Pass 3 (per round): the windows of the round's sets are written, with entry 255 and the
+  // entries past it as sentinels above any target.
+  auto window_pass = [&]() __attribute__((always_inline)) {
+    const int n_rows = nu * msets * 64;
+    for (int base = wave; base * 2 < n_rows; base += nwaves * kStageBatch) {
+      uint4 v[kStageBatch];
+      int rows[kStageBatch];
+#pragma unroll
+      for (int i = 0; i < kStageBatch; ++i) {
+        const int rr = (base + i * nwaves) * 2 + half;
+        const int t = rr & 63, st = (rr >> 6) % msets, uu = min((rr >> 6) / msets, nu - 1);
+        const int unit2 = ublk * nu + uu;
+        const int ch = (unit2 % P.nblk) * 64 + t;
+        const int lset = s_level_of_set[uu][st];
+        const bool ok = (rr < n_rows) & (unit2 < n_units) & (st < (int)s_nsets[uu]) & (ch < P.C);
+        const int64_t trow = ((int64_t)lset * P.L * 2 + unit2 / P.nblk) * P.C + ch;
+        v[i] = reinterpret_cast<const uint4*>(cdfD + (ok ? trow : 0) * 256)[piece];
+        rows[i] = ok ? rr : -1;
+      }
+#pragma unroll
+      for (int i = 0; i < kStageBatch; ++i) {
+        // cum[8 piece + j], j = 0..8 (the ninth from the next lane; cum[255] = 65536)
+        const uint32_t e0 = v[i].x & 0xFFFFu, e1 = v[i].x >> 16, e2 = v[i].y & 0xFFFFu;
+        const uint32_t e3 = v[i].y >> 16, e4 = v[i].z & 0xFFFFu, e5 = v[i].z >> 16;
+        const uint32_t e6 = v[i].w & 0xFFFFu;
+        const uint32_t e7 = piece == 31 ? CG_TOTAL : v[i].w >> 16;
+        const uint32_t e8 = (uint32_t)__shfl_down((int)e0, 1, 32);
+        const uint32_t e[9] = {e0, e1, e2, e3, e4, e5, e6, e7, e8};
+        int lo = 255, hi = -1;
+#pragma unroll
+        for (int jj = 7; jj >= 0; --jj)
+          if (8 * piece + jj < CG_NSYM && e[jj + 1] - e[jj] != 1u) lo = 8 * piece + jj;
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj)
+          if (8 * piece + jj < CG_NSYM && e[jj + 1] - e[jj] != 1u) hi = 8 * piece + jj;
+#pragma unroll
+        for (int o = 16; o >= 1; o >>= 1) {
+          lo = min(lo, __shfl_xor(lo, o, 32));
+          hi = max(hi, __shfl_xor(hi, o, 32));
+        }
+        if (hi < lo) { lo = 0; hi = CG_NSYM - 1; }   // no such frequency: not a valid table
+        if (rows[i] >= 0 && piece == 0) {
+          const int g0 = max(lo / 16 - 1, 0), g1 = min(hi / 16 + 1, 15);
+          desc[rows[i]] = (uint32_t)g0 | ((uint32_t)g1 << 4) | ((uint32_t)((g1 - g0 + 1) * 32 + 8) << 8);
+        }
+      }
+    }
+  };
+  auto layout_pass = [&]() __attribute__((always_inline)) {
+    if (wave >= nu) return;   // one wave per unit (uniform)
+    const int uu = wave;
+    const int unit2 = ublk * nu + uu;
+    const int pool = 2 * ustride;
+    const bool chok = unit2 < n_units && (unit2 % P.nblk) * 64 + lane < P.C;
+    int round = 0, acc = 0;
+    for (int st = 0; st < msets; ++st) {
+      const int idx = (uu * msets + st) * 64 + lane;
+      const bool ok = chok && st < (int)s_nsets[uu];
+      const uint32_t d = ok ? desc[idx] : 0u;
+      const uint32_t sz = d >> 8;
+      const uint32_t incl = cg_wave_incl_scan(sz);
+      const int tot = uni((int)__shfl(incl, 63, 64));
+      if (acc > 0 && acc + tot > pool) { ++round; acc = 0; }
+      if (ok) desc[idx] = (uint32_t)(acc + (int)(incl - sz)) | ((d & 0xFFu) << 20);
+      if (lane == 0) s_round[uu][st] = (uint8_t)round;
+      acc += tot;
+    }
+    if (lane == 0) s_nrounds[uu] = (uint8_t)(round + 1);
+  };
+  auto stage_round = [&](int rd) __attribute__((always_inline)) {
+    const int n_rows = nu * msets * 64;
+    for (int base = wave; base * 2 < n_rows; base += nwaves * kStageBatch) {
+      uint4 v[kStageBatch];
+      int dsto[kStageBatch], k0s[kStageBatch], kends[kStageBatch];
+#pragma unroll
+      for (int i = 0; i < kStageBatch; ++i) {
+        const int rr = (base + i * nwaves) * 2 + half;
+        const int t = rr & 63, st = (rr >> 6) % msets, uu = min((rr >> 6) / msets, nu - 1);
+        const int unit2 = ublk * nu + uu;
+        const int ch = (unit2 % P.nblk) * 64 + t;
+        const int lset = s_level_of_set[uu][st];
+        const bool ok = (rr < n_rows) & (unit2 < n_units) & (st < (int)s_nsets[uu]) &
+                        (ch < P.C) && (int)s_round[uu][st] == rd;
+        const int64_t trow = ((int64_t)lset * P.L * 2 + unit2 / P.nblk) * P.C + ch;
+        v[i] = reinterpret_cast<const uint4*>(cdfD + (ok ? trow : 0) * 256)[piece];
+        const uint32_t d = ok ? desc[min(rr, n_rows - 1)] : 0u;
+        const int g0 = (int)((d >> 20) & 15u), g1 = (int)((d >> 24) & 15u);
+        dsto[i] = ok ? uu * ustride + (int)((d & 0xFFFFFu) >> 1) : -1;
+        k0s[i] = 16 * g0;
+        kends[i] = 16 * (g1 + 1) + 4;
+      }
+#pragma unroll
+      for (int i = 0; i < kStageBatch; ++i) {
+        if (dsto[i] < 0) continue;
+        uint16_t* dst = tabs + dsto[i] - k0s[i];   // entry k of the table at dst[k]
+        const int e = 8 * piece;
+        uint4 x = v[i];
+        if (piece == 31) x.w = (x.w & 0xFFFFu) | 0xFFFF0000u;   // entry 255: sentinel
+        if (e >= k0s[i] && e < kends[i])
+          *reinterpret_cast<uint2*>(dst + e) = make_uint2(x.x, x.y);
+        if (e + 4 >= k0s[i] && e + 4 < kends[i])
+          *reinterpret_cast<uint2*>(dst + e + 4) = make_uint2(x.z, x.w);
+        if (piece == 31 && kends[i] > 256)   // entries 256..259
+          *reinterpret_cast<uint2*>(dst + 256) = make_uint2(0xFFFFFFFFu, 0xFFFFFFFFu);
+      }
+    }
+  };
+
   stage(true);
+  if constexpr (kCompact) window_pass();
   __syncthreads();
+  if constexpr (kCompact) {
+    layout_pass();
+    __syncthreads();
+  }
 
   const int ch = cb * 64 + lane;
   const bool valid = ch < P.C;
@@ -836,7 +1021,7 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   const int chv = cb * 64 + lsrc;
   const int64_t rstride = P.C;
   uint16_t* row0 = out + cg_elem(P, b, l, k, tok0, cb * 64);   // token tok0, channel cb * 64
-  const uint16_t* tab0 = tabs + (u * msets * 64 + lsrc) * kTabStride;   // set 0 of the unit
+  const uint16_t* tab0 = tabs + u * ustride + lsrc * kTabStride;   // anchor table of the lane
   G10Lane st;
   const uint32_t* sbase = words;
   uint32_t cap = 0;
@@ -885,7 +1070,7 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
       for (int r = 0; r < kAnchorRun; ++r) {
         const int g = g0 + r;
         if (g < na) {
-          const int qi = g10_symbol(st, fA, tab0, tbA, kqA);
+          const int qi = g10_symbol(st, fA, FullTab{tab0}, tbA, kqA);
           // wave-uniform row pointers, the lane's column as the index
           uint16_t* ra = row0 + (int64_t)g * kG10 * rstride;
           uint16_t* rq = g * kG10 + 1 < n ? ra + rstride : ra;
@@ -897,16 +1082,10 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     }
   }
 
-  // ---- delta phase: the delta tables replace the anchor tables --------------------------
-  __syncthreads();
-  stage(false);
-  __syncthreads();
-  if (!active || n < 2) return;
+  auto delta_groups = [&](const auto& T, const uint32_t (&fD)[17], uint32_t tbD)
+                          __attribute__((always_inline)) {
   set_priority(n - na);
-  const uint16_t* dtab = tabs + ((u * msets + s_set_of_level[u][lv]) * 64 + lsrc) * kTabStride;
-  uint32_t fD[17];
-  g10_fences(fD, dtab);
-  const uint32_t tbD = lds_addr(dtab), kqD = 0u - (tbD / 2u + 127u);
+  const uint32_t kqD = 0u - (tbD / 2u + 127u);
 
   uint16_t* obuf = obuf_all + wave * kG10 * 64;
   const int cbase = cb * 64;
@@ -927,17 +1106,17 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   for (int gi = 0; gi < ngr; ++gi) {
     st.a = anext;
     g10_epoch(st, sbase, cap);
-    g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 1, lane);
-    g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 2, lane);
-    g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 3, lane);
-    g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 4, lane);
-    g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 5, lane);
+    g10_delta(st, fD, T, tbD, kqD, w, obuf, 1, lane);
+    g10_delta(st, fD, T, tbD, kqD, w, obuf, 2, lane);
+    g10_delta(st, fD, T, tbD, kqD, w, obuf, 3, lane);
+    g10_delta(st, fD, T, tbD, kqD, w, obuf, 4, lane);
+    g10_delta(st, fD, T, tbD, kqD, w, obuf, 5, lane);
     g10_epoch(st, sbase, cap);
     const uint32_t qnext = q_of(gi + 1);   // requested a group ahead
-    g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 6, lane);
-    g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 7, lane);
-    g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 8, lane);
-    g10_delta(st, fD, dtab, tbD, kqD, w, obuf, 9, lane);
+    g10_delta(st, fD, T, tbD, kqD, w, obuf, 6, lane);
+    g10_delta(st, fD, T, tbD, kqD, w, obuf, 7, lane);
+    g10_delta(st, fD, T, tbD, kqD, w, obuf, 8, lane);
+    g10_delta(st, fD, T, tbD, kqD, w, obuf, 9, lane);
     if constexpr (decltype(kFull)::value) g10_flush_full(obuf, row, rstride, lane);
     else g10_flush(obuf, row, rstride, 1, kG10, lane, cbase, P.C);
     row += kG10 * rstride;
@@ -955,9 +1134,43 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     g10_epoch(st, sbase, cap);
     for (int r = 1; r < rem; ++r) {
       if (r == 6) g10_epoch(st, sbase, cap);
-      g10_delta(st, fD, dtab, tbD, kqD, w, obuf, r, lane);
+      g10_delta(st, fD, T, tbD, kqD, w, obuf, r, lane);
     }
     g10_flush(obuf, row, rstride, 1, rem, lane, cbase, P.C);
+  }
+  };
+
+  // ---- delta phase: the delta tables replace the anchor tables --------------------------
+  // (in rounds when compact windows of all sets do not fit a unit's region at once; every wave
+  // takes part in every round's staging and barriers, and decodes in its set's round)
+  __syncthreads();
+  int nrounds = 1;
+  if constexpr (kCompact) {
+    for (int uu = 0; uu < nu; ++uu) nrounds = max(nrounds, (int)s_nrounds[uu]);
+    nrounds = uni(nrounds);
+  }
+  for (int rd = 0; rd < nrounds; ++rd) {
+    if (rd > 0) __syncthreads();   // the previous round's readers are done
+    if constexpr (kCompact) stage_round(rd);
+    else stage(false);
+    __syncthreads();
+    if (!active || n < 2) continue;
+    const int set = s_set_of_level[u][lv];
+    if constexpr (kCompact) {
+      if ((int)s_round[u][set] != rd) continue;
+      const uint32_t d = desc[(u * msets + set) * 64 + lsrc];
+      const int g0 = (int)((d >> 20) & 15u), g1 = (int)((d >> 24) & 15u);
+      const WinTab T{lds_addr(tabs + u * ustride) + (d & 0xFFFFFu) - 32u * (uint32_t)g0, 16 * g0,
+                     16 * (g1 + 1)};
+      uint32_t fD[17];
+      g10_fences_win(fD, T, g0, g1);
+      delta_groups(T, fD, T.rb);
+    } else {
+      const uint16_t* dtab = tabs + u * ustride + (set * 64 + lsrc) * kTabStride;
+      uint32_t fD[17];
+      g10_fences(fD, dtab);
+      delta_groups(FullTab{dtab}, fD, lds_addr(dtab));
+    }
   }
 }
 
@@ -1195,17 +1408,44 @@ hipError_t cg_launch_decode(const KParams& P, const uint32_t* words, const uint6
     while (nu < kMaxUnits && (nu + 1) * nw <= kMaxWaves && lds_for(nw, nu + 1) <= kLdsBudget &&
            (n_units + nu) / (nu + 1) * n_groups >= 256)
       ++nu;
-    const int64_t grid = (n_units + nu - 1) / nu * n_groups;
-    const size_t lds = lds_for(nw, nu);
-    hipError_t e = hipFuncSetAttribute((const void*)decode_g10_kernel,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    const int msets = nw < P.NLV ? nw : P.NLV;
+    // With several levels, the delta tables can instead be staged as windows (decode_g10_kernel
+    // <true>): a unit then needs a region of one table set (its anchor tables) plus window
+    // descriptors, so more units fit a workgroup. Used when that allows more units.
+    const size_t rows = (size_t)nw * kG10 * 64 * sizeof(uint16_t);   // per unit
+    const size_t set_bytes = (size_t)64 * kTabStride * sizeof(uint16_t);
+    const size_t desc_bytes = (size_t)msets * 64 * sizeof(uint32_t);
+    int nuc = 1;
+    while (nuc < kMaxUnits && (nuc + 1) * nw <= kMaxWaves &&
+           (size_t)(nuc + 1) * (rows + set_bytes + desc_bytes) <= kLdsBudget &&
+           (n_units + nuc) / (nuc + 1) * n_groups >= 256)
+      ++nuc;
+    const bool compact = msets > 1 && nuc > nu;
+    int units = nu, ustride = (int)((size_t)msets * 64 * kTabStride);
+    size_t lds = lds_for(nw, nu);
+    if (compact) {
+      units = nuc;
+      // each unit's region: what the LDS budget leaves, in 16-byte multiples
+      const size_t per_unit = kLdsBudget / (size_t)nuc - rows - desc_bytes;
+      ustride = (int)((per_unit & ~(size_t)15) / sizeof(uint16_t));
+      lds = (size_t)nuc * (rows + desc_bytes) + (size_t)nuc * ustride * sizeof(uint16_t);
+    }
+    const int64_t grid = cg_xcd_grid((n_units + units - 1) / units, n_groups);
+    const void* kfn = compact ? (const void*)decode_g10_kernel<true>
+                              : (const void*)decode_g10_kernel<false>;
+    hipError_t e = hipFuncSetAttribute(kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(decode_g10_kernel, dim3((unsigned)grid), dim3(64 * nw * nu), lds, st, P,
-                       words, offsets, scales, chunk_level, cdf_anchor, cdf_delta, c_begin, c_end,
-                       nw, nu, out);
+    if (compact)
+      hipLaunchKernelGGL(decode_g10_kernel<true>, dim3((unsigned)grid), dim3(64 * nw * units), lds,
+                         st, P, words, offsets, scales, chunk_level, cdf_anchor, cdf_delta,
+                         c_begin, c_end, nw, units, ustride, out);
+    else
+      hipLaunchKernelGGL(decode_g10_kernel<false>, dim3((unsigned)grid), dim3(64 * nw * units),
+                         lds, st, P, words, offsets, scales, chunk_level, cdf_anchor, cdf_delta,
+                         c_begin, c_end, nw, units, ustride, out);
     return hipGetLastError();
   }
-  const int64_t grid = n_units * n_groups;
+  const int64_t grid = cg_xcd_grid(n_units, n_groups);
   const size_t lds = lds_for(nw, 1);
   hipError_t e = hipFuncSetAttribute((const void*)decode_kernel,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);

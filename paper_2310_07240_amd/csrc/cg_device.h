@@ -108,6 +108,22 @@ __device__ __forceinline__ int64_t tok_stream(const KParams& P, int b, int c, in
   return ((int64_t)b * P.T + (int64_t)c * P.CL) * (2 * P.L) + (int64_t)lk * n + j;
 }
 
+// Workgroup -> (unit block, pair group) for grids of n_ublk unit blocks x n_groups pair groups.
+// The hardware deals workgroups to the 8 XCDs in turn (block i to XCD i mod 8). Blocks are
+// numbered in stripes of 8 unit blocks x n_groups: the pair groups of one unit block land on one
+// XCD (they share the unit's tables in that XCD's L2), and every XCD cycles through the pair
+// groups (their chunk lengths and contexts differ). The grid is cg_xcd_grid() blocks; blocks of
+// the last, partial stripe past n_ublk get ublk >= n_ublk and must leave.
+__device__ __forceinline__ void cg_xcd_map(int n_groups, int& ublk, int& grp) {
+  const int stripe = 8 * n_groups;
+  const int b = (int)blockIdx.x;
+  grp = (b % stripe) / 8;
+  ublk = (b / stripe) * 8 + b % 8;
+}
+inline int64_t cg_xcd_grid(int64_t n_ublk, int64_t n_groups) {
+  return n_groups == 1 ? n_ublk : (n_ublk + 7) / 8 * 8 * n_groups;
+}
+
 template <typename T>
 __device__ __forceinline__ T cg_wave_sum(T v) {
 #pragma unroll

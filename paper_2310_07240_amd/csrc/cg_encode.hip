@@ -248,15 +248,20 @@ __global__ __launch_bounds__(1024) void encode_kernel(
   const int n_pairs = P.B * P.NC;
   const int n_groups = (n_pairs + nw - 1) / nw;
   const int n_units = P.L * 2 * P.nblk;
-  const int grp = blockIdx.x % n_groups;
-  const int ublk = blockIdx.x / n_groups;
+  int ublk, grp;
+  cg_xcd_map(n_groups, ublk, grp);
+  if (ublk * nu >= n_units) {   // past the last unit block (uniform over the workgroup)
+    if (threadIdx.x == 0) wflags[blockIdx.x] = 0u;
+    return;
+  }
   const int unit = ublk * nu + u;
   const int cb = unit % P.nblk;
   const int k = (unit / P.nblk) & 1, l = (unit / P.nblk) >> 1;
   const int pair = __builtin_amdgcn_readfirstlane(grp * nw + j);
   const bool active = unit < n_units && pair < n_pairs;
-  const int b = active ? pair / P.NC : 0;
-  const int c = active ? pair % P.NC : 0;
+  // pairs chunk-major: the waves of a workgroup code the same chunk of consecutive contexts
+  const int b = active ? pair % P.B : 0;
+  const int c = active ? pair / P.B : 0;
   const int lv = active ? min((int)chunk_level[(int64_t)b * P.NC + c], P.NLV - 1) : 0;
   const int n = active ? min(P.CL, P.T - c * P.CL) : 0;
 
@@ -893,7 +898,7 @@ EncGeom enc_geometry(const KParams& P) {
   g.nu = nu;
   g.nsets = nw < P.NLV ? nw : P.NLV;
   g.n_groups = n_groups;
-  g.g1 = (n_units + nu - 1) / nu * n_groups;
+  g.g1 = cg_xcd_grid((n_units + nu - 1) / nu, n_groups);
   g.lds = lds_for(nw, nu);
   return g;
 }

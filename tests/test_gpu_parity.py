@@ -168,3 +168,84 @@ def test_corrupt_payload_decodes_within_bounds(kind):
         torch.cuda.synchronize()
         assert torch.equal(a, b)
         assert bool(torch.isfinite(a.view(torch.float16).float()).all())
+
+
+# Four levels over six chunks with enough (layer, K/V, channel block) units for two per
+# workgroup: the group-of-10 decoder then stages the delta tables as windows of their 16-entry
+# blocks (closed forms outside them). With heavy-tailed values the windows of one unit's four
+# sets exceed the unit's LDS region and are staged in two rounds.
+COMPACT = [
+    W.small(name="compact_l4_c4096", n_layers=4, n_channels=4096, n_tokens=120, chunk_len=20,
+            level_mult=(1.0, 2.0, 4.0, 8.0), seed=21),
+    W.small(name="compact_heavy_rounds", n_layers=4, n_channels=4096, n_tokens=120,
+            chunk_len=20, level_mult=(1.0, 2.0, 4.0, 8.0), heavy_ctx=(0,), seed=22),
+    W.small(name="compact_c4100_tail", n_layers=4, n_channels=4100, n_tokens=117, chunk_len=20,
+            level_mult=(1.0, 2.0, 4.0, 8.0), seed=23),
+]
+# the decoder's region per unit with two units of six 10-row waves: an LDS budget of 159 KB
+# halved, less the rows (6 x 1280 B) and the window descriptors (4 sets x 64 x 4 B)
+REGION_BYTES = 159 * 1024 // 2 - 6 * 1280 - 4 * 64 * 4
+
+
+def _window_rounds(w, cd):
+    """Staging rounds the windowed decoder needs per unit (computed from the oracle's tables the
+    way the kernel lays them out), to show which cases exercise more than one round."""
+    cum = cd.astype(np.int64).copy()
+    cum[..., 255] = 65536
+    nonflat = np.diff(cum, axis=-1) != 1                       # [lv, L, 2, C, 255]
+    idx = np.arange(255)
+    lo = np.where(nonflat, idx, 255).min(-1)
+    hi = np.where(nonflat, idx, -1).max(-1)
+    g0 = np.maximum(lo // 16 - 1, 0)
+    g1 = np.minimum(hi // 16 + 1, 15)
+    size = (g1 - g0 + 1) * 32 + 8
+    levels = sorted(set(int(v) for v in w.chunk_levels().reshape(-1)))
+    rounds = []
+    for l in range(w.n_layers):
+        for k in range(2):
+            for cb in range(0, w.n_channels, 64):
+                acc, r = 0, 0
+                for lv in levels:
+                    tot = int(size[lv, l, k, cb:cb + 64].sum())
+                    if acc > 0 and acc + tot > REGION_BYTES:
+                        r, acc = r + 1, 0
+                    acc += tot
+                rounds.append(r + 1)
+    return max(rounds)
+
+
+@pytest.mark.parametrize("w", COMPACT, ids=lambda w: w.name)
+def test_windowed_delta_tables_bit_exact(w):
+    kv = W.generate(w)
+    o = run_oracle(w, kv)
+    assert len(set(w.chunk_levels().reshape(-1).tolist())) > 1
+    rounds = _window_rounds(w, o["cd"])
+    say(f"{w.name}: windowed tables, {rounds} staging round(s)")
+    if w.name == "compact_heavy_rounds":
+        assert rounds > 1
+    g = run_gpu(w, kv, decode_oracle_payload=(o["words"], o["offsets"], o["scales"], o["ca"], o["cd"]))
+    compare_full(w, g, o)
+    assert_same("decode of oracle payload", g["out_from_oracle_payload"], o["out"])
+
+
+def test_windowed_tables_chunk_ranges():
+    """Chunk-range decodes of a windowed case (fewer pairs per workgroup, other unit counts):
+    each range equals the oracle's rows and leaves every other row untouched."""
+    torch = torch_cuda()
+    from paper_2310_07240_amd.cachegen import Codec, CodecParams
+    w = COMPACT[1]
+    kv_np = W.generate(w)
+    o = run_oracle(w, kv_np)
+    codec = Codec(CodecParams.of(w))
+    kv = torch.from_numpy(kv_np.view(np.int16)).cuda()
+    cl = torch.from_numpy(w.chunk_levels()).cuda()
+    ca, cd = codec.fit(kv)
+    words, offsets, scales = codec.encode(kv, cl, ca, cd)
+    for c0, c1 in [(1, 5), (0, 3), (5, 6), (2, 6)]:
+        say(f"{w.name}: decode chunks [{c0}, {c1})")
+        part = codec.decode(words, offsets, scales, cl, ca, cd, c0, c1).cpu().numpy().view(np.uint16)
+        t0, t1 = c0 * w.chunk_len, min(c1 * w.chunk_len, w.n_tokens)
+        assert_same(f"chunks {c0}:{c1}", part[..., t0:t1, :], o["out"][..., t0:t1, :])
+        mask = np.ones(w.n_tokens, bool)
+        mask[t0:t1] = False
+        assert np.all(part[..., mask, :] == 0)
