@@ -3,7 +3,7 @@
 plus encode throughput and bits per element.
 
 One step = the whole codec over one KV cache resident in HBM: fit the distributions of every
-level (cg_fit_cdf), encode (cg_encode), decode (cg_decode). `value` is the decode throughput
+level (cg_fit_cdf_levels), encode (cg_encode), decode (cg_decode). `value` is the decode throughput
 (fp16 bytes of KV produced per second of cg_decode, HIP events on the launch stream) on the
 Mistral-7B-shaped 4K-token cache.
 
@@ -102,10 +102,8 @@ class Run:
         self.stream = torch.cuda.current_stream()
 
     def fit(self):
-        from paper_2310_07240_amd.cachegen import cg_fit_cdf
-        for lv in range(self.w.n_levels):
-            cg_fit_cdf(self.p, self.kv, lv, self.ca if lv == 0 else None, self.cd[lv],
-                       self.stream)
+        from paper_2310_07240_amd.cachegen import cg_fit_cdf_levels
+        cg_fit_cdf_levels(self.p, self.kv, self.ca, self.cd, None, self.stream)
 
     def encode(self):
         from paper_2310_07240_amd.cachegen import cg_encode

@@ -75,7 +75,7 @@ enum {
                              in [1, 8], or a size whose index space overflows 64 bits       */
   CG_ERR_CAPACITY = -3,   /* words_cap or workspace_bytes below what the call needs        */
   CG_ERR_NONFINITE = -4,  /* the KV input holds NaN or +-Inf (reported by cg_get_status after
-                             cg_encode, and by cg_check_finite)                             */
+                             cg_encode or cg_fit_cdf_levels, and by cg_check_finite)        */
   CG_ERR_HIP = -5,        /* a HIP runtime call or kernel launch failed                     */
   CG_ERR_PARAM = -6,      /* a layer_bin or level_mult entry is not finite and > 0          */
   CG_ERR_SCRATCH = -7     /* cg_encode_noalloc: the cache needs more scratch than
@@ -130,6 +130,22 @@ uint64_t cg_encode_workspace_bytes(const cg_params* p);
  * (cg_check_finite does). */
 int cg_fit_cdf(const cg_params* p, const uint16_t* kv_f16, int32_t level,
                uint16_t* cdf_anchor, uint16_t* cdf_delta_level, hipStream_t stream);
+
+/* Fit the tables of every encoding level at once (Sec. 5.2 "Arithmetic coding": one
+ * distribution per channel-layer for deltas and one for anchors; Sec. 6: counted over the
+ * symbols of the context being coded; Sec. 5.3: one table set per encoding level). The result
+ * equals cg_fit_cdf at every level (anchor tables from any of them), but the scale and the
+ * anchors of each chunk are found once for up to three levels, so the cache is read once per
+ * three or four levels instead of once per level.
+ *   kv_f16       [B][L][2][T][C] fp16, device.
+ *   cdf_anchor   out [L][2][C][256], device.
+ *   cdf_delta    out [n_levels][L][2][C][256], device.
+ *   status       NULL, or a device uint32_t (4-byte aligned) that receives 0, or a non-zero
+ *                value when the KV holds NaN or +-Inf (the tables are then meaningless);
+ *                cg_get_status(status, stream) reads it.
+ * Asynchronous. */
+int cg_fit_cdf_levels(const cg_params* p, const uint16_t* kv_f16, uint16_t* cdf_anchor,
+                      uint16_t* cdf_delta, uint32_t* status, hipStream_t stream);
 
 /* Device scratch that cg_fit_cdf_global needs (bytes). */
 #define CG_FIT_GLOBAL_WORKSPACE_BYTES 8192
@@ -290,11 +306,12 @@ typedef struct cg_adapt_params {
 int cg_adapt_schedule(const cg_adapt_params* a, const double* bandwidth_gbps,
                       int32_t* choice_out, double* ttft_ms_out);
 
-/* Status of the last cg_encode that used `workspace` (device, the encode workspace): waits for
- * `stream` (synchronous), then returns CG_OK, or CG_ERR_NONFINITE if the encoded KV held NaN or
- * +-Inf; CG_ERR_ARG for a null or misaligned workspace, CG_ERR_HIP if the copy fails. The word
- * is written by every cg_encode, so it never needs clearing; calls that share a workspace on
- * different streams race. */
+/* Read a status word on the device: the first word of a cg_encode workspace (the status of
+ * the last cg_encode that used it), or the status argument of cg_fit_cdf_levels or
+ * cg_encode_noalloc. Waits for `stream` (synchronous), then returns CG_OK, or CG_ERR_NONFINITE
+ * if the KV of that call held NaN or +-Inf; CG_ERR_ARG for a null or not 4-byte aligned
+ * pointer, CG_ERR_HIP if the copy fails. Every call writes its word, so it never needs
+ * clearing; calls that share one on different streams race. */
 int cg_get_status(const void* workspace, hipStream_t stream);
 
 /* Scan kv_f16 [n_elem] for NaN / Inf (fp16 exponent field all ones), using flag_dev, one

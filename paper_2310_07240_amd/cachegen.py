@@ -28,7 +28,7 @@ EXPORTS = ("cg_num_chunks", "cg_num_streams", "cg_encode_bound_words",
            "cg_num_token_streams", "cg_encode_tokens_bound_words",
            "cg_encode_tokens_workspace_bytes", "cg_decode_tokens_workspace_bytes",
            "cg_encode_tokens", "cg_decode_tokens", "cg_get_status", "cg_encode_noalloc",
-           "cg_strerror")
+           "cg_fit_cdf_levels", "cg_strerror")
 CG_FIT_GLOBAL_WORKSPACE_BYTES = 8192
 CG_NOALLOC_SCRATCH_BYTES = 64 << 20
 
@@ -89,6 +89,8 @@ def lib():
         L.cg_encode_workspace_bytes.restype = ctypes.c_uint64
         L.cg_fit_cdf.argtypes = [PP, _P, ctypes.c_int32, _P, _P, _P]
         L.cg_fit_cdf.restype = ctypes.c_int
+        L.cg_fit_cdf_levels.argtypes = [PP, _P, _P, _P, _P, _P]
+        L.cg_fit_cdf_levels.restype = ctypes.c_int
         L.cg_fit_cdf_global.argtypes = [PP, _P, ctypes.c_int32, _P, _P, _P, ctypes.c_uint64, _P]
         L.cg_fit_cdf_global.restype = ctypes.c_int
         L.cg_encode.argtypes = [PP, _P, _P, _P, _P, _P, ctypes.c_uint64, _P, _P, _P,
@@ -210,6 +212,14 @@ def cg_fit_cdf(p: CodecParams, kv, level: int, cdf_anchor, cdf_delta_level, stre
     s, keep = p.c()
     _check(lib().cg_fit_cdf(ctypes.byref(s), _ptr(kv), int(level), _ptr(cdf_anchor),
                             _ptr(cdf_delta_level), _stream(stream)), "cg_fit_cdf")
+
+
+def cg_fit_cdf_levels(p: CodecParams, kv, cdf_anchor, cdf_delta, status=None, stream=None):
+    """Every level's tables in one call (cdf_delta [n_levels, L, 2, C, 256]); `status` is an
+    optional device int32 tensor of one element (0, or non-zero for NaN / Inf in kv)."""
+    s, keep = p.c()
+    _check(lib().cg_fit_cdf_levels(ctypes.byref(s), _ptr(kv), _ptr(cdf_anchor), _ptr(cdf_delta),
+                                   _ptr(status), _stream(stream)), "cg_fit_cdf_levels")
 
 
 def cg_fit_cdf_global(p: CodecParams, kv, level: int, cdf_anchor, cdf_delta_level, workspace,
@@ -378,8 +388,18 @@ class Codec:
     def _empty(self, shape, dtype):
         return self.torch.empty(shape, dtype=dtype, device=self.device)
 
-    def fit(self, kv, stream=None):
-        """Anchor tables [L,2,C,256] and delta tables of every level [NLV,L,2,C,256]."""
+    def fit(self, kv, stream=None, status=None):
+        """Anchor tables [L,2,C,256] and delta tables of every level [NLV,L,2,C,256], in one
+        cg_fit_cdf_levels call."""
+        t = self.torch
+        L, C = self.p.n_layers, self.p.n_channels
+        ca = self._empty((L, 2, C, 256), t.int16)
+        cd = self._empty((self.p.n_levels, L, 2, C, 256), t.int16)
+        cg_fit_cdf_levels(self.p, kv, ca, cd, status, stream)
+        return ca, cd
+
+    def fit_per_level(self, kv, stream=None):
+        """The same tables from one cg_fit_cdf call per level."""
         t = self.torch
         L, C = self.p.n_layers, self.p.n_channels
         ca = self._empty((L, 2, C, 256), t.int16)

@@ -125,6 +125,20 @@ int cg_fit_cdf(const cg_params* p, const uint16_t* kv_f16, int32_t level, uint16
              : CG_ERR_HIP;
 }
 
+int cg_fit_cdf_levels(const cg_params* p, const uint16_t* kv_f16, uint16_t* cdf_anchor,
+                      uint16_t* cdf_delta, uint32_t* status, hipStream_t stream) {
+  KParams K;
+  int rc = make_kparams(p, &K);
+  if (rc != CG_OK) return rc;
+  if (!kv_f16 || !cdf_anchor || !cdf_delta) return CG_ERR_ARG;
+  if (!aligned(cdf_anchor, 16) || !aligned(cdf_delta, 16) || !aligned(kv_f16, 2) ||
+      (status && !aligned(status, 4)))
+    return CG_ERR_ARG;
+  return cg_launch_fit_levels(K, kv_f16, cdf_anchor, cdf_delta, status, stream) == hipSuccess
+             ? CG_OK
+             : CG_ERR_HIP;
+}
+
 int cg_fit_cdf_global(const cg_params* p, const uint16_t* kv_f16, int32_t level,
                       uint16_t* cdf_anchor, uint16_t* cdf_delta_level, void* workspace,
                       uint64_t workspace_bytes, hipStream_t stream) {
@@ -424,7 +438,7 @@ int cg_adapt_schedule(const cg_adapt_params* a, const double* bandwidth_gbps,
 }
 
 int cg_get_status(const void* workspace, hipStream_t stream) {
-  if (!workspace || !aligned(workspace, 256)) return CG_ERR_ARG;
+  if (!workspace || !aligned(workspace, 4)) return CG_ERR_ARG;
   uint32_t h = 0;
   if (hipMemcpyAsync(&h, workspace, 4, hipMemcpyDeviceToHost, stream) != hipSuccess)
     return CG_ERR_HIP;

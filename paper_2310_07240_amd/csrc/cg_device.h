@@ -155,6 +155,11 @@ __device__ __forceinline__ uint64_t cg_wave_incl_scan64(uint64_t v) {
 // Launchers (return hipError_t of the launch).
 hipError_t cg_launch_fit(const KParams& P, const uint16_t* kv, int level, uint16_t* cdf_anchor,
                          uint16_t* cdf_delta_level, hipStream_t st);
+// Every level's tables in as few passes as 16-bit counts allow (see cg_fit.hip); status, if not
+// null, receives 0 or 1 (NaN or Inf in the KV).
+hipError_t cg_launch_fit_levels(const KParams& P, const uint16_t* kv, uint16_t* cdf_anchor,
+                                uint16_t* cdf_delta, uint32_t* status, hipStream_t st);
+int64_t cg_fit_max_count(const KParams& P);
 hipError_t cg_launch_fit_global(const KParams& P, const uint16_t* kv, int level,
                                 uint16_t* cdf_anchor, uint16_t* cdf_delta_level, void* ws,
                                 hipStream_t st);

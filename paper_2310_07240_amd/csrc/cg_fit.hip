@@ -25,16 +25,18 @@ constexpr int kFitThreads = kFitWaves * 64;
 constexpr int kHist = 257;  // 255 symbols, padded; odd stride spreads lanes over the banks
 constexpr int kHalf = 56;   // longest half slice per lane held in registers (one dword per token)
 
-// Normalise one histogram [255] into cum[256] (entry 255 = 0) with one wave.
+// Normalise one histogram [255] into cum[256] (entry 255 = 0) with one wave. With shift >= 0
+// the counts are the 16-bit fields at that bit position of 32-bit words.
 template <typename CountT>
-__device__ void normalize_wave(const CountT* cnt, uint16_t* out) {
+__device__ void normalize_wave(const CountT* cnt, uint16_t* out, int shift = -1) {
   const int lane = threadIdx.x & 63;
   uint64_t c[4];
   uint64_t local = 0;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     int i = lane * 4 + j;
-    c[j] = i < CG_NSYM ? cnt[i] : 0u;
+    const uint64_t v = i < CG_NSYM ? (uint64_t)cnt[i] : 0u;
+    c[j] = shift < 0 ? v : (v >> shift) & 0xFFFFu;
     local += c[j];
   }
   uint64_t N = cg_wave_sum<uint64_t>(local);
@@ -106,20 +108,26 @@ template <bool kPool, bool kRegs>
 __global__ __launch_bounds__(kFitThreads) void fit_kernel(KParams P, const uint16_t* __restrict__ kv,
                                                          int level, uint16_t* __restrict__ cdf_anchor,
                                                          uint16_t* __restrict__ cdf_delta,
-                                                         unsigned long long* __restrict__ pool) {
+                                                         unsigned long long* __restrict__ pool,
+                                                         uint32_t* __restrict__ status) {
   extern __shared__ uint32_t cnt[];  // [2 kinds][64 channels][kHist]
-  __shared__ float part[kFitWaves][64];
+  // partial absolute maxima as magnitude bits (x & 0x7fff): for finite halves they order like
+  // |x|, and NaN or Inf gives at least 0x7c00
+  __shared__ uint32_t part[kFitWaves][64];
+  __shared__ uint32_t s_bad;
   const int cb = blockIdx.x % P.nblk;
   const int lk = blockIdx.x / P.nblk;
   const int l = lk >> 1, k = lk & 1;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
 
   for (int i = threadIdx.x; i < 2 * 64 * kHist; i += kFitThreads) cnt[i] = 0;
+  if (threadIdx.x == 0) s_bad = 0u;
   __syncthreads();
 
   const int ch = cb * 64 + lane;
   const bool act = ch < P.C;
   const float wfac = P.layer_bin[l] * P.level_mult[level];
+  uint32_t bad = 0u;
   uint32_t* ha = cnt + lane * kHist;
   uint32_t* hd = cnt + (64 + lane) * kHist;
   const int pairs = P.B * P.NC;
@@ -147,28 +155,31 @@ __global__ __launch_bounds__(kFitThreads) void fit_kernel(KParams P, const uint1
       half2_t pk[kHalf];
 #pragma unroll
       for (int u = 0; u < kHalf; ++u) pk[u] = xw[(int64_t)min(h0 + u, n - 1) * rw];
-      float m0 = 0.0f, m1 = 0.0f;
+      uint32_t b0 = 0u, b1 = 0u;
 #pragma unroll
       for (int u = 0; u < kHalf; ++u) {
         if (u < len) {
-          m0 = fmaxf(m0, fabsf((float)pk[u].x));
-          m1 = fmaxf(m1, fabsf((float)pk[u].y));
+          const uint32_t bits = __builtin_bit_cast(uint32_t, pk[u]);
+          b0 = max(b0, bits & 0x7FFFu);
+          b1 = max(b1, (bits >> 16) & 0x7FFFu);
         }
       }
-      m0 = fmaxf(m0, __shfl_xor(m0, 32, 64));
-      m1 = fmaxf(m1, __shfl_xor(m1, 32, 64));
+      b0 = max(b0, (uint32_t)__shfl_xor((int)b0, 32, 64));
+      b1 = max(b1, (uint32_t)__shfl_xor((int)b1, 32, 64));
       if (th == 0) {
-        part[wave][2 * cp] = m0;
-        part[wave][2 * cp + 1] = m1;
+        part[wave][2 * cp] = b0;
+        part[wave][2 * cp + 1] = b1;
       }
       __syncthreads();
-      m0 = 0.0f;
-      m1 = 0.0f;
+      b0 = 0u;
+      b1 = 0u;
 #pragma unroll
       for (int v = 0; v < kFitWaves; ++v) {
-        m0 = fmaxf(m0, part[v][2 * cp]);
-        m1 = fmaxf(m1, part[v][2 * cp + 1]);
+        b0 = max(b0, part[v][2 * cp]);
+        b1 = max(b1, part[v][2 * cp + 1]);
       }
+      bad |= (b0 >= 0x7C00u) | (b1 >= 0x7C00u);
+      const float m0 = cg_h2f((uint16_t)b0), m1 = cg_h2f((uint16_t)b1);
       const float s0 = (m0 == 0.0f) ? 1.0f : m0 / 127.0f;
       const float s1 = (m1 == 0.0f) ? 1.0f : m1 / 127.0f;
       const float w0 = wfac * s0, w1 = wfac * s1;
@@ -187,14 +198,16 @@ __global__ __launch_bounds__(kFitThreads) void fit_kernel(KParams P, const uint1
       }
     } else {
       // pass 1: absmax of this wave's slice, combined over the waves in LDS
-      float m = 0.0f;
+      uint32_t mb = 0u;
 #pragma unroll 8
-      for (int j = j0; j < j1; ++j) m = fmaxf(m, fabsf(cg_h2f(x[(int64_t)j * rs])));
-      part[wave][lane] = m;
+      for (int j = j0; j < j1; ++j) mb = max(mb, (uint32_t)x[(int64_t)j * rs] & 0x7FFFu);
+      part[wave][lane] = mb;
       __syncthreads();
-      m = 0.0f;
+      mb = 0u;
 #pragma unroll
-      for (int v = 0; v < kFitWaves; ++v) m = fmaxf(m, part[v][lane]);
+      for (int v = 0; v < kFitWaves; ++v) mb = max(mb, part[v][lane]);
+      bad |= act && mb >= 0x7C00u;
+      const float m = cg_h2f((uint16_t)mb);
       const float s = (m == 0.0f) ? 1.0f : m / 127.0f;
       const float w = wfac * s;
       const float is = 1.0f / s, iw = 1.0f / w;
@@ -210,6 +223,11 @@ __global__ __launch_bounds__(kFitThreads) void fit_kernel(KParams P, const uint1
       }
     }
     __syncthreads();   // `part` is reused by the next pair
+  }
+  if (status) {
+    if (bad) s_bad = 1u;   // benign race: every writer stores 1
+    __syncthreads();
+    if (threadIdx.x == 0 && s_bad) atomicOr(status, 1u);
   }
 
   if constexpr (kPool) {
@@ -259,6 +277,180 @@ __global__ __launch_bounds__(256) void pool_broadcast(const uint16_t* __restrict
   reinterpret_cast<uint64_t*>(dst + t * 256)[lane] = v;
 }
 
+
+// ---- several levels in one pass -------------------------------------------------------------
+// fit_levels_kernel: the fit of the anchors (with_anchor) and of kNl consecutive levels lv0 ..
+// from one quantization of each slice: the chunk's scale, the anchors and the deltas to them are
+// found once for all those levels. Counts are 16-bit, the two neighbouring channels 2 cp and
+// 2 cp + 1 in the low and high half of one 32-bit LDS word (the two channels a lane of the
+// register path takes), so four kinds take the LDS of two 32-bit ones; the host uses this
+// kernel only when no count can reach 2^16. A slice whose absolute maximum has the exponent
+// bits all ones (NaN or Inf) sets *status.
+constexpr int kLevelKinds = 4;   // anchor + levels, or levels, per workgroup
+
+template <bool kRegs, int kNl>
+__global__ __launch_bounds__(kFitThreads) void fit_levels_kernel(
+    KParams P, const uint16_t* __restrict__ kv, int lv0, int with_anchor,
+    uint16_t* __restrict__ cdf_anchor, uint16_t* __restrict__ cdf_delta,
+    uint32_t* __restrict__ status) {
+  extern __shared__ uint32_t cnt[];   // [kinds][32 channel pairs][kHist]
+  __shared__ uint32_t part[kFitWaves][64];
+  __shared__ uint32_t s_bad;
+  const int cb = blockIdx.x % P.nblk;
+  const int lk = blockIdx.x / P.nblk;
+  const int l = lk >> 1, k = lk & 1;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int nk = with_anchor + kNl;
+  for (int i = threadIdx.x; i < nk * 32 * kHist; i += kFitThreads) cnt[i] = 0;
+  if (threadIdx.x == 0) s_bad = 0u;
+  __syncthreads();
+
+  float wfac[kNl];
+#pragma unroll
+  for (int v = 0; v < kNl; ++v) wfac[v] = P.layer_bin[l] * P.level_mult[lv0 + v];
+  uint32_t* const hist_d = cnt + with_anchor * 32 * kHist;   // kind v: hist_d + v * 32 * kHist
+  const int pairs = P.B * P.NC;
+  const int64_t rs = P.C;
+  uint32_t bad = 0u;
+  // count one token of a channel (histogram row h of its pair, increment inc for its half)
+  auto count = [&](float x, int g, float s, float is, const float (&w)[kNl],
+                   const float (&iw)[kNl], float& a, int h, uint32_t inc)
+                   __attribute__((always_inline)) {
+    if (g == 0) {
+      const int q = cg_quant_inv(x, s, is);
+      a = (float)q * s;
+      if (with_anchor) atomicAdd(&cnt[h * kHist + q + 127], inc);
+    } else {
+      const float d = x - a;
+#pragma unroll
+      for (int v = 0; v < kNl; ++v) {
+        const int q = cg_quant_inv(d, w[v], iw[v]);
+        atomicAdd(&hist_d[(v * 32 + h) * kHist + q + 127], inc);
+      }
+    }
+  };
+  for (int pr = 0; pr < pairs; ++pr) {
+    const int b = pr / P.NC, c = pr % P.NC;
+    const int t0 = c * P.CL;
+    const int n = min(P.CL, P.T - t0);
+    const int ng = (n + P.G - 1) / P.G;                 // groups in the chunk
+    const int gpw = (ng + kFitWaves - 1) / kFitWaves;   // groups per wave
+    const int j0 = min(n, wave * gpw * P.G), j1 = min(n, (wave + 1) * gpw * P.G);
+    if constexpr (kRegs) {
+      // lane = (channel pair cp, token half th), as in fit_kernel's register path
+      const int cp = lane & 31, th = lane >> 5;
+      const int gh = (gpw + 1) >> 1;
+      const int h0 = min(j1, j0 + th * gh * P.G), h1 = min(j1, j0 + (th + 1) * gh * P.G);
+      const int len = h1 - h0;
+      const uint32_t* xw =
+          reinterpret_cast<const uint32_t*>(kv + cg_elem(P, b, l, k, t0, cb * 64)) + cp;
+      const int64_t rw = P.C >> 1;
+      uint32_t pk[kHalf];
+#pragma unroll
+      for (int u = 0; u < kHalf; ++u) pk[u] = xw[(int64_t)min(h0 + u, n - 1) * rw];
+      // magnitude bits: their maximum orders like |x| for finite halves and reaches 0x7c00
+      // exactly when a NaN or Inf is present
+      uint32_t m0 = 0u, m1 = 0u;
+#pragma unroll
+      for (int u = 0; u < kHalf; ++u) {
+        if (u < len) {
+          m0 = max(m0, pk[u] & 0x7FFFu);
+          m1 = max(m1, (pk[u] >> 16) & 0x7FFFu);
+        }
+      }
+      m0 = max(m0, (uint32_t)__shfl_xor((int)m0, 32, 64));
+      m1 = max(m1, (uint32_t)__shfl_xor((int)m1, 32, 64));
+      if (th == 0) {
+        part[wave][2 * cp] = m0;
+        part[wave][2 * cp + 1] = m1;
+      }
+      __syncthreads();
+      m0 = 0u;
+      m1 = 0u;
+#pragma unroll
+      for (int v = 0; v < kFitWaves; ++v) {
+        m0 = max(m0, part[v][2 * cp]);
+        m1 = max(m1, part[v][2 * cp + 1]);
+      }
+      bad |= (m0 >= 0x7C00u) | (m1 >= 0x7C00u);
+      const float mx0 = cg_h2f((uint16_t)m0), mx1 = cg_h2f((uint16_t)m1);
+      const float s0 = (mx0 == 0.0f) ? 1.0f : mx0 / 127.0f;
+      const float s1 = (mx1 == 0.0f) ? 1.0f : mx1 / 127.0f;
+      const float is0 = 1.0f / s0, is1 = 1.0f / s1;
+      float w0[kNl], w1[kNl], iw0[kNl], iw1[kNl];
+#pragma unroll
+      for (int v = 0; v < kNl; ++v) {
+        w0[v] = wfac[v] * s0;
+        w1[v] = wfac[v] * s1;
+        iw0[v] = 1.0f / w0[v];
+        iw1[v] = 1.0f / w1[v];
+      }
+      float a0 = 0.0f, a1 = 0.0f;
+      int g = 0;
+#pragma unroll
+      for (int u = 0; u < kHalf; ++u) {
+        if (u < len) {
+          count(cg_h2f((uint16_t)(pk[u] & 0xFFFFu)), g, s0, is0, w0, iw0, a0, cp, 1u);
+          count(cg_h2f((uint16_t)(pk[u] >> 16)), g, s1, is1, w1, iw1, a1, cp, 0x10000u);
+        }
+        g = (g + 1 == P.G) ? 0 : g + 1;
+      }
+    } else {
+      // a lane per channel; channel lane of the block is half (lane & 1) of pair lane / 2
+      const int ch = cb * 64 + lane;
+      const bool act = ch < P.C;
+      const uint16_t* x = kv + cg_elem(P, b, l, k, t0, act ? ch : cb * 64);
+      uint32_t m = 0u;
+#pragma unroll 8
+      for (int j = j0; j < j1; ++j) m = max(m, (uint32_t)x[(int64_t)j * rs] & 0x7FFFu);
+      part[wave][lane] = m;
+      __syncthreads();
+      m = 0u;
+#pragma unroll
+      for (int v = 0; v < kFitWaves; ++v) m = max(m, part[v][lane]);
+      bad |= act && m >= 0x7C00u;
+      const float mx = cg_h2f((uint16_t)m);
+      const float s = (mx == 0.0f) ? 1.0f : mx / 127.0f;
+      const float is = 1.0f / s;
+      float w[kNl], iw[kNl];
+#pragma unroll
+      for (int v = 0; v < kNl; ++v) {
+        w[v] = wfac[v] * s;
+        iw[v] = 1.0f / w[v];
+      }
+      if (act) {
+        float a = 0.0f;
+        int g = 0;
+        const uint32_t inc = (lane & 1) ? 0x10000u : 1u;
+#pragma unroll 4
+        for (int j = j0; j < j1; ++j) {
+          count(cg_h2f(x[(int64_t)j * rs]), g, s, is, w, iw, a, lane >> 1, inc);
+          g = (g + 1 == P.G) ? 0 : g + 1;
+        }
+      }
+    }
+    __syncthreads();   // `part` is reused by the next pair
+  }
+  if (bad) s_bad = 1u;   // benign race: every writer stores 1
+  __syncthreads();
+  if (threadIdx.x == 0 && s_bad && status) atomicOr(status, 1u);
+
+  for (int tb = wave; tb < nk * 64; tb += kFitWaves) {
+    const int kind = tb >> 6, cl = tb & 63;
+    const int chx = cb * 64 + cl;
+    if (chx >= P.C) continue;
+    uint16_t* dst = (with_anchor && kind == 0)
+                        ? cdf_anchor + ((int64_t)lk * P.C + chx) * 256
+                        : cdf_delta + (((int64_t)(lv0 + kind - with_anchor) * P.L * 2 + lk) * P.C +
+                                       chx) * 256;
+    normalize_wave<uint32_t>(cnt + (kind * 32 + (cl >> 1)) * kHist, dst, 16 * (cl & 1));
+  }
+}
+
+__global__ __launch_bounds__(64) void zero_word(uint32_t* w) {
+  if (threadIdx.x == 0) *w = 0u;
+}
+
 }  // namespace
 
 namespace {
@@ -275,14 +467,15 @@ bool fit_slice_in_registers(const KParams& P) {
 template <bool kPool, bool kRegs>
 hipError_t launch_fit_kernel(const KParams& P, const uint16_t* kv, int level,
                              uint16_t* cdf_anchor, uint16_t* cdf_delta_level,
-                             unsigned long long* pool, hipStream_t st) {
+                             unsigned long long* pool, hipStream_t st,
+                             uint32_t* status = nullptr) {
   const size_t lds = 2 * 64 * kHist * sizeof(uint32_t);
   hipError_t e = hipFuncSetAttribute((const void*)fit_kernel<kPool, kRegs>,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   const int64_t grid = (int64_t)P.L * 2 * P.nblk;
   hipLaunchKernelGGL((fit_kernel<kPool, kRegs>), dim3((unsigned)grid), dim3(kFitThreads), lds,
-                     st, P, kv, level, cdf_anchor, cdf_delta_level, pool);
+                     st, P, kv, level, cdf_anchor, cdf_delta_level, pool, status);
   return hipGetLastError();
 }
 }  // namespace
@@ -314,4 +507,73 @@ hipError_t cg_launch_fit_global(const KParams& P, const uint16_t* kv, int level,
   hipLaunchKernelGGL(pool_broadcast, dim3((unsigned)blocks), dim3(256), 0, st, tab, n_tables,
                      cdf_anchor, cdf_delta_level);
   return hipGetLastError();
+}
+
+namespace {
+template <bool kRegs>
+hipError_t launch_fit_levels(const KParams& P, const uint16_t* kv, int lv0, int nl,
+                             int with_anchor, uint16_t* cdf_anchor, uint16_t* cdf_delta,
+                             uint32_t* status, hipStream_t st) {
+  const size_t lds = (size_t)(with_anchor + nl) * 32 * kHist * sizeof(uint32_t);
+  const void* fn = nl == 1 ? (const void*)fit_levels_kernel<kRegs, 1>
+                 : nl == 2 ? (const void*)fit_levels_kernel<kRegs, 2>
+                 : nl == 3 ? (const void*)fit_levels_kernel<kRegs, 3>
+                           : (const void*)fit_levels_kernel<kRegs, 4>;
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  const dim3 grid((unsigned)((int64_t)P.L * 2 * P.nblk)), block(kFitThreads);
+  switch (nl) {
+    case 1: hipLaunchKernelGGL((fit_levels_kernel<kRegs, 1>), grid, block, lds, st, P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status); break;
+    case 2: hipLaunchKernelGGL((fit_levels_kernel<kRegs, 2>), grid, block, lds, st, P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status); break;
+    case 3: hipLaunchKernelGGL((fit_levels_kernel<kRegs, 3>), grid, block, lds, st, P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status); break;
+    default: hipLaunchKernelGGL((fit_levels_kernel<kRegs, 4>), grid, block, lds, st, P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status); break;
+  }
+  return hipGetLastError();
+}
+}  // namespace
+
+// Largest count any (channel, kind, symbol) of the fit can reach: the anchors or the deltas of
+// one channel over every chunk of every context.
+int64_t cg_fit_max_count(const KParams& P) {
+  int64_t na = 0, nd = 0;
+  for (int c = 0; c < P.NC; ++c) {
+    const int64_t n = (int64_t)(c + 1) * P.CL <= P.T ? P.CL : P.T - (int64_t)c * P.CL;
+    const int64_t a = (n + P.G - 1) / P.G;
+    na += a;
+    nd += n - a;
+  }
+  return (int64_t)P.B * (na > nd ? na : nd);
+}
+
+hipError_t cg_launch_fit_levels(const KParams& P, const uint16_t* kv, uint16_t* cdf_anchor,
+                                uint16_t* cdf_delta, uint32_t* status, hipStream_t st) {
+  if (cg_fit_max_count(P) >= 65536) {
+    // 16-bit counts could overflow: one 32-bit pass per level, and the finiteness scan
+    for (int v = 0; v < P.NLV; ++v) {
+      hipError_t e = cg_launch_fit(P, kv, v, v == 0 ? cdf_anchor : nullptr,
+                                   cdf_delta + (size_t)v * P.L * 2 * P.C * 256, st);
+      if (e != hipSuccess) return e;
+    }
+    return status ? cg_launch_check_finite(kv, (int64_t)P.B * P.L * 2 * P.T * P.C, status, st)
+                  : hipSuccess;
+  }
+  if (status) hipLaunchKernelGGL(zero_word, dim3(1), dim3(64), 0, st, status);
+  const bool regs = fit_slice_in_registers(P);
+  if (P.NLV == 1)   // one level: the 32-bit kernel of cg_fit_cdf (measured faster there)
+    return regs ? launch_fit_kernel<false, true>(P, kv, 0, cdf_anchor, cdf_delta, nullptr, st,
+                                                 status)
+                : launch_fit_kernel<false, false>(P, kv, 0, cdf_anchor, cdf_delta, nullptr, st,
+                                                  status);
+  // the anchors and up to three levels in the first pass, up to four levels in each further one
+  for (int lv0 = 0, pass = 0; lv0 < P.NLV; ++pass) {
+    const int wa = pass == 0 ? 1 : 0;
+    const int nl = min(P.NLV - lv0, kLevelKinds - wa);
+    hipError_t e = regs ? launch_fit_levels<true>(P, kv, lv0, nl, wa, cdf_anchor, cdf_delta,
+                                                  status, st)
+                        : launch_fit_levels<false>(P, kv, lv0, nl, wa, cdf_anchor, cdf_delta,
+                                                   status, st);
+    if (e != hipSuccess) return e;
+    lv0 += nl;
+  }
+  return hipSuccess;
 }

@@ -154,4 +154,9 @@ def test_alignment_is_checked_the_same_way_everywhere():
     assert lib.cg_decode_tokens(ctypes.byref(s), ok, ok, odd2, ok, ok, ok, ok, ws, dws, None) == -1
     # status: null or misaligned workspace
     assert lib.cg_get_status(None, None) == -1
-    assert lib.cg_get_status(ctypes.c_void_p(A + 16), None) == -1
+    assert lib.cg_get_status(ctypes.c_void_p(A + 2), None) == -1
+    # all-level fit: misaligned tables or status
+    assert lib.cg_fit_cdf_levels(ctypes.byref(s), ok, t8, ok, None, None) == -1
+    assert lib.cg_fit_cdf_levels(ctypes.byref(s), ok, ok, t8, None, None) == -1
+    assert lib.cg_fit_cdf_levels(ctypes.byref(s), ok, ok, ok, odd2, None) == -1
+    assert lib.cg_fit_cdf_levels(ctypes.byref(s), ok, None, ok, None, None) == -1

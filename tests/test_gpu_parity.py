@@ -249,3 +249,43 @@ def test_windowed_tables_chunk_ranges():
         mask = np.ones(w.n_tokens, bool)
         mask[t0:t1] = False
         assert np.all(part[..., mask, :] == 0)
+
+
+FIT_CASES = [
+    W.MISTRAL_7B_4K.with_(name="fit_mistral_l3", n_layers=3, layer_bin=(0.5, 1.0, 1.5)),
+    W.small(name="fit_levels4_regs", n_layers=2, n_channels=128, n_tokens=1600, chunk_len=1536,
+            level_mult=(1.0, 2.0, 4.0, 8.0)),
+    W.small(name="fit_levels8_c70", n_layers=2, n_channels=70, n_tokens=300, chunk_len=64,
+            level_mult=(1.0, 2.0, 4.0, 8.0, 16.0, 32.0, 64.0, 128.0)),
+    W.small(name="fit_levels5_g7", group_size=7, n_layers=2, n_channels=64, n_tokens=200,
+            chunk_len=50, level_mult=(1.0, 1.5, 2.0, 3.0, 5.0)),
+    # more than 2^16 deltas of one channel: the 32-bit per-level path
+    W.small(name="fit_long_t76000", n_layers=1, n_channels=64, n_tokens=76000, chunk_len=1536,
+            level_mult=(1.0, 4.0)),
+]
+
+
+@pytest.mark.parametrize("w", FIT_CASES, ids=lambda w: w.name)
+def test_fit_all_levels_equals_oracle_and_per_level(w):
+    """cg_fit_cdf_levels (every level in one call) against the oracle's per-level fit and
+    against cg_fit_cdf level by level, bit for bit; its status word reports NaN."""
+    torch = torch_cuda()
+    import oracle
+    from paper_2310_07240_amd.cachegen import Codec, CodecParams, cg_get_status
+    kv_np = W.generate(w)
+    oca, ocd = oracle.fit_all_levels(kv_np, oracle.shape_from(w))
+    codec = Codec(CodecParams.of(w))
+    kv = torch.from_numpy(kv_np.view(np.int16)).cuda()
+    st = torch.full((1,), 7, dtype=torch.int32, device="cuda")
+    ca, cd = codec.fit(kv, status=st)
+    ca1, cd1 = codec.fit_per_level(kv)
+    torch.cuda.synchronize()
+    assert cg_get_status(st) == 0
+    assert_same("anchor tables", ca.cpu().numpy().view(np.uint16), oca)
+    assert_same("delta tables", cd.cpu().numpy().view(np.uint16), ocd)
+    assert_same("per-level anchor tables", ca1.cpu().numpy(), ca.cpu().numpy())
+    assert_same("per-level delta tables", cd1.cpu().numpy(), cd.cpu().numpy())
+    bad = kv.clone()
+    bad.view(-1)[bad.numel() // 3] = 0x7C00     # +Inf
+    codec.fit(bad, status=st)
+    assert cg_get_status(st) == -4

@@ -106,7 +106,7 @@ def test_get_status_rejects_bad_workspace():
     import ctypes
     s = torch.cuda.current_stream()
     assert cg.lib().cg_get_status(None, ctypes.c_void_p(s.cuda_stream)) == -1
-    assert cg.lib().cg_get_status(ctypes.c_void_p(ws.data_ptr() + 4),
+    assert cg.lib().cg_get_status(ctypes.c_void_p(ws.data_ptr() + 2),
                                   ctypes.c_void_p(s.cuda_stream)) == -1
 
 
