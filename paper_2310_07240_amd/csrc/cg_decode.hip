@@ -917,30 +917,9 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
       }
 #pragma unroll
       for (int i = 0; i < kStageBatch; ++i) {
-        // cum[8 piece + j], j = 0..8 (the ninth from the next lane; cum[255] = 65536)
-        const uint32_t e0 = v[i].x & 0xFFFFu, e1 = v[i].x >> 16, e2 = v[i].y & 0xFFFFu;
-        const uint32_t e3 = v[i].y >> 16, e4 = v[i].z & 0xFFFFu, e5 = v[i].z >> 16;
-        const uint32_t e6 = v[i].w & 0xFFFFu;
-        const uint32_t e7 = piece == 31 ? CG_TOTAL : v[i].w >> 16;
-        const uint32_t e8 = (uint32_t)__shfl_down((int)e0, 1, 32);
-        const uint32_t e[9] = {e0, e1, e2, e3, e4, e5, e6, e7, e8};
-        int lo = 255, hi = -1;
-#pragma unroll
-        for (int jj = 7; jj >= 0; --jj)
-          if (8 * piece + jj < CG_NSYM && e[jj + 1] - e[jj] != 1u) lo = 8 * piece + jj;
-#pragma unroll
-        for (int jj = 0; jj < 8; ++jj)
-          if (8 * piece + jj < CG_NSYM && e[jj + 1] - e[jj] != 1u) hi = 8 * piece + jj;
-#pragma unroll
-        for (int o = 16; o >= 1; o >>= 1) {
-          lo = min(lo, __shfl_xor(lo, o, 32));
-          hi = max(hi, __shfl_xor(hi, o, 32));
-        }
-        if (hi < lo) { lo = 0; hi = CG_NSYM - 1; }   // no such frequency: not a valid table
-        if (rows[i] >= 0 && piece == 0) {
-          const int g0 = max(lo / 16 - 1, 0), g1 = min(hi / 16 + 1, 15);
-          desc[rows[i]] = (uint32_t)g0 | ((uint32_t)g1 << 4) | ((uint32_t)((g1 - g0 + 1) * 32 + 8) << 8);
-        }
+        int lo, hi;
+        cg_table_window(v[i], piece, lo, hi);
+        if (rows[i] >= 0 && piece == 0) desc[rows[i]] = cg_window_desc(lo, hi);
       }
     }
   };
@@ -1149,15 +1128,21 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     for (int uu = 0; uu < nu; ++uu) nrounds = max(nrounds, (int)s_nrounds[uu]);
     nrounds = uni(nrounds);
   }
-  for (int rd = 0; rd < nrounds; ++rd) {
+  // this wave's round (past the last one: nothing to decode); the rounds before and after it
+  // only stage and wait, so that the decoding runs outside any loop
+  const int set = active ? (int)s_set_of_level[u][lv] : 0;
+  const int myr = uni(!active || n < 2 ? nrounds : (kCompact ? (int)s_round[u][set] : 0));
+  auto round_stage = [&](int rd) __attribute__((always_inline)) {
     if (rd > 0) __syncthreads();   // the previous round's readers are done
     if constexpr (kCompact) stage_round(rd);
     else stage(false);
     __syncthreads();
-    if (!active || n < 2) continue;
-    const int set = s_set_of_level[u][lv];
+  };
+  for (int rd = 0; rd < myr; ++rd) round_stage(rd);
+  if (myr >= nrounds) return;
+  round_stage(myr);
+  {
     if constexpr (kCompact) {
-      if ((int)s_round[u][set] != rd) continue;
       const uint32_t d = desc[(u * msets + set) * 64 + lsrc];
       const int g0 = (int)((d >> 20) & 15u), g1 = (int)((d >> 24) & 15u);
       const WinTab T{lds_addr(tabs + u * ustride) + (d & 0xFFFFFu) - 32u * (uint32_t)g0, 16 * g0,
@@ -1172,6 +1157,7 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
       delta_groups(FullTab{dtab}, fD, lds_addr(dtab));
     }
   }
+  for (int rd = myr + 1; rd < nrounds; ++rd) round_stage(rd);
 }
 
 // ---- token-parallel layout (Sec. 6: the paper's decoder runs one thread per token) -----------

@@ -124,6 +124,44 @@ inline int64_t cg_xcd_grid(int64_t n_ublk, int64_t n_groups) {
   return n_groups == 1 ? n_ublk : (n_ublk + 7) / 8 * 8 * n_groups;
 }
 
+// Window of a cumulative table held by 32 lanes of a wave, 16 bytes (8 entries) each: piece p
+// holds cum[8 p .. 8 p + 7] in v (the other half of the wave may hold another table). Returns
+// in lo / hi the first and the last symbol i in [0, 254] whose frequency cum[i + 1] - cum[i] is
+// not 1 (entry 255 is padding; the total 65536 stands in for it), the same in all 32 lanes. A
+// table without such a frequency (not a valid table) gives [0, 254]. Every frequency outside
+// [lo, hi] is 1, so cum[i] = i for i <= lo and cum[i] = 65281 + i for i > hi.
+__device__ __forceinline__ void cg_table_window(const uint4& v, int piece, int& lo, int& hi) {
+  const uint32_t e0 = v.x & 0xFFFFu, e1 = v.x >> 16, e2 = v.y & 0xFFFFu, e3 = v.y >> 16;
+  const uint32_t e4 = v.z & 0xFFFFu, e5 = v.z >> 16, e6 = v.w & 0xFFFFu;
+  const uint32_t e7 = piece == 31 ? CG_TOTAL : v.w >> 16;
+  const uint32_t e8 = (uint32_t)__shfl_down((int)e0, 1, 32);   // the next lane's first entry
+  const uint32_t e[9] = {e0, e1, e2, e3, e4, e5, e6, e7, e8};
+  lo = 255;
+  hi = -1;
+#pragma unroll
+  for (int jj = 7; jj >= 0; --jj)
+    if (8 * piece + jj < CG_NSYM && e[jj + 1] - e[jj] != 1u) lo = 8 * piece + jj;
+#pragma unroll
+  for (int jj = 0; jj < 8; ++jj)
+    if (8 * piece + jj < CG_NSYM && e[jj + 1] - e[jj] != 1u) hi = 8 * piece + jj;
+#pragma unroll
+  for (int o = 16; o >= 1; o >>= 1) {
+    lo = min(lo, __shfl_xor(lo, o, 32));
+    hi = max(hi, __shfl_xor(hi, o, 32));
+  }
+  if (hi < lo) {
+    lo = 0;
+    hi = CG_NSYM - 1;
+  }
+}
+
+// The 16-entry blocks g0 .. g1 a window keeps: the blocks holding lo and hi extended by one
+// block on each side (g1 > g0), and its size in bytes: entries 16 g0 .. 16 (g1 + 1) + 3.
+__device__ __forceinline__ uint32_t cg_window_desc(int lo, int hi) {
+  const int g0 = max(lo / 16 - 1, 0), g1 = min(hi / 16 + 1, 15);
+  return (uint32_t)g0 | ((uint32_t)g1 << 4) | ((uint32_t)((g1 - g0 + 1) * 32 + 8) << 8);
+}
+
 template <typename T>
 __device__ __forceinline__ T cg_wave_sum(T v) {
 #pragma unroll

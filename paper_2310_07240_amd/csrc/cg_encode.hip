@@ -33,11 +33,15 @@ namespace {
 
 constexpr int kEncMaxWaves = 16;
 constexpr int kEncMaxUnits = 16;   // (layer, K/V, channel block) units per workgroup
+// waves per workgroup with windowed delta tables: their lookups need more registers than 16
+// waves per CU leave (at 12, three waves per SIMD, each may hold 168)
+constexpr int kEncWinWaves = 12;
 constexpr int kEncStageBatch = 8;  // table-staging loads in flight per lane
 constexpr int kCompactRows = 128;  // slot rows per pass of the compaction
 // static LDS of the kernel with several units (masks, level maps, SIMD ids, remaining counts);
 // the dynamic LDS budget leaves 1 KB for it
-static_assert(4 * kEncMaxUnits + 3 * kEncMaxUnits * CG_MAX_LEVELS + kEncMaxWaves + 4 * kEncMaxWaves <= 1024 - 64,
+static_assert(4 * kEncMaxUnits + 4 * kEncMaxUnits * CG_MAX_LEVELS + 2 * kEncMaxUnits + kEncMaxWaves +
+                  4 * kEncMaxWaves + 4 <= 1024 - 64,
               "static LDS exceeds the reserve");
 constexpr size_t kEncLdsBudget = 160 * 1024 - 1024;   // dynamic LDS per workgroup (CDNA4: 160 KB)
 constexpr int kEncTabStride = 258;   // u16 per delta table in LDS (odd word stride: lanes spread over banks)
@@ -223,18 +227,24 @@ __device__ __forceinline__ void enc_finish(EncState& e, BitSink& o) {
 // group (kG = 10: the anchor is always the step's first token, so every step issues the same
 // memory operations); other group sizes use steps of 8 tokens (kG = 0).
 
-template <int kG>
-__global__ __launch_bounds__(1024) void encode_kernel(
+// kWin: the delta tables are staged as windows of their 16-entry blocks (cg_table_window):
+// each unit has a region of ustride u16 (at least one whole table set), holding its anchor
+// tables for the anchor pass and then the packed windows of its delta tables; sets that do not
+// fit together are staged in rounds. Entries outside a window follow the flat closed forms.
+// Otherwise the region holds nsets_lds whole sets.
+template <int kG, bool kWin>
+__global__ __launch_bounds__(kWin ? 64 * kEncWinWaves : 1024) void encode_kernel(
     KParams P, const uint16_t* __restrict__ kv, const uint8_t* __restrict__ chunk_level,
     const uint16_t* __restrict__ cdfA, const uint16_t* __restrict__ cdfD,
     uint32_t* __restrict__ slots, uint32_t slot_words, uint32_t* __restrict__ lens,
-    float* __restrict__ scales, uint32_t* __restrict__ wflags, int nw, int nu, int nsets_lds) {
+    float* __restrict__ scales, uint32_t* __restrict__ wflags, int nw, int nu, int nsets_lds,
+    int ustride) {
   // workgroup = nu units (layer, K/V, 64-channel block) x nw (context, chunk) pairs; wave w
   // codes pair slot w / nu of unit w % nu (one workgroup per CU where the grid allows, so the
   // hardware spreads its waves evenly over the SIMDs). The anchor tables of the units are
   // staged in LDS for the anchor pass, then the delta tables of the levels their pairs use for
   // the delta pass.
-  extern __shared__ __attribute__((aligned(16))) uint16_t tabs[];   // [nu][nsets][64][kEncTabStride], then words [nu * nw][kRing][64]
+  extern __shared__ __attribute__((aligned(16))) uint16_t tabs[];   // [nu][ustride], then words [nu * nw][kRing][64], then window descriptors [nu][nsets][64] (kWin)
   __shared__ uint32_t s_mask[kEncMaxUnits];
   __shared__ uint8_t s_set_of_level[kEncMaxUnits][CG_MAX_LEVELS];
   __shared__ uint8_t s_level_of_set[kEncMaxUnits][CG_MAX_LEVELS];
@@ -242,6 +252,8 @@ __global__ __launch_bounds__(1024) void encode_kernel(
   __shared__ uint8_t s_simd[kEncMaxWaves];   // SIMD of each wave
   __shared__ int s_left[kEncMaxWaves];   // symbols each wave has left to code
   __shared__ uint32_t s_bad;               // some stream of the workgroup holds NaN or Inf
+  __shared__ uint8_t s_round[kEncMaxUnits][CG_MAX_LEVELS];   // staging round of each set (kWin)
+  __shared__ uint8_t s_nrounds[kEncMaxUnits];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int nwaves = blockDim.x >> 6;
   const int u = wave % nu, j = wave / nu;
@@ -310,7 +322,7 @@ __global__ __launch_bounds__(1024) void encode_kernel(
         const int64_t trow = anchors ? (int64_t)lk * P.C + chs
                                      : ((int64_t)lset * P.L * 2 + lk) * P.C + chs;
         v[i] = reinterpret_cast<const uint4*>(srcbase + (ok ? trow : 0) * 256)[piece];
-        dsto[i] = ok ? ((uu * nsets_lds + st) * 64 + t) * kEncTabStride + piece * 8 : -1;
+        dsto[i] = ok ? uu * ustride + (st * 64 + t) * kEncTabStride + piece * 8 : -1;
       }
 #pragma unroll
       for (int i = 0; i < kEncStageBatch; ++i) {
@@ -323,8 +335,99 @@ __global__ __launch_bounds__(1024) void encode_kernel(
       }
     }
   };
+  uint32_t* const rings_base = reinterpret_cast<uint32_t*>(tabs + (size_t)nu * ustride);
+  uint32_t* const desc = rings_base + (size_t)nu * nw * kRing * 64;   // kWin
+  // Window staging of the delta tables (kWin): pass 1 finds each table's window, pass 2 (one
+  // wave per unit) lays the windows out set after set with a new round whenever a set does not
+  // fit the region any more, and stage_round writes the windows of one round's sets.
+  auto window_pass = [&]() __attribute__((always_inline)) {
+    const int n_rows = nu * nsets_lds * 64;
+    for (int base = wave; base * 2 < n_rows; base += nwaves * kEncStageBatch) {
+      uint4 v[kEncStageBatch];
+      int rows[kEncStageBatch];
+#pragma unroll
+      for (int i = 0; i < kEncStageBatch; ++i) {
+        const int rr = (base + i * nwaves) * 2 + half;
+        const int t = rr & 63, st = (rr >> 6) % nsets_lds;
+        const int uu = min((rr >> 6) / nsets_lds, nu - 1);
+        const int unit2 = ublk * nu + uu;
+        const int chs = (unit2 % P.nblk) * 64 + t;
+        const int lset = s_level_of_set[uu][st];
+        const bool ok = (rr < n_rows) & (unit2 < n_units) & (st < (int)s_nsets[uu]) & (chs < P.C);
+        const int64_t trow = ((int64_t)lset * P.L * 2 + unit2 / P.nblk) * P.C + chs;
+        v[i] = reinterpret_cast<const uint4*>(cdfD + (ok ? trow : 0) * 256)[piece];
+        rows[i] = ok ? rr : -1;
+      }
+#pragma unroll
+      for (int i = 0; i < kEncStageBatch; ++i) {
+        int lo, hi;
+        cg_table_window(v[i], piece, lo, hi);
+        if (rows[i] >= 0 && piece == 0) desc[rows[i]] = cg_window_desc(lo, hi);
+      }
+    }
+  };
+  auto layout_pass = [&]() __attribute__((always_inline)) {
+    if (wave >= nu) return;   // one wave per unit (uniform)
+    const int uu = wave;
+    const int unit2 = ublk * nu + uu;
+    const int pool = 2 * ustride;
+    const bool chok = unit2 < n_units && (unit2 % P.nblk) * 64 + lane < P.C;
+    int round = 0, acc = 0;
+    for (int st = 0; st < nsets_lds; ++st) {
+      const int idx = (uu * nsets_lds + st) * 64 + lane;
+      const bool ok = chok && st < (int)s_nsets[uu];
+      const uint32_t d = ok ? desc[idx] : 0u;
+      const uint32_t sz = d >> 8;
+      const uint32_t incl = cg_wave_incl_scan(sz);
+      const int tot = __builtin_amdgcn_readfirstlane((int)__shfl(incl, 63, 64));
+      if (acc > 0 && acc + tot > pool) { ++round; acc = 0; }
+      if (ok) desc[idx] = (uint32_t)(acc + (int)(incl - sz)) | ((d & 0xFFu) << 20);
+      if (lane == 0) s_round[uu][st] = (uint8_t)round;
+      acc += tot;
+    }
+    if (lane == 0) s_nrounds[uu] = (uint8_t)(round + 1);
+  };
+  auto stage_round = [&](int rd) __attribute__((always_inline)) {
+    const int n_rows = nu * nsets_lds * 64;
+    for (int base = wave; base * 2 < n_rows; base += nwaves * kEncStageBatch) {
+      uint4 v[kEncStageBatch];
+      int dsto[kEncStageBatch], k0s[kEncStageBatch], kends[kEncStageBatch];
+#pragma unroll
+      for (int i = 0; i < kEncStageBatch; ++i) {
+        const int rr = (base + i * nwaves) * 2 + half;
+        const int t = rr & 63, st = (rr >> 6) % nsets_lds;
+        const int uu = min((rr >> 6) / nsets_lds, nu - 1);
+        const int unit2 = ublk * nu + uu;
+        const int chs = (unit2 % P.nblk) * 64 + t;
+        const int lset = s_level_of_set[uu][st];
+        const bool ok = (rr < n_rows) & (unit2 < n_units) & (st < (int)s_nsets[uu]) &
+                        (chs < P.C) && (int)s_round[uu][st] == rd;
+        const int64_t trow = ((int64_t)lset * P.L * 2 + unit2 / P.nblk) * P.C + chs;
+        v[i] = reinterpret_cast<const uint4*>(cdfD + (ok ? trow : 0) * 256)[piece];
+        const uint32_t d = ok ? desc[min(rr, n_rows - 1)] : 0u;
+        dsto[i] = ok ? uu * ustride + (int)((d & 0xFFFFFu) >> 1) : -1;
+        k0s[i] = 16 * (int)((d >> 20) & 15u);
+        kends[i] = 16 * ((int)((d >> 24) & 15u) + 1) + 4;
+      }
+#pragma unroll
+      for (int i = 0; i < kEncStageBatch; ++i) {
+        if (dsto[i] < 0) continue;
+        uint16_t* dst = tabs + dsto[i] - k0s[i];   // entry k of the table at dst[k]
+        const int e = 8 * piece;
+        if (e >= k0s[i] && e < kends[i])
+          *reinterpret_cast<uint2*>(dst + e) = make_uint2(v[i].x, v[i].y);
+        if (e + 4 >= k0s[i] && e + 4 < kends[i])
+          *reinterpret_cast<uint2*>(dst + e + 4) = make_uint2(v[i].z, v[i].w);
+      }
+    }
+  };
   stage(true);
+  if constexpr (kWin) window_pass();
   __syncthreads();
+  if constexpr (kWin) {
+    layout_pass();
+    __syncthreads();
+  }
 
   // Absmax of the streams. When the workgroup holds four channel-contiguous units of one
   // (layer, K/V) and all its pairs are valid (uniform over the workgroup), the four waves of a
@@ -340,7 +443,7 @@ __global__ __launch_bounds__(1024) void encode_kernel(
   // least 0x7c00, which flags the stream as outside the quantizer's domain.
   uint32_t mx_coop = 0u;
   if (coop) {
-    uint32_t* part = reinterpret_cast<uint32_t*>(tabs + nu * nsets_lds * 64 * kEncTabStride);
+    uint32_t* part = rings_base;
     const uint16_t* xr = kv + cg_elem(P, b, l, k, c * P.CL, cb0 * 64) + 4 * lane;
     const int64_t rs4 = P.C;
     const int nr = (n - u + 3) / 4;   // rows u, u + 4, ... below n
@@ -411,11 +514,13 @@ __global__ __launch_bounds__(1024) void encode_kernel(
   const float w = bw * s;
   const float is = 1.0f / s, iw = 1.0f / w;
 
-  cg_lds_u16* tabA = (cg_lds_u16*)(tabs + (u * nsets_lds * 64 + lane) * kEncTabStride);   // set 0
-  cg_lds_u16* tabD =
-      (cg_lds_u16*)(tabs + ((u * nsets_lds + s_set_of_level[u][lv]) * 64 + lane) * kEncTabStride);
+  cg_lds_u16* tabA = (cg_lds_u16*)(tabs + u * ustride + lane * kEncTabStride);   // anchors
+  // the lane's delta table: the whole table (entry i at tabD[i]), or its window (entries wk0
+  // .. wk1 + 3 at tabD[i], the rest by the closed forms); set for the delta pass
+  cg_lds_u16* tabD = nullptr;
+  int wk0 = 0, wk1 = 0;
   EncState e{0u, 0xFFFFFFFFu, 0u};
-  uint32_t* rings = reinterpret_cast<uint32_t*>(tabs + nu * nsets_lds * 64 * kEncTabStride);
+  uint32_t* rings = rings_base;
   // the slots of a wave's 64 streams, interleaved by 16-byte chunk
   const uint64_t slot_group = (uint64_t)bclk * P.nblk + cb;
   BitSink o{slots + slot_group * slot_words * 64 + lane * 4, slot_words, 0u, 0u, 0ull, 0u,
@@ -425,7 +530,6 @@ __global__ __launch_bounds__(1024) void encode_kernel(
   // body is written out for both so no buffer is ever copied: a copy of a register that a
   // load is still filling would make the copy wait for that load and for every memory
   // operation issued after it). xr*: row values; lo* / hi*: the table entries of a step.
-  uint32_t xr0[kPipe], xr1[kPipe], lo0[kPipe], hi0[kPipe], lo1[kPipe], hi1[kPipe];
   const int last = n - 1;
   float a = 0.0f;
   int gq = 0;   // group position of the next token to quantize (uniform)
@@ -445,6 +549,16 @@ __global__ __launch_bounds__(1024) void encode_kernel(
         a = (float)q * s;
         clo[u] = 0u;
         chi[u] = 0u;
+      } else if constexpr (kWin) {
+        // sc = sym clamped so that sc and sc + 1 lie in the window. Every frequency from sc
+        // out to sym is 1 (below the window cum[i] = i up to the first other frequency, above
+        // it cum[i] = 65281 + i from past the last one), so cum[sym] = cum[sc] + (sym - sc) and
+        // cum[sym + 1] = cum[sc + 1] + (sym - sc) exactly, inside the window too (sym = sc)
+        const int sc = min(max(sym, wk0), wk1 - 1);
+        const uint32_t dsym = (uint32_t)(sym - sc);
+        clo[u] = (uint32_t)tabD[sc] + dsym;
+        chi[u] = (uint32_t)tabD[sc + 1] + dsym;
+        chi[u] = sym == CG_NSYM - 1 ? CG_TOTAL : chi[u];
       } else {
         clo[u] = tabD[sym];
         chi[u] = tabD[sym1];
@@ -557,12 +671,10 @@ __global__ __launch_bounds__(1024) void encode_kernel(
       set_priority(max(na - (st + 2) * kPipeA, 0));
     }
   }
-  // the delta tables replace the anchor tables
-  __syncthreads();
-  if (threadIdx.x == 0) wflags[blockIdx.x] = s_bad;   // every workgroup writes its flag
-  stage(false);
-  __syncthreads();
-  if (!lane_ok) return;
+  // the delta pass: a software pipeline over steps of kPipe tokens (rows two steps ahead,
+  // table entries one step ahead), then the termination and the stream's word count
+  auto delta_pass = [&]() __attribute__((always_inline)) {
+  uint32_t xr0[kPipe], xr1[kPipe], lo0[kPipe], hi0[kPipe], lo1[kPipe], hi1[kPipe];
   load_rows(xr0, 0);
   load_rows(xr1, 1);
   quantize_step(xr0, lo0, hi0);
@@ -588,6 +700,42 @@ __global__ __launch_bounds__(1024) void encode_kernel(
   // the coder's bound for n symbols; the compaction never writes past the sum of these
   const uint32_t own_bound = (uint32_t)((18ull * (uint64_t)n + 2ull + 31ull) / 32ull);
   lens[sidx] = min(o.nwords, min(own_bound, slot_words));
+  };
+
+  // the delta tables replace the anchor tables (in rounds when windows of all sets do not fit a
+  // unit's region at once: every wave takes part in every round's staging and barriers, and
+  // codes in its set's round)
+  __syncthreads();
+  if (threadIdx.x == 0) wflags[blockIdx.x] = s_bad;   // every workgroup writes its flag
+  int nrounds = 1;
+  if constexpr (kWin) {
+    for (int uu = 0; uu < nu; ++uu) nrounds = max(nrounds, (int)s_nrounds[uu]);
+    nrounds = __builtin_amdgcn_readfirstlane(nrounds);
+  }
+  const int set = active ? (int)s_set_of_level[u][lv] : 0;
+  // this wave's round (past the last one: no coding); the rounds before and after it only
+  // stage and wait, so that the coding runs outside any loop
+  const int myr = __builtin_amdgcn_readfirstlane(
+      !active ? nrounds : (kWin ? (int)s_round[u][set] : 0));
+  auto round_stage = [&](int rd) __attribute__((always_inline)) {
+    if (rd > 0) __syncthreads();   // the previous round's readers are done
+    if constexpr (kWin) stage_round(rd);
+    else stage(false);
+    __syncthreads();
+  };
+  for (int rd = 0; rd < myr; ++rd) round_stage(rd);
+  if (myr >= nrounds) return;
+  round_stage(myr);
+  if constexpr (kWin) {
+    const uint32_t d = desc[(u * nsets_lds + set) * 64 + (lane_ok ? lane : 0)];
+    wk0 = 16 * (int)((d >> 20) & 15u);
+    wk1 = 16 * ((int)((d >> 24) & 15u) + 1);
+    tabD = (cg_lds_u16*)(tabs + u * ustride + (d & 0xFFFFFu) / 2) - wk0;
+  } else {
+    tabD = (cg_lds_u16*)(tabs + u * ustride + (set * 64 + lane) * kEncTabStride);
+  }
+  if (lane_ok) delta_pass();
+  for (int rd = myr + 1; rd < nrounds; ++rd) round_stage(rd);
 }
 
 // Block reduction helper: sum of one value per thread of a 256-thread block.
@@ -875,6 +1023,8 @@ struct EncGeom {
   int nw, nu, nsets;
   int64_t n_groups, g1;
   size_t lds;
+  bool win;      // delta tables staged as windows (encode_kernel<kG, true>)
+  int ustride;   // u16 per unit region
 };
 
 EncGeom enc_geometry(const KParams& P) {
@@ -895,11 +1045,31 @@ EncGeom enc_geometry(const KParams& P) {
          lds_for(nw, nu + 1) <= kEncLdsBudget && (n_units + nu) / (nu + 1) * n_groups >= 256)
     ++nu;
   g.nw = nw;
-  g.nu = nu;
   g.nsets = nw < P.NLV ? nw : P.NLV;
   g.n_groups = n_groups;
-  g.g1 = cg_xcd_grid((n_units + nu - 1) / nu, n_groups);
-  g.lds = lds_for(nw, nu);
+  // With several levels the delta tables can be staged as windows: a unit then needs a region
+  // of one whole table set (its anchor tables) plus its rings and window descriptors, so more
+  // units fit a workgroup. Used when that allows more units.
+  const size_t rings = (size_t)nw * kRing * 64 * sizeof(uint32_t);   // per unit
+  const size_t set_bytes = (size_t)64 * kEncTabStride * sizeof(uint16_t);
+  const size_t desc_bytes = (size_t)g.nsets * 64 * sizeof(uint32_t);
+  int nuc = 1;
+  while (nuc < kEncMaxUnits && (nuc + 1) * nw <= kEncWinWaves &&
+         (size_t)(nuc + 1) * (rings + set_bytes + desc_bytes) <= kEncLdsBudget &&
+         (n_units + nuc) / (nuc + 1) * n_groups >= 256)
+    ++nuc;
+  g.win = g.nsets > 1 && nuc > nu;
+  if (g.win) {
+    g.nu = nuc;
+    const size_t per_unit = kEncLdsBudget / (size_t)nuc - rings - desc_bytes;
+    g.ustride = (int)((per_unit & ~(size_t)15) / sizeof(uint16_t));
+    g.lds = (size_t)nuc * (rings + desc_bytes) + (size_t)nuc * g.ustride * sizeof(uint16_t);
+  } else {
+    g.nu = nu;
+    g.ustride = g.nsets * 64 * kEncTabStride;
+    g.lds = lds_for(nw, nu);
+  }
+  g.g1 = cg_xcd_grid((n_units + g.nu - 1) / g.nu, n_groups);
   return g;
 }
 
@@ -936,18 +1106,26 @@ hipError_t cg_launch_encode(const KParams& P, const uint16_t* kv, const uint8_t*
   uint64_t* partial = reinterpret_cast<uint64_t*>(base + lay.partial_off);
 
   const EncGeom g = enc_geometry(P);
-  const void* kfn = P.G == 10 ? (const void*)encode_kernel<10> : (const void*)encode_kernel<0>;
+  const void* kfn = P.G == 10 ? (g.win ? (const void*)encode_kernel<10, true>
+                                       : (const void*)encode_kernel<10, false>)
+                              : (g.win ? (const void*)encode_kernel<0, true>
+                                       : (const void*)encode_kernel<0, false>);
   hipError_t e =
       hipFuncSetAttribute(kfn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)g.lds);
   if (e != hipSuccess) return e;
-  if (P.G == 10)
-    hipLaunchKernelGGL(encode_kernel<10>, dim3((unsigned)g.g1), dim3(64 * g.nw * g.nu), g.lds,
-                       st, P, kv, chunk_level, cdf_anchor, cdf_delta, slots, slot_words, lens,
-                       scales, wflags, g.nw, g.nu, g.nsets);
-  else
-    hipLaunchKernelGGL(encode_kernel<0>, dim3((unsigned)g.g1), dim3(64 * g.nw * g.nu), g.lds,
-                       st, P, kv, chunk_level, cdf_anchor, cdf_delta, slots, slot_words, lens,
-                       scales, wflags, g.nw, g.nu, g.nsets);
+  const dim3 grid((unsigned)g.g1), block(64 * g.nw * g.nu);
+#define CG_ENCODE_LAUNCH(KG, KW)                                                              \
+  hipLaunchKernelGGL((encode_kernel<KG, KW>), grid, block, g.lds, st, P, kv, chunk_level,     \
+                     cdf_anchor, cdf_delta, slots, slot_words, lens, scales, wflags, g.nw,    \
+                     g.nu, g.nsets, g.ustride)
+  if (P.G == 10) {
+    if (g.win) CG_ENCODE_LAUNCH(10, true);
+    else CG_ENCODE_LAUNCH(10, false);
+  } else {
+    if (g.win) CG_ENCODE_LAUNCH(0, true);
+    else CG_ENCODE_LAUNCH(0, false);
+  }
+#undef CG_ENCODE_LAUNCH
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t nb = (P.S + kScanBlock - 1) / kScanBlock;
