@@ -162,7 +162,7 @@ __global__ __launch_bounds__(1024) void decode_kernel(
   const int n_pairs = P.B * ncr;
   const int n_groups = (n_pairs + nw - 1) / nw;
   int rest, grp;
-  cg_xcd_map(n_groups, rest, grp);
+  cg_xcd_map(P.L * 2 * P.nblk, n_groups, rest, grp);
   if (rest >= P.L * 2 * P.nblk) return;   // past the last unit (uniform over the workgroup)
   const int cb = rest % P.nblk;
   rest /= P.nblk;
@@ -792,7 +792,7 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   const int n_groups = (n_pairs + nw - 1) / nw;
   const int n_units = P.L * 2 * P.nblk;
   int ublk, grp;
-  cg_xcd_map(n_groups, ublk, grp);
+  cg_xcd_map((n_units + nu - 1) / nu, n_groups, ublk, grp);
   if (ublk * nu >= n_units) return;   // past the last unit block (uniform over the workgroup)
   const int unit = ublk * nu + u;
   const int cb = unit % P.nblk;

@@ -109,16 +109,18 @@ __device__ __forceinline__ int64_t tok_stream(const KParams& P, int b, int c, in
 }
 
 // Workgroup -> (unit block, pair group) for grids of n_ublk unit blocks x n_groups pair groups.
-// The hardware deals workgroups to the 8 XCDs in turn (block i to XCD i mod 8). Blocks are
-// numbered in stripes of 8 unit blocks x n_groups: the pair groups of one unit block land on one
-// XCD (they share the unit's tables in that XCD's L2), and every XCD cycles through the pair
-// groups (their chunk lengths and contexts differ). The grid is cg_xcd_grid() blocks; blocks of
-// the last, partial stripe past n_ublk get ublk >= n_ublk and must leave.
-__device__ __forceinline__ void cg_xcd_map(int n_groups, int& ublk, int& grp) {
-  const int stripe = 8 * n_groups;
+// Workgroups are dispatched in block order, each as soon as a CU of its XCD can take it, and the
+// hardware deals them to the 8 XCDs in turn (block i to XCD i mod 8). Blocks go pair group by
+// pair group: pair groups follow chunk order, so the workgroups of the long chunks start first
+// and those of a short last chunk fill in at the end (with the pair group as the fastest index,
+// a CU that finished a short workgroup waited for the next long one ahead of its own in the
+// queue). Unit blocks are numbered to a multiple of 8 per pair group, so all pair groups of a
+// unit block run on one XCD (its tables stay in that XCD's L2); blocks past n_ublk must leave.
+__device__ __forceinline__ void cg_xcd_map(int n_ublk, int n_groups, int& ublk, int& grp) {
+  const int pad = n_groups == 1 ? n_ublk : (n_ublk + 7) / 8 * 8;
   const int b = (int)blockIdx.x;
-  grp = (b % stripe) / 8;
-  ublk = (b / stripe) * 8 + b % 8;
+  grp = b / pad;
+  ublk = b - grp * pad;
 }
 inline int64_t cg_xcd_grid(int64_t n_ublk, int64_t n_groups) {
   return n_groups == 1 ? n_ublk : (n_ublk + 7) / 8 * 8 * n_groups;

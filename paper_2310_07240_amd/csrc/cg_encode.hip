@@ -261,7 +261,7 @@ __global__ __launch_bounds__(kWin ? 64 * kEncWinWaves : 1024) void encode_kernel
   const int n_groups = (n_pairs + nw - 1) / nw;
   const int n_units = P.L * 2 * P.nblk;
   int ublk, grp;
-  cg_xcd_map(n_groups, ublk, grp);
+  cg_xcd_map((n_units + nu - 1) / nu, n_groups, ublk, grp);
   if (ublk * nu >= n_units) {   // past the last unit block (uniform over the workgroup)
     if (threadIdx.x == 0) wflags[blockIdx.x] = 0u;
     return;
