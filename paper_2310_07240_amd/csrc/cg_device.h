@@ -64,12 +64,19 @@ __device__ __forceinline__ int cg_quant(float v, float step) {
 // (-127, 127) (ties round to even), so when the clamped r is farther than 2^-14 from every
 // half-integer, r and the correctly rounded quotient give the same integer; otherwise (about
 // one value in 8000) the division is done as above. Clamped values (|r| >= 127) are 0.5 from
-// the nearest half-integer and give +-127 either way.
+// the nearest half-integer and give +-127 either way. The distance to the nearest half-integer
+// is 0.5 - |r - rint(r)| (exact: |r| < 2^23). The division sits behind a wave-uniform test, so
+// the wave branches over it unless one of its lanes is that close to a half-integer (under 1 %
+// of the waves); written as a plain branch, the compiler evaluates it on every call.
 __device__ __forceinline__ int cg_quant_inv(float v, float step, float inv) {
-  const float r = fminf(fmaxf(v * inv, -127.0f), 127.0f);
-  const float fr = r - __builtin_floorf(r);   // exact: |r| < 2^23
-  if (__builtin_fabsf(fr - 0.5f) <= 0x1p-14f) return cg_quant(v, step);
-  return (int)__builtin_rintf(r);
+  const float r = __builtin_amdgcn_fmed3f(v * inv, -127.0f, 127.0f);
+  const float rn = __builtin_rintf(r);
+  int q = (int)rn;
+  const bool near_half = __builtin_fabsf(r - rn) >= 0.5f - 0x1p-14f;
+  if (__builtin_expect(__builtin_amdgcn_ballot_w64(near_half) != 0, 0)) {
+    if (near_half) q = cg_quant(v, step);
+  }
+  return q;
 }
 
 // Stream index of (b, c, l, kv, ch): chunk-major so each chunk's streams are contiguous.

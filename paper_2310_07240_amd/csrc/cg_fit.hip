@@ -2,20 +2,24 @@
 // distribution per channel-layer for deltas and one for anchors; Sec. 6: frequencies counted
 // over the context's quantized symbols).
 //
-// One workgroup of 16 waves per (layer, K/V, 64-channel block); a lane owns one channel. The
-// workgroup takes the (context, chunk) pairs of that block one after the other and splits each
-// chunk's groups across its waves: every wave first reduces the absmax of its token slice, the
-// slices are combined in LDS into the chunk's scale, then every wave quantizes its slice (groups
-// are independent once the scale is known) and counts the symbols into LDS histograms. Rows
-// are read 64 channels (128 B) at a time, so every load is one coalesced line. When the channel
-// count is a multiple of 64 and half of a wave's slice is at most kHalf tokens (the paper's
-// 1.5K-token chunks: 48-50), a lane takes two neighbouring channels (one dword per token) over
-// half of the wave's groups; the slice is read once, into registers, with all its loads in
-// flight together, and both passes work from the registers. Otherwise the rows are read once
-// per pass, a lane per channel. Histograms use a
-// 257-word stride so lanes that count the same symbol hit different banks. At the end each
-// wave normalises histograms to 16-bit cumulative tables: per-lane partial sums, a wave
-// reduction for the total, the argmax and the frequency sum, and a wave prefix scan.
+// One workgroup of 16 waves per (layer, K/V, 64-channel block). The workgroup takes the
+// (context, chunk) pairs of that block one after the other and splits each chunk's groups across
+// its waves: every wave first reduces the absmax of its token slice, the slices are combined in
+// LDS into the chunk's scale, then every wave quantizes its slice (groups are independent once
+// the scale is known) and counts the symbols into LDS histograms. Rows are read 64 channels
+// (128 B) at a time, so every load is one coalesced line.
+//
+// fit_kernel fits one level with 32-bit counts. When the channel count is a multiple of 64 and
+// half of a wave's slice is at most kHalf tokens (the paper's 1.5K-token chunks: 48-50), a lane
+// takes two neighbouring channels (one dword per token) over half of the wave's groups; the
+// slice is read once, into registers, with all its loads in flight together, and both passes
+// work from the registers. Otherwise the rows are read once per pass, a lane per channel.
+// fit_pass_kernel (whole 64-channel blocks) and fit_levels_kernel (any channel count) fit the
+// anchors and several levels from one quantization with 16-bit counts.
+//
+// Histograms use an odd row stride so lanes that count the same symbol hit different banks. At
+// the end each wave normalises histograms to 16-bit cumulative tables: per-lane partial sums, a
+// wave reduction for the total, the argmax and the frequency sum, and a wave prefix scan.
 #include "cg_device.h"
 
 namespace {
@@ -278,17 +282,176 @@ __global__ __launch_bounds__(256) void pool_broadcast(const uint16_t* __restrict
 }
 
 
-// ---- several levels in one pass -------------------------------------------------------------
-// fit_levels_kernel: the fit of the anchors (with_anchor) and of kNl consecutive levels lv0 ..
-// from one quantization of each slice: the chunk's scale, the anchors and the deltas to them are
-// found once for all those levels. Counts are 16-bit, the two neighbouring channels 2 cp and
-// 2 cp + 1 in the low and high half of one 32-bit LDS word (the two channels a lane of the
-// register path takes), so four kinds take the LDS of two 32-bit ones; the host uses this
-// kernel only when no count can reach 2^16. A slice whose absolute maximum has the exponent
-// bits all ones (NaN or Inf) sets *status.
-constexpr int kLevelKinds = 4;   // anchor + levels, or levels, per workgroup
+// ---- several levels in one pass ---------------------------------------------------------------
+// Both kernels fit the anchors (with_anchor) and kNl consecutive levels lv0 .. from one
+// quantization of each slice: the chunk's scale, the anchors and the deltas to them are found
+// once for all those levels. Counts are 16-bit: the two neighbouring channels 2 cp and 2 cp + 1
+// sit in the low and high half of one 32-bit LDS word, so a kind takes the LDS of half a 32-bit
+// histogram; the host uses these kernels only when no count can reach 2^16. A slice whose
+// absolute maximum has the exponent bits all ones (NaN or Inf) sets *status.
+constexpr int kLevelKinds = 4;   // fit_levels_kernel: anchor + levels, or levels, per workgroup
+constexpr int kPassKinds = 5;    // fit_pass_kernel: anchor + four levels, 255-word rows
+constexpr int kHistP = 255;      // 255 symbols, no padding (odd, so rows fall on other banks)
+constexpr int kBufWord3 = 0x00020000;   // raw buffer descriptor: 32-bit data format
 
-template <bool kRegs, int kNl>
+// fit_pass_kernel: whole 64-channel blocks. A lane takes a channel pair cp (one dword per
+// token) over one of 32 slices of each chunk's groups (slice = 2 wave + lane / 32). The slice is
+// read twice: first for the magnitude maximum (combined over the slices in LDS into the chunk's
+// scale), then group by group from the last one back, so that the rows read last, the likeliest
+// to be still in the L2, are read again first. The rows come through a buffer descriptor of the
+// (context, layer, K/V) slab: a row outside the slab reads as zero and such tokens are never
+// counted. kG = 10: the group's loads are issued together and the group is unrolled; kG = 0 takes
+// the group size from P.
+template <int kNl, int kG>
+__global__ __launch_bounds__(kFitThreads) void fit_pass_kernel(
+    KParams P, const uint16_t* __restrict__ kv, int lv0, int with_anchor,
+    uint16_t* __restrict__ cdf_anchor, uint16_t* __restrict__ cdf_delta,
+    uint32_t* __restrict__ status) {
+  extern __shared__ uint32_t cnt[];   // [kinds][32 channel pairs][kHistP]
+  // chunk maxima: (pair index + 1) << 16 | magnitude bits, per channel, alternating buffers (a
+  // wave can only reach pair pr + 2 once every wave has read pair pr's buffer)
+  __shared__ uint32_t s_max[2][64];
+  __shared__ uint32_t s_bad;
+  const int cb = blockIdx.x % P.nblk;
+  const int lk = blockIdx.x / P.nblk;
+  const int l = lk >> 1, k = lk & 1;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int cp = lane & 31;
+  const int slice = wave * 2 + (lane >> 5);
+  const int nk = with_anchor + kNl;
+  for (int i = threadIdx.x; i < nk * 32 * kHistP; i += kFitThreads) cnt[i] = 0;
+  if (threadIdx.x < 128) s_max[threadIdx.x >> 6][threadIdx.x & 63] = 0u;
+  if (threadIdx.x == 0) s_bad = 0u;
+  __syncthreads();
+
+  const int G = kG > 0 ? kG : P.G;
+  float wfac[kNl];
+#pragma unroll
+  for (int v = 0; v < kNl; ++v) wfac[v] = P.layer_bin[l] * P.level_mult[lv0 + v];
+  // bin of symbol q in this lane's row of a kind: row[q], q in [-127, 127]
+  uint32_t* const ha = cnt + cp * kHistP + 127;
+  uint32_t* hrow[kNl];
+#pragma unroll
+  for (int v = 0; v < kNl; ++v) hrow[v] = cnt + ((with_anchor + v) * 32 + cp) * kHistP + 127;
+  const int rowb = P.C * 2;                          // bytes per token row (host: slab < 2^31)
+  const int slab_bytes = P.T * rowb;
+  const int pairs = P.B * P.NC;
+  uint32_t bad = 0u;
+  typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+  for (int pr = 0; pr < pairs; ++pr) {
+    const int b = pr / P.NC, c = pr % P.NC;
+    const int t0 = c * P.CL;
+    const int n = min(P.CL, P.T - t0);
+    const int ng = (n + G - 1) / G;
+    const int gps = (ng + 31) >> 5;                   // groups per slice
+    const int s0 = min(n, slice * gps * G);
+    const int len = min(n, (slice + 1) * gps * G) - s0;
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(kv + cg_elem(P, b, l, k, 0, 0)), (short)0, slab_bytes, kBufWord3);
+    const int voff = (t0 + s0) * rowb + (cb * 64 + 2 * cp) * 2;
+    // pass 1: magnitude bits of both channels, maximum over the slice (16-bit lanes)
+    u16x2 m = {0, 0};
+    const u16x2 mag = {0x7FFF, 0x7FFF};
+#pragma unroll 8
+    for (int u = 0; u < gps * G; ++u) {
+      const uint32_t x = __builtin_amdgcn_raw_buffer_load_b32(rs, voff + u * rowb, 0, 0);
+      const u16x2 xm = __builtin_bit_cast(u16x2, x) & mag;
+      m = u < len ? __builtin_elementwise_max(m, xm) : m;
+    }
+    uint32_t* const sm = s_max[pr & 1];
+    const uint32_t tag = (uint32_t)(pr + 1) << 16;
+    atomicMax(&sm[2 * cp], tag | m.x);
+    atomicMax(&sm[2 * cp + 1], tag | m.y);
+    __syncthreads();
+    const uint32_t b0 = sm[2 * cp] & 0xFFFFu, b1 = sm[2 * cp + 1] & 0xFFFFu;
+    bad |= (b0 >= 0x7C00u) | (b1 >= 0x7C00u);
+    const float m0 = cg_h2f((uint16_t)b0), m1 = cg_h2f((uint16_t)b1);
+    const float sc0 = (m0 == 0.0f) ? 1.0f : m0 / 127.0f;
+    const float sc1 = (m1 == 0.0f) ? 1.0f : m1 / 127.0f;
+    const float is0 = 1.0f / sc0, is1 = 1.0f / sc1;
+    float w0[kNl], w1[kNl], iw0[kNl], iw1[kNl];
+#pragma unroll
+    for (int v = 0; v < kNl; ++v) {
+      w0[v] = wfac[v] * sc0;
+      w1[v] = wfac[v] * sc1;
+      iw0[v] = 1.0f / w0[v];
+      iw1[v] = 1.0f / w1[v];
+    }
+    // one token of both channels: the anchor (u == 0) or the deltas to the group's anchors
+    float a0 = 0.0f, a1 = 0.0f;
+    auto token = [&](uint32_t x, bool anchor) __attribute__((always_inline)) {
+      const u16x2 h = __builtin_bit_cast(u16x2, x);
+      const float x0 = cg_h2f(h.x), x1 = cg_h2f(h.y);
+      if (anchor) {
+        const int q0 = cg_quant_inv(x0, sc0, is0), q1 = cg_quant_inv(x1, sc1, is1);
+        a0 = (float)q0 * sc0;
+        a1 = (float)q1 * sc1;
+        if (with_anchor) {
+          atomicAdd(&ha[q0], 1u);
+          atomicAdd(&ha[q1], 0x10000u);
+        }
+      } else {
+        const float d0 = x0 - a0, d1 = x1 - a1;
+#pragma unroll
+        for (int v = 0; v < kNl; ++v) {
+          atomicAdd(&hrow[v][cg_quant_inv(d0, w0[v], iw0[v])], 1u);
+          atomicAdd(&hrow[v][cg_quant_inv(d1, w1[v], iw1[v])], 0x10000u);
+        }
+      }
+    };
+    // pass 2: the slice's groups, last first
+    if constexpr (kG > 0) {
+      uint32_t xc[kG], xn[kG];
+      auto load = [&](uint32_t (&x)[kG], int gi) __attribute__((always_inline)) {
+#pragma unroll
+        for (int u = 0; u < kG; ++u)
+          x[u] = __builtin_amdgcn_raw_buffer_load_b32(rs, voff + (gi * kG + u) * rowb, 0, 0);
+      };
+      if (gps > 0) load(xc, gps - 1);
+      for (int gi = gps - 1; gi >= 0; --gi) {
+        if (gi > 0) load(xn, gi - 1);
+        const int base = gi * kG;
+        if (__builtin_amdgcn_ballot_w64(base + kG > len) == 0) {
+          // every lane of the wave has the whole group
+#pragma unroll
+          for (int u = 0; u < kG; ++u) token(xc[u], u == 0);
+        } else if (base < len) {
+#pragma unroll
+          for (int u = 0; u < kG; ++u)
+            if (base + u < len) token(xc[u], u == 0);
+        }
+#pragma unroll
+        for (int u = 0; u < kG; ++u) xc[u] = xn[u];
+      }
+    } else {
+      for (int gi = gps - 1; gi >= 0; --gi) {
+        const int base = gi * G;
+        if (base >= len) continue;
+        const int e = min(G, len - base);
+        for (int u = 0; u < e; ++u)
+          token(__builtin_amdgcn_raw_buffer_load_b32(rs, voff + (base + u) * rowb, 0, 0),
+                u == 0);
+      }
+    }
+  }
+  if (bad) s_bad = 1u;   // benign race: every writer stores 1
+  __syncthreads();
+  if (threadIdx.x == 0 && s_bad && status) atomicOr(status, 1u);
+
+  for (int tb = wave; tb < nk * 64; tb += kFitWaves) {
+    const int kind = tb >> 6, cl = tb & 63;
+    const int chx = cb * 64 + cl;
+    uint16_t* dst = (with_anchor && kind == 0)
+                        ? cdf_anchor + ((int64_t)lk * P.C + chx) * 256
+                        : cdf_delta + (((int64_t)(lv0 + kind - with_anchor) * P.L * 2 + lk) * P.C +
+                                       chx) * 256;
+    normalize_wave<uint32_t>(cnt + (kind * 32 + (cl >> 1)) * kHistP, dst, 16 * (cl & 1));
+  }
+}
+
+// fit_levels_kernel: any channel count, a lane per channel (channel lane of the block is half
+// lane & 1 of pair lane / 2 of the counts); each pass reads the slice from memory.
+template <int kNl>
 __global__ __launch_bounds__(kFitThreads) void fit_levels_kernel(
     KParams P, const uint16_t* __restrict__ kv, int lv0, int with_anchor,
     uint16_t* __restrict__ cdf_anchor, uint16_t* __restrict__ cdf_delta,
@@ -312,23 +475,10 @@ __global__ __launch_bounds__(kFitThreads) void fit_levels_kernel(
   const int pairs = P.B * P.NC;
   const int64_t rs = P.C;
   uint32_t bad = 0u;
-  // count one token of a channel (histogram row h of its pair, increment inc for its half)
-  auto count = [&](float x, int g, float s, float is, const float (&w)[kNl],
-                   const float (&iw)[kNl], float& a, int h, uint32_t inc)
-                   __attribute__((always_inline)) {
-    if (g == 0) {
-      const int q = cg_quant_inv(x, s, is);
-      a = (float)q * s;
-      if (with_anchor) atomicAdd(&cnt[h * kHist + q + 127], inc);
-    } else {
-      const float d = x - a;
-#pragma unroll
-      for (int v = 0; v < kNl; ++v) {
-        const int q = cg_quant_inv(d, w[v], iw[v]);
-        atomicAdd(&hist_d[(v * 32 + h) * kHist + q + 127], inc);
-      }
-    }
-  };
+  const int ch = cb * 64 + lane;
+  const bool act = ch < P.C;
+  const int h = lane >> 1;
+  const uint32_t inc = (lane & 1) ? 0x10000u : 1u;
   for (int pr = 0; pr < pairs; ++pr) {
     const int b = pr / P.NC, c = pr % P.NC;
     const int t0 = c * P.CL;
@@ -336,97 +486,44 @@ __global__ __launch_bounds__(kFitThreads) void fit_levels_kernel(
     const int ng = (n + P.G - 1) / P.G;                 // groups in the chunk
     const int gpw = (ng + kFitWaves - 1) / kFitWaves;   // groups per wave
     const int j0 = min(n, wave * gpw * P.G), j1 = min(n, (wave + 1) * gpw * P.G);
-    if constexpr (kRegs) {
-      // lane = (channel pair cp, token half th), as in fit_kernel's register path
-      const int cp = lane & 31, th = lane >> 5;
-      const int gh = (gpw + 1) >> 1;
-      const int h0 = min(j1, j0 + th * gh * P.G), h1 = min(j1, j0 + (th + 1) * gh * P.G);
-      const int len = h1 - h0;
-      const uint32_t* xw =
-          reinterpret_cast<const uint32_t*>(kv + cg_elem(P, b, l, k, t0, cb * 64)) + cp;
-      const int64_t rw = P.C >> 1;
-      uint32_t pk[kHalf];
+    const uint16_t* x = kv + cg_elem(P, b, l, k, t0, act ? ch : cb * 64);
+    uint32_t m = 0u;
+#pragma unroll 8
+    for (int j = j0; j < j1; ++j) m = max(m, (uint32_t)x[(int64_t)j * rs] & 0x7FFFu);
+    part[wave][lane] = m;
+    __syncthreads();
+    m = 0u;
 #pragma unroll
-      for (int u = 0; u < kHalf; ++u) pk[u] = xw[(int64_t)min(h0 + u, n - 1) * rw];
-      // magnitude bits: their maximum orders like |x| for finite halves and reaches 0x7c00
-      // exactly when a NaN or Inf is present
-      uint32_t m0 = 0u, m1 = 0u;
+    for (int v = 0; v < kFitWaves; ++v) m = max(m, part[v][lane]);
+    bad |= act && m >= 0x7C00u;
+    const float mx = cg_h2f((uint16_t)m);
+    const float s = (mx == 0.0f) ? 1.0f : mx / 127.0f;
+    const float is = 1.0f / s;
+    float w[kNl], iw[kNl];
 #pragma unroll
-      for (int u = 0; u < kHalf; ++u) {
-        if (u < len) {
-          m0 = max(m0, pk[u] & 0x7FFFu);
-          m1 = max(m1, (pk[u] >> 16) & 0x7FFFu);
-        }
-      }
-      m0 = max(m0, (uint32_t)__shfl_xor((int)m0, 32, 64));
-      m1 = max(m1, (uint32_t)__shfl_xor((int)m1, 32, 64));
-      if (th == 0) {
-        part[wave][2 * cp] = m0;
-        part[wave][2 * cp + 1] = m1;
-      }
-      __syncthreads();
-      m0 = 0u;
-      m1 = 0u;
-#pragma unroll
-      for (int v = 0; v < kFitWaves; ++v) {
-        m0 = max(m0, part[v][2 * cp]);
-        m1 = max(m1, part[v][2 * cp + 1]);
-      }
-      bad |= (m0 >= 0x7C00u) | (m1 >= 0x7C00u);
-      const float mx0 = cg_h2f((uint16_t)m0), mx1 = cg_h2f((uint16_t)m1);
-      const float s0 = (mx0 == 0.0f) ? 1.0f : mx0 / 127.0f;
-      const float s1 = (mx1 == 0.0f) ? 1.0f : mx1 / 127.0f;
-      const float is0 = 1.0f / s0, is1 = 1.0f / s1;
-      float w0[kNl], w1[kNl], iw0[kNl], iw1[kNl];
-#pragma unroll
-      for (int v = 0; v < kNl; ++v) {
-        w0[v] = wfac[v] * s0;
-        w1[v] = wfac[v] * s1;
-        iw0[v] = 1.0f / w0[v];
-        iw1[v] = 1.0f / w1[v];
-      }
-      float a0 = 0.0f, a1 = 0.0f;
+    for (int v = 0; v < kNl; ++v) {
+      w[v] = wfac[v] * s;
+      iw[v] = 1.0f / w[v];
+    }
+    if (act) {
+      float a = 0.0f;
       int g = 0;
+#pragma unroll 4
+      for (int j = j0; j < j1; ++j) {
+        const float xv = cg_h2f(x[(int64_t)j * rs]);
+        if (g == 0) {
+          const int q = cg_quant_inv(xv, s, is);
+          a = (float)q * s;
+          if (with_anchor) atomicAdd(&cnt[h * kHist + q + 127], inc);
+        } else {
+          const float d = xv - a;
 #pragma unroll
-      for (int u = 0; u < kHalf; ++u) {
-        if (u < len) {
-          count(cg_h2f((uint16_t)(pk[u] & 0xFFFFu)), g, s0, is0, w0, iw0, a0, cp, 1u);
-          count(cg_h2f((uint16_t)(pk[u] >> 16)), g, s1, is1, w1, iw1, a1, cp, 0x10000u);
+          for (int v = 0; v < kNl; ++v) {
+            const int q = cg_quant_inv(d, w[v], iw[v]);
+            atomicAdd(&hist_d[(v * 32 + h) * kHist + q + 127], inc);
+          }
         }
         g = (g + 1 == P.G) ? 0 : g + 1;
-      }
-    } else {
-      // a lane per channel; channel lane of the block is half (lane & 1) of pair lane / 2
-      const int ch = cb * 64 + lane;
-      const bool act = ch < P.C;
-      const uint16_t* x = kv + cg_elem(P, b, l, k, t0, act ? ch : cb * 64);
-      uint32_t m = 0u;
-#pragma unroll 8
-      for (int j = j0; j < j1; ++j) m = max(m, (uint32_t)x[(int64_t)j * rs] & 0x7FFFu);
-      part[wave][lane] = m;
-      __syncthreads();
-      m = 0u;
-#pragma unroll
-      for (int v = 0; v < kFitWaves; ++v) m = max(m, part[v][lane]);
-      bad |= act && m >= 0x7C00u;
-      const float mx = cg_h2f((uint16_t)m);
-      const float s = (mx == 0.0f) ? 1.0f : mx / 127.0f;
-      const float is = 1.0f / s;
-      float w[kNl], iw[kNl];
-#pragma unroll
-      for (int v = 0; v < kNl; ++v) {
-        w[v] = wfac[v] * s;
-        iw[v] = 1.0f / w[v];
-      }
-      if (act) {
-        float a = 0.0f;
-        int g = 0;
-        const uint32_t inc = (lane & 1) ? 0x10000u : 1u;
-#pragma unroll 4
-        for (int j = j0; j < j1; ++j) {
-          count(cg_h2f(x[(int64_t)j * rs]), g, s, is, w, iw, a, lane >> 1, inc);
-          g = (g + 1 == P.G) ? 0 : g + 1;
-        }
       }
     }
     __syncthreads();   // `part` is reused by the next pair
@@ -510,25 +607,61 @@ hipError_t cg_launch_fit_global(const KParams& P, const uint16_t* kv, int level,
 }
 
 namespace {
-template <bool kRegs>
 hipError_t launch_fit_levels(const KParams& P, const uint16_t* kv, int lv0, int nl,
                              int with_anchor, uint16_t* cdf_anchor, uint16_t* cdf_delta,
                              uint32_t* status, hipStream_t st) {
   const size_t lds = (size_t)(with_anchor + nl) * 32 * kHist * sizeof(uint32_t);
-  const void* fn = nl == 1 ? (const void*)fit_levels_kernel<kRegs, 1>
-                 : nl == 2 ? (const void*)fit_levels_kernel<kRegs, 2>
-                 : nl == 3 ? (const void*)fit_levels_kernel<kRegs, 3>
-                           : (const void*)fit_levels_kernel<kRegs, 4>;
+  const void* fn = nl == 1 ? (const void*)fit_levels_kernel<1>
+                 : nl == 2 ? (const void*)fit_levels_kernel<2>
+                 : nl == 3 ? (const void*)fit_levels_kernel<3>
+                           : (const void*)fit_levels_kernel<4>;
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   const dim3 grid((unsigned)((int64_t)P.L * 2 * P.nblk)), block(kFitThreads);
   switch (nl) {
-    case 1: hipLaunchKernelGGL((fit_levels_kernel<kRegs, 1>), grid, block, lds, st, P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status); break;
-    case 2: hipLaunchKernelGGL((fit_levels_kernel<kRegs, 2>), grid, block, lds, st, P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status); break;
-    case 3: hipLaunchKernelGGL((fit_levels_kernel<kRegs, 3>), grid, block, lds, st, P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status); break;
-    default: hipLaunchKernelGGL((fit_levels_kernel<kRegs, 4>), grid, block, lds, st, P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status); break;
+    case 1: hipLaunchKernelGGL((fit_levels_kernel<1>), grid, block, lds, st, P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status); break;
+    case 2: hipLaunchKernelGGL((fit_levels_kernel<2>), grid, block, lds, st, P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status); break;
+    case 3: hipLaunchKernelGGL((fit_levels_kernel<3>), grid, block, lds, st, P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status); break;
+    default: hipLaunchKernelGGL((fit_levels_kernel<4>), grid, block, lds, st, P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status); break;
   }
   return hipGetLastError();
+}
+
+template <int kNl>
+hipError_t launch_fit_pass_nl(const KParams& P, const uint16_t* kv, int lv0, int with_anchor,
+                              uint16_t* cdf_anchor, uint16_t* cdf_delta, uint32_t* status,
+                              hipStream_t st) {
+  const size_t lds = (size_t)(with_anchor + kNl) * 32 * kHistP * sizeof(uint32_t);
+  const bool g10 = P.G == 10;
+  const void* fn = g10 ? (const void*)fit_pass_kernel<kNl, 10> : (const void*)fit_pass_kernel<kNl, 0>;
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  const dim3 grid((unsigned)((int64_t)P.L * 2 * P.nblk)), block(kFitThreads);
+  if (g10)
+    hipLaunchKernelGGL((fit_pass_kernel<kNl, 10>), grid, block, lds, st, P, kv, lv0, with_anchor,
+                       cdf_anchor, cdf_delta, status);
+  else
+    hipLaunchKernelGGL((fit_pass_kernel<kNl, 0>), grid, block, lds, st, P, kv, lv0, with_anchor,
+                       cdf_anchor, cdf_delta, status);
+  return hipGetLastError();
+}
+
+hipError_t launch_fit_pass(const KParams& P, const uint16_t* kv, int lv0, int nl, int with_anchor,
+                           uint16_t* cdf_anchor, uint16_t* cdf_delta, uint32_t* status,
+                           hipStream_t st) {
+  switch (nl) {
+    case 1: return launch_fit_pass_nl<1>(P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status, st);
+    case 2: return launch_fit_pass_nl<2>(P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status, st);
+    case 3: return launch_fit_pass_nl<3>(P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status, st);
+    default: return launch_fit_pass_nl<4>(P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status, st);
+  }
+}
+
+// fit_pass_kernel's conditions: whole 64-channel blocks, and byte offsets inside one (context,
+// layer, K/V) slab, plus the reads a slice makes past the last token (under 1/32 of a chunk and
+// a group), that stay below 2^31
+bool fit_pass_applies(const KParams& P) {
+  return P.C % 64 == 0 && (int64_t)P.T * P.C * 2 < ((int64_t)1 << 30);
 }
 }  // namespace
 
@@ -564,14 +697,14 @@ hipError_t cg_launch_fit_levels(const KParams& P, const uint16_t* kv, uint16_t* 
                                                  status)
                 : launch_fit_kernel<false, false>(P, kv, 0, cdf_anchor, cdf_delta, nullptr, st,
                                                   status);
-  // the anchors and up to three levels in the first pass, up to four levels in each further one
-  for (int lv0 = 0, pass = 0; lv0 < P.NLV; ++pass) {
-    const int wa = pass == 0 ? 1 : 0;
-    const int nl = min(P.NLV - lv0, kLevelKinds - wa);
-    hipError_t e = regs ? launch_fit_levels<true>(P, kv, lv0, nl, wa, cdf_anchor, cdf_delta,
-                                                  status, st)
-                        : launch_fit_levels<false>(P, kv, lv0, nl, wa, cdf_anchor, cdf_delta,
-                                                   status, st);
+  // fit_pass_kernel: the anchors and up to four levels in the first pass, up to four levels in
+  // each further one; fit_levels_kernel: up to four kinds per pass
+  const bool pass = fit_pass_applies(P);
+  for (int lv0 = 0, i = 0; lv0 < P.NLV; ++i) {
+    const int wa = i == 0 ? 1 : 0;
+    const int nl = min(P.NLV - lv0, pass ? kPassKinds - 1 : kLevelKinds - wa);
+    hipError_t e = pass ? launch_fit_pass(P, kv, lv0, nl, wa, cdf_anchor, cdf_delta, status, st)
+                        : launch_fit_levels(P, kv, lv0, nl, wa, cdf_anchor, cdf_delta, status, st);
     if (e != hipSuccess) return e;
     lv0 += nl;
   }

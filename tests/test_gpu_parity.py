@@ -259,6 +259,13 @@ FIT_CASES = [
             level_mult=(1.0, 2.0, 4.0, 8.0, 16.0, 32.0, 64.0, 128.0)),
     W.small(name="fit_levels5_g7", group_size=7, n_layers=2, n_channels=64, n_tokens=200,
             chunk_len=50, level_mult=(1.0, 1.5, 2.0, 3.0, 5.0)),
+    # 64-channel blocks, eight levels in two passes of four, three contexts; chunks of 7 groups
+    # leave most of the 32 slices of a chunk empty, the last chunk has 5 tokens
+    W.small(name="fit_levels8_b3_c128", n_ctx=3, n_layers=2, n_channels=128, n_tokens=205,
+            chunk_len=64, level_mult=(1.0, 1.25, 1.5, 2.0, 3.0, 4.0, 6.0, 8.0)),
+    # a chunk of 4 groups per slice and a ragged group inside the last slice
+    W.small(name="fit_levels2_t2995", n_layers=1, n_channels=192, n_tokens=2995, chunk_len=1280,
+            level_mult=(1.0, 2.0)),
     # more than 2^16 deltas of one channel: the 32-bit per-level path
     W.small(name="fit_long_t76000", n_layers=1, n_channels=64, n_tokens=76000, chunk_len=1536,
             level_mult=(1.0, 4.0)),
