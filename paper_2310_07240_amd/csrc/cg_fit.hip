@@ -338,26 +338,40 @@ __global__ __launch_bounds__(kFitThreads) void fit_pass_kernel(
   const int pairs = P.B * P.NC;
   uint32_t bad = 0u;
   typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
-  for (int pr = 0; pr < pairs; ++pr) {
+  // this lane's slice of pair pr: buffer of the slab, byte offset of its first token, its
+  // length in tokens and the groups per slice
+  struct Slice {
+    __amdgpu_buffer_rsrc_t rs;
+    int voff, len, gps;
+  };
+  auto slice_of = [&](int pr) __attribute__((always_inline)) {
+    Slice q;
     const int b = pr / P.NC, c = pr % P.NC;
     const int t0 = c * P.CL;
     const int n = min(P.CL, P.T - t0);
-    const int ng = (n + G - 1) / G;
-    const int gps = (ng + 31) >> 5;                   // groups per slice
-    const int s0 = min(n, slice * gps * G);
-    const int len = min(n, (slice + 1) * gps * G) - s0;
-    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(kv + cg_elem(P, b, l, k, 0, 0)), (short)0, slab_bytes, kBufWord3);
-    const int voff = (t0 + s0) * rowb + (cb * 64 + 2 * cp) * 2;
-    // pass 1: magnitude bits of both channels, maximum over the slice (16-bit lanes)
-    u16x2 m = {0, 0};
-    const u16x2 mag = {0x7FFF, 0x7FFF};
+    q.gps = ((n + G - 1) / G + 31) >> 5;
+    const int s0 = min(n, slice * q.gps * G);
+    q.len = min(n, (slice + 1) * q.gps * G) - s0;
+    q.rs = __builtin_amdgcn_make_buffer_rsrc((void*)(kv + cg_elem(P, b, l, k, 0, 0)), (short)0,
+                                             slab_bytes, kBufWord3);
+    q.voff = (t0 + s0) * rowb + (cb * 64 + 2 * cp) * 2;
+    return q;
+  };
+  auto load = [&](const Slice& q, int u) __attribute__((always_inline)) {
+    return __builtin_amdgcn_raw_buffer_load_b32(q.rs, q.voff + u * rowb, 0, 0);
+  };
+  // magnitude bits of both channels of token u of slice q into the running maxima m
+  const u16x2 mag = {0x7FFF, 0x7FFF};
+  auto max_in = [&](u16x2& m, uint32_t x, int u, int len) __attribute__((always_inline)) {
+    const u16x2 xm = __builtin_bit_cast(u16x2, x) & mag;
+    m = u < len ? __builtin_elementwise_max(m, xm) : m;
+  };
+  // pass 1 of the first pair; that of every further pair runs inside the previous pair's pass 2
+  Slice cur = slice_of(0);
+  u16x2 m = {0, 0};
 #pragma unroll 8
-    for (int u = 0; u < gps * G; ++u) {
-      const uint32_t x = __builtin_amdgcn_raw_buffer_load_b32(rs, voff + u * rowb, 0, 0);
-      const u16x2 xm = __builtin_bit_cast(u16x2, x) & mag;
-      m = u < len ? __builtin_elementwise_max(m, xm) : m;
-    }
+  for (int u = 0; u < cur.gps * G; ++u) max_in(m, load(cur, u), u, cur.len);
+  for (int pr = 0; pr < pairs; ++pr) {
     uint32_t* const sm = s_max[pr & 1];
     const uint32_t tag = (uint32_t)(pr + 1) << 16;
     atomicMax(&sm[2 * cp], tag | m.x);
@@ -399,40 +413,55 @@ __global__ __launch_bounds__(kFitThreads) void fit_pass_kernel(
         }
       }
     };
-    // pass 2: the slice's groups, last first
+    // pass 2: the slice's groups, last first, and pass 1 of the next pair alongside
+    const bool more = pr + 1 < pairs;
+    const Slice nxt = more ? slice_of(pr + 1) : cur;
+    const int span_n = more ? nxt.gps * G : 0;
+    u16x2 mn = {0, 0};
+    int covered = 0;   // tokens of the next slice already in mn
     if constexpr (kG > 0) {
-      uint32_t xc[kG], xn[kG];
-      auto load = [&](uint32_t (&x)[kG], int gi) __attribute__((always_inline)) {
+      uint32_t xc[kG], xn[kG], y[kG];
 #pragma unroll
-        for (int u = 0; u < kG; ++u)
-          x[u] = __builtin_amdgcn_raw_buffer_load_b32(rs, voff + (gi * kG + u) * rowb, 0, 0);
-      };
-      if (gps > 0) load(xc, gps - 1);
-      for (int gi = gps - 1; gi >= 0; --gi) {
-        if (gi > 0) load(xn, gi - 1);
+      for (int u = 0; u < kG; ++u) xc[u] = load(cur, (cur.gps - 1) * kG + u);
+      for (int gi = cur.gps - 1; gi >= 0; --gi) {
         const int base = gi * kG;
-        if (__builtin_amdgcn_ballot_w64(base + kG > len) == 0) {
+        if (base < span_n) {
+#pragma unroll
+          for (int u = 0; u < kG; ++u) y[u] = load(nxt, base + u);
+        }
+        if (gi > 0) {
+#pragma unroll
+          for (int u = 0; u < kG; ++u) xn[u] = load(cur, base - kG + u);
+        }
+        if (__builtin_amdgcn_ballot_w64(base + kG > cur.len) == 0) {
           // every lane of the wave has the whole group
 #pragma unroll
           for (int u = 0; u < kG; ++u) token(xc[u], u == 0);
-        } else if (base < len) {
+        } else if (base < cur.len) {
 #pragma unroll
           for (int u = 0; u < kG; ++u)
-            if (base + u < len) token(xc[u], u == 0);
+            if (base + u < cur.len) token(xc[u], u == 0);
+        }
+        if (base < span_n) {
+#pragma unroll
+          for (int u = 0; u < kG; ++u) max_in(mn, y[u], base + u, nxt.len);
         }
 #pragma unroll
         for (int u = 0; u < kG; ++u) xc[u] = xn[u];
       }
+      covered = min(cur.gps * kG, span_n);
     } else {
-      for (int gi = gps - 1; gi >= 0; --gi) {
+      for (int gi = cur.gps - 1; gi >= 0; --gi) {
         const int base = gi * G;
-        if (base >= len) continue;
-        const int e = min(G, len - base);
-        for (int u = 0; u < e; ++u)
-          token(__builtin_amdgcn_raw_buffer_load_b32(rs, voff + (base + u) * rowb, 0, 0),
-                u == 0);
+        if (base >= cur.len) continue;
+        const int e = min(G, cur.len - base);
+        for (int u = 0; u < e; ++u) token(load(cur, base + u), u == 0);
       }
     }
+#pragma unroll 8
+    for (int u = covered; u < span_n; ++u) max_in(mn, load(nxt, u), u, nxt.len);
+    m = mn;
+    cur = nxt;
   }
   if (bad) s_bad = 1u;   // benign race: every writer stores 1
   __syncthreads();
@@ -691,15 +720,15 @@ hipError_t cg_launch_fit_levels(const KParams& P, const uint16_t* kv, uint16_t* 
                   : hipSuccess;
   }
   if (status) hipLaunchKernelGGL(zero_word, dim3(1), dim3(64), 0, st, status);
-  const bool regs = fit_slice_in_registers(P);
-  if (P.NLV == 1)   // one level: the 32-bit kernel of cg_fit_cdf (measured faster there)
-    return regs ? launch_fit_kernel<false, true>(P, kv, 0, cdf_anchor, cdf_delta, nullptr, st,
-                                                 status)
-                : launch_fit_kernel<false, false>(P, kv, 0, cdf_anchor, cdf_delta, nullptr, st,
-                                                  status);
+  const bool pass = fit_pass_applies(P);
+  if (P.NLV == 1 && !pass)   // one level, any channel count: the 32-bit kernel of cg_fit_cdf
+    return fit_slice_in_registers(P)
+               ? launch_fit_kernel<false, true>(P, kv, 0, cdf_anchor, cdf_delta, nullptr, st,
+                                                status)
+               : launch_fit_kernel<false, false>(P, kv, 0, cdf_anchor, cdf_delta, nullptr, st,
+                                                 status);
   // fit_pass_kernel: the anchors and up to four levels in the first pass, up to four levels in
   // each further one; fit_levels_kernel: up to four kinds per pass
-  const bool pass = fit_pass_applies(P);
   for (int lv0 = 0, i = 0; lv0 < P.NLV; ++i) {
     const int wa = i == 0 ? 1 : 0;
     const int nl = min(P.NLV - lv0, pass ? kPassKinds - 1 : kLevelKinds - wa);
