@@ -457,23 +457,28 @@ __global__ __launch_bounds__(1024) void decode_kernel(
 //     anchor's q (requested a group ahead), decodes its nine deltas with epochs before deltas
 //     1 and 6, and stores rows 1..9 (over the kept q).
 // Both searches start from the 15 fences cum[16 f] of the table in registers (a 4-step select
-// search, no memory round trip), then take two LDS round trips (one 4-ary level, the leaf).
+// search, no memory round trip), then take three LDS round trips: one 4-ary level and the
+// leaf (each two compare / select steps over entries read together), and the candidate's two
+// bounds, read from its address.
 constexpr int kG10 = 10;
 constexpr int kAnchorRun = 5;   // anchors per bitstream epoch (a symbol takes <= 18 bits)
 
 // Per-lane decoder state of the group-of-10 kernel (plain scalars: it lives in registers).
-// Bitstream reader: the 128 bits after the code value's own are held in w0..w3, of which the
-// first `pos` bits of w0 are already consumed. A token takes n <= 18 bits (the interval is
-// wider than 2^30 before a symbol and at least 2^14 after it, and renormalisation doubles it
-// to at most 2^32), so it crosses at most one word boundary and w0 moves up by at most one
-// word; five tokens take at most 90 bits, which from an epoch start with pos < 32 never reach
-// past w3 (31 + 90 < 128), so at most three words leave between two epoch boundaries. (Bits
-// that the 32-bit window read takes past the token's own come from words already moved and are
-// shifted out unused.)
+// Bitstream reader: the next stream bits are the last `avail` bits of w0 (0..31; 0 when w0 is
+// used up), then w1, w2, w3. A token takes n <= 18 bits (the interval is wider than 2^30
+// before a symbol and at least 2^14 after it, and renormalisation doubles it to at most 2^32),
+// so it crosses at most one word boundary and w0 moves up by at most one word; five tokens take
+// at most 90 bits, which from an epoch start never reach past w3 (90 < 96), so at most three
+// words leave between two epoch boundaries. (Bits that the 32-bit window read takes past the
+// token's own come from words already moved and are shifted out unused.)
 struct G10Lane {
-  uint32_t D, low, rm1;          // code value - low, low, high - low
+  // low is kept as the value before its last renormalisation shift by lsh, and only its low 31
+  // bits are kept exact: the interval update reads low << lsh + lo_off, and renormalisation
+  // uses that sum's bits below the top one (its top bit and that of high = low + hoff - 1 are
+  // both off by the same amount, which the xor cancels and the run count masks)
+  uint32_t D, low, lsh, rm1;     // code value - low, low (see above), high - low
   uint32_t w0, w1, w2, w3;       // the next stream words, w0 partly consumed
-  uint32_t pos;                  // bits of w0 already taken (< 32)
+  uint32_t avail;                // bits of w0 not yet taken (< 32)
   uint32_t t0, t1, t2, t3;       // the four words after w3, requested one epoch ahead
   uint32_t hcnt;                 // words moved out of w0 since the last epoch (<= 3)
   uint32_t widx;                 // index of t0's word from the stream's first word
@@ -516,29 +521,30 @@ __device__ __forceinline__ void g10_advance(G10Lane& st, uint32_t lo_off, uint32
   // renormalisation: n1 shared leading bits of low and high, then the middle-half run of
   // f - 1 steps, read as in e3_run from (low & ~high) << n1 (the same bits as L1 & ~H1, with
   // L1 = low << n1 and H1 = high << n1); in all nsh = n1 + f - 1 shifts, after which the new
-  // low is low << nsh without its top bit
-  const uint32_t low = st.low + lo_off;
-  const uint32_t high = st.low + hoff - 1u;
+  // low is low << nsh without its top bit (the shift waits for the next symbol)
+  const uint32_t low = (st.low << st.lsh) + lo_off;
+  const uint32_t high = low + rsz - 1u;
   const uint32_t n1 = (uint32_t)__builtin_clz(low ^ high);
   uint32_t e, f;
   asm("v_bfi_b32 %0, %1, 0, %2" : "=v"(e) : "v"(high), "v"(low));   // low & ~high
   asm("v_ffbh_i32 %0, %1" : "=v"(f) : "v"((e << n1) | 0x80000000u));   // run + 1
   const uint32_t nsh = n1 + f - 1u;
-  st.low = (low << nsh) & 0x7FFFFFFFu;
+  st.low = low;
+  st.lsh = nsh;
   // high - low + 1 scales by 2^nsh (a result of 2^32 wraps to 0, giving rm1 = 2^32 - 1)
   st.rm1 = (rsz << nsh) - 1u;
-  // D takes the next nsh stream bits: the 32 bits at `pos` of w0:w1, then a 64-bit shift
-  const uint64_t wp = ((uint64_t)st.w0 << 32) | st.w1;
-  const uint32_t win = (uint32_t)((wp << st.pos) >> 32);
+  // D takes the next nsh stream bits: the 32 bits after the taken ones of w0:w1, then a 64-bit
+  // shift
+  const uint32_t win = __builtin_amdgcn_alignbit(st.w0, st.w1, st.avail);
   uint32_t Dn = (uint32_t)(((((uint64_t)d) << 32) | win) << nsh >> 32);
   asm("" : "+v"(Dn));   // keep D a 32-bit value (not the top half of a 64-bit one)
   st.D = Dn;
-  const uint32_t p2 = st.pos + nsh;
-  const bool adv = p2 >= 32u;
+  const uint32_t a2 = st.avail - nsh;
+  const bool adv = (int32_t)a2 < 0;
   st.w0 = adv ? st.w1 : st.w0;
   st.w1 = adv ? st.w2 : st.w1;
   st.w2 = adv ? st.w3 : st.w2;
-  st.pos = p2 & 31u;
+  st.avail = a2 & 31u;
   st.hcnt += adv ? 1u : 0u;
 }
 
@@ -613,11 +619,12 @@ __device__ __forceinline__ void g10_fences_win(uint32_t (&fT)[17], const WinTab&
 }
 
 // One symbol under the table whose entry 0 sits (really, or for a window table virtually) at
-// LDS byte address tb, with tagged fences fT; kq = -(tb / 2 + 127); T is the same table for the
-// rare correction walk. Returns q = symbol - 127 after the interval update and the refill of D.
+// LDS byte address tb, with tagged fences fT; kq2 = -(tb + 254); T is the same table for the
+// rare correction walk. Returns 2 q = 2 (symbol - 127) after the interval update and the refill
+// of D.
 template <class Tab>
 __device__ __forceinline__ int g10_symbol(G10Lane& st, const uint32_t (&fT)[17], const Tab& T,
-                                          uint32_t tb, uint32_t kq) {
+                                          uint32_t tb, uint32_t kq2) {
   const float te = (float)st.D * (65536.0f * __builtin_amdgcn_rcpf((float)st.rm1));
   const uint32_t ti = min((uint32_t)te, 65534u);
   const uint32_t th = (ti << 16) + 0x10000u;   // (ti + 1) << 16
@@ -638,34 +645,23 @@ __device__ __forceinline__ int g10_symbol(G10Lane& st, const uint32_t (&fT)[17],
   asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 "
       "src1_sel:DWORD" : "=v"(qa) : "v"(p1), "v"(c0 ? tb + 32u : tb));
   // 4-ary level: cum[16 f + 4 m], m = 1..3
-  const uint32_t kneg = ~ti;
-  const uint32_t qb = qa + 8u * (((lds_ld16(qa + 8u) + kneg) >> 31) +
-                                 ((lds_ld16(qa + 16u) + kneg) >> 31) +
-                                 ((lds_ld16(qa + 24u) + kneg) >> 31));
+  // two steps over the three sorted entries: cum[16 f + 8], then cum[16 f + 12] or cum[16 f + 4]
+  const uint32_t c4 = lds_ld16(qa + 8u), c8 = lds_ld16(qa + 16u), c12 = lds_ld16(qa + 24u);
+  const bool b8 = c8 <= ti;
+  const bool b4 = (b8 ? c12 : c4) <= ti;
+  const uint32_t qb = qa + (b8 ? 16u : 0u) + (b4 ? 8u : 0u);
   // leaf: cum[i .. i+3], i = (qb - tb) / 2, in x = cum[i] | cum[i+1] << 16 and y = cum[i+2] |
-  // cum[i+3] << 16, cum[i+4] in x4 (the layout of delta_leaf; here the count takes 32-bit sign
-  // tests, which measured slightly faster than its packed 16-bit forms)
+  // cum[i+3] << 16; the candidate i + c (c = the number of cum[i+1 .. i+3] <= ti, two steps as
+  // above) and the bounds cum[i + c], cum[i + c + 1] are read from its address
   const uint2 xy = lds_ld64(qb);
-  const uint32_t x4 = lds_ld16(qb + 8u);
-  // c = [cum[i+1] <= ti] + [cum[i+2] <= ti] + [cum[i+3] <= ti] (cum[i] <= ti always), each a
-  // sign bit of cum + ~ti with the 16-bit entry taken straight from its half of x or y
-  uint32_t e1, e2, e3;
-  asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_1 "
-      "src1_sel:DWORD" : "=v"(e1) : "v"(xy.x), "v"(kneg));
-  asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 "
-      "src1_sel:DWORD" : "=v"(e2) : "v"(xy.y), "v"(kneg));
-  asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_1 "
-      "src1_sel:DWORD" : "=v"(e3) : "v"(xy.y), "v"(kneg));
-  const uint32_t c = (e1 >> 31) + (e2 >> 31) + (e3 >> 31);
-  // (cum[i + c], cum[i + c + 1]) is the 32-bit window at 16 c bits of x : y : x4 (the shift
-  // takes its low five bits: 16 (c & 1))
-  const bool cge2 = c >= 2u;
-  const uint32_t hi2 = cge2 ? x4 : xy.y;
-  const uint32_t lo2 = cge2 ? xy.y : xy.x;
-  const uint32_t pr = __builtin_amdgcn_alignbit(hi2, lo2, c << 4);
-  int qi = (int)((qb >> 1) + c + kq);
-  uint32_t clo = pr & 0xFFFFu;
-  uint32_t chi = qi == CG_NSYM - 1 - 127 ? CG_TOTAL : pr >> 16;
+  const bool b2 = (xy.y & 0xFFFFu) <= ti;
+  const bool b1 = ((b2 ? xy.y : xy.x) >> 16) <= ti;
+  const uint32_t pa = qb + (b2 ? 4u : 0u) + (b1 ? 2u : 0u);
+  uint32_t clo = lds_ld16(pa);
+  const uint32_t chr = lds_ld16(pa + 2u);
+  // 2 q = 2 (symbol - 127) from the entry's address; the top symbol's upper bound is the total
+  int q2 = (int)(pa + kq2);
+  uint32_t chi = q2 == 2 * (CG_NSYM - 1 - 127) ? CG_TOTAL : chr;
   const uint32_t D = st.D, rm1 = st.rm1;
   // offsets of the candidate's interval from low: [lo_off, hoff) (hoff mod 2^32). The candidate
   // is the symbol iff D - lo_off < hoff - lo_off (unsigned): below lo_off the difference wraps
@@ -675,7 +671,7 @@ __device__ __forceinline__ int g10_symbol(G10Lane& st, const uint32_t (&fT)[17],
   uint32_t d = D - lo_off;
   uint32_t rsz = hoff - lo_off;
   if (d >= rsz) {
-    int sym = qi + 127;
+    int sym = (q2 >> 1) + 127;
     int nxt = T.first(sym, ti, D < lo_off);
     for (int guard = 0; guard < CG_NSYM; ++guard) {
       sym = nxt;
@@ -690,20 +686,21 @@ __device__ __forceinline__ int g10_symbol(G10Lane& st, const uint32_t (&fT)[17],
       if (d < rsz) break;
       nxt = (D < lo_off) ? max(sym - 1, 0) : min(sym + 1, CG_NSYM - 1);
     }
-    qi = sym - 127;
+    q2 = 2 * (sym - 127);
   }
   g10_advance(st, lo_off, hoff, d, rsz);
-  return qi;
+  return q2;
 }
 
 // One delta token: its symbol under the delta table, dequantized against the group's anchor
 // into row r of the wave's staging buffer.
+// w2 = w / 2 (exact), so 2 q times w2 is the same real number as q times w.
 template <class Tab>
 __device__ __forceinline__ void g10_delta(G10Lane& st, const uint32_t (&fD)[17], const Tab& T,
-                                          uint32_t tb, uint32_t kq, float w, uint16_t* obuf,
+                                          uint32_t tb, uint32_t kq2, float w2, uint16_t* obuf,
                                           int r, int lane) {
-  const int qi = g10_symbol(st, fD, T, tb, kq);
-  obuf[r * 64 + lane] = cg_f2h(st.a + (float)qi * w);
+  const int q2 = g10_symbol(st, fD, T, tb, kq2);
+  obuf[r * 64 + lane] = cg_f2h(st.a + (float)q2 * w2);
 }
 
 // Store rows first .. rows-1 of the staged group: lane L stores 16 bytes (8 channels) of row
@@ -1014,29 +1011,30 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     w = P.layer_bin[l] * P.level_mult[lv] * s;
     uint32_t fA[17];   // tagged fences of the anchor table
     g10_fences(fA, tab0);
-    const uint32_t tbA = lds_addr(tab0), kqA = 0u - (tbA / 2u + 127u);
-    // bitstream reader: the code value, w0..w3 and the four requested words t0..t3 are the
-    // stream's first 13 words; every read stays below offsets[S] + 4 (the requests are clamped
+    const uint32_t tbA = lds_addr(tab0), kqA = 0u - (tbA + 254u);
+    // bitstream reader: the code value, w1..w3 and the four requested words t0..t3 are the
+    // stream's first 8 words; every read stays below offsets[S] + 4 (the requests are clamped
     // to it), inside the readable tail
     const uint64_t o0 = offsets[sidx];
     const uint64_t ob = o0 < total ? o0 : total;
     sbase = words + ob;
     cap = (uint32_t)((total - ob) < 0xFFFFFFF0ull ? (total - ob) : 0xFFFFFFF0ull);
     st.D = sbase[0];
-    st.w0 = sbase[1];
-    st.w1 = sbase[2];
-    st.w2 = sbase[3];
-    st.w3 = sbase[4];
-    st.pos = 0;
+    st.w0 = 0u;   // used up: the stream continues with w1
+    st.w1 = sbase[1];
+    st.w2 = sbase[2];
+    st.w3 = sbase[3];
+    st.avail = 0;
     st.hcnt = 0;
-    st.widx = 5;
-    const uint32_t* tq0 = sbase + (5u < cap ? 5u : cap);
+    st.widx = 4;
+    const uint32_t* tq0 = sbase + (4u < cap ? 4u : cap);
     st.t0 = tq0[0];
     st.t1 = tq0[1];
     st.t2 = tq0[2];
     st.t3 = tq0[3];
     settle(st.D); settle(st.w0); settle(st.w1); settle(st.w2); settle(st.w3);
     st.low = 0u;
+    st.lsh = 0u;
     st.rm1 = 0xFFFFFFFFu;
     st.a = 0.0f;
 
@@ -1049,7 +1047,7 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
       for (int r = 0; r < kAnchorRun; ++r) {
         const int g = g0 + r;
         if (g < na) {
-          const int qi = g10_symbol(st, fA, FullTab{tab0}, tbA, kqA);
+          const int qi = g10_symbol(st, fA, FullTab{tab0}, tbA, kqA) >> 1;
           // wave-uniform row pointers, the lane's column as the index
           uint16_t* ra = row0 + (int64_t)g * kG10 * rstride;
           uint16_t* rq = g * kG10 + 1 < n ? ra + rstride : ra;
@@ -1064,7 +1062,8 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   auto delta_groups = [&](const auto& T, const uint32_t (&fD)[17], uint32_t tbD)
                           __attribute__((always_inline)) {
   set_priority(n - na);
-  const uint32_t kqD = 0u - (tbD / 2u + 127u);
+  const uint32_t kqD = 0u - (tbD + 254u);
+  const float w2 = w * 0.5f;
 
   uint16_t* obuf = obuf_all + wave * kG10 * 64;
   const int cbase = cb * 64;
@@ -1085,17 +1084,17 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   for (int gi = 0; gi < ngr; ++gi) {
     st.a = anext;
     g10_epoch(st, sbase, cap);
-    g10_delta(st, fD, T, tbD, kqD, w, obuf, 1, lane);
-    g10_delta(st, fD, T, tbD, kqD, w, obuf, 2, lane);
-    g10_delta(st, fD, T, tbD, kqD, w, obuf, 3, lane);
-    g10_delta(st, fD, T, tbD, kqD, w, obuf, 4, lane);
-    g10_delta(st, fD, T, tbD, kqD, w, obuf, 5, lane);
+    g10_delta(st, fD, T, tbD, kqD, w2, obuf, 1, lane);
+    g10_delta(st, fD, T, tbD, kqD, w2, obuf, 2, lane);
+    g10_delta(st, fD, T, tbD, kqD, w2, obuf, 3, lane);
+    g10_delta(st, fD, T, tbD, kqD, w2, obuf, 4, lane);
+    g10_delta(st, fD, T, tbD, kqD, w2, obuf, 5, lane);
     g10_epoch(st, sbase, cap);
     const uint32_t qnext = q_of(gi + 1);   // requested a group ahead
-    g10_delta(st, fD, T, tbD, kqD, w, obuf, 6, lane);
-    g10_delta(st, fD, T, tbD, kqD, w, obuf, 7, lane);
-    g10_delta(st, fD, T, tbD, kqD, w, obuf, 8, lane);
-    g10_delta(st, fD, T, tbD, kqD, w, obuf, 9, lane);
+    g10_delta(st, fD, T, tbD, kqD, w2, obuf, 6, lane);
+    g10_delta(st, fD, T, tbD, kqD, w2, obuf, 7, lane);
+    g10_delta(st, fD, T, tbD, kqD, w2, obuf, 8, lane);
+    g10_delta(st, fD, T, tbD, kqD, w2, obuf, 9, lane);
     if constexpr (decltype(kFull)::value) g10_flush_full(obuf, row, rstride, lane);
     else g10_flush(obuf, row, rstride, 1, kG10, lane, cbase, P.C);
     row += kG10 * rstride;
@@ -1113,7 +1112,7 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     g10_epoch(st, sbase, cap);
     for (int r = 1; r < rem; ++r) {
       if (r == 6) g10_epoch(st, sbase, cap);
-      g10_delta(st, fD, T, tbD, kqD, w, obuf, r, lane);
+      g10_delta(st, fD, T, tbD, kqD, w2, obuf, r, lane);
     }
     g10_flush(obuf, row, rstride, 1, rem, lane, cbase, P.C);
   }
@@ -1258,20 +1257,21 @@ __global__ __launch_bounds__(256) void tok_decode_kernel(
   const uint32_t* sbase = words + ob;
   const uint32_t cap = (uint32_t)((total - ob) < 0xFFFFFFF0ull ? (total - ob) : 0xFFFFFFF0ull);
   st.D = sbase[0];
-  st.w0 = sbase[1];
-  st.w1 = sbase[2];
-  st.w2 = sbase[3];
-  st.w3 = sbase[4];
-  st.pos = 0;
+  st.w0 = 0u;   // used up: the stream continues with w1
+  st.w1 = sbase[1];
+  st.w2 = sbase[2];
+  st.w3 = sbase[3];
+  st.avail = 0;
   st.hcnt = 0;
-  st.widx = 5;
-  const uint32_t* tq0 = sbase + (5u < cap ? 5u : cap);
+  st.widx = 4;
+  const uint32_t* tq0 = sbase + (4u < cap ? 4u : cap);
   st.t0 = tq0[0];
   st.t1 = tq0[1];
   st.t2 = tq0[2];
   st.t3 = tq0[3];
   settle(st.D); settle(st.w0); settle(st.w1); settle(st.w2); settle(st.w3);
   st.low = 0u;
+  st.lsh = 0u;
   st.rm1 = 0xFFFFFFFFu;
   st.a = 0.0f;
 
