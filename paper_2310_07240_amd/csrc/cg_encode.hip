@@ -182,11 +182,11 @@ __device__ __forceinline__ void enc_symbol(EncState& e, BitSink& o, uint32_t clo
 __device__ __forceinline__ void enc_symbol_fast(EncState& e, BitSink& o, uint32_t clo,
                                                 uint32_t chi, bool& rare) {
   const uint32_t lo_off = (uint32_t)(((uint64_t)e.rm1 * clo + clo) >> 16);
-  const uint32_t hm1 = (uint32_t)((((uint64_t)e.rm1 * chi + chi) >> 16) - 1ull);
+  // the new interval's size (2^32 wraps to 0, which the shift below turns into the full range)
+  const uint32_t rsz = (uint32_t)(((uint64_t)e.rm1 * chi + chi) >> 16) - lo_off;
   const uint32_t low = e.low + lo_off;
-  const uint32_t rm1 = hm1 - lo_off;
-  const uint32_t high = low + rm1;
-  const uint32_t n1 = __clz(low ^ high);
+  const uint32_t high = low + rsz - 1u;
+  const uint32_t n1 = (uint32_t)__builtin_clz(low ^ high);   // high > low
   const uint32_t P = e.pending;
   const bool emit = n1 != 0;
   const uint32_t E = emit ? P + n1 : 0u;
@@ -195,18 +195,24 @@ __device__ __forceinline__ void enc_symbol_fast(EncState& e, BitSink& o, uint32_
   const uint32_t runb = ((1u << (P & 31u)) - 1u) << ((n1 - 1u) & 31u);
   const uint32_t val = emit ? H + runb : 0u;
   o.acc = (o.acc << E) | val;   // bits above the nacc valid ones are never read
-  o.nacc += E;
-  const bool full = o.nacc >= 32u;
-  o.nacc -= full ? 32u : 0u;
-  o.ring[(o.nwords & (kRing - 1)) * 64] = (uint32_t)(o.acc >> o.nacc);
+  const uint32_t t = o.nacc + E;   // < 64
+  const bool full = t >= 32u;
+  o.nacc = t & 31u;
+  // ring slot (nwords mod kRing) * 64 words: kept as an index and a shift-add (else the compiler
+  // turns it into a shift, a mask and an add)
+  uint32_t slot = o.nwords & (kRing - 1);
+  asm("" : "+v"(slot));
+  o.ring[slot * 64] = (uint32_t)(o.acc >> o.nacc);
   o.nwords += full ? 1u : 0u;
-  const uint32_t L1 = low << n1, H1 = high << n1;
-  const uint32_t m = L1 & ~H1;
-  const uint32_t n3 = __clz(~(m << 1));
-  e.pending = (emit ? 0u : P) + n3;
-  e.low = (L1 << n3) & 0x7FFFFFFFu;
-  const uint32_t n = n1 + n3;
-  e.rm1 = (rm1 << n) | ((1u << n) - 1u);
+  // the middle-half run: f - 1 leading ones of (low & ~high) << (n1 + 1), from v_ffbh_i32 (the
+  // count of leading bits equal to the sign bit) of (low & ~high) << n1 with its top bit set
+  uint32_t lh, f;
+  asm("v_bfi_b32 %0, %1, 0, %2" : "=v"(lh) : "v"(high), "v"(low));   // low & ~high
+  asm("v_ffbh_i32 %0, %1" : "=v"(f) : "v"((lh << n1) | 0x80000000u));
+  e.pending = (emit ? 0u : P) + f - 1u;
+  const uint32_t n = n1 + f - 1u;
+  e.low = (low << n) & 0x7FFFFFFFu;
+  e.rm1 = (rsz << n) - 1u;
 }
 
 __device__ __forceinline__ void enc_finish(EncState& e, BitSink& o) {
@@ -544,7 +550,6 @@ __global__ __launch_bounds__(kWin ? 64 * kEncWinWaves : 1024) void encode_kernel
       const bool anc = kG > 0 ? u == 0 : gq == 0;
       const int q = anc ? cg_quant_inv(v, s, is) : cg_quant_inv(v - a, w, iw);
       const int sym = q + 127;
-      const int sym1 = min(sym + 1, CG_NSYM - 1);
       if (anc) {   // coded in the anchor pass; here only the base of the group's deltas
         a = (float)q * s;
         clo[u] = 0u;
@@ -560,8 +565,9 @@ __global__ __launch_bounds__(kWin ? 64 * kEncWinWaves : 1024) void encode_kernel
         chi[u] = (uint32_t)tabD[sc + 1] + dsym;
         chi[u] = sym == CG_NSYM - 1 ? CG_TOTAL : chi[u];
       } else {
+        // entry 255 of a staged table is its padding: read for the top symbol, then replaced
         clo[u] = tabD[sym];
-        chi[u] = tabD[sym1];
+        chi[u] = tabD[sym + 1];
         chi[u] = sym == CG_NSYM - 1 ? CG_TOTAL : chi[u];
       }
       if (kG == 0) gq = (gq + 1 == P.G) ? 0 : gq + 1;
@@ -639,7 +645,7 @@ __global__ __launch_bounds__(kWin ? 64 * kEncWinWaves : 1024) void encode_kernel
         // both entries loaded unconditionally (a load under a condition would be waited for
         // at once), the top symbol's upper bound selected afterwards
         clo[u] = tabA[sym];
-        chi[u] = tabA[min(sym + 1, CG_NSYM - 1)];
+        chi[u] = tabA[sym + 1];   // entry 255 (padding) for the top symbol, then replaced
         chi[u] = sym == CG_NSYM - 1 ? CG_TOTAL : chi[u];
       }
     };
