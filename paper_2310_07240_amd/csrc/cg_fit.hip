@@ -301,9 +301,10 @@ constexpr int kBufWord3 = 0x00020000;   // raw buffer descriptor: 32-bit data fo
 // to be still in the L2, are read again first. The rows come through a buffer descriptor of the
 // (context, layer, K/V) slab: a row outside the slab reads as zero and such tokens are never
 // counted. kG = 10: the group's loads are issued together and the group is unrolled; kG = 0 takes
-// the group size from P.
+// the group size from P. With several levels the next group's rows and the next pair's maxima
+// are loaded while a group is counted; with one level two workgroups share a CU instead.
 template <int kNl, int kG>
-__global__ __launch_bounds__(kFitThreads) void fit_pass_kernel(
+__global__ __launch_bounds__(kFitThreads, kNl == 1 ? 8 : 4) void fit_pass_kernel(
     KParams P, const uint16_t* __restrict__ kv, int lv0, int with_anchor,
     uint16_t* __restrict__ cdf_anchor, uint16_t* __restrict__ cdf_delta,
     uint32_t* __restrict__ status) {
@@ -419,7 +420,25 @@ __global__ __launch_bounds__(kFitThreads) void fit_pass_kernel(
     const int span_n = more ? nxt.gps * G : 0;
     u16x2 mn = {0, 0};
     int covered = 0;   // tokens of the next slice already in mn
-    if constexpr (kG > 0) {
+    if constexpr (kG > 0 && kNl == 1) {
+      // one level (the anchors and one delta kind: 65 KB of counts): no prefetch and no
+      // interleaved maxima, so that a lane stays within 64 registers and two workgroups share a
+      // CU, whose waves hide each other's load latency instead (measured faster)
+      for (int gi = cur.gps - 1; gi >= 0; --gi) {
+        const int base = gi * kG;
+        uint32_t xc[kG];
+#pragma unroll
+        for (int u = 0; u < kG; ++u) xc[u] = load(cur, base + u);
+        if (__builtin_amdgcn_ballot_w64(base + kG > cur.len) == 0) {
+#pragma unroll
+          for (int u = 0; u < kG; ++u) token(xc[u], u == 0);
+        } else if (base < cur.len) {
+#pragma unroll
+          for (int u = 0; u < kG; ++u)
+            if (base + u < cur.len) token(xc[u], u == 0);
+        }
+      }
+    } else if constexpr (kG > 0) {
       uint32_t xc[kG], xn[kG], y[kG];
 #pragma unroll
       for (int u = 0; u < kG; ++u) xc[u] = load(cur, (cur.gps - 1) * kG + u);
