@@ -263,6 +263,11 @@ FIT_CASES = [
     # leave most of the 32 slices of a chunk empty, the last chunk has 5 tokens
     W.small(name="fit_levels8_b3_c128", n_ctx=3, n_layers=2, n_channels=128, n_tokens=205,
             chunk_len=64, level_mult=(1.0, 1.25, 1.5, 2.0, 3.0, 4.0, 6.0, 8.0)),
+    # three levels in one pass; one level with another group size (the generic group loop)
+    W.small(name="fit_levels3_c192", n_layers=2, n_channels=192, n_tokens=700, chunk_len=320,
+            level_mult=(1.0, 2.0, 4.0)),
+    W.small(name="fit_level1_g7_c128", group_size=7, n_layers=2, n_channels=128, n_tokens=500,
+            chunk_len=200, level_mult=(1.0,)),
     # a chunk of 4 groups per slice and a ragged group inside the last slice
     W.small(name="fit_levels2_t2995", n_layers=1, n_channels=192, n_tokens=2995, chunk_len=1280,
             level_mult=(1.0, 2.0)),
