@@ -3,7 +3,8 @@
 plus encode throughput and bits per element.
 
 One step = the whole codec over one KV cache resident in HBM: fit the distributions of every
-level (cg_fit_cdf_levels), encode (cg_encode), decode (cg_decode). `value` is the decode throughput
+level and the streams' scales (cg_fit_cdf_levels), encode with those scales
+(cg_encode_with_scales), decode (cg_decode). `value` is the decode throughput
 (fp16 bytes of KV produced per second of cg_decode, HIP events on the launch stream) on the
 Mistral-7B-shaped 4K-token cache.
 
@@ -102,13 +103,15 @@ class Run:
         self.stream = torch.cuda.current_stream()
 
     def fit(self):
+        # the tables of every level, and the streams' scales from the same maxima
         from paper_2310_07240_amd.cachegen import cg_fit_cdf_levels
-        cg_fit_cdf_levels(self.p, self.kv, self.ca, self.cd, None, self.stream)
+        cg_fit_cdf_levels(self.p, self.kv, self.ca, self.cd, None, self.stream, self.scales)
 
     def encode(self):
-        from paper_2310_07240_amd.cachegen import cg_encode
-        cg_encode(self.p, self.kv, self.cl, self.ca, self.cd, self.words, self.offsets,
-                  self.scales, self.ws, self.stream)
+        # the encoder takes the fit's scales instead of finding the maxima again
+        from paper_2310_07240_amd.cachegen import cg_encode_with_scales
+        cg_encode_with_scales(self.p, self.kv, self.cl, self.ca, self.cd, self.scales,
+                              self.words, self.offsets, self.ws, self.stream)
 
     def decode(self):
         from paper_2310_07240_amd.cachegen import cg_decode

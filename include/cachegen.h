@@ -135,17 +135,22 @@ int cg_fit_cdf(const cg_params* p, const uint16_t* kv_f16, int32_t level,
  * distribution per channel-layer for deltas and one for anchors; Sec. 6: counted over the
  * symbols of the context being coded; Sec. 5.3: one table set per encoding level). The result
  * equals cg_fit_cdf at every level (anchor tables from any of them), but the scale and the
- * anchors of each chunk are found once for up to three levels, so the cache is read once per
- * three or four levels instead of once per level.
+ * anchors of each chunk are found once for up to four levels, so the cache is read once per
+ * four levels instead of once per level.
  *   kv_f16       [B][L][2][T][C] fp16, device.
  *   cdf_anchor   out [L][2][C][256], device.
  *   cdf_delta    out [n_levels][L][2][C][256], device.
  *   status       NULL, or a device uint32_t (4-byte aligned) that receives 0, or a non-zero
  *                value when the KV holds NaN or +-Inf (the tables are then meaningless);
  *                cg_get_status(status, stream) reads it.
+ *   scales       NULL, or out [S] fp32, device (4-byte aligned): every stream's scale s
+ *                (Sec. 5.2 "Layer-wise quantization": absmax / 127, 1 for an all-zero stream),
+ *                taken from the same maxima the fit quantizes with; these are the scales
+ *                cg_encode computes for the same KV, for cg_encode_with_scales.
  * Asynchronous. */
 int cg_fit_cdf_levels(const cg_params* p, const uint16_t* kv_f16, uint16_t* cdf_anchor,
-                      uint16_t* cdf_delta, uint32_t* status, hipStream_t stream);
+                      uint16_t* cdf_delta, uint32_t* status, float* scales,
+                      hipStream_t stream);
 
 /* Device scratch that cg_fit_cdf_global needs (bytes). */
 #define CG_FIT_GLOBAL_WORKSPACE_BYTES 8192
@@ -184,6 +189,19 @@ int cg_encode(const cg_params* p, const uint16_t* kv_f16, const uint8_t* chunk_l
               const uint16_t* cdf_anchor, const uint16_t* cdf_delta,
               uint32_t* words, uint64_t words_cap, uint64_t* offsets, float* scales,
               void* workspace, uint64_t workspace_bytes, hipStream_t stream);
+
+/* cg_encode with the streams' scales as an input instead of an output (the vectorwise scale of
+ * Sec. 5.2 is found once for fit and encode): `scales` [S] fp32, device (4-byte aligned), as
+ * cg_fit_cdf_levels wrote them for the same KV. The encoder then takes no absolute maxima, and
+ * words and offsets equal those of cg_encode. Other scales code the cache under those scales
+ * (a valid payload; its values are whatever they give). Non-finite input is not looked for:
+ * the fit's status reports it, and the status word in the workspace is 0. Other arguments,
+ * errors and asynchrony as for cg_encode. */
+int cg_encode_with_scales(const cg_params* p, const uint16_t* kv_f16, const uint8_t* chunk_level,
+                          const uint16_t* cdf_anchor, const uint16_t* cdf_delta,
+                          const float* scales, uint32_t* words, uint64_t words_cap,
+                          uint64_t* offsets, void* workspace, uint64_t workspace_bytes,
+                          hipStream_t stream);
 
 /* Bytes of the static device scratch of cg_encode_noalloc (held by every GPU the library runs
  * on until the process ends). */

@@ -28,7 +28,7 @@ EXPORTS = ("cg_num_chunks", "cg_num_streams", "cg_encode_bound_words",
            "cg_num_token_streams", "cg_encode_tokens_bound_words",
            "cg_encode_tokens_workspace_bytes", "cg_decode_tokens_workspace_bytes",
            "cg_encode_tokens", "cg_decode_tokens", "cg_get_status", "cg_encode_noalloc",
-           "cg_fit_cdf_levels", "cg_strerror")
+           "cg_fit_cdf_levels", "cg_encode_with_scales", "cg_strerror")
 CG_FIT_GLOBAL_WORKSPACE_BYTES = 8192
 CG_NOALLOC_SCRATCH_BYTES = 64 << 20
 
@@ -89,13 +89,16 @@ def lib():
         L.cg_encode_workspace_bytes.restype = ctypes.c_uint64
         L.cg_fit_cdf.argtypes = [PP, _P, ctypes.c_int32, _P, _P, _P]
         L.cg_fit_cdf.restype = ctypes.c_int
-        L.cg_fit_cdf_levels.argtypes = [PP, _P, _P, _P, _P, _P]
+        L.cg_fit_cdf_levels.argtypes = [PP, _P, _P, _P, _P, _P, _P]
         L.cg_fit_cdf_levels.restype = ctypes.c_int
         L.cg_fit_cdf_global.argtypes = [PP, _P, ctypes.c_int32, _P, _P, _P, ctypes.c_uint64, _P]
         L.cg_fit_cdf_global.restype = ctypes.c_int
         L.cg_encode.argtypes = [PP, _P, _P, _P, _P, _P, ctypes.c_uint64, _P, _P, _P,
                                 ctypes.c_uint64, _P]
         L.cg_encode.restype = ctypes.c_int
+        L.cg_encode_with_scales.argtypes = [PP, _P, _P, _P, _P, _P, _P, ctypes.c_uint64, _P, _P,
+                                            ctypes.c_uint64, _P]
+        L.cg_encode_with_scales.restype = ctypes.c_int
         L.cg_decode.argtypes = [PP, _P, _P, _P, _P, _P, _P, ctypes.c_int32, ctypes.c_int32, _P, _P]
         L.cg_decode.restype = ctypes.c_int
         L.cg_decode_streamed.argtypes = [PP, _P, _P, _P, ctypes.c_uint64, _P, _P, _P, _P, _P, _P,
@@ -214,12 +217,15 @@ def cg_fit_cdf(p: CodecParams, kv, level: int, cdf_anchor, cdf_delta_level, stre
                             _ptr(cdf_delta_level), _stream(stream)), "cg_fit_cdf")
 
 
-def cg_fit_cdf_levels(p: CodecParams, kv, cdf_anchor, cdf_delta, status=None, stream=None):
+def cg_fit_cdf_levels(p: CodecParams, kv, cdf_anchor, cdf_delta, status=None, stream=None,
+                      scales=None):
     """Every level's tables in one call (cdf_delta [n_levels, L, 2, C, 256]); `status` is an
-    optional device int32 tensor of one element (0, or non-zero for NaN / Inf in kv)."""
+    optional device int32 tensor of one element (0, or non-zero for NaN / Inf in kv);
+    `scales`, an optional device float32 tensor [S], receives every stream's scale."""
     s, keep = p.c()
     _check(lib().cg_fit_cdf_levels(ctypes.byref(s), _ptr(kv), _ptr(cdf_anchor), _ptr(cdf_delta),
-                                   _ptr(status), _stream(stream)), "cg_fit_cdf_levels")
+                                   _ptr(status), _ptr(scales), _stream(stream)),
+           "cg_fit_cdf_levels")
 
 
 def cg_fit_cdf_global(p: CodecParams, kv, level: int, cdf_anchor, cdf_delta_level, workspace,
@@ -239,6 +245,18 @@ def cg_encode(p: CodecParams, kv, chunk_level, cdf_anchor, cdf_delta, words, off
                            _ptr(cdf_delta), _ptr(words), words.numel(), _ptr(offsets),
                            _ptr(scales), _ptr(workspace), workspace.numel() * workspace.element_size(),
                            _stream(stream)), "cg_encode")
+
+
+def cg_encode_with_scales(p: CodecParams, kv, chunk_level, cdf_anchor, cdf_delta, scales, words,
+                          offsets, workspace, stream=None):
+    """cg_encode with the streams' scales as an input (as cg_fit_cdf_levels wrote them)."""
+    s, keep = p.c()
+    _check(lib().cg_encode_with_scales(ctypes.byref(s), _ptr(kv), _ptr(chunk_level),
+                                       _ptr(cdf_anchor), _ptr(cdf_delta), _ptr(scales),
+                                       _ptr(words), words.numel(), _ptr(offsets),
+                                       _ptr(workspace),
+                                       workspace.numel() * workspace.element_size(),
+                                       _stream(stream)), "cg_encode_with_scales")
 
 
 def cg_encode_noalloc(p: CodecParams, kv, chunk_level, cdf_anchor, cdf_delta, words, offsets,
@@ -388,14 +406,15 @@ class Codec:
     def _empty(self, shape, dtype):
         return self.torch.empty(shape, dtype=dtype, device=self.device)
 
-    def fit(self, kv, stream=None, status=None):
+    def fit(self, kv, stream=None, status=None, scales=None):
         """Anchor tables [L,2,C,256] and delta tables of every level [NLV,L,2,C,256], in one
-        cg_fit_cdf_levels call."""
+        cg_fit_cdf_levels call (which also writes the streams' scales into `scales` [S] if
+        given)."""
         t = self.torch
         L, C = self.p.n_layers, self.p.n_channels
         ca = self._empty((L, 2, C, 256), t.int16)
         cd = self._empty((self.p.n_levels, L, 2, C, 256), t.int16)
-        cg_fit_cdf_levels(self.p, kv, ca, cd, status, stream)
+        cg_fit_cdf_levels(self.p, kv, ca, cd, status, stream, scales)
         return ca, cd
 
     def fit_per_level(self, kv, stream=None):
@@ -430,6 +449,17 @@ class Codec:
         cg_encode(self.p, kv, chunk_level, cdf_anchor, cdf_delta, words, offsets, scales,
                   self.workspace(), stream)
         return words, offsets, scales
+
+    def encode_with_scales(self, kv, chunk_level, cdf_anchor, cdf_delta, scales, stream=None,
+                           words=None):
+        """(words, offsets) from cg_encode_with_scales, `scales` [S] being the fit's."""
+        t = self.torch
+        if words is None:
+            words = self._empty((self.bound_words,), t.int32)
+        offsets = self._empty((self.n_streams + 1,), t.int64)
+        cg_encode_with_scales(self.p, kv, chunk_level, cdf_anchor, cdf_delta, scales, words,
+                              offsets, self.workspace(), stream)
+        return words, offsets
 
     def decode(self, words, offsets, scales, chunk_level, cdf_anchor, cdf_delta,
                chunk_begin=0, chunk_end=None, out=None, stream=None):

@@ -126,15 +126,16 @@ int cg_fit_cdf(const cg_params* p, const uint16_t* kv_f16, int32_t level, uint16
 }
 
 int cg_fit_cdf_levels(const cg_params* p, const uint16_t* kv_f16, uint16_t* cdf_anchor,
-                      uint16_t* cdf_delta, uint32_t* status, hipStream_t stream) {
+                      uint16_t* cdf_delta, uint32_t* status, float* scales, hipStream_t stream) {
   KParams K;
   int rc = make_kparams(p, &K);
   if (rc != CG_OK) return rc;
   if (!kv_f16 || !cdf_anchor || !cdf_delta) return CG_ERR_ARG;
   if (!aligned(cdf_anchor, 16) || !aligned(cdf_delta, 16) || !aligned(kv_f16, 2) ||
-      (status && !aligned(status, 4)))
+      (status && !aligned(status, 4)) || (scales && !aligned(scales, 4)))
     return CG_ERR_ARG;
-  return cg_launch_fit_levels(K, kv_f16, cdf_anchor, cdf_delta, status, stream) == hipSuccess
+  return cg_launch_fit_levels(K, kv_f16, cdf_anchor, cdf_delta, status, scales, stream) ==
+                 hipSuccess
              ? CG_OK
              : CG_ERR_HIP;
 }
@@ -176,6 +177,32 @@ int cg_encode(const cg_params* p, const uint16_t* kv_f16, const uint8_t* chunk_l
   if (workspace_bytes < cg_encode_ws_layout(K, slot).total) return CG_ERR_CAPACITY;
   return cg_launch_encode(K, kv_f16, chunk_level, cdf_anchor, cdf_delta, words, offsets, scales,
                           workspace, slot, stream) == hipSuccess
+             ? CG_OK
+             : CG_ERR_HIP;
+}
+
+int cg_encode_with_scales(const cg_params* p, const uint16_t* kv_f16, const uint8_t* chunk_level,
+                          const uint16_t* cdf_anchor, const uint16_t* cdf_delta,
+                          const float* scales, uint32_t* words, uint64_t words_cap,
+                          uint64_t* offsets, void* workspace, uint64_t workspace_bytes,
+                          hipStream_t stream) {
+  KParams K;
+  int rc = make_kparams(p, &K);
+  if (rc != CG_OK) return rc;
+  if (!kv_f16 || !chunk_level || !cdf_anchor || !cdf_delta || !words || !offsets || !scales ||
+      !workspace)
+    return CG_ERR_ARG;
+  if (!aligned(workspace, 256) || !aligned(offsets, 8) || !aligned(words, 4) ||
+      !aligned(scales, 4) || !aligned(kv_f16, 2) || !aligned(cdf_anchor, 16) ||
+      !aligned(cdf_delta, 16))
+    return CG_ERR_ARG;
+  if (words_cap < cg_encode_bound_words(p)) return CG_ERR_CAPACITY;
+  const uint32_t slot = slot_words_for(K);
+  if (workspace_bytes < cg_encode_ws_layout(K, slot).total) return CG_ERR_CAPACITY;
+  // the kernels only read `scales` in this mode
+  return cg_launch_encode(K, kv_f16, chunk_level, cdf_anchor, cdf_delta, words, offsets,
+                          const_cast<float*>(scales), workspace, slot, stream, nullptr,
+                          true) == hipSuccess
              ? CG_OK
              : CG_ERR_HIP;
 }

@@ -200,21 +200,26 @@ __device__ __forceinline__ uint64_t cg_wave_incl_scan64(uint64_t v) {
 }
 
 // Launchers (return hipError_t of the launch).
+// scales, if not null: receives every stream's scale s (the encoder's value for the same KV).
 hipError_t cg_launch_fit(const KParams& P, const uint16_t* kv, int level, uint16_t* cdf_anchor,
-                         uint16_t* cdf_delta_level, hipStream_t st);
+                         uint16_t* cdf_delta_level, hipStream_t st, float* scales = nullptr);
 // Every level's tables in as few passes as 16-bit counts allow (see cg_fit.hip); status, if not
-// null, receives 0 or 1 (NaN or Inf in the KV).
+// null, receives 0 or 1 (NaN or Inf in the KV); scales as for cg_launch_fit.
 hipError_t cg_launch_fit_levels(const KParams& P, const uint16_t* kv, uint16_t* cdf_anchor,
-                                uint16_t* cdf_delta, uint32_t* status, hipStream_t st);
+                                uint16_t* cdf_delta, uint32_t* status, float* scales,
+                                hipStream_t st);
 int64_t cg_fit_max_count(const KParams& P);
 hipError_t cg_launch_fit_global(const KParams& P, const uint16_t* kv, int level,
                                 uint16_t* cdf_anchor, uint16_t* cdf_delta_level, void* ws,
                                 hipStream_t st);
 // status_out: where the non-finite status word goes (nullptr: the workspace's first word).
+// scales_given: scales holds every stream's scale on entry (the encoder then takes no absolute
+// maxima and checks no finiteness); otherwise it receives them.
 hipError_t cg_launch_encode(const KParams& P, const uint16_t* kv, const uint8_t* chunk_level,
                             const uint16_t* cdf_anchor, const uint16_t* cdf_delta,
                             uint32_t* words, uint64_t* offsets, float* scales, void* ws,
-                            uint32_t slot_words, hipStream_t st, uint32_t* status_out = nullptr);
+                            uint32_t slot_words, hipStream_t st, uint32_t* status_out = nullptr,
+                            bool scales_given = false);
 hipError_t cg_launch_decode(const KParams& P, const uint32_t* words, const uint64_t* offsets,
                             const float* scales, const uint8_t* chunk_level,
                             const uint16_t* cdf_anchor, const uint16_t* cdf_delta, int c_begin,

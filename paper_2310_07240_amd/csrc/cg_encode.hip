@@ -244,7 +244,7 @@ __global__ __launch_bounds__(kWin ? 64 * kEncWinWaves : 1024) void encode_kernel
     const uint16_t* __restrict__ cdfA, const uint16_t* __restrict__ cdfD,
     uint32_t* __restrict__ slots, uint32_t slot_words, uint32_t* __restrict__ lens,
     float* __restrict__ scales, uint32_t* __restrict__ wflags, int nw, int nu, int nsets_lds,
-    int ustride) {
+    int ustride, int scales_given) {
   // workgroup = nu units (layer, K/V, 64-channel block) x nw (context, chunk) pairs; wave w
   // codes pair slot w / nu of unit w % nu (one workgroup per CU where the grid allows, so the
   // hardware spreads its waves evenly over the SIMDs). The anchor tables of the units are
@@ -441,8 +441,9 @@ __global__ __launch_bounds__(kWin ? 64 * kEncWinWaves : 1024) void encode_kernel
   // a row, 8 bytes (4 channels) per lane; the partial maxima meet in LDS, in the ring area
   // that coding uses only later. Otherwise every wave reads its own 64 channels row by row.
   const int cb0 = (ublk * nu) % P.nblk;
-  const bool coop = nu == 4 && (ublk + 1) * nu <= n_units && cb0 + nu <= P.nblk &&
-                    (cb0 + nu) * 64 <= P.C && (grp + 1) * nw <= n_pairs && (P.C & 3) == 0 &&
+  const bool coop = !scales_given && nu == 4 && (ublk + 1) * nu <= n_units &&
+                    cb0 + nu <= P.nblk && (cb0 + nu) * 64 <= P.C && (grp + 1) * nw <= n_pairs &&
+                    (P.C & 3) == 0 &&
                     (reinterpret_cast<uintptr_t>(kv) & 7) == 0;   // 8-byte aligned row loads
   // The maximum is taken over the magnitude bits (x & 0x7fff) as integers: for finite halves
   // their order is the order of |x|, and NaN or Inf (exponent all ones) gives a maximum of at
@@ -506,15 +507,17 @@ __global__ __launch_bounds__(kWin ? 64 * kEncWinWaves : 1024) void encode_kernel
   const int64_t rs = P.C;
 
   uint32_t mbits = mx_coop;
-  if (!coop && lane_ok) {
+  if (!coop && !scales_given && lane_ok) {
 #pragma unroll 16
     for (int t = 0; t < n; ++t) mbits = max(mbits, (uint32_t)x[(int64_t)t * rs] & 0x7FFFu);
   }
   if (__builtin_amdgcn_ballot_w64(lane_ok && mbits >= 0x7C00u) != 0ull && lane == 0)
     atomicOr(&s_bad, 1u);
   const float mx = cg_h2f((uint16_t)mbits);
-  const float s = (mx == 0.0f) ? 1.0f : mx / 127.0f;
-  if (lane_ok) scales[sidx] = s;
+  // with scales_given the stream's scale comes in (from the fit's maxima of the same rows)
+  const float s = scales_given ? (lane_ok ? scales[sidx] : 1.0f)
+                               : (mx == 0.0f) ? 1.0f : mx / 127.0f;
+  if (lane_ok && !scales_given) scales[sidx] = s;
   constexpr int kPipe = kG > 0 ? kG : 8;
   const float bw = P.layer_bin[l] * P.level_mult[lv];
   const float w = bw * s;
@@ -1101,7 +1104,8 @@ EncWorkspace cg_encode_ws_layout(const KParams& P, uint32_t slot_words) {
 hipError_t cg_launch_encode(const KParams& P, const uint16_t* kv, const uint8_t* chunk_level,
                             const uint16_t* cdf_anchor, const uint16_t* cdf_delta,
                             uint32_t* words, uint64_t* offsets, float* scales, void* ws,
-                            uint32_t slot_words, hipStream_t st, uint32_t* status_out) {
+                            uint32_t slot_words, hipStream_t st, uint32_t* status_out,
+                            bool scales_given) {
   const EncWorkspace lay = cg_encode_ws_layout(P, slot_words);
   uint8_t* base = static_cast<uint8_t*>(ws);
   uint32_t* status =
@@ -1123,7 +1127,7 @@ hipError_t cg_launch_encode(const KParams& P, const uint16_t* kv, const uint8_t*
 #define CG_ENCODE_LAUNCH(KG, KW)                                                              \
   hipLaunchKernelGGL((encode_kernel<KG, KW>), grid, block, g.lds, st, P, kv, chunk_level,     \
                      cdf_anchor, cdf_delta, slots, slot_words, lens, scales, wflags, g.nw,    \
-                     g.nu, g.nsets, g.ustride)
+                     g.nu, g.nsets, g.ustride, scales_given ? 1 : 0)
   if (P.G == 10) {
     if (g.win) CG_ENCODE_LAUNCH(10, true);
     else CG_ENCODE_LAUNCH(10, false);

@@ -108,12 +108,20 @@ __device__ __forceinline__ void fit_count(float v, int g, float s, float w, floa
   }
 }
 
+// The scale s of the stream (context b, chunk c, layer l, K/V k, channel ch), the value the
+// encoder computes from the same maxima, into scales[S].
+__device__ __forceinline__ void put_scale(float* scales, const KParams& P, int b, int c, int l,
+                                          int k, int ch, float s) {
+  scales[cg_stream(P, (((int64_t)b * P.NC + c) * P.L + l) * 2 + k, ch)] = s;
+}
+
 template <bool kPool, bool kRegs>
 __global__ __launch_bounds__(kFitThreads) void fit_kernel(KParams P, const uint16_t* __restrict__ kv,
                                                          int level, uint16_t* __restrict__ cdf_anchor,
                                                          uint16_t* __restrict__ cdf_delta,
                                                          unsigned long long* __restrict__ pool,
-                                                         uint32_t* __restrict__ status) {
+                                                         uint32_t* __restrict__ status,
+                                                         float* __restrict__ scales) {
   extern __shared__ uint32_t cnt[];  // [2 kinds][64 channels][kHist]
   // partial absolute maxima as magnitude bits (x & 0x7fff): for finite halves they order like
   // |x|, and NaN or Inf gives at least 0x7c00
@@ -186,6 +194,10 @@ __global__ __launch_bounds__(kFitThreads) void fit_kernel(KParams P, const uint1
       const float m0 = cg_h2f((uint16_t)b0), m1 = cg_h2f((uint16_t)b1);
       const float s0 = (m0 == 0.0f) ? 1.0f : m0 / 127.0f;
       const float s1 = (m1 == 0.0f) ? 1.0f : m1 / 127.0f;
+      if (scales && wave == 0 && th == 0) {   // every wave holds the same maxima
+        put_scale(scales, P, b, c, l, k, cb * 64 + 2 * cp, s0);
+        put_scale(scales, P, b, c, l, k, cb * 64 + 2 * cp + 1, s1);
+      }
       const float w0 = wfac * s0, w1 = wfac * s1;
       const float is0 = 1.0f / s0, is1 = 1.0f / s1, iw0 = 1.0f / w0, iw1 = 1.0f / w1;
       uint32_t* ha0 = cnt + (2 * cp) * kHist;
@@ -213,6 +225,7 @@ __global__ __launch_bounds__(kFitThreads) void fit_kernel(KParams P, const uint1
       bad |= act && mb >= 0x7C00u;
       const float m = cg_h2f((uint16_t)mb);
       const float s = (m == 0.0f) ? 1.0f : m / 127.0f;
+      if (scales && wave == 0 && act) put_scale(scales, P, b, c, l, k, ch, s);
       const float w = wfac * s;
       const float is = 1.0f / s, iw = 1.0f / w;
       // pass 2: quantize the slice (it starts on a group boundary) and count
@@ -307,7 +320,7 @@ template <int kNl, int kG>
 __global__ __launch_bounds__(kFitThreads, kNl == 1 ? 8 : 4) void fit_pass_kernel(
     KParams P, const uint16_t* __restrict__ kv, int lv0, int with_anchor,
     uint16_t* __restrict__ cdf_anchor, uint16_t* __restrict__ cdf_delta,
-    uint32_t* __restrict__ status) {
+    uint32_t* __restrict__ status, float* __restrict__ scales) {
   extern __shared__ uint32_t cnt[];   // [kinds][32 channel pairs][kHistP]
   // chunk maxima: (pair index + 1) << 16 | magnitude bits, per channel, alternating buffers (a
   // wave can only reach pair pr + 2 once every wave has read pair pr's buffer)
@@ -383,6 +396,10 @@ __global__ __launch_bounds__(kFitThreads, kNl == 1 ? 8 : 4) void fit_pass_kernel
     const float m0 = cg_h2f((uint16_t)b0), m1 = cg_h2f((uint16_t)b1);
     const float sc0 = (m0 == 0.0f) ? 1.0f : m0 / 127.0f;
     const float sc1 = (m1 == 0.0f) ? 1.0f : m1 / 127.0f;
+    if (scales && with_anchor && wave == 0 && lane < 32) {   // every wave holds the maxima
+      put_scale(scales, P, pr / P.NC, pr % P.NC, l, k, cb * 64 + 2 * cp, sc0);
+      put_scale(scales, P, pr / P.NC, pr % P.NC, l, k, cb * 64 + 2 * cp + 1, sc1);
+    }
     const float is0 = 1.0f / sc0, is1 = 1.0f / sc1;
     float w0[kNl], w1[kNl], iw0[kNl], iw1[kNl];
 #pragma unroll
@@ -503,7 +520,7 @@ template <int kNl>
 __global__ __launch_bounds__(kFitThreads) void fit_levels_kernel(
     KParams P, const uint16_t* __restrict__ kv, int lv0, int with_anchor,
     uint16_t* __restrict__ cdf_anchor, uint16_t* __restrict__ cdf_delta,
-    uint32_t* __restrict__ status) {
+    uint32_t* __restrict__ status, float* __restrict__ scales) {
   extern __shared__ uint32_t cnt[];   // [kinds][32 channel pairs][kHist]
   __shared__ uint32_t part[kFitWaves][64];
   __shared__ uint32_t s_bad;
@@ -546,6 +563,7 @@ __global__ __launch_bounds__(kFitThreads) void fit_levels_kernel(
     bad |= act && m >= 0x7C00u;
     const float mx = cg_h2f((uint16_t)m);
     const float s = (mx == 0.0f) ? 1.0f : mx / 127.0f;
+    if (scales && with_anchor && wave == 0 && act) put_scale(scales, P, b, c, l, k, ch, s);
     const float is = 1.0f / s;
     float w[kNl], iw[kNl];
 #pragma unroll
@@ -613,25 +631,25 @@ template <bool kPool, bool kRegs>
 hipError_t launch_fit_kernel(const KParams& P, const uint16_t* kv, int level,
                              uint16_t* cdf_anchor, uint16_t* cdf_delta_level,
                              unsigned long long* pool, hipStream_t st,
-                             uint32_t* status = nullptr) {
+                             uint32_t* status = nullptr, float* scales = nullptr) {
   const size_t lds = 2 * 64 * kHist * sizeof(uint32_t);
   hipError_t e = hipFuncSetAttribute((const void*)fit_kernel<kPool, kRegs>,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   const int64_t grid = (int64_t)P.L * 2 * P.nblk;
   hipLaunchKernelGGL((fit_kernel<kPool, kRegs>), dim3((unsigned)grid), dim3(kFitThreads), lds,
-                     st, P, kv, level, cdf_anchor, cdf_delta_level, pool, status);
+                     st, P, kv, level, cdf_anchor, cdf_delta_level, pool, status, scales);
   return hipGetLastError();
 }
 }  // namespace
 
 hipError_t cg_launch_fit(const KParams& P, const uint16_t* kv, int level, uint16_t* cdf_anchor,
-                         uint16_t* cdf_delta_level, hipStream_t st) {
+                         uint16_t* cdf_delta_level, hipStream_t st, float* scales) {
   return fit_slice_in_registers(P)
              ? launch_fit_kernel<false, true>(P, kv, level, cdf_anchor, cdf_delta_level,
-                                              nullptr, st)
+                                              nullptr, st, nullptr, scales)
              : launch_fit_kernel<false, false>(P, kv, level, cdf_anchor, cdf_delta_level,
-                                               nullptr, st);
+                                               nullptr, st, nullptr, scales);
 }
 
 hipError_t cg_launch_fit_global(const KParams& P, const uint16_t* kv, int level,
@@ -657,7 +675,7 @@ hipError_t cg_launch_fit_global(const KParams& P, const uint16_t* kv, int level,
 namespace {
 hipError_t launch_fit_levels(const KParams& P, const uint16_t* kv, int lv0, int nl,
                              int with_anchor, uint16_t* cdf_anchor, uint16_t* cdf_delta,
-                             uint32_t* status, hipStream_t st) {
+                             uint32_t* status, float* scales, hipStream_t st) {
   const size_t lds = (size_t)(with_anchor + nl) * 32 * kHist * sizeof(uint32_t);
   const void* fn = nl == 1 ? (const void*)fit_levels_kernel<1>
                  : nl == 2 ? (const void*)fit_levels_kernel<2>
@@ -667,10 +685,10 @@ hipError_t launch_fit_levels(const KParams& P, const uint16_t* kv, int lv0, int 
   if (e != hipSuccess) return e;
   const dim3 grid((unsigned)((int64_t)P.L * 2 * P.nblk)), block(kFitThreads);
   switch (nl) {
-    case 1: hipLaunchKernelGGL((fit_levels_kernel<1>), grid, block, lds, st, P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status); break;
-    case 2: hipLaunchKernelGGL((fit_levels_kernel<2>), grid, block, lds, st, P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status); break;
-    case 3: hipLaunchKernelGGL((fit_levels_kernel<3>), grid, block, lds, st, P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status); break;
-    default: hipLaunchKernelGGL((fit_levels_kernel<4>), grid, block, lds, st, P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status); break;
+    case 1: hipLaunchKernelGGL((fit_levels_kernel<1>), grid, block, lds, st, P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status, scales); break;
+    case 2: hipLaunchKernelGGL((fit_levels_kernel<2>), grid, block, lds, st, P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status, scales); break;
+    case 3: hipLaunchKernelGGL((fit_levels_kernel<3>), grid, block, lds, st, P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status, scales); break;
+    default: hipLaunchKernelGGL((fit_levels_kernel<4>), grid, block, lds, st, P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status, scales); break;
   }
   return hipGetLastError();
 }
@@ -678,7 +696,7 @@ hipError_t launch_fit_levels(const KParams& P, const uint16_t* kv, int lv0, int 
 template <int kNl>
 hipError_t launch_fit_pass_nl(const KParams& P, const uint16_t* kv, int lv0, int with_anchor,
                               uint16_t* cdf_anchor, uint16_t* cdf_delta, uint32_t* status,
-                              hipStream_t st) {
+                              float* scales, hipStream_t st) {
   const size_t lds = (size_t)(with_anchor + kNl) * 32 * kHistP * sizeof(uint32_t);
   const bool g10 = P.G == 10;
   const void* fn = g10 ? (const void*)fit_pass_kernel<kNl, 10> : (const void*)fit_pass_kernel<kNl, 0>;
@@ -687,21 +705,21 @@ hipError_t launch_fit_pass_nl(const KParams& P, const uint16_t* kv, int lv0, int
   const dim3 grid((unsigned)((int64_t)P.L * 2 * P.nblk)), block(kFitThreads);
   if (g10)
     hipLaunchKernelGGL((fit_pass_kernel<kNl, 10>), grid, block, lds, st, P, kv, lv0, with_anchor,
-                       cdf_anchor, cdf_delta, status);
+                       cdf_anchor, cdf_delta, status, scales);
   else
     hipLaunchKernelGGL((fit_pass_kernel<kNl, 0>), grid, block, lds, st, P, kv, lv0, with_anchor,
-                       cdf_anchor, cdf_delta, status);
+                       cdf_anchor, cdf_delta, status, scales);
   return hipGetLastError();
 }
 
 hipError_t launch_fit_pass(const KParams& P, const uint16_t* kv, int lv0, int nl, int with_anchor,
                            uint16_t* cdf_anchor, uint16_t* cdf_delta, uint32_t* status,
-                           hipStream_t st) {
+                           float* scales, hipStream_t st) {
   switch (nl) {
-    case 1: return launch_fit_pass_nl<1>(P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status, st);
-    case 2: return launch_fit_pass_nl<2>(P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status, st);
-    case 3: return launch_fit_pass_nl<3>(P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status, st);
-    default: return launch_fit_pass_nl<4>(P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status, st);
+    case 1: return launch_fit_pass_nl<1>(P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status, scales, st);
+    case 2: return launch_fit_pass_nl<2>(P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status, scales, st);
+    case 3: return launch_fit_pass_nl<3>(P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status, scales, st);
+    default: return launch_fit_pass_nl<4>(P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status, scales, st);
   }
 }
 
@@ -727,12 +745,14 @@ int64_t cg_fit_max_count(const KParams& P) {
 }
 
 hipError_t cg_launch_fit_levels(const KParams& P, const uint16_t* kv, uint16_t* cdf_anchor,
-                                uint16_t* cdf_delta, uint32_t* status, hipStream_t st) {
+                                uint16_t* cdf_delta, uint32_t* status, float* scales,
+                                hipStream_t st) {
   if (cg_fit_max_count(P) >= 65536) {
     // 16-bit counts could overflow: one 32-bit pass per level, and the finiteness scan
     for (int v = 0; v < P.NLV; ++v) {
       hipError_t e = cg_launch_fit(P, kv, v, v == 0 ? cdf_anchor : nullptr,
-                                   cdf_delta + (size_t)v * P.L * 2 * P.C * 256, st);
+                                   cdf_delta + (size_t)v * P.L * 2 * P.C * 256, st,
+                                   v == 0 ? scales : nullptr);
       if (e != hipSuccess) return e;
     }
     return status ? cg_launch_check_finite(kv, (int64_t)P.B * P.L * 2 * P.T * P.C, status, st)
@@ -743,16 +763,17 @@ hipError_t cg_launch_fit_levels(const KParams& P, const uint16_t* kv, uint16_t* 
   if (P.NLV == 1 && !pass)   // one level, any channel count: the 32-bit kernel of cg_fit_cdf
     return fit_slice_in_registers(P)
                ? launch_fit_kernel<false, true>(P, kv, 0, cdf_anchor, cdf_delta, nullptr, st,
-                                                status)
+                                                status, scales)
                : launch_fit_kernel<false, false>(P, kv, 0, cdf_anchor, cdf_delta, nullptr, st,
-                                                 status);
+                                                 status, scales);
   // fit_pass_kernel: the anchors and up to four levels in the first pass, up to four levels in
   // each further one; fit_levels_kernel: up to four kinds per pass
   for (int lv0 = 0, i = 0; lv0 < P.NLV; ++i) {
     const int wa = i == 0 ? 1 : 0;
     const int nl = min(P.NLV - lv0, pass ? kPassKinds - 1 : kLevelKinds - wa);
-    hipError_t e = pass ? launch_fit_pass(P, kv, lv0, nl, wa, cdf_anchor, cdf_delta, status, st)
-                        : launch_fit_levels(P, kv, lv0, nl, wa, cdf_anchor, cdf_delta, status, st);
+    hipError_t e =
+        pass ? launch_fit_pass(P, kv, lv0, nl, wa, cdf_anchor, cdf_delta, status, scales, st)
+             : launch_fit_levels(P, kv, lv0, nl, wa, cdf_anchor, cdf_delta, status, scales, st);
     if (e != hipSuccess) return e;
     lv0 += nl;
   }

@@ -155,8 +155,18 @@ def test_alignment_is_checked_the_same_way_everywhere():
     # status: null or misaligned workspace
     assert lib.cg_get_status(None, None) == -1
     assert lib.cg_get_status(ctypes.c_void_p(A + 2), None) == -1
-    # all-level fit: misaligned tables or status
-    assert lib.cg_fit_cdf_levels(ctypes.byref(s), ok, t8, ok, None, None) == -1
-    assert lib.cg_fit_cdf_levels(ctypes.byref(s), ok, ok, t8, None, None) == -1
-    assert lib.cg_fit_cdf_levels(ctypes.byref(s), ok, ok, ok, odd2, None) == -1
-    assert lib.cg_fit_cdf_levels(ctypes.byref(s), ok, None, ok, None, None) == -1
+    # all-level fit: misaligned tables, status or scales
+    assert lib.cg_fit_cdf_levels(ctypes.byref(s), ok, t8, ok, None, None, None) == -1
+    assert lib.cg_fit_cdf_levels(ctypes.byref(s), ok, ok, t8, None, None, None) == -1
+    assert lib.cg_fit_cdf_levels(ctypes.byref(s), ok, ok, ok, odd2, None, None) == -1
+    assert lib.cg_fit_cdf_levels(ctypes.byref(s), ok, ok, ok, None, odd2, None) == -1
+    assert lib.cg_fit_cdf_levels(ctypes.byref(s), ok, None, ok, None, None, None) == -1
+    # encode with given scales: misaligned or missing scales, misaligned tables
+    assert lib.cg_encode_with_scales(ctypes.byref(s), ok, ok, ok, ok, odd2, ok, bound, ok, ws,
+                                     wsb, None) == -1
+    assert lib.cg_encode_with_scales(ctypes.byref(s), ok, ok, ok, ok, None, ok, bound, ok, ws,
+                                     wsb, None) == -1
+    assert lib.cg_encode_with_scales(ctypes.byref(s), ok, ok, t8, ok, ok, ok, bound, ok, ws,
+                                     wsb, None) == -1
+    assert lib.cg_encode_with_scales(ctypes.byref(s), ok, ok, ok, ok, ok, ok, bound - 1, ok, ws,
+                                     wsb, None) == -3

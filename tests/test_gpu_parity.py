@@ -301,3 +301,38 @@ def test_fit_all_levels_equals_oracle_and_per_level(w):
     bad.view(-1)[bad.numel() // 3] = 0x7C00     # +Inf
     codec.fit(bad, status=st)
     assert cg_get_status(st) == -4
+
+
+SCALE_CASES = [
+    FIT_CASES[0],   # one level, 64-channel blocks
+    W.small(name="scales_one_level_c70", n_tokens=37, chunk_len=1536, level_mult=(1.0,),
+            random_levels=False),   # one level, ragged channels: the 32-bit fit kernel
+    W.small(name="scales_levels8_c70", n_layers=2, n_channels=70, n_tokens=300, chunk_len=64,
+            level_mult=(1.0, 2.0, 4.0, 8.0, 16.0, 32.0, 64.0, 128.0)),   # a lane per channel
+    COMPACT[0],     # windowed delta tables in the encoder, coop absmax path in cg_encode
+    FIT_CASES[-1],  # more than 2^16 deltas per channel: the per-level 32-bit path
+]
+
+
+@pytest.mark.parametrize("w", SCALE_CASES, ids=lambda w: w.name)
+def test_fit_scales_feed_the_encoder(w):
+    """cg_fit_cdf_levels' scales equal cg_encode's, and cg_encode_with_scales on them gives
+    cg_encode's words and offsets, bit for bit."""
+    torch = torch_cuda()
+    from paper_2310_07240_amd.cachegen import Codec, CodecParams
+    codec = Codec(CodecParams.of(w))
+    kv_np = W.generate(w)
+    o = run_oracle(w, kv_np)
+    kv = torch.from_numpy(kv_np.view(np.int16)).cuda()
+    cl = torch.from_numpy(w.chunk_levels()).cuda()
+    sc = torch.full((codec.n_streams,), float("nan"), dtype=torch.float32, device="cuda")
+    ca, cd = codec.fit(kv, scales=sc)
+    assert_same("fit scales vs oracle", sc.cpu().numpy(), o["scales"])
+    words, offsets, scales = codec.encode(kv, cl, ca, cd)
+    assert codec.status() == 0
+    assert_same("fit scales vs encode", sc.cpu().numpy(), scales.cpu().numpy())
+    w2, o2 = codec.encode_with_scales(kv, cl, ca, cd, sc)
+    assert codec.status() == 0
+    n = int(offsets[-1].item())
+    assert_same("offsets", o2.cpu().numpy().view(np.uint64), o["offsets"].view(np.uint64))
+    assert_same("words", w2[:n].cpu().numpy().view(np.uint32), o["words"][:n].view(np.uint32))
