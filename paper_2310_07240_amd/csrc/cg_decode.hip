@@ -72,6 +72,9 @@ __device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlan
 // both the multiplier and the low half of the addend).
 __device__ __forceinline__ uint32_t scaled_off(uint32_t x, uint32_t c) {
   uint64_t r, carry;
+  // c as a plain 32-bit value: a table entry loaded as 16 bits would otherwise be masked to
+  // 16 bits again before it is widened for the addend
+  asm("" : "+v"(c));
   asm("v_mad_u64_u32 %0, %1, %2, %3, %4" : "=v"(r), "=s"(carry) : "v"(x), "v"(c), "v"((uint64_t)c));
   return (uint32_t)(r >> 16);
 }
@@ -539,8 +542,9 @@ __device__ __forceinline__ void g10_advance(G10Lane& st, uint32_t lo_off, uint32
   uint32_t Dn = (uint32_t)(((((uint64_t)d) << 32) | win) << nsh >> 32);
   asm("" : "+v"(Dn));   // keep D a 32-bit value (not the top half of a 64-bit one)
   st.D = Dn;
-  const uint32_t a2 = st.avail - nsh;
-  const bool adv = (int32_t)a2 < 0;
+  // the borrow of avail - nsh is the word advance (one subtract with carry out, no compare)
+  uint32_t a2;
+  const bool adv = __builtin_sub_overflow(st.avail, nsh, &a2);
   st.w0 = adv ? st.w1 : st.w0;
   st.w1 = adv ? st.w2 : st.w1;
   st.w2 = adv ? st.w3 : st.w2;
@@ -562,8 +566,9 @@ __device__ __forceinline__ uint2 lds_ld64(uint32_t a) {
 }
 
 // Fence registers of a table: cum[16 f] << 16 in the high half, and in the low half the byte
-// offset 32 (f - 1) of block f - 1 from the table's start. A fence is <= ti exactly when it is
-// below (ti + 1) << 16, and the fence the search ends on carries the block address with it.
+// offset 32 (f - 1) of block f - 1 from the table's start. A fence's cum[16 f] is <= ti exactly
+// when the tagged fence is <= (ti << 16) | 0xFFFF, and the fence the search ends on carries the
+// block address with it.
 // Entries 0 and 16 (cum[0] = 0 and the total) are never compared and stay zero.
 __device__ __forceinline__ void g10_fences(uint32_t (&fT)[17], const uint16_t* tab) {
   fT[0] = 0u;
@@ -625,21 +630,26 @@ __device__ __forceinline__ void g10_fences_win(uint32_t (&fT)[17], const WinTab&
 template <class Tab>
 __device__ __forceinline__ int g10_symbol(G10Lane& st, const uint32_t (&fT)[17], const Tab& T,
                                           uint32_t tb, uint32_t kq2) {
-  const float te = (float)st.D * (65536.0f * __builtin_amdgcn_rcpf((float)st.rm1));
-  const uint32_t ti = min((uint32_t)te, 65534u);
-  const uint32_t th = (ti << 16) + 0x10000u;   // (ti + 1) << 16
+  // The scale is 2^16 less 5 ulps (5 * 2^-8): with D <= rm1, the reciprocal within 1 ulp and
+  // two roundings, te stays below 2^16, so ti <= 65535 needs no clamp. A target of 65535 may
+  // select entry 255, a sentinel of empty width, which the walk resolves (D then lies in the
+  // interval's top 2^-16). The scale's shortfall of 3e-7 moves te down by at most 0.02. (Were
+  // te to reach 2^16 regardless, th would wrap and the walk would still find the symbol.)
+  const float te = (float)st.D * (65535.98046875f * __builtin_amdgcn_rcpf((float)st.rm1));
+  const uint32_t ti = (uint32_t)te;
+  const uint32_t th = (ti << 16) | 0xFFFFu;   // a fence (cum << 16 | tag) is <= th iff cum <= ti
   // binary search over the fences by selects (four compare / select steps)
-  const bool c3 = fT[8] < th;
+  const bool c3 = fT[8] <= th;
   const uint32_t p4 = c3 ? fT[12] : fT[4];
   const uint32_t p2a = c3 ? fT[10] : fT[2], p2b = c3 ? fT[14] : fT[6];
   const uint32_t p1a = c3 ? fT[9] : fT[1], p1b = c3 ? fT[11] : fT[3];
   const uint32_t p1c = c3 ? fT[13] : fT[5], p1d = c3 ? fT[15] : fT[7];
-  const bool c2 = p4 < th;
+  const bool c2 = p4 <= th;
   const uint32_t p2 = c2 ? p2b : p2a;
   const uint32_t p1e = c2 ? p1c : p1a, p1f = c2 ? p1d : p1b;
-  const bool c1 = p2 < th;
+  const bool c1 = p2 <= th;
   const uint32_t p1 = c1 ? p1f : p1e;
-  const bool c0 = p1 < th;
+  const bool c0 = p1 <= th;
   // block f = (index of p1) - 1 + c0 starts at byte 32 f
   uint32_t qa;
   asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 "
@@ -656,7 +666,9 @@ __device__ __forceinline__ int g10_symbol(G10Lane& st, const uint32_t (&fT)[17],
   const uint2 xy = lds_ld64(qb);
   const bool b2 = (xy.y & 0xFFFFu) <= ti;
   const bool b1 = ((b2 ? xy.y : xy.x) >> 16) <= ti;
-  const uint32_t pa = qb + (b2 ? 4u : 0u) + (b1 ? 2u : 0u);
+  // one three-input add (the compiler would merge the two disjoint constants with an OR first)
+  uint32_t pa;
+  asm("v_add3_u32 %0, %1, %2, %3" : "=v"(pa) : "v"(qb), "v"(b2 ? 4u : 0u), "v"(b1 ? 2u : 0u));
   uint32_t clo = lds_ld16(pa);
   const uint32_t chr = lds_ld16(pa + 2u);
   // 2 q = 2 (symbol - 127) from the entry's address; the top symbol's upper bound is the total
