@@ -30,7 +30,9 @@ constexpr int kHist = 257;  // 255 symbols, padded; odd stride spreads lanes ove
 constexpr int kHalf = 56;   // longest half slice per lane held in registers (one dword per token)
 
 // Normalise one histogram [255] into cum[256] (entry 255 = 0) with one wave. With shift >= 0
-// the counts are the 16-bit fields at that bit position of 32-bit words.
+// the counts are the 16-bit fields at that bit position of 32-bit words. Frequencies are
+// 1 + floor(c (2^16 - 255) / N) for the symbol counts c over their total N, the rest of 2^16
+// going to the most frequent symbol (the lowest index on ties).
 template <typename CountT>
 __device__ void normalize_wave(const CountT* cnt, uint16_t* out, int shift = -1) {
   const int lane = threadIdx.x & 63;
@@ -49,27 +51,62 @@ __device__ void normalize_wave(const CountT* cnt, uint16_t* out, int shift = -1)
     for (int j = 0; j < 4; ++j) c[j] = (lane * 4 + j) < CG_NSYM ? 1u : 0u;
     N = CG_NSYM;
   }
-  // argmax with the lowest index on ties
-  uint64_t best = 0;
-  int besti = 0x7fffffff;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int i = lane * 4 + j;
-    if (i < CG_NSYM && (besti == 0x7fffffff || c[j] > best)) { best = c[j]; besti = i; }
-  }
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
-    uint64_t ob = __shfl_xor(best, o, 64);
-    int oi = __shfl_xor(besti, o, 64);
-    if (ob > best || (ob == best && oi < besti)) { best = ob; besti = oi; }
-  }
+  constexpr uint32_t kSpread = CG_TOTAL - CG_NSYM;
   uint32_t f[4];
   uint32_t fl = 0;
+  int besti = 0x7fffffff;
+  if (N <= 0xFFFFFFFFull) {   // wave-uniform: every count and the total fit 32 bits
+    // argmax with the lowest index on ties
+    uint32_t best = 0;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    int i = lane * 4 + j;
-    f[j] = i < CG_NSYM ? 1u + (uint32_t)((c[j] * (CG_TOTAL - CG_NSYM)) / N) : 0u;
-    fl += f[j];
+    for (int j = 0; j < 4; ++j) {
+      const int i = lane * 4 + j;
+      if (i < CG_NSYM && (besti == 0x7fffffff || (uint32_t)c[j] > best)) {
+        best = (uint32_t)c[j];
+        besti = i;
+      }
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      const uint32_t ob = __shfl_xor(best, o, 64);
+      const int oi = __shfl_xor(besti, o, 64);
+      if (ob > best || (ob == best && oi < besti)) { best = ob; besti = oi; }
+    }
+    // floor(c kSpread / N) without a 64-bit division: a float estimate within 0.016 of the
+    // quotient (four roundings of 2^-24 each), so its truncation is within one of the floor,
+    // then one exact correction step with the 64-bit products
+    const uint32_t Nu = (uint32_t)N;
+    const float ratio = (float)kSpread / (float)Nu;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t cj = (uint32_t)c[j];
+      uint32_t q = (uint32_t)((float)cj * ratio);
+      const uint64_t num = (uint64_t)cj * kSpread;
+      const uint64_t pq = (uint64_t)q * Nu;
+      if (pq > num) q -= 1u;
+      else if (num - pq >= Nu) q += 1u;
+      f[j] = lane * 4 + j < CG_NSYM ? 1u + q : 0u;
+      fl += f[j];
+    }
+  } else {
+    uint64_t best = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int i = lane * 4 + j;
+      if (i < CG_NSYM && (besti == 0x7fffffff || c[j] > best)) { best = c[j]; besti = i; }
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      uint64_t ob = __shfl_xor(best, o, 64);
+      int oi = __shfl_xor(besti, o, 64);
+      if (ob > best || (ob == best && oi < besti)) { best = ob; besti = oi; }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      int i = lane * 4 + j;
+      f[j] = i < CG_NSYM ? 1u + (uint32_t)((c[j] * kSpread) / N) : 0u;
+      fl += f[j];
+    }
   }
   uint32_t sumf = cg_wave_sum<uint32_t>(fl);
   uint32_t rem = CG_TOTAL - sumf;
