@@ -192,7 +192,9 @@ __device__ __forceinline__ void enc_symbol_fast(EncState& e, BitSink& o, uint32_
   const uint32_t E = emit ? P + n1 : 0u;
   rare |= E > 32u;
   const uint32_t H = low >> ((32u - n1) & 31u);
-  const uint32_t runb = ((1u << (P & 31u)) - 1u) << ((n1 - 1u) & 31u);
+  // ((1 << P) - 1) << (n1 - 1), both amounts mod 32, as one bitfield-mask instruction
+  uint32_t runb;
+  asm("v_bfm_b32 %0, %1, %2" : "=v"(runb) : "v"(P), "v"(n1 - 1u));
   const uint32_t val = emit ? H + runb : 0u;
   o.acc = (o.acc << E) | val;   // bits above the nacc valid ones are never read
   const uint32_t t = o.nacc + E;   // < 64
