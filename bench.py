@@ -155,6 +155,17 @@ class Run:
         dec = [e[2].elapsed_time(e[3]) for e in events]
         return fit, enc, dec, wall
 
+    def warm(self, seconds):
+        """Steps, each waited for, until `seconds` of wall time have passed (the clock of a GPU
+        out of idle ramps up over its first ~20-30 ms of work); returns the number of steps."""
+        t0 = time.perf_counter()
+        n = 0
+        while n == 0 or time.perf_counter() - t0 < seconds:
+            self.step()
+            self.torch.cuda.synchronize()
+            n += 1
+        return n
+
     def summary(self, fit, enc, dec):
         """Throughputs, bits per element and the decode's HBM fraction."""
         w = self.w
@@ -350,9 +361,16 @@ def main():
             if name == w.name:
                 continue
             r = Run(wo, dev)
-            f2, e2, d2, _ = r.timed(args.per_workload_steps, 1)
+            gc.collect()
+            gc.disable()
+            try:
+                nwarm = r.warm(0.05)   # 50 ms of steps, then the timed ones
+                f2, e2, d2, _ = r.timed(args.per_workload_steps, 1)
+            finally:
+                gc.enable()
             per[name] = r.summary(f2, e2, d2)
             per[name]["steps"] = args.per_workload_steps
+            per[name]["warmup_steps"] = nwarm + 1
             log(f"{name}: decode {per[name]['decode_GBps']} GB/s, "
                 f"encode {per[name]['encode_GBps']} GB/s, fit {per[name]['fit_ms']} ms")
             r.release()
