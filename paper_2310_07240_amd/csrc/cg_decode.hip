@@ -566,9 +566,9 @@ __device__ __forceinline__ uint2 lds_ld64(uint32_t a) {
 }
 
 // Fence registers of a table: cum[16 f] << 16 in the high half, and in the low half the byte
-// offset 32 (f - 1) of block f - 1 from the table's start. A fence's cum[16 f] is <= ti exactly
-// when the tagged fence is <= (ti << 16) | 0xFFFF, and the fence the search ends on carries the
-// block address with it.
+// offset 32 (f - 1) of block f - 1 from the table's start, compared against the target's
+// fixed-point form ti << 16 | fraction; the fence the search ends on carries the block address
+// with it.
 // Entries 0 and 16 (cum[0] = 0 and the total) are never compared and stay zero.
 __device__ __forceinline__ void g10_fences(uint32_t (&fT)[17], const uint16_t* tab) {
   fT[0] = 0u;
@@ -630,14 +630,18 @@ __device__ __forceinline__ void g10_fences_win(uint32_t (&fT)[17], const WinTab&
 template <class Tab>
 __device__ __forceinline__ int g10_symbol(G10Lane& st, const uint32_t (&fT)[17], const Tab& T,
                                           uint32_t tb, uint32_t kq2) {
-  // The scale is 2^16 less 5 ulps (5 * 2^-8): with D <= rm1, the reciprocal within 1 ulp and
-  // two roundings, te stays below 2^16, so ti <= 65535 needs no clamp. A target of 65535 may
-  // select entry 255, a sentinel of empty width, which the walk resolves (D then lies in the
-  // interval's top 2^-16). The scale's shortfall of 3e-7 moves te down by at most 0.02. (Were
-  // te to reach 2^16 regardless, th would wrap and the walk would still find the symbol.)
-  const float te = (float)st.D * (65535.98046875f * __builtin_amdgcn_rcpf((float)st.rm1));
-  const uint32_t ti = (uint32_t)te;
-  const uint32_t th = (ti << 16) | 0xFFFFu;   // a fence (cum << 16 | tag) is <= th iff cum <= ti
+  // th = ti << 16 | (16 fraction bits) from one conversion, ti = th >> 16 the target. The scale
+  // is 2^32 less 5 ulps (5 * 2^8): with D <= rm1, the reciprocal within 1 ulp and two roundings,
+  // te stays below 2^32, so ti <= 65535 needs no clamp. A target of 65535 may select entry 255,
+  // a sentinel of empty width, which the walk resolves (D then lies in the interval's top
+  // 2^-16). The scale's shortfall of 3e-7 moves ti down by at most 0.02. The entries below
+  // compare against ti as the high half of th (SDWA word selects, no shift); a tagged fence
+  // (cum << 16 | tag) is <= th iff cum < ti, or cum == ti and tag <= the fraction (a tag is at
+  // most 448, so a target exactly on a fence goes to the block below at most once in 146, and
+  // the walk takes the one step up).
+  const float te = (float)st.D * (4294966016.0f * __builtin_amdgcn_rcpf((float)st.rm1));
+  const uint32_t th = (uint32_t)te;
+  const uint32_t ti = th >> 16;
   // binary search over the fences by selects (four compare / select steps)
   const bool c3 = fT[8] <= th;
   const uint32_t p4 = c3 ? fT[12] : fT[4];
