@@ -454,11 +454,11 @@ __global__ __launch_bounds__(1024) void decode_kernel(
 // Same decoder, same results, for the paper's group of 10 tokens (one anchor, nine deltas). A
 // stream holds its chunk's anchors first, then its deltas, so the kernel runs in two phases:
 //   * anchor phase: the anchor tables of the workgroup's units are staged in LDS; each wave
-//     decodes its anchors, kAnchorRun per bitstream epoch, stores each anchor's fp16 value in
-//     its row and keeps the quantized value q in the group's first delta row;
+//     decodes its anchors, kAnchorRun per bitstream epoch, and keeps each anchor's quantized
+//     value q in the anchor's own row;
 //   * delta phase: the delta tables replace the anchor tables in LDS; each group reads back its
 //     anchor's q (requested a group ahead), decodes its nine deltas with epochs before deltas
-//     1 and 6, and stores rows 1..9 (over the kept q).
+//     1 and 6, and stores rows 0..9 (the anchor's fp16 value over the kept q).
 // Both searches start from the 15 fences cum[16 f] of the table in registers (a 4-step select
 // search, no memory round trip), then take three LDS round trips: one 4-ary level and the
 // leaf (each two compare / select steps over entries read together), and the candidate's two
@@ -488,10 +488,11 @@ struct G10Lane {
   float a;                       // dequantized anchor of the current group
 };
 
-// Epoch boundary: the hcnt words dropped from the front of w0..w3 since the last boundary are
-// replaced at the back by as many requested words, and the next four are requested.
-__device__ __forceinline__ void g10_epoch(G10Lane& st, const uint32_t* __restrict__ sbase,
-                                          uint32_t cap) {
+// Epoch boundary, in two halves: g10_epoch_take replaces the hcnt words dropped from the front
+// of w0..w3 since the last boundary at the back by as many requested words (it waits for the
+// previous request); g10_epoch_request requests the next four. A caller may issue stores
+// between the two, so that the next boundary's wait (for this request) covers them long after.
+__device__ __forceinline__ void g10_epoch_take(G10Lane& st) {
   const uint32_t h = st.hcnt;
   // register copies behind an empty asm: selects between the fields themselves could be
   // turned into a select of their addresses, which would move the state to scratch memory
@@ -509,12 +510,20 @@ __device__ __forceinline__ void g10_epoch(G10Lane& st, const uint32_t* __restric
   st.w3 = w3;
   st.widx += h;
   st.hcnt = 0;
+}
+__device__ __forceinline__ void g10_epoch_request(G10Lane& st, const uint32_t* __restrict__ sbase,
+                                                  uint32_t cap) {
   __builtin_amdgcn_sched_barrier(0);
   const uint32_t* tq = sbase + (st.widx < cap ? st.widx : cap);
   st.t0 = tq[0];
   st.t1 = tq[1];
   st.t2 = tq[2];
   st.t3 = tq[3];
+}
+__device__ __forceinline__ void g10_epoch(G10Lane& st, const uint32_t* __restrict__ sbase,
+                                          uint32_t cap) {
+  g10_epoch_take(st);
+  g10_epoch_request(st, sbase, cap);
 }
 
 // Interval update after the symbol [lo_off, hoff) (offsets from low; d = D - lo_off, rsz =
@@ -749,21 +758,21 @@ __device__ __forceinline__ void g10_flush(const uint16_t* obuf, uint16_t* row, i
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Rows 1..9 of a whole group of a full, 16-byte aligned 64-channel block: two unconditional
-// 16-byte stores per lane (rows 1..8, then row 9, which lanes 8..63 store again with the same
-// bytes as lanes 0..7). With the same two stores on every path, the wait at the next epoch
-// covers only the words it needs, not the stores just issued.
+// Rows 0..9 of a whole group of a full, 16-byte aligned 64-channel block: two unconditional
+// 16-byte stores per lane (rows 0..7, then rows 8 and 9, which lanes 16..63 store again with the
+// same bytes as lanes 0..15). With the same two stores on every path, the wait at the next
+// epoch covers only the words it needs, not the stores just issued.
 __device__ __forceinline__ void g10_flush_full(const uint16_t* obuf, uint16_t* row,
                                                int64_t rstride, int lane) {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   const int cc = (lane & 7) * 8;
-  const int r0 = 1 + (lane >> 3);
+  const int r0 = lane >> 3, r1 = 8 + ((lane >> 3) & 1);
   const uint4 v0 = *reinterpret_cast<const uint4*>(obuf + r0 * 64 + cc);
-  const uint4 v1 = *reinterpret_cast<const uint4*>(obuf + 9 * 64 + cc);
+  const uint4 v1 = *reinterpret_cast<const uint4*>(obuf + r1 * 64 + cc);
   store_row16(row + r0 * rstride + cc, v0);
-  store_row16(row + 9 * rstride + cc, v1);
+  store_row16(row + r1 * rstride + cc, v1);
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -1054,24 +1063,35 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     st.rm1 = 0xFFFFFFFFu;
     st.a = 0.0f;
 
-    // kAnchorRun anchors per epoch. Each stores its fp16 value in its row and its quantized
-    // value q in the group's first delta row (when the group has one; else into its own row
-    // first, which the value then overwrites), both unconditionally
-    for (int g0 = 0; g0 < na; g0 += kAnchorRun) {
-      g10_epoch(st, sbase, cap);
+    // kAnchorRun anchors per epoch. The quantized value q of each anchor goes into the anchor's
+    // own row, where the delta phase reads it back and its flush then writes the anchor's fp16
+    // value. A run's q values are stored at the next epoch, between the wait for the words
+    // requested one epoch earlier and the next request, so that no wait for words also waits
+    // for stores just issued.
+    int qrun[kAnchorRun];
+    auto store_run = [&](int gs) __attribute__((always_inline)) {
 #pragma unroll
-      for (int r = 0; r < kAnchorRun; ++r) {
-        const int g = g0 + r;
-        if (g < na) {
-          const int qi = g10_symbol(st, fA, FullTab{tab0}, tbA, kqA) >> 1;
-          // wave-uniform row pointers, the lane's column as the index
-          uint16_t* ra = row0 + (int64_t)g * kG10 * rstride;
-          uint16_t* rq = g * kG10 + 1 < n ? ra + rstride : ra;
-          rq[lsrc] = (uint16_t)qi;
-          ra[lsrc] = cg_f2h((float)qi * s);
-        }
-      }
+      for (int r = 0; r < kAnchorRun; ++r)
+        if (gs + r < na) (row0 + (int64_t)(gs + r) * kG10 * rstride)[lsrc] = (uint16_t)qrun[r];
+    };
+    for (int g0 = 0; g0 < na; g0 += kAnchorRun) {
+      g10_epoch_take(st);
+      if (g0 > 0) store_run(g0 - kAnchorRun);
+      g10_epoch_request(st, sbase, cap);
+#pragma unroll
+      for (int r = 0; r < kAnchorRun; ++r)
+        if (g0 + r < na) qrun[r] = g10_symbol(st, fA, FullTab{tab0}, tbA, kqA) >> 1;
       set_priority(max(na - g0 - kAnchorRun, 0));
+    }
+    const int glast = (na - 1) / kAnchorRun * kAnchorRun;   // first anchor of the last run
+    store_run(glast);
+    // a last group without deltas (n = 1 mod 10) has no flush: its anchor row takes the value
+    if ((na - 1) * kG10 + 1 >= n) {
+      const int rl = na - 1 - glast;
+      int ql = qrun[0];
+#pragma unroll
+      for (int r = 1; r < kAnchorRun; ++r) ql = rl == r ? qrun[r] : ql;
+      (row0 + (int64_t)(na - 1) * kG10 * rstride)[lsrc] = cg_f2h((float)ql * s);
     }
   }
 
@@ -1085,9 +1105,9 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   const int cbase = cb * 64;
   const int ngr = n / kG10;
   const int gmax = (n - 2) / kG10;                    // last group with a delta
-  // the anchor's q of group g (kept in the group's first delta row)
+  // the anchor's q of group g (kept in the anchor's row until the group's flush)
   auto q_of = [&](int g) __attribute__((always_inline)) {
-    const uint16_t* rq = row0 + ((int64_t)min(g, gmax) * kG10 + 1) * rstride;   // uniform
+    const uint16_t* rq = row0 + (int64_t)min(g, gmax) * kG10 * rstride;   // uniform
     return (uint32_t)rq[lsrc];
   };
   // the anchor value of the next group, carried as a float so that the loop head uses no
@@ -1099,6 +1119,7 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   auto groups = [&](auto kFull) __attribute__((always_inline)) {
   for (int gi = 0; gi < ngr; ++gi) {
     st.a = anext;
+    obuf[lane] = cg_f2h(anext);   // row 0: the anchor's value
     g10_epoch(st, sbase, cap);
     g10_delta(st, fD, T, tbD, kqD, w2, obuf, 1, lane);
     g10_delta(st, fD, T, tbD, kqD, w2, obuf, 2, lane);
@@ -1112,7 +1133,7 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     g10_delta(st, fD, T, tbD, kqD, w2, obuf, 8, lane);
     g10_delta(st, fD, T, tbD, kqD, w2, obuf, 9, lane);
     if constexpr (decltype(kFull)::value) g10_flush_full(obuf, row, rstride, lane);
-    else g10_flush(obuf, row, rstride, 1, kG10, lane, cbase, P.C);
+    else g10_flush(obuf, row, rstride, 0, kG10, lane, cbase, P.C);
     row += kG10 * rstride;
     anext = (float)(int)(int16_t)qnext * s;
     // every other group: the ranking reads three LDS words and takes a dozen scalar
@@ -1125,12 +1146,13 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   const int rem = n - ngr * kG10;   // last, partial group (uniform)
   if (rem > 1) {
     st.a = anext;
+    obuf[lane] = cg_f2h(anext);
     g10_epoch(st, sbase, cap);
     for (int r = 1; r < rem; ++r) {
       if (r == 6) g10_epoch(st, sbase, cap);
       g10_delta(st, fD, T, tbD, kqD, w2, obuf, r, lane);
     }
-    g10_flush(obuf, row, rstride, 1, rem, lane, cbase, P.C);
+    g10_flush(obuf, row, rstride, 0, rem, lane, cbase, P.C);
   }
   };
 
