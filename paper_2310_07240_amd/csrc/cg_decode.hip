@@ -641,9 +641,10 @@ __device__ __forceinline__ int g10_symbol(G10Lane& st, const uint32_t (&fT)[17],
                                           uint32_t tb, uint32_t kq2) {
   // th = ti << 16 | (16 fraction bits) from one conversion, ti = th >> 16 the target. The scale
   // is 2^32 less 5 ulps (5 * 2^8): with D <= rm1, the reciprocal within 1 ulp and two roundings,
-  // te stays below 2^32, so ti <= 65535 needs no clamp. A target of 65535 may select entry 255,
-  // a sentinel of empty width, which the walk resolves (D then lies in the interval's top
-  // 2^-16). The scale's shortfall of 3e-7 moves ti down by at most 0.02. The entries below
+  // te stays below 2^32, so ti <= 65535 needs no clamp. The staged entries 255..259 repeat
+  // cum[254], so a target at or above cum[254] (the top symbol, whose upper bound, the total,
+  // does not fit 16 bits) selects candidate 255, of empty width, and the walk resolves it with
+  // the exact bound. The scale's shortfall of 3e-7 moves ti down by at most 0.02. The entries below
   // compare against ti as the high half of th (SDWA word selects, no shift); a tagged fence
   // (cum << 16 | tag) is <= th iff cum < ti, or cum == ti and tag <= the fraction (a tag is at
   // most 448, so a target exactly on a fence goes to the block below at most once in 146, and
@@ -684,9 +685,9 @@ __device__ __forceinline__ int g10_symbol(G10Lane& st, const uint32_t (&fT)[17],
   asm("v_add3_u32 %0, %1, %2, %3" : "=v"(pa) : "v"(qb), "v"(b2 ? 4u : 0u), "v"(b1 ? 2u : 0u));
   uint32_t clo = lds_ld16(pa);
   const uint32_t chr = lds_ld16(pa + 2u);
-  // 2 q = 2 (symbol - 127) from the entry's address; the top symbol's upper bound is the total
+  // 2 q = 2 (symbol - 127) from the entry's address (the candidate is never the top symbol)
   int q2 = (int)(pa + kq2);
-  uint32_t chi = q2 == 2 * (CG_NSYM - 1 - 127) ? CG_TOTAL : chr;
+  uint32_t chi = chr;
   const uint32_t D = st.D, rm1 = st.rm1;
   // offsets of the candidate's interval from low: [lo_off, hoff) (hoff mod 2^32). The candidate
   // is the symbol iff D - lo_off < hoff - lo_off (unsigned): below lo_off the difference wraps
@@ -873,7 +874,8 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   // Stage tables into LDS: the anchor table of every unit (set 0), or the delta tables of the
   // levels each unit's pairs use. A row (one table, 512 bytes) is 32 lanes x 16 bytes, so a
   // wave moves two rows per load instruction; kStageBatch loads per lane are in flight before
-  // their stores. Entry 255 becomes a sentinel above any target, entries 256..259 too.
+  // their stores. Entries 255..259 repeat cum[254] (candidates past the top symbol have empty
+  // intervals, and the walk resolves the top symbol).
   const int half = lane >> 5, piece = lane & 31;
   auto stage = [&](bool anchors) __attribute__((always_inline)) {
     const int sets = anchors ? 1 : msets;
@@ -904,8 +906,9 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
         uint2* dst = reinterpret_cast<uint2*>(tabs + dsto[i]);   // 8-byte aligned (520-byte rows)
         uint4 x = v[i];
         if (piece == 31) {
-          x.w = (x.w & 0xFFFFu) | 0xFFFF0000u;
-          dst[2] = make_uint2(0xFFFFFFFFu, 0xFFFFFFFFu);
+          const uint32_t top = (x.w & 0xFFFFu) * 0x10001u;   // cum[254] in both halves
+          x.w = top;
+          dst[2] = make_uint2(top, top);
         }
         dst[0] = make_uint2(x.x, x.y);
         dst[1] = make_uint2(x.z, x.w);
@@ -918,8 +921,8 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   // blocks g0 = max(i0 / 16 - 1, 0) .. g1 = min(i1 / 16 + 1, 15) are kept, entries 16 g0 ..
   // 16 (g1 + 1) + 3 (8-byte multiple). Pass 2 (layout, one wave per unit): offsets of the
   // windows, set after set, and a new round whenever a set does not fit the region any more.
-  // Pass 3 (per round): the windows of the round's sets are written, with entry 255 and the
-  // entries past it as sentinels above any target.
+  // Pass 3 (per round): the windows of the round's sets are written, with entries 255..259
+  // repeating cum[254] as in the full tables.
   auto window_pass = [&]() __attribute__((always_inline)) {
     const int n_rows = nu * msets * 64;
     for (int base = wave; base * 2 < n_rows; base += nwaves * kStageBatch) {
@@ -994,13 +997,13 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
         uint16_t* dst = tabs + dsto[i] - k0s[i];   // entry k of the table at dst[k]
         const int e = 8 * piece;
         uint4 x = v[i];
-        if (piece == 31) x.w = (x.w & 0xFFFFu) | 0xFFFF0000u;   // entry 255: sentinel
+        if (piece == 31) x.w = (x.w & 0xFFFFu) * 0x10001u;   // entry 255 = cum[254]
         if (e >= k0s[i] && e < kends[i])
           *reinterpret_cast<uint2*>(dst + e) = make_uint2(x.x, x.y);
         if (e + 4 >= k0s[i] && e + 4 < kends[i])
           *reinterpret_cast<uint2*>(dst + e + 4) = make_uint2(x.z, x.w);
-        if (piece == 31 && kends[i] > 256)   // entries 256..259
-          *reinterpret_cast<uint2*>(dst + 256) = make_uint2(0xFFFFFFFFu, 0xFFFFFFFFu);
+        if (piece == 31 && kends[i] > 256)   // entries 256..259 = cum[254]
+          *reinterpret_cast<uint2*>(dst + 256) = make_uint2(x.w, x.w);
       }
     }
   };
