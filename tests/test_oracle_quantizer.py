@@ -36,6 +36,23 @@ def test_float_to_half_matches_numpy_rne():
     assert bad.size == 0, [(float(vals[i]), hex(got[i]), hex(ref[i])) for i in bad[:5]]
 
 
+
+def test_anchor_value_has_no_double_rounding_hazard():
+    """An anchor reconstructs as fp16(fp32(q * s)) with s = fp32(m / 127), m an fp16 magnitude
+    (Sec. 5.2, vectorwise 8-bit anchors). For every finite m and every q in [-127, 127] this
+    equals the single rounding of the exact product q * s to fp16: q * m / 127 lies at least
+    2^-18 (relative) from every fp16 midpoint while fp32 rounding moves it by at most 2^-24, so
+    a GPU instruction that converts the exact product to fp16 in one step gives the same bits."""
+    m = np.arange(0, 0x7c00, dtype=np.uint16).view(np.float16).astype(np.float32)
+    s = (m / np.float32(127)).astype(np.float32)
+    s[m == 0] = 1.0
+    q = np.arange(-127, 128, dtype=np.float64)
+    for i in range(0, s.size, 4096):
+        exact = s[i:i + 4096].astype(np.float64)[:, None] * q[None, :]   # exact: <= 31 bits
+        twice = exact.astype(np.float32).astype(np.float16).view(np.uint16)
+        once = exact.astype(np.float16).view(np.uint16)
+        assert np.array_equal(twice, once), i
+
 def _smooth(n, C, seed=1, scale=1.0):
     rng = np.random.default_rng(seed)
     sc = np.exp(rng.uniform(np.log(0.1), np.log(4), size=C)) * scale
