@@ -59,6 +59,8 @@ constexpr int kMaxUnits = 16;   // (layer, K/V, channel block) units per workgro
 static_assert(4 * kMaxUnits + 3 * kMaxUnits * CG_MAX_LEVELS + kMaxWaves + 4 * kMaxWaves <= 1024 - 64,
               "static LDS exceeds the reserve");
 constexpr int kStageBatch = 8;  // table-staging loads in flight per lane
+constexpr int kDeltaPre = 8;
+constexpr int kAnchorPre = 12;  // anchor-table loads per lane issued first   // delta-table loads per lane issued before the phase barrier
 constexpr size_t kLdsBudget = 160 * 1024 - 1024;   // dynamic LDS per workgroup (CDNA4: 160 KB)
 constexpr int kTabStride = 260;    // u16 per delta table in LDS (256 + 4 pad -> 520 bytes)
 constexpr int kFenceStride = 18;   // u16 per anchor fence row (16 + 2 pad -> 36 bytes)
@@ -569,6 +571,11 @@ __device__ __forceinline__ uint32_t lds_addr(const uint16_t* p) {
   return (uint32_t)(uintptr_t)(lds_cu16*)p;
 }
 __device__ __forceinline__ uint32_t lds_ld16(uint32_t a) { return *(lds_cu16*)(uintptr_t)a; }
+__device__ __forceinline__ uint2 lds_ld2x32(uint32_t a) {   // dwords at a and a + 16
+  const uint32_t x = *(__attribute__((address_space(3))) const uint32_t*)(uintptr_t)a;
+  const uint32_t y = *(__attribute__((address_space(3))) const uint32_t*)(uintptr_t)(a + 16u);
+  return make_uint2(x, y);
+}
 __device__ __forceinline__ uint2 lds_ld64(uint32_t a) {
   const uint64_t v = *(lds_cu64*)(uintptr_t)a;
   return make_uint2((uint32_t)v, (uint32_t)(v >> 32));
@@ -670,9 +677,11 @@ __device__ __forceinline__ int g10_symbol(G10Lane& st, const uint32_t (&fT)[17],
       "src1_sel:DWORD" : "=v"(qa) : "v"(p1), "v"(c0 ? tb + 32u : tb));
   // 4-ary level: cum[16 f + 4 m], m = 1..3
   // two steps over the three sorted entries: cum[16 f + 8], then cum[16 f + 12] or cum[16 f + 4]
-  const uint32_t c4 = lds_ld16(qa + 8u), c8 = lds_ld16(qa + 16u), c12 = lds_ld16(qa + 24u);
+  // (cum[16 f + 4] and cum[16 f + 12] in the low halves of one two-dword read)
+  const uint2 c412 = lds_ld2x32(qa + 8u);
+  const uint32_t c8 = lds_ld16(qa + 16u);
   const bool b8 = c8 <= ti;
-  const bool b4 = (b8 ? c12 : c4) <= ti;
+  const bool b4 = ((b8 ? c412.y : c412.x) & 0xFFFFu) <= ti;
   const uint32_t qb = qa + (b8 ? 16u : 0u) + (b4 ? 8u : 0u);
   // leaf: cum[i .. i+3], i = (qb - tb) / 2, in x = cum[i] | cum[i+1] << 16 and y = cum[i+2] |
   // cum[i+3] << 16; the candidate i + c (c = the number of cum[i+1 .. i+3] <= ti, two steps as
@@ -790,7 +799,7 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     const uint16_t* __restrict__ cdfA, const uint16_t* __restrict__ cdfD, int c_begin,
     int c_end, int nw, int nu, int ustride, uint16_t* __restrict__ out) {
   extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
-  __shared__ uint32_t s_mask[kMaxUnits];
+  __shared__ int s_wlv[kMaxWaves];               // bit of the level of each wave's pair (0: none)
   __shared__ uint8_t s_set_of_level[kMaxUnits][CG_MAX_LEVELS];
   __shared__ uint8_t s_level_of_set[kMaxUnits][CG_MAX_LEVELS];
   __shared__ uint8_t s_nsets[kMaxUnits];
@@ -803,9 +812,6 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   uint16_t* tabs = obuf_all + nu * nw * kG10 * 64;    // [nu][ustride]
   // window descriptors of the delta tables [nu][msets][64] (compact): size / offset, g0, g1
   uint32_t* desc = reinterpret_cast<uint32_t*>(tabs + (size_t)nu * ustride);
-
-  const uint64_t total = offsets[P.S];
-  if (total == 0) return;   // no payload at all: nothing to decode (uniform over the grid)
 
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int nwaves = blockDim.x >> 6;
@@ -821,24 +827,99 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   const int cb = unit % P.nblk;
   const int k = (unit / P.nblk) & 1, l = (unit / P.nblk) >> 1;
 
+  // Stage tables into LDS: the anchor tables of every unit (set 0), or the delta tables of the
+  // levels each unit's pairs use. The nw waves of a unit stage that unit's rows (one table, 512
+  // bytes, is 32 lanes x 16 bytes, so a wave moves two rows per load instruction): wave slot j
+  // takes row pairs j, j + nw, ..., whose unit, set and table row are uniform but for the half.
+  // stage_issue loads batch i0 .. i0 + N - 1 into registers, stage_put writes it; the first
+  // anchor batch goes out before any other load of the kernel, the first delta batch before
+  // the barrier that ends the anchor phase. Entries 255..259 repeat cum[254] (candidates past
+  // the top symbol have empty intervals, and the walk resolves the top symbol).
+  const int half = lane >> 5, piece = lane & 31;
+  const bool unit_ok = unit < n_units;
+  const int64_t lk_row = (int64_t)(l * 2 + k) * P.C + cb * 64;   // table row of channel cb*64
+  // levels used by this wave's unit, a bit per level (set after the first barrier); the set of
+  // a level is its rank among them
+  uint32_t umask = 0u;
+  auto level_of_set = [&](int st) __attribute__((always_inline)) {
+    uint32_t m = umask;
+    for (int i = 0; i < st; ++i) m &= m - 1u;
+    return (int)__builtin_ctz(m | (1u << 31));
+  };
+  auto stage_issue = [&](bool anchors, int i0, auto& v, auto& dsto)
+                         __attribute__((always_inline)) {
+    constexpr int N = sizeof(dsto) / sizeof(dsto[0]);
+    const int sets = anchors ? 1 : __builtin_popcount(umask);
+    const uint16_t* srcbase = anchors ? cdfA : cdfD;
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      // unconditional loads (a row that is not staged reads the first table instead), so
+      // that all of them are in flight before the first store waits
+      const int q = uni(j + nw * (i0 + i));      // row pair of the unit
+      const int st = uni(q >> 5), t = ((q & 31) << 1) + half;
+      const int lset = anchors ? 0 : level_of_set(st);
+      const bool ok = (st < sets) & unit_ok & (cb * 64 + t < P.C);
+      const int64_t trow = lk_row + t + (anchors ? 0 : (int64_t)lset * P.L * 2 * P.C);
+      v[i] = reinterpret_cast<const uint4*>(srcbase + (ok ? trow : 0) * 256)[piece];
+      dsto[i] = ok ? u * ustride + (st * 64 + t) * kTabStride + piece * 8 : -1;
+    }
+  };
+  auto stage_put = [&](const auto& v, const auto& dsto) __attribute__((always_inline)) {
+    constexpr int N = sizeof(dsto) / sizeof(dsto[0]);
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      if (dsto[i] < 0) continue;
+      uint2* dst = reinterpret_cast<uint2*>(tabs + dsto[i]);   // 8-byte aligned (520-byte rows)
+      uint4 x = v[i];
+      if (piece == 31) {
+        const uint32_t top = (x.w & 0xFFFFu) * 0x10001u;   // cum[254] in both halves
+        x.w = top;
+        dst[2] = make_uint2(top, top);
+      }
+      dst[0] = make_uint2(x.x, x.y);
+      dst[1] = make_uint2(x.z, x.w);
+    }
+  };
+  // the batches from i0 on
+  auto stage_rest = [&](bool anchors, int i0) __attribute__((always_inline)) {
+    const int pairs = (anchors ? 1 : __builtin_popcount(umask)) * 32;
+    for (int i = i0; j + nw * i < pairs; i += kStageBatch) {
+      uint4 v[kStageBatch];
+      int dsto[kStageBatch];
+      stage_issue(anchors, i, v, dsto);
+      stage_put(v, dsto);
+    }
+  };
+
+  uint4 anc_v[kAnchorPre];
+  int anc_d[kAnchorPre];
+  stage_issue(true, 0, anc_v, anc_d);
+  // a call without payload decodes nothing (uniform over the grid; checked after the staging)
+  const uint64_t total = offsets[P.S];
+
   const int pair = uni(grp * nw + j);
-  const bool active = unit < n_units && pair < n_pairs;
+  const bool active = unit_ok && pair < n_pairs;
   // pairs chunk-major: the waves of a workgroup decode the same chunk of consecutive contexts,
   // so they have the same token count and finish together
   const int b = uni(active ? pair % P.B : 0);
   const int c = uni(active ? c_begin + pair / P.B : 0);
-  const int lv = uni(active ? min((int)chunk_level[(int64_t)b * P.NC + c], P.NLV - 1) : 0);
+  const int lv = P.NLV == 1 ? 0
+                            : uni(active ? min((int)chunk_level[(int64_t)b * P.NC + c], P.NLV - 1)
+                                         : 0);
   const int tok0 = c * P.CL;
   const int n = uni(active ? min(P.CL, P.T - tok0) : 0);
   const int na = (n + kG10 - 1) / kG10;               // anchors (coded first)
 
   const int simd = (int)((__builtin_amdgcn_s_getreg((31 << 11) | 4) >> 4) & 3u);   // HW_ID
-  if (threadIdx.x < nu) s_mask[threadIdx.x] = 0u;
   if (lane == 0) {
     s_simd[wave] = simd;
     lds_put(&s_left[wave], na);
+    lds_put(&s_wlv[wave], active ? (1 << lv) : 0);
   }
-  __syncthreads();
+  stage_put(anc_v, anc_d);
+  stage_rest(true, kAnchorPre);
+  __syncthreads();   // anchor tables, SIMDs, levels and counts of every wave
+  for (int jj = 0; jj < nw; ++jj) umask |= (uint32_t)uni(lds_get(&s_wlv[u + jj * nu]));
   // the (up to three) other waves of this workgroup on this wave's SIMD
   int p0 = wave, p1 = wave, p2 = wave, np = 0;
   for (int w2 = 0; w2 < nwaves; ++w2) {
@@ -860,61 +941,19 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     else if (rank == 2) __builtin_amdgcn_s_setprio(1);
     else __builtin_amdgcn_s_setprio(0);
   };
-  if (active && lane == 0) atomicOr(&s_mask[u], 1u << lv);
-  __syncthreads();
-  if (threadIdx.x < nu) {
-    const int uu = threadIdx.x;
-    int m = 0;
-    for (int v = 0; v < P.NLV; ++v)
-      if ((s_mask[uu] >> v) & 1u) { s_set_of_level[uu][v] = m; s_level_of_set[uu][m] = v; ++m; }
-    s_nsets[uu] = m;
-  }
-  __syncthreads();
-
-  // Stage tables into LDS: the anchor table of every unit (set 0), or the delta tables of the
-  // levels each unit's pairs use. A row (one table, 512 bytes) is 32 lanes x 16 bytes, so a
-  // wave moves two rows per load instruction; kStageBatch loads per lane are in flight before
-  // their stores. Entries 255..259 repeat cum[254] (candidates past the top symbol have empty
-  // intervals, and the walk resolves the top symbol).
-  const int half = lane >> 5, piece = lane & 31;
-  auto stage = [&](bool anchors) __attribute__((always_inline)) {
-    const int sets = anchors ? 1 : msets;
-    const int n_rows = nu * sets * 64;
-    const uint16_t* srcbase = anchors ? cdfA : cdfD;
-    for (int base = wave; base * 2 < n_rows; base += nwaves * kStageBatch) {
-      uint4 v[kStageBatch];
-      int dsto[kStageBatch];
-#pragma unroll
-      for (int i = 0; i < kStageBatch; ++i) {
-        // unconditional loads (a row that is not staged reads the first table instead), so
-        // that all of them are in flight before the first store waits
-        const int rr = (base + i * nwaves) * 2 + half;
-        const int t = rr & 63, st = (rr >> 6) % sets, uu = min((rr >> 6) / sets, nu - 1);
-        const int unit2 = ublk * nu + uu;
-        const int ch = (unit2 % P.nblk) * 64 + t;
-        const int lset = s_level_of_set[uu][st], nset = anchors ? 1 : s_nsets[uu];
-        const bool ok = (rr < n_rows) & (unit2 < n_units) & (st < nset) & (ch < P.C);
-        const int lk = unit2 / P.nblk;   // l * 2 + k
-        const int64_t trow = anchors ? (int64_t)lk * P.C + ch
-                                     : ((int64_t)lset * P.L * 2 + lk) * P.C + ch;
-        v[i] = reinterpret_cast<const uint4*>(srcbase + (ok ? trow : 0) * 256)[piece];
-        dsto[i] = ok ? uu * ustride + (st * 64 + t) * kTabStride + piece * 8 : -1;
-      }
-#pragma unroll
-      for (int i = 0; i < kStageBatch; ++i) {
-        if (dsto[i] < 0) continue;
-        uint2* dst = reinterpret_cast<uint2*>(tabs + dsto[i]);   // 8-byte aligned (520-byte rows)
-        uint4 x = v[i];
-        if (piece == 31) {
-          const uint32_t top = (x.w & 0xFFFFu) * 0x10001u;   // cum[254] in both halves
-          x.w = top;
-          dst[2] = make_uint2(top, top);
-        }
-        dst[0] = make_uint2(x.x, x.y);
-        dst[1] = make_uint2(x.z, x.w);
-      }
+  // the windowed kernel's passes read the level sets of every unit of the workgroup
+  if constexpr (kCompact) {
+    if (threadIdx.x < nu) {
+      const int uu = threadIdx.x;
+      uint32_t mk = 0u;
+      for (int jj = 0; jj < nw; ++jj) mk |= (uint32_t)lds_get(&s_wlv[uu + jj * nu]);
+      int m = 0;
+      for (int v = 0; v < P.NLV; ++v)
+        if ((mk >> v) & 1u) { s_set_of_level[uu][v] = m; s_level_of_set[uu][m] = v; ++m; }
+      s_nsets[uu] = m;
     }
-  };
+    __syncthreads();
+  }
 
   // Compact staging of the delta tables. Pass 1 (window): each table's first and last
   // frequency other than 1 (i0, i1), from the 8 entries a lane holds and the next lane's first;
@@ -1008,9 +1047,11 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     }
   };
 
-  stage(true);
-  if constexpr (kCompact) window_pass();
-  __syncthreads();
+  if constexpr (kCompact) {
+    window_pass();
+    __syncthreads();
+  }
+  if (total == 0) return;
   if constexpr (kCompact) {
     layout_pass();
     __syncthreads();
@@ -1161,7 +1202,11 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
 
   // ---- delta phase: the delta tables replace the anchor tables --------------------------
   // (in rounds when compact windows of all sets do not fit a unit's region at once; every wave
-  // takes part in every round's staging and barriers, and decodes in its set's round)
+  // takes part in every round's staging and barriers, and decodes in its set's round). Whole
+  // tables: the first kDeltaPre loads per lane go out before the barrier.
+  uint4 dpre_v[kCompact ? 1 : kDeltaPre];
+  int dpre_d[kCompact ? 1 : kDeltaPre];
+  if constexpr (!kCompact) stage_issue(false, 0, dpre_v, dpre_d);
   __syncthreads();
   int nrounds = 1;
   if constexpr (kCompact) {
@@ -1170,12 +1215,18 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   }
   // this wave's round (past the last one: nothing to decode); the rounds before and after it
   // only stage and wait, so that the decoding runs outside any loop
-  const int set = active ? (int)s_set_of_level[u][lv] : 0;
+  const int set = !active ? 0
+                  : kCompact ? (int)s_set_of_level[u][lv]
+                             : __builtin_popcount(umask & ((1u << lv) - 1u));
   const int myr = uni(!active || n < 2 ? nrounds : (kCompact ? (int)s_round[u][set] : 0));
   auto round_stage = [&](int rd) __attribute__((always_inline)) {
     if (rd > 0) __syncthreads();   // the previous round's readers are done
-    if constexpr (kCompact) stage_round(rd);
-    else stage(false);
+    if constexpr (kCompact) {
+      stage_round(rd);
+    } else {
+      stage_put(dpre_v, dpre_d);
+      stage_rest(false, kDeltaPre);
+    }
     __syncthreads();
   };
   for (int rd = 0; rd < myr; ++rd) round_stage(rd);
