@@ -63,6 +63,7 @@ constexpr int kDeltaPre = 8;
 constexpr int kAnchorPre = 12;  // anchor-table loads per lane issued first   // delta-table loads per lane issued before the phase barrier
 constexpr size_t kLdsBudget = 160 * 1024 - 1024;   // dynamic LDS per workgroup (CDNA4: 160 KB)
 constexpr int kTabStride = 260;    // u16 per delta table in LDS (256 + 4 pad -> 520 bytes)
+constexpr int kColSet = 260 * 64;  // u16 of a 64-table set in the column layout (rows of 64)
 constexpr int kFenceStride = 18;   // u16 per anchor fence row (16 + 2 pad -> 36 bytes)
 constexpr int kEpoch = 4;          // tokens between bitstream requests
 constexpr int kRows = 8;           // decoded token rows staged in LDS per wave before a store
@@ -581,27 +582,46 @@ __device__ __forceinline__ uint2 lds_ld64(uint32_t a) {
   return make_uint2((uint32_t)v, (uint32_t)(v >> 32));
 }
 
-// Fence registers of a table: cum[16 f] << 16 in the high half, and in the low half the byte
-// offset 32 (f - 1) of block f - 1 from the table's start, compared against the target's
-// fixed-point form ti << 16 | fraction; the fence the search ends on carries the block address
-// with it.
-// Entries 0 and 16 (cum[0] = 0 and the total) are never compared and stay zero.
-__device__ __forceinline__ void g10_fences(uint32_t (&fT)[17], const uint16_t* tab) {
-  fT[0] = 0u;
-  fT[16] = 0u;
-#pragma unroll
-  for (int f = 1; f < 16; ++f) fT[f] = ((uint32_t)tab[16 * f] << 16) | (32u * (f - 1));
-}
-
-// Views of a table for the rare correction walk after a missed candidate: cum(i) for a symbol
-// i in [0, 254], and the first symbol the walk tries.
-struct FullTab {   // all 256 entries in LDS
-  const uint16_t* tab;
-  __device__ __forceinline__ uint32_t cum(int i) const { return tab[i]; }
+// Views of a staged table. kS is the distance in bytes between consecutive entries of one
+// lane's table: 2 for a table stored contiguously, 128 for the column layout, where entry i of
+// the lane in column L of a 64-column block sits at u16 index 64 i + L. In the column layout a
+// lane's LDS bank depends on its column only, so a wave's 64 lookups at 64 different entries do
+// not collide in the banks (contiguous tables put them in random banks). tb is the byte address
+// of the lane's entry 0; cum(i) reads entry i for the rare correction walk after a missed
+// candidate, first() gives the first symbol the walk tries; q2f / q_of turn the address of
+// the decoded symbol's entry into 2 q (as a float, for the dequantization) or q.
+struct ColTab {   // all 256 entries in LDS, column layout
+  static constexpr uint32_t kS = 128;
+  const uint16_t* tab;   // the lane's column
+  uint32_t tb;
+  int kqi;               // -((tb >> 7) + 127)
+  float kc;              // -(tb / 64 + 254), exact
+  __device__ __forceinline__ ColTab(const uint16_t* t)
+      : tab(t), tb((uint32_t)(uintptr_t)(__attribute__((address_space(3))) const uint16_t*)t),
+        kqi(-(int)((tb >> 7) + 127u)), kc(-((float)tb * 0.015625f + 254.0f)) {}
+  __device__ __forceinline__ uint32_t cum(int i) const { return tab[64 * i]; }
   __device__ __forceinline__ int first(int sym, uint32_t, bool down) const {
     return down ? max(sym - 1, 0) : min(sym + 1, CG_NSYM - 1);
   }
+  // the entry's address is tb + 128 sym: pa / 64 - tb / 64 - 254 = 2 sym - 254 exactly
+  __device__ __forceinline__ float q2f(uint32_t pa) const {
+    return __builtin_fmaf((float)pa, 0.015625f, kc);
+  }
+  __device__ __forceinline__ int q_of(uint32_t pa) const { return (int)(pa >> 7) + kqi; }
 };
+
+// Fence registers of a whole table: cum[16 f] << 16 in the high half, and in the low half the
+// byte offset 16 kS (f - 1) of block f - 1 from the lane's entry 0, compared against the
+// target's fixed-point form ti << 16 | fraction; the fence the search ends on carries the
+// block address with it.
+// Entries 0 and 16 (cum[0] = 0 and the total) are never compared and stay zero.
+template <class Tab>
+__device__ __forceinline__ void g10_fences(uint32_t (&fT)[17], const Tab& T) {
+  fT[0] = 0u;
+  fT[16] = 0u;
+#pragma unroll
+  for (int f = 1; f < 16; ++f) fT[f] = (T.cum(16 * f) << 16) | (16u * Tab::kS * (f - 1));
+}
 
 // A table of which only entries k0 .. k1 are in LDS (entry i at byte address rb + 2 i), the
 // rest following closed forms: every frequency below the first one that differs from 1 is 1,
@@ -610,8 +630,15 @@ struct FullTab {   // all 256 entries in LDS
 // stored 16-entry blocks g0 .. g1, which extend the blocks holding those two frequencies by one
 // block on each side. A target in a flat region jumps straight to its symbol.
 struct WinTab {
+  static constexpr uint32_t kS = 2;
   uint32_t rb;
   int k0, k1;
+  uint32_t tb;   // = rb
+  int kq2;       // -(rb + 254)
+  __device__ __forceinline__ WinTab(uint32_t r, int a, int b)
+      : rb(r), k0(a), k1(b), tb(r), kq2(-(int)(r + 254u)) {}
+  __device__ __forceinline__ float q2f(uint32_t pa) const { return (float)(int)(pa + kq2); }
+  __device__ __forceinline__ int q_of(uint32_t pa) const { return (int)(pa + kq2) >> 1; }
   __device__ __forceinline__ uint32_t cum(int i) const {
     return i < k0 ? (uint32_t)i
                   : (i > k1 ? 65281u + (uint32_t)i : lds_ld16(rb + 2u * (uint32_t)i));
@@ -639,13 +666,14 @@ __device__ __forceinline__ void g10_fences_win(uint32_t (&fT)[17], const WinTab&
   }
 }
 
-// One symbol under the table whose entry 0 sits (really, or for a window table virtually) at
-// LDS byte address tb, with tagged fences fT; kq2 = -(tb + 254); T is the same table for the
-// rare correction walk. Returns 2 q = 2 (symbol - 127) after the interval update and the refill
-// of D.
+// One symbol under the table T whose entry 0 sits (really, or for a window table virtually) at
+// LDS byte address T.tb, entries T.kS bytes apart, with tagged fences fT. Returns the byte
+// address of the decoded symbol's entry after the interval update and the refill of D.
 template <class Tab>
-__device__ __forceinline__ int g10_symbol(G10Lane& st, const uint32_t (&fT)[17], const Tab& T,
-                                          uint32_t tb, uint32_t kq2) {
+__device__ __forceinline__ uint32_t g10_symbol(G10Lane& st, const uint32_t (&fT)[17],
+                                               const Tab& T) {
+  constexpr uint32_t kS = Tab::kS;
+  const uint32_t tb = T.tb;
   // th = ti << 16 | (16 fraction bits) from one conversion, ti = th >> 16 the target. The scale
   // is 2^32 less 5 ulps (5 * 2^8): with D <= rm1, the reciprocal within 1 ulp and two roundings,
   // te stays below 2^32, so ti <= 65535 needs no clamp. The staged entries 255..259 repeat
@@ -671,31 +699,47 @@ __device__ __forceinline__ int g10_symbol(G10Lane& st, const uint32_t (&fT)[17],
   const bool c1 = p2 <= th;
   const uint32_t p1 = c1 ? p1f : p1e;
   const bool c0 = p1 <= th;
-  // block f = (index of p1) - 1 + c0 starts at byte 32 f
+  // block f = (index of p1) - 1 + c0 starts at byte 16 kS f
   uint32_t qa;
   asm("v_add_u32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 "
-      "src1_sel:DWORD" : "=v"(qa) : "v"(p1), "v"(c0 ? tb + 32u : tb));
+      "src1_sel:DWORD" : "=v"(qa) : "v"(p1), "v"(c0 ? tb + 16u * kS : tb));
   // 4-ary level: cum[16 f + 4 m], m = 1..3
   // two steps over the three sorted entries: cum[16 f + 8], then cum[16 f + 12] or cum[16 f + 4]
-  // (cum[16 f + 4] and cum[16 f + 12] in the low halves of one two-dword read)
-  const uint2 c412 = lds_ld2x32(qa + 8u);
-  const uint32_t c8 = lds_ld16(qa + 16u);
-  const bool b8 = c8 <= ti;
-  const bool b4 = ((b8 ? c412.y : c412.x) & 0xFFFFu) <= ti;
-  const uint32_t qb = qa + (b8 ? 16u : 0u) + (b4 ? 8u : 0u);
-  // leaf: cum[i .. i+3], i = (qb - tb) / 2, in x = cum[i] | cum[i+1] << 16 and y = cum[i+2] |
-  // cum[i+3] << 16; the candidate i + c (c = the number of cum[i+1 .. i+3] <= ti, two steps as
-  // above) and the bounds cum[i + c], cum[i + c + 1] are read from its address
-  const uint2 xy = lds_ld64(qb);
-  const bool b2 = (xy.y & 0xFFFFu) <= ti;
-  const bool b1 = ((b2 ? xy.y : xy.x) >> 16) <= ti;
+  bool b8, b4;
+  if constexpr (kS == 2) {
+    // (cum[16 f + 4] and cum[16 f + 12] in the low halves of one two-dword read)
+    const uint2 c412 = lds_ld2x32(qa + 8u);
+    const uint32_t c8 = lds_ld16(qa + 16u);
+    b8 = c8 <= ti;
+    b4 = ((b8 ? c412.y : c412.x) & 0xFFFFu) <= ti;
+  } else {
+    const uint32_t c4 = lds_ld16(qa + 4u * kS), c8 = lds_ld16(qa + 8u * kS),
+                   c12 = lds_ld16(qa + 12u * kS);
+    b8 = c8 <= ti;
+    b4 = (b8 ? c12 : c4) <= ti;
+  }
+  const uint32_t qb = qa + (b8 ? 8u * kS : 0u) + (b4 ? 4u * kS : 0u);
+  // leaf: cum[i .. i+3], i = (qb - tb) / kS; the candidate i + c (c = the number of
+  // cum[i+1 .. i+3] <= ti, two steps as above) and the bounds cum[i + c], cum[i + c + 1] are
+  // read from its address (contiguous tables: x = cum[i] | cum[i+1] << 16 and y = cum[i+2] |
+  // cum[i+3] << 16 from one 8-byte read)
+  bool b2, b1;
+  if constexpr (kS == 2) {
+    const uint2 xy = lds_ld64(qb);
+    b2 = (xy.y & 0xFFFFu) <= ti;
+    b1 = ((b2 ? xy.y : xy.x) >> 16) <= ti;
+  } else {
+    const uint32_t x1 = lds_ld16(qb + kS), x2 = lds_ld16(qb + 2u * kS),
+                   x3 = lds_ld16(qb + 3u * kS);
+    b2 = x2 <= ti;
+    b1 = (b2 ? x3 : x1) <= ti;
+  }
   // one three-input add (the compiler would merge the two disjoint constants with an OR first)
   uint32_t pa;
-  asm("v_add3_u32 %0, %1, %2, %3" : "=v"(pa) : "v"(qb), "v"(b2 ? 4u : 0u), "v"(b1 ? 2u : 0u));
+  asm("v_add3_u32 %0, %1, %2, %3" : "=v"(pa) : "v"(qb), "v"(b2 ? 2u * kS : 0u), "v"(b1 ? kS : 0u));
   uint32_t clo = lds_ld16(pa);
-  const uint32_t chr = lds_ld16(pa + 2u);
-  // 2 q = 2 (symbol - 127) from the entry's address (the candidate is never the top symbol)
-  int q2 = (int)(pa + kq2);
+  const uint32_t chr = lds_ld16(pa + kS);
+  // (the candidate is never the top symbol)
   uint32_t chi = chr;
   const uint32_t D = st.D, rm1 = st.rm1;
   // offsets of the candidate's interval from low: [lo_off, hoff) (hoff mod 2^32). The candidate
@@ -706,7 +750,7 @@ __device__ __forceinline__ int g10_symbol(G10Lane& st, const uint32_t (&fT)[17],
   uint32_t d = D - lo_off;
   uint32_t rsz = hoff - lo_off;
   if (d >= rsz) {
-    int sym = (q2 >> 1) + 127;
+    int sym = (int)((pa - tb) / kS);
     int nxt = T.first(sym, ti, D < lo_off);
     for (int guard = 0; guard < CG_NSYM; ++guard) {
       sym = nxt;
@@ -721,10 +765,10 @@ __device__ __forceinline__ int g10_symbol(G10Lane& st, const uint32_t (&fT)[17],
       if (d < rsz) break;
       nxt = (D < lo_off) ? max(sym - 1, 0) : min(sym + 1, CG_NSYM - 1);
     }
-    q2 = 2 * (sym - 127);
+    pa = tb + kS * (uint32_t)sym;
   }
   g10_advance(st, lo_off, hoff, d, rsz);
-  return q2;
+  return pa;
 }
 
 // One delta token: its symbol under the delta table, dequantized against the group's anchor
@@ -732,10 +776,9 @@ __device__ __forceinline__ int g10_symbol(G10Lane& st, const uint32_t (&fT)[17],
 // w2 = w / 2 (exact), so 2 q times w2 is the same real number as q times w.
 template <class Tab>
 __device__ __forceinline__ void g10_delta(G10Lane& st, const uint32_t (&fD)[17], const Tab& T,
-                                          uint32_t tb, uint32_t kq2, float w2, uint16_t* obuf,
-                                          int r, int lane) {
-  const int q2 = g10_symbol(st, fD, T, tb, kq2);
-  obuf[r * 64 + lane] = cg_f2h(st.a + (float)q2 * w2);
+                                          float w2, uint16_t* obuf, int r, int lane) {
+  const uint32_t pa = g10_symbol(st, fD, T);
+  obuf[r * 64 + lane] = cg_f2h(st.a + T.q2f(pa) * w2);
 }
 
 // Store rows first .. rows-1 of the staged group: lane L stores 16 bytes (8 channels) of row
@@ -827,17 +870,25 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   const int cb = unit % P.nblk;
   const int k = (unit / P.nblk) & 1, l = (unit / P.nblk) >> 1;
 
-  // Stage tables into LDS: the anchor tables of every unit (set 0), or the delta tables of the
-  // levels each unit's pairs use. The nw waves of a unit stage that unit's rows (one table, 512
-  // bytes, is 32 lanes x 16 bytes, so a wave moves two rows per load instruction): wave slot j
-  // takes row pairs j, j + nw, ..., whose unit, set and table row are uniform but for the half.
-  // stage_issue loads batch i0 .. i0 + N - 1 into registers, stage_put writes it; the first
-  // anchor batch goes out before any other load of the kernel, the first delta batch before
-  // the barrier that ends the anchor phase. Entries 255..259 repeat cum[254] (candidates past
-  // the top symbol have empty intervals, and the walk resolves the top symbol).
+  // Stage whole tables into LDS in the column layout (entry i of channel cb * 64 + L at u16
+  // 64 i + L of its set): the anchor tables of every unit (set 0), or the delta tables of the
+  // levels each unit's pairs use. The nw waves of a unit stage that unit's tables; a load
+  // instruction covers the 16 columns of one residue mod 4, four neighbouring lanes taking four
+  // consecutive 16-byte pieces (entries 8 p .. 8 p + 7) of one table, so it touches 16 half
+  // cache lines and its column stores put four lanes on a bank (with one lane per table the
+  // 64 cache lines of every load made the staging slower, with eight the stores conflicted
+  // eight ways). Instruction z of a set (32 of them) takes the columns c with c mod 4 = z mod 4
+  // and pieces 4 ((z mod 32) / 4) + (0 .. 3); wave slot j takes instructions j, j + nw, ... of
+  // the unit's sets (set and instruction uniform). stage_issue
+  // loads batch i0 .. i0 + N - 1 into registers, stage_put writes them (eight 2-byte stores a
+  // piece); the first anchor batch
+  // goes out before any other load of the kernel, the first delta batch before the barrier
+  // that ends the anchor phase. Entries 255..259 repeat cum[254] (candidates past the top
+  // symbol have empty intervals, and the walk resolves the top symbol).
   const int half = lane >> 5, piece = lane & 31;
   const bool unit_ok = unit < n_units;
   const int64_t lk_row = (int64_t)(l * 2 + k) * P.C + cb * 64;   // table row of channel cb*64
+  const int pcol = ((lane >> 2) << 2);   // the first column of the lane's group of four
   // levels used by this wave's unit, a bit per level (set after the first barrier); the set of
   // a level is its rank among them
   uint32_t umask = 0u;
@@ -853,15 +904,16 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     const uint16_t* srcbase = anchors ? cdfA : cdfD;
 #pragma unroll
     for (int i = 0; i < N; ++i) {
-      // unconditional loads (a row that is not staged reads the first table instead), so
+      // unconditional loads (a piece that is not staged reads the first table instead), so
       // that all of them are in flight before the first store waits
-      const int q = uni(j + nw * (i0 + i));      // row pair of the unit
-      const int st = uni(q >> 5), t = ((q & 31) << 1) + half;
+      const int z = uni(j + nw * (i0 + i));      // load instruction of the unit's sets
+      const int st = uni(z >> 5);
+      const int col = pcol + (z & 3), pc = ((z & 31) >> 2) * 4 + (lane & 3);
       const int lset = anchors ? 0 : level_of_set(st);
-      const bool ok = (st < sets) & unit_ok & (cb * 64 + t < P.C);
-      const int64_t trow = lk_row + t + (anchors ? 0 : (int64_t)lset * P.L * 2 * P.C);
-      v[i] = reinterpret_cast<const uint4*>(srcbase + (ok ? trow : 0) * 256)[piece];
-      dsto[i] = ok ? u * ustride + (st * 64 + t) * kTabStride + piece * 8 : -1;
+      const bool ok = (st < sets) & unit_ok & (cb * 64 + col < P.C);
+      const int64_t trow = lk_row + col + (anchors ? 0 : (int64_t)lset * P.L * 2 * P.C);
+      v[i] = reinterpret_cast<const uint4*>(srcbase + (ok ? trow : 0) * 256)[pc];
+      dsto[i] = ok ? u * ustride + st * kColSet + pc * 8 * 64 + col : -1;
     }
   };
   auto stage_put = [&](const auto& v, const auto& dsto) __attribute__((always_inline)) {
@@ -869,15 +921,22 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
 #pragma unroll
     for (int i = 0; i < N; ++i) {
       if (dsto[i] < 0) continue;
-      uint2* dst = reinterpret_cast<uint2*>(tabs + dsto[i]);   // 8-byte aligned (520-byte rows)
-      uint4 x = v[i];
-      if (piece == 31) {
-        const uint32_t top = (x.w & 0xFFFFu) * 0x10001u;   // cum[254] in both halves
-        x.w = top;
-        dst[2] = make_uint2(top, top);
+      uint16_t* dst = tabs + dsto[i];
+      const uint4 x = v[i];
+      const bool last = ((dsto[i] - u * ustride) % kColSet) >= 31 * 8 * 64;   // entries 248..
+      const uint32_t top = x.w & 0xFFFFu;   // cum[254] in piece 31
+      dst[0 * 64] = (uint16_t)x.x;
+      dst[1 * 64] = (uint16_t)(x.x >> 16);
+      dst[2 * 64] = (uint16_t)x.y;
+      dst[3 * 64] = (uint16_t)(x.y >> 16);
+      dst[4 * 64] = (uint16_t)x.z;
+      dst[5 * 64] = (uint16_t)(x.z >> 16);
+      dst[6 * 64] = (uint16_t)x.w;
+      dst[7 * 64] = (uint16_t)(last ? top : x.w >> 16);
+      if (last) {
+#pragma unroll
+        for (int e = 8; e < 12; ++e) dst[e * 64] = (uint16_t)top;   // entries 256..259
       }
-      dst[0] = make_uint2(x.x, x.y);
-      dst[1] = make_uint2(x.z, x.w);
     }
   };
   // the batches from i0 on
@@ -1066,7 +1125,7 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
   const int chv = cb * 64 + lsrc;
   const int64_t rstride = P.C;
   uint16_t* row0 = out + cg_elem(P, b, l, k, tok0, cb * 64);   // token tok0, channel cb * 64
-  const uint16_t* tab0 = tabs + u * ustride + lsrc * kTabStride;   // anchor table of the lane
+  const uint16_t* tab0 = tabs + u * ustride + lsrc;   // anchor table of the lane (column)
   G10Lane st;
   const uint32_t* sbase = words;
   uint32_t cap = 0;
@@ -1079,8 +1138,8 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     s = scales[sidx];
     w = P.layer_bin[l] * P.level_mult[lv] * s;
     uint32_t fA[17];   // tagged fences of the anchor table
-    g10_fences(fA, tab0);
-    const uint32_t tbA = lds_addr(tab0), kqA = 0u - (tbA + 254u);
+    const ColTab TA(tab0);
+    g10_fences(fA, TA);
     // bitstream reader: the code value, w1..w3 and the four requested words t0..t3 are the
     // stream's first 8 words; every read stays below offsets[S] + 4 (the requests are clamped
     // to it), inside the readable tail
@@ -1124,7 +1183,7 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
       g10_epoch_request(st, sbase, cap);
 #pragma unroll
       for (int r = 0; r < kAnchorRun; ++r)
-        if (g0 + r < na) qrun[r] = g10_symbol(st, fA, FullTab{tab0}, tbA, kqA) >> 1;
+        if (g0 + r < na) qrun[r] = TA.q_of(g10_symbol(st, fA, TA));
       set_priority(max(na - g0 - kAnchorRun, 0));
     }
     const int glast = (na - 1) / kAnchorRun * kAnchorRun;   // first anchor of the last run
@@ -1139,10 +1198,9 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     }
   }
 
-  auto delta_groups = [&](const auto& T, const uint32_t (&fD)[17], uint32_t tbD)
+  auto delta_groups = [&](const auto& T, const uint32_t (&fD)[17])
                           __attribute__((always_inline)) {
   set_priority(n - na);
-  const uint32_t kqD = 0u - (tbD + 254u);
   const float w2 = w * 0.5f;
 
   uint16_t* obuf = obuf_all + wave * kG10 * 64;
@@ -1165,17 +1223,17 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     st.a = anext;
     obuf[lane] = cg_f2h(anext);   // row 0: the anchor's value
     g10_epoch(st, sbase, cap);
-    g10_delta(st, fD, T, tbD, kqD, w2, obuf, 1, lane);
-    g10_delta(st, fD, T, tbD, kqD, w2, obuf, 2, lane);
-    g10_delta(st, fD, T, tbD, kqD, w2, obuf, 3, lane);
-    g10_delta(st, fD, T, tbD, kqD, w2, obuf, 4, lane);
-    g10_delta(st, fD, T, tbD, kqD, w2, obuf, 5, lane);
+    g10_delta(st, fD, T, w2, obuf, 1, lane);
+    g10_delta(st, fD, T, w2, obuf, 2, lane);
+    g10_delta(st, fD, T, w2, obuf, 3, lane);
+    g10_delta(st, fD, T, w2, obuf, 4, lane);
+    g10_delta(st, fD, T, w2, obuf, 5, lane);
     g10_epoch(st, sbase, cap);
     const uint32_t qnext = q_of(gi + 1);   // requested a group ahead
-    g10_delta(st, fD, T, tbD, kqD, w2, obuf, 6, lane);
-    g10_delta(st, fD, T, tbD, kqD, w2, obuf, 7, lane);
-    g10_delta(st, fD, T, tbD, kqD, w2, obuf, 8, lane);
-    g10_delta(st, fD, T, tbD, kqD, w2, obuf, 9, lane);
+    g10_delta(st, fD, T, w2, obuf, 6, lane);
+    g10_delta(st, fD, T, w2, obuf, 7, lane);
+    g10_delta(st, fD, T, w2, obuf, 8, lane);
+    g10_delta(st, fD, T, w2, obuf, 9, lane);
     if constexpr (decltype(kFull)::value) g10_flush_full(obuf, row, rstride, lane);
     else g10_flush(obuf, row, rstride, 0, kG10, lane, cbase, P.C);
     row += kG10 * rstride;
@@ -1194,7 +1252,7 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     g10_epoch(st, sbase, cap);
     for (int r = 1; r < rem; ++r) {
       if (r == 6) g10_epoch(st, sbase, cap);
-      g10_delta(st, fD, T, tbD, kqD, w2, obuf, r, lane);
+      g10_delta(st, fD, T, w2, obuf, r, lane);
     }
     g10_flush(obuf, row, rstride, 0, rem, lane, cbase, P.C);
   }
@@ -1236,16 +1294,16 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     if constexpr (kCompact) {
       const uint32_t d = desc[(u * msets + set) * 64 + lsrc];
       const int g0 = (int)((d >> 20) & 15u), g1 = (int)((d >> 24) & 15u);
-      const WinTab T{lds_addr(tabs + u * ustride) + (d & 0xFFFFFu) - 32u * (uint32_t)g0, 16 * g0,
-                     16 * (g1 + 1)};
+      const WinTab T(lds_addr(tabs + u * ustride) + (d & 0xFFFFFu) - 32u * (uint32_t)g0, 16 * g0,
+                     16 * (g1 + 1));
       uint32_t fD[17];
       g10_fences_win(fD, T, g0, g1);
-      delta_groups(T, fD, T.rb);
+      delta_groups(T, fD);
     } else {
-      const uint16_t* dtab = tabs + u * ustride + (set * 64 + lsrc) * kTabStride;
+      const ColTab T(tabs + u * ustride + set * kColSet + lsrc);
       uint32_t fD[17];
-      g10_fences(fD, dtab);
-      delta_groups(FullTab{dtab}, fD, lds_addr(dtab));
+      g10_fences(fD, T);
+      delta_groups(T, fD);
     }
   }
   for (int rd = myr + 1; rd < nrounds; ++rd) round_stage(rd);
