@@ -5,12 +5,16 @@
 //   One lane per stream. A wave decodes the 64 consecutive channels of one (context, chunk,
 //   layer, K/V), so each decoded token row is one coalesced 128-byte store. A workgroup holds
 //   up to 16 such waves that share (layer, K/V, channel block) and therefore share their
-//   distribution tables; the delta tables (9 of 10 symbols) of the levels present are staged in
-//   LDS once per workgroup: the whole 16-bit cumulative table, 256 entries, at a 520-byte stride
-//   (8-byte aligned; neighbouring lanes start in different banks), entries 255..259 holding
-//   0xFFFF sentinels. Anchor tables (1 of 10 symbols) stay in global memory; a symbol reads one
-//   32-byte block of 16 entries and finishes with a select search in registers. Fewer waves
-//   per workgroup when the worst-case table sets would not fit in a CU's LDS.
+//   distribution tables. decode_kernel stages the delta tables (9 of 10 symbols) of the levels
+//   present in LDS once per workgroup: the whole 16-bit cumulative table, 256 entries, at a
+//   520-byte stride (8-byte aligned; neighbouring lanes start in different banks), entries
+//   255..259 holding 0xFFFF sentinels; its anchor tables (1 of 10 symbols) stay in global
+//   memory, a symbol reading one 32-byte block of 16 entries and finishing with a select search
+//   in registers. decode_g10_kernel stages the anchor tables, then the delta tables, in a column
+//   layout (entry i of the lane in column L at u16 64 i + L, so that a wave's 64 lookups fall in
+//   different banks), or the delta tables of several levels as windows of contiguous entries
+//   (see the kernel's comment). Fewer waves per workgroup when the worst-case table sets would
+//   not fit in a CU's LDS.
 //   decode_g10_kernel puts several such units (layer, K/V, channel block) in one workgroup
 //   while the grid still covers every CU: a CU then runs one workgroup, whose waves the
 //   hardware spreads evenly over the four SIMDs (several small workgroups per CU can land four
