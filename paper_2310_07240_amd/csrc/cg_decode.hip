@@ -1176,22 +1176,30 @@ __global__ __launch_bounds__(1024) void decode_g10_kernel(
     // requested one epoch earlier and the next request, so that no wait for words also waits
     // for stores just issued.
     int qrun[kAnchorRun];
+    // row of anchor gs, advanced by whole runs (uniform; the rows of a run at fixed offsets)
+    const int64_t astep = (int64_t)kG10 * rstride;
+    uint16_t* qrow = row0;
     auto store_run = [&](int gs) __attribute__((always_inline)) {
 #pragma unroll
       for (int r = 0; r < kAnchorRun; ++r)
-        if (gs + r < na) (row0 + (int64_t)(gs + r) * kG10 * rstride)[lsrc] = (uint16_t)qrun[r];
+        if (gs + r < na) (qrow + r * astep)[lsrc] = (uint16_t)qrun[r];
     };
     for (int g0 = 0; g0 < na; g0 += kAnchorRun) {
       g10_epoch_take(st);
-      if (g0 > 0) store_run(g0 - kAnchorRun);
+      if (g0 > 0) {
+        store_run(g0 - kAnchorRun);
+        qrow += kAnchorRun * astep;
+      }
       g10_epoch_request(st, sbase, cap);
 #pragma unroll
       for (int r = 0; r < kAnchorRun; ++r)
         if (g0 + r < na) qrun[r] = TA.q_of(g10_symbol(st, fA, TA));
-      set_priority(max(na - g0 - kAnchorRun, 0));
+      // every other run (the ranking reads three LDS words and takes a dozen scalar
+      // instructions)
+      if ((g0 / kAnchorRun) & 1) set_priority(max(na - g0 - kAnchorRun, 0));
     }
     const int glast = (na - 1) / kAnchorRun * kAnchorRun;   // first anchor of the last run
-    store_run(glast);
+    store_run(glast);   // qrow is the row of anchor glast
     // a last group without deltas (n = 1 mod 10) has no flush: its anchor row takes the value
     if ((na - 1) * kG10 + 1 >= n) {
       const int rl = na - 1 - glast;
