@@ -128,6 +128,99 @@ __device__ void normalize_wave(const CountT* cnt, uint16_t* out, int shift = -1)
   reinterpret_cast<uint64_t*>(out)[lane] = packed;
 }
 
+// Inclusive prefix of v over the 64 lanes with DPP moves (no LDS): a Hillis-Steele scan inside
+// each row of 16 lanes (row_shr 1, 2, 4, 8, zero from outside the row), then lane 15 of rows 0
+// and 2 into rows 1 and 3 (row_bcast:15) and lane 31 into rows 2 and 3 (row_bcast:31). kMax
+// takes the running maximum instead of the sum (values must be non-negative). Lane 63 ends with
+// the whole wave's sum or maximum.
+template <bool kMax>
+__device__ __forceinline__ uint32_t dpp_incl_scan(uint32_t v) {
+  auto op = [](uint32_t a, uint32_t b) { return kMax ? max(a, b) : a + b; };
+  v = op(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xf, 0xf, true));
+  v = op(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xf, 0xf, true));
+  v = op(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xf, 0xf, true));
+  v = op(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xf, 0xf, true));
+  v = op(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xa, 0xf, false));
+  v = op(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xc, 0xf, false));
+  return v;
+}
+
+// normalize_wave for 16-bit counts (the 16-bit field at bit `shift` of each word) whose total
+// is below 2^16, as the fit's 16-bit kernels guarantee: the same tables from 32-bit arithmetic.
+// Every product c (2^16 - 255) and q N stays below 2^32 (c, N <= 65535; q <= 2^16 - 254), so the
+// floor comes from the float estimate and one exact correction with 24-bit multiplies; the total,
+// the argmax (key count << 8 | 255 - index: the largest count, then the lowest index) and the
+// frequency prefix are DPP scans.
+__device__ void normalize16_wave(const uint32_t* cnt, uint16_t* out, int shift) {
+  const int lane = threadIdx.x & 63;
+  uint32_t c[4];
+  uint32_t local = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int i = lane * 4 + j;
+    c[j] = i < CG_NSYM ? (cnt[i] >> shift) & 0xFFFFu : 0u;
+    local += c[j];
+  }
+  uint32_t N = (uint32_t)__builtin_amdgcn_readlane((int)dpp_incl_scan<false>(local), 63);
+  if (N == 0) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) c[j] = (lane * 4 + j) < CG_NSYM ? 1u : 0u;
+    N = CG_NSYM;
+  }
+  constexpr uint32_t kSpread = CG_TOTAL - CG_NSYM;
+  uint32_t key = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int i = lane * 4 + j;
+    if (i < CG_NSYM) key = max(key, (c[j] << 8) | (uint32_t)(255 - i));
+  }
+  const uint32_t kmax = (uint32_t)__builtin_amdgcn_readlane((int)dpp_incl_scan<true>(key), 63);
+  const int besti = 255 - (int)(kmax & 0xFFu);
+  const float ratio = (float)kSpread / (float)N;
+  uint32_t f[4];
+  uint32_t fl = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    uint32_t q = (uint32_t)((float)c[j] * ratio);
+    const uint32_t num = __umul24(c[j], kSpread);
+    const uint32_t pq = __umul24(q, N);
+    if (pq > num) q -= 1u;
+    else if (num - pq >= N) q += 1u;
+    f[j] = lane * 4 + j < CG_NSYM ? 1u + q : 0u;
+    fl += f[j];
+  }
+  const uint32_t sumf = (uint32_t)__builtin_amdgcn_readlane((int)dpp_incl_scan<false>(fl), 63);
+  const uint32_t rem = CG_TOTAL - sumf;
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    if (lane * 4 + j == besti) { f[j] += rem; fl += rem; }
+  uint32_t run = dpp_incl_scan<false>(fl) - fl;
+  uint16_t o[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    o[j] = lane * 4 + j < CG_NSYM ? (uint16_t)run : (uint16_t)0;
+    run += f[j];
+  }
+  const uint64_t packed = (uint64_t)o[0] | ((uint64_t)o[1] << 16) | ((uint64_t)o[2] << 32) |
+                          ((uint64_t)o[3] << 48);
+  reinterpret_cast<uint64_t*>(out)[lane] = packed;
+}
+
+// x - a for the fp16 value in the low (kHi false) or high half of w: one v_fma_mix_f32 computing
+// x * 1 - a with the widening fused in. x * 1 is exact and the sum is rounded once, so the result
+// is bit for bit the f32 subtraction of the widened value.
+template <bool kHi>
+__device__ __forceinline__ float sub_half(uint32_t w, float a) {
+  float d;
+  if constexpr (kHi)
+    asm("v_fma_mix_f32 %0, %1, 1.0, -%2 op_sel:[1,0,0] op_sel_hi:[1,0,0]"
+        : "=v"(d) : "v"(w), "v"(a));
+  else
+    asm("v_fma_mix_f32 %0, %1, 1.0, -%2 op_sel_hi:[1,0,0]"
+        : "=v"(d) : "v"(w), "v"(a));
+  return d;
+}
+
 // kPool: instead of normalising per channel, add the workgroup's counts (summed over its 64
 // channels) to the global counts pool[2][256] (anchor, delta): the one-distribution baseline.
 // Count one quantized token of a slice: the anchor (group position g == 0) under the 8-bit
@@ -449,9 +542,9 @@ __global__ __launch_bounds__(kFitThreads, kNl == 1 ? 8 : 4) void fit_pass_kernel
     // one token of both channels: the anchor (u == 0) or the deltas to the group's anchors
     float a0 = 0.0f, a1 = 0.0f;
     auto token = [&](uint32_t x, bool anchor) __attribute__((always_inline)) {
-      const u16x2 h = __builtin_bit_cast(u16x2, x);
-      const float x0 = cg_h2f(h.x), x1 = cg_h2f(h.y);
       if (anchor) {
+        const u16x2 h = __builtin_bit_cast(u16x2, x);
+        const float x0 = cg_h2f(h.x), x1 = cg_h2f(h.y);
         const int q0 = cg_quant_inv(x0, sc0, is0), q1 = cg_quant_inv(x1, sc1, is1);
         a0 = (float)q0 * sc0;
         a1 = (float)q1 * sc1;
@@ -460,7 +553,7 @@ __global__ __launch_bounds__(kFitThreads, kNl == 1 ? 8 : 4) void fit_pass_kernel
           atomicAdd(&ha[q1], 0x10000u);
         }
       } else {
-        const float d0 = x0 - a0, d1 = x1 - a1;
+        const float d0 = sub_half<false>(x, a0), d1 = sub_half<true>(x, a1);
 #pragma unroll
         for (int v = 0; v < kNl; ++v) {
           atomicAdd(&hrow[v][cg_quant_inv(d0, w0[v], iw0[v])], 1u);
@@ -547,7 +640,7 @@ __global__ __launch_bounds__(kFitThreads, kNl == 1 ? 8 : 4) void fit_pass_kernel
                         ? cdf_anchor + ((int64_t)lk * P.C + chx) * 256
                         : cdf_delta + (((int64_t)(lv0 + kind - with_anchor) * P.L * 2 + lk) * P.C +
                                        chx) * 256;
-    normalize_wave<uint32_t>(cnt + (kind * 32 + (cl >> 1)) * kHistP, dst, 16 * (cl & 1));
+    normalize16_wave(cnt + (kind * 32 + (cl >> 1)) * kHistP, dst, 16 * (cl & 1));
   }
 }
 
@@ -643,7 +736,7 @@ __global__ __launch_bounds__(kFitThreads) void fit_levels_kernel(
                         ? cdf_anchor + ((int64_t)lk * P.C + chx) * 256
                         : cdf_delta + (((int64_t)(lv0 + kind - with_anchor) * P.L * 2 + lk) * P.C +
                                        chx) * 256;
-    normalize_wave<uint32_t>(cnt + (kind * 32 + (cl >> 1)) * kHist, dst, 16 * (cl & 1));
+    normalize16_wave(cnt + (kind * 32 + (cl >> 1)) * kHist, dst, 16 * (cl & 1));
   }
 }
 
