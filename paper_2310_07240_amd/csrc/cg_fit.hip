@@ -510,16 +510,75 @@ __global__ __launch_bounds__(kFitThreads, kNl == 1 ? 8 : 4) void fit_pass_kernel
     const u16x2 xm = __builtin_bit_cast(u16x2, x) & mag;
     m = u < len ? __builtin_elementwise_max(m, xm) : m;
   };
-  // pass 1 of the first pair; that of every further pair runs inside the previous pair's pass 2
+  // One level: the maxima of pair pr from 16-byte pieces of the chunk's rows. Lane (r = lane >> 3,
+  // o = lane & 7) takes channels 8o .. 8o + 7 of the block in rows 8 wave + r + 128 i, four loads
+  // in flight together; mw[j] holds channels 8o + 2j and 8o + 2j + 1. Past the chunk's last round
+  // the last round is read again (the maxima do not change).
+  constexpr bool kWide = kNl == 1 && kG > 0;
+  typedef unsigned int u32x4 __attribute__((vector_size(16)));
+  u16x2 mw[4];
+  auto max_wide = [&](int pr) __attribute__((always_inline)) {
+    const int b = pr / P.NC, c = pr % P.NC;
+    const int t0 = c * P.CL;
+    const int n = min(P.CL, P.T - t0);
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(kv + cg_elem(P, b, l, k, 0, 0)), (short)0, slab_bytes, kBufWord3);
+    const int r0 = wave * 8 + (lane >> 3);
+    const int voff = (t0 + r0) * rowb + cb * 128 + (lane & 7) * 16;
+    const int last = (n - 1) >> 7;   // last round holding a row of the chunk
+#pragma unroll
+    for (int j = 0; j < 4; ++j) mw[j] = u16x2{0, 0};
+    for (int i = 0; i <= last; i += 4) {
+      u32x4 v[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        v[e] = __builtin_amdgcn_raw_buffer_load_b128(rs, voff + min(i + e, last) * 128 * rowb, 0, 0);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const bool in = r0 + min(i + e, last) * 128 < n;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          // the element is copied out first: a bit cast of the vector element itself read
+          // element 0 for every j
+          const uint32_t w = v[e][j];
+          mw[j] = in ? __builtin_elementwise_max(mw[j], __builtin_bit_cast(u16x2, w) & mag) : mw[j];
+        }
+      }
+    }
+  };
+  // pass 1 of the first pair; that of every further pair runs inside or after the previous
+  // pair's pass 2
   Slice cur = slice_of(0);
   u16x2 m = {0, 0};
+  if constexpr (kWide) {
+    max_wide(0);
+  } else {
 #pragma unroll 8
-  for (int u = 0; u < cur.gps * G; ++u) max_in(m, load(cur, u), u, cur.len);
+    for (int u = 0; u < cur.gps * G; ++u) max_in(m, load(cur, u), u, cur.len);
+  }
   for (int pr = 0; pr < pairs; ++pr) {
     uint32_t* const sm = s_max[pr & 1];
     const uint32_t tag = (uint32_t)(pr + 1) << 16;
-    atomicMax(&sm[2 * cp], tag | m.x);
-    atomicMax(&sm[2 * cp + 1], tag | m.y);
+    if constexpr (kWide) {
+      // the wave's eight rows of each octet combined, then the first row's lanes publish
+#pragma unroll
+      for (int o = 8; o < 64; o <<= 1) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          mw[j] = __builtin_elementwise_max(
+              mw[j], __builtin_bit_cast(u16x2, __shfl_xor(__builtin_bit_cast(uint32_t, mw[j]), o, 64)));
+      }
+      if (lane < 8) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          atomicMax(&sm[8 * lane + 2 * j], tag | mw[j].x);
+          atomicMax(&sm[8 * lane + 2 * j + 1], tag | mw[j].y);
+        }
+      }
+    } else {
+      atomicMax(&sm[2 * cp], tag | m.x);
+      atomicMax(&sm[2 * cp + 1], tag | m.y);
+    }
     __syncthreads();
     const uint32_t b0 = sm[2 * cp] & 0xFFFFu, b1 = sm[2 * cp + 1] & 0xFFFFu;
     bad |= (b0 >= 0x7C00u) | (b1 >= 0x7C00u);
@@ -624,9 +683,13 @@ __global__ __launch_bounds__(kFitThreads, kNl == 1 ? 8 : 4) void fit_pass_kernel
         for (int u = 0; u < e; ++u) token(load(cur, base + u), u == 0);
       }
     }
+    if constexpr (kWide) {
+      if (more) max_wide(pr + 1);
+    } else {
 #pragma unroll 8
-    for (int u = covered; u < span_n; ++u) max_in(mn, load(nxt, u), u, nxt.len);
-    m = mn;
+      for (int u = covered; u < span_n; ++u) max_in(mn, load(nxt, u), u, nxt.len);
+      m = mn;
+    }
     cur = nxt;
   }
   if (bad) s_bad = 1u;   // benign race: every writer stores 1
@@ -854,10 +917,11 @@ hipError_t launch_fit_pass(const KParams& P, const uint16_t* kv, int lv0, int nl
 }
 
 // fit_pass_kernel's conditions: whole 64-channel blocks, and byte offsets inside one (context,
-// layer, K/V) slab, plus the reads a slice makes past the last token (under 1/32 of a chunk and
-// a group), that stay below 2^31
+// layer, K/V) slab, plus the reads past the last token (a slice's: under 1/32 of a chunk and a
+// group; the one-level maxima pass's: under 128 rows), that stay below 2^31
 bool fit_pass_applies(const KParams& P) {
-  return P.C % 64 == 0 && (int64_t)P.T * P.C * 2 < ((int64_t)1 << 30);
+  return P.C % 64 == 0 && (int64_t)P.T * P.C * 2 < ((int64_t)1 << 30) &&
+         (int64_t)(P.T + 128) * P.C * 2 < ((int64_t)1 << 31);
 }
 }  // namespace
 
