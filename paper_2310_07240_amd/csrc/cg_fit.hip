@@ -435,6 +435,7 @@ __global__ __launch_bounds__(256) void pool_broadcast(const uint16_t* __restrict
 constexpr int kLevelKinds = 4;   // fit_levels_kernel: anchor + levels, or levels, per workgroup
 constexpr int kPassKinds = 5;    // fit_pass_kernel: anchor + four levels, 255-word rows
 constexpr int kHistP = 255;      // 255 symbols, no padding (odd, so rows fall on other banks)
+constexpr int kHoldGroups = 5;   // fit_hold_kernel: groups of a slice held (1536-token chunks: 5)
 constexpr int kBufWord3 = 0x00020000;   // raw buffer descriptor: 32-bit data format
 
 // fit_pass_kernel: whole 64-channel blocks. A lane takes a channel pair cp (one dword per
@@ -707,6 +708,170 @@ __global__ __launch_bounds__(kFitThreads, kNl == 1 ? 8 : 4) void fit_pass_kernel
   }
 }
 
+// fit_hold_kernel: one level, G = 10, whole 64-channel blocks, at most kH groups per slice (the
+// paper's 1536-token chunks: 5). The lanes and slices of fit_pass_kernel, but a slice stays in
+// registers from its maxima to its count, so the cache is read once: as each group is counted,
+// its registers take the same rows of the next slice, whose maxima are taken one group later.
+// The workgroups stay resident (one per CU) and take the (64-channel block, layer, K/V) items
+// in turn, so the next item's first slice loads while the finished item's tables are
+// normalised. Slice maxima meet in LDS under a tag that counts the workgroup's steps.
+template <int kH>
+__global__ __launch_bounds__(kFitThreads, 4) void fit_hold_kernel(
+    KParams P, const uint16_t* __restrict__ kv, int lv0, int with_anchor,
+    uint16_t* __restrict__ cdf_anchor, uint16_t* __restrict__ cdf_delta,
+    uint32_t* __restrict__ status, float* __restrict__ scales) {
+  constexpr int kG = 10, kHR = kH * kG;
+  extern __shared__ uint32_t cnt[];   // [kinds][32 channel pairs][kHistP]
+  __shared__ uint32_t s_max[2][64];   // (step + 1) << 16 | magnitude bits, alternating buffers
+  __shared__ uint32_t s_bad;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int cp = lane & 31;
+  const int slice = wave * 2 + (lane >> 5);
+  const int nk = with_anchor + 1;
+  const int n_items = P.L * 2 * P.nblk;
+  if ((int)blockIdx.x >= n_items) return;   // uniform; the host launches at most n_items
+  for (int i = threadIdx.x; i < nk * 32 * kHistP; i += kFitThreads) cnt[i] = 0;
+  if (threadIdx.x < 128) s_max[threadIdx.x >> 6][threadIdx.x & 63] = 0u;
+  if (threadIdx.x == 0) s_bad = 0u;
+  __syncthreads();
+  uint32_t* const ha = cnt + cp * kHistP + 127;
+  uint32_t* const hd = cnt + (with_anchor * 32 + cp) * kHistP + 127;
+  const int rowb = P.C * 2;
+  const int slab_bytes = P.T * rowb;
+  const int pairs = P.B * P.NC;
+  uint32_t bad = 0u;
+  typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+  struct Slice {
+    __amdgpu_buffer_rsrc_t rs;
+    int voff, len;
+  };
+  // this lane's slice of pair pr of item it (block it % nblk of layer-K/V it / nblk)
+  auto slice_of = [&](int it, int pr) __attribute__((always_inline)) {
+    Slice q;
+    const int cb = it % P.nblk, lk = it / P.nblk;
+    const int b = pr / P.NC, c = pr % P.NC;
+    const int t0 = c * P.CL;
+    const int n = min(P.CL, P.T - t0);
+    const int gps = ((n + kG - 1) / kG + 31) >> 5;
+    const int s0 = min(n, slice * gps * kG);
+    q.len = min(n, (slice + 1) * gps * kG) - s0;
+    q.rs = __builtin_amdgcn_make_buffer_rsrc((void*)(kv + cg_elem(P, b, lk >> 1, lk & 1, 0, 0)),
+                                             (short)0, slab_bytes, kBufWord3);
+    q.voff = (t0 + s0) * rowb + (cb * 64 + 2 * cp) * 2;
+    return q;
+  };
+  auto load = [&](const Slice& q, int u) __attribute__((always_inline)) {
+    return __builtin_amdgcn_raw_buffer_load_b32(q.rs, q.voff + u * rowb, 0, 0);
+  };
+  const u16x2 mag = {0x7FFF, 0x7FFF};
+  auto max_in = [&](u16x2& mm, uint32_t x, int u, int len) __attribute__((always_inline)) {
+    const u16x2 xm = __builtin_bit_cast(u16x2, x) & mag;
+    mm = u < len ? __builtin_elementwise_max(mm, xm) : mm;
+  };
+  int it = blockIdx.x, pr = 0;
+  Slice cur = slice_of(it, 0);
+  uint32_t xs[kHR];   // rows past the slice are loaded too (another slice's, or zero) and skipped
+#pragma unroll
+  for (int u = 0; u < kHR; ++u) xs[u] = load(cur, u);
+  u16x2 m = {0, 0};
+#pragma unroll
+  for (int u = 0; u < kHR; ++u) max_in(m, xs[u], u, cur.len);
+  for (int step = 0;; ++step) {
+    const int cb = it % P.nblk, lk = it / P.nblk;
+    const int l = lk >> 1, k = lk & 1;
+    int nit = it, npr = pr + 1;
+    if (npr == pairs) {
+      npr = 0;
+      nit = it + (int)gridDim.x;
+    }
+    const bool more = nit < n_items;
+    const Slice nxt = more ? slice_of(nit, npr) : cur;
+    uint32_t* const sm = s_max[step & 1];
+    const uint32_t tag = (uint32_t)(step + 1) << 16;
+    atomicMax(&sm[2 * cp], tag | m.x);
+    atomicMax(&sm[2 * cp + 1], tag | m.y);
+    __syncthreads();
+    const uint32_t b0 = sm[2 * cp] & 0xFFFFu, b1 = sm[2 * cp + 1] & 0xFFFFu;
+    bad |= (b0 >= 0x7C00u) | (b1 >= 0x7C00u);
+    const float m0 = cg_h2f((uint16_t)b0), m1 = cg_h2f((uint16_t)b1);
+    const float sc0 = (m0 == 0.0f) ? 1.0f : m0 / 127.0f;
+    const float sc1 = (m1 == 0.0f) ? 1.0f : m1 / 127.0f;
+    if (scales && with_anchor && wave == 0 && lane < 32) {
+      put_scale(scales, P, pr / P.NC, pr % P.NC, l, k, cb * 64 + 2 * cp, sc0);
+      put_scale(scales, P, pr / P.NC, pr % P.NC, l, k, cb * 64 + 2 * cp + 1, sc1);
+    }
+    const float is0 = 1.0f / sc0, is1 = 1.0f / sc1;
+    const float wf = P.layer_bin[l] * P.level_mult[lv0];
+    const float w0 = wf * sc0, w1 = wf * sc1;
+    const float iw0 = 1.0f / w0, iw1 = 1.0f / w1;
+    float a0 = 0.0f, a1 = 0.0f;
+    auto token = [&](uint32_t x, bool anchor) __attribute__((always_inline)) {
+      if (anchor) {
+        const u16x2 h = __builtin_bit_cast(u16x2, x);
+        const int q0 = cg_quant_inv(cg_h2f(h.x), sc0, is0), q1 = cg_quant_inv(cg_h2f(h.y), sc1, is1);
+        a0 = (float)q0 * sc0;
+        a1 = (float)q1 * sc1;
+        if (with_anchor) {
+          atomicAdd(&ha[q0], 1u);
+          atomicAdd(&ha[q1], 0x10000u);
+        }
+      } else {
+        const float d0 = sub_half<false>(x, a0), d1 = sub_half<true>(x, a1);
+        atomicAdd(&hd[cg_quant_inv(d0, w0, iw0)], 1u);
+        atomicAdd(&hd[cg_quant_inv(d1, w1, iw1)], 0x10000u);
+      }
+    };
+    u16x2 mn = {0, 0};
+#pragma unroll
+    for (int g = 0; g < kH; ++g) {
+      const int base = g * kG;
+      if (__builtin_amdgcn_ballot_w64(base + kG > cur.len) == 0) {
+#pragma unroll
+        for (int u = 0; u < kG; ++u) token(xs[base + u], u == 0);
+      } else if (base < cur.len) {
+#pragma unroll
+        for (int u = 0; u < kG; ++u)
+          if (base + u < cur.len) token(xs[base + u], u == 0);
+      }
+      if (more) {
+#pragma unroll
+        for (int u = 0; u < kG; ++u) xs[base + u] = load(nxt, base + u);
+        if (g > 0) {
+#pragma unroll
+          for (int u = base - kG; u < base; ++u) max_in(mn, xs[u], u, nxt.len);
+        }
+      }
+    }
+    if (more) {
+#pragma unroll
+      for (int u = kHR - kG; u < kHR; ++u) max_in(mn, xs[u], u, nxt.len);
+    }
+    m = mn;
+    if (npr == 0 || !more) {   // the item's last pair is counted: its tables
+      __syncthreads();
+      for (int tb = wave; tb < nk * 64; tb += kFitWaves) {
+        const int kind = tb >> 6, cl = tb & 63;
+        const int chx = cb * 64 + cl;
+        uint16_t* dst = (with_anchor && kind == 0)
+                            ? cdf_anchor + ((int64_t)lk * P.C + chx) * 256
+                            : cdf_delta + (((int64_t)(lv0 + kind - with_anchor) * P.L * 2 + lk) *
+                                               P.C + chx) * 256;
+        normalize16_wave(cnt + (kind * 32 + (cl >> 1)) * kHistP, dst, 16 * (cl & 1));
+      }
+      if (!more) break;
+      __syncthreads();
+      // the next step's barrier orders these stores before any count of the next item
+      for (int i = threadIdx.x; i < nk * 32 * kHistP; i += kFitThreads) cnt[i] = 0;
+    }
+    it = nit;
+    pr = npr;
+    cur = nxt;
+  }
+  if (bad) s_bad = 1u;   // benign race: every writer stores 1
+  __syncthreads();
+  if (threadIdx.x == 0 && s_bad && status) atomicOr(status, 1u);
+}
+
 // fit_levels_kernel: any channel count, a lane per channel (channel lane of the block is half
 // lane & 1 of pair lane / 2 of the counts); each pass reads the slice from memory.
 template <int kNl>
@@ -886,12 +1051,40 @@ hipError_t launch_fit_levels(const KParams& P, const uint16_t* kv, int lv0, int 
   return hipGetLastError();
 }
 
+// fit_hold_kernel's grid (one workgroup per CU, at most one per item), or 0 where it does not
+// apply: G = 10, the longest chunk's groups in 32 slices of at most kHoldGroups groups, and
+// under 2^16 steps per workgroup (the maxima tag)
+int fit_hold_grid(const KParams& P) {
+  if (P.G != 10) return 0;
+  const int64_t n = P.CL < P.T ? P.CL : P.T;
+  if ((((n + 9) / 10 + 31) >> 5) > kHoldGroups) return 0;
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus <= 0)
+    return 0;
+  const int64_t items = (int64_t)P.L * 2 * P.nblk;
+  const int64_t grid = items < cus ? items : cus;
+  const int64_t steps = (items + grid - 1) / grid * P.B * P.NC;
+  return steps < 65535 ? (int)grid : 0;
+}
+
 template <int kNl>
 hipError_t launch_fit_pass_nl(const KParams& P, const uint16_t* kv, int lv0, int with_anchor,
                               uint16_t* cdf_anchor, uint16_t* cdf_delta, uint32_t* status,
                               float* scales, hipStream_t st) {
   const size_t lds = (size_t)(with_anchor + kNl) * 32 * kHistP * sizeof(uint32_t);
   const bool g10 = P.G == 10;
+  if constexpr (kNl == 1) {
+    if (const int grid = fit_hold_grid(P)) {
+      const void* fn = (const void*)fit_hold_kernel<kHoldGroups>;
+      hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL((fit_hold_kernel<kHoldGroups>), dim3((unsigned)grid), dim3(kFitThreads),
+                         lds, st, P, kv, lv0, with_anchor, cdf_anchor, cdf_delta, status, scales);
+      return hipGetLastError();
+    }
+  }
   const void* fn = g10 ? (const void*)fit_pass_kernel<kNl, 10> : (const void*)fit_pass_kernel<kNl, 0>;
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
