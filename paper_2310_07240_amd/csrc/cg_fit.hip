@@ -15,7 +15,9 @@
 // slice is read once, into registers, with all its loads in flight together, and both passes
 // work from the registers. Otherwise the rows are read once per pass, a lane per channel.
 // fit_pass_kernel (whole 64-channel blocks) and fit_levels_kernel (any channel count) fit the
-// anchors and several levels from one quantization with 16-bit counts.
+// anchors and several levels from one quantization with 16-bit counts; fit_hold_kernel is
+// fit_pass_kernel's one-level case at G = 10 with the slice held in registers between its
+// maxima and its count (the cache read once) and resident workgroups that walk the blocks.
 //
 // Histograms use an odd row stride so lanes that count the same symbol hit different banks. At
 // the end each wave normalises histograms to 16-bit cumulative tables: per-lane partial sums, a
