@@ -271,6 +271,14 @@ FIT_CASES = [
     # a chunk of 4 groups per slice and a ragged group inside the last slice
     W.small(name="fit_levels2_t2995", n_layers=1, n_channels=192, n_tokens=2995, chunk_len=1280,
             level_mult=(1.0, 2.0)),
+    # five levels at G = 10: the second pass fits one level without the anchors (the one-read
+    # kernel's with_anchor = 0 case)
+    W.small(name="fit_levels5_g10_c128", n_layers=2, n_channels=128, n_tokens=700, chunk_len=320,
+            level_mult=(1.0, 2.0, 4.0, 8.0, 16.0)),
+    # 270 (block, layer, K/V) items, more than the one-read kernel's resident workgroups (one
+    # per CU): some workgroups take two items, the next item's first slice loaded across
+    W.small(name="fit_level1_items270", n_layers=3, n_channels=2880, n_tokens=300, chunk_len=128,
+            level_mult=(1.0,)),
     # more than 2^16 deltas of one channel: the 32-bit per-level path
     W.small(name="fit_long_t76000", n_layers=1, n_channels=64, n_tokens=76000, chunk_len=1536,
             level_mult=(1.0, 4.0)),
