@@ -524,6 +524,8 @@ __global__ __launch_bounds__(kWin ? 64 * kEncWinWaves : 1024) void encode_kernel
   const float bw = P.layer_bin[l] * P.level_mult[lv];
   const float w = bw * s;
   const float is = 1.0f / s, iw = 1.0f / w;
+  float one;   // 1.0 that the compiler cannot fold away
+  asm volatile("s_mov_b32 %0, 1.0" : "=s"(one));
 
   cg_lds_u16* tabA = (cg_lds_u16*)(tabs + u * ustride + lane * kEncTabStride);   // anchors
   // the lane's delta table: the whole table (entry i at tabD[i]), or its window (entries wk0
@@ -553,7 +555,9 @@ __global__ __launch_bounds__(kWin ? 64 * kEncWinWaves : 1024) void encode_kernel
     for (int u = 0; u < kPipe; ++u) {
       const float v = cg_h2f((uint16_t)xv[u]);
       const bool anc = kG > 0 ? u == 0 : gq == 0;
-      const int q = anc ? cg_quant_inv(v, s, is) : cg_quant_inv(v - a, w, iw);
+      // v - a as fma(v, 1, -a): the same value (v * 1 exact, one rounding), and with the 1 in a
+      // register the compiler fuses the fp16 widening into it (one v_fma_mix_f32)
+      const int q = anc ? cg_quant_inv(v, s, is) : cg_quant_inv(__builtin_fmaf(v, one, -a), w, iw);
       const int sym = q + 127;
       if (anc) {   // coded in the anchor pass; here only the base of the group's deltas
         a = (float)q * s;
